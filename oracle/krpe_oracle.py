@@ -1,0 +1,143 @@
+"""Plain fp64 CPU oracle for kernelized attention with RPE.
+
+TEST INFRASTRUCTURE ONLY.  This module is imported by the test-suite, by the
+smoke check of the build entry point and by the CPU-baseline leg of the
+benchmark, and by nothing else: the library's compute path never calls it.
+
+It computes the *definitions* written in the paper, directly and slowly, in
+float64 (inputs given in fp32 or bf16 are converted exactly):
+
+* ``prf_features``      -- Eq. (5), the positive random feature map.
+* ``toeplitz_matrix``   -- the positional-correlation matrix C = {c_{j-i}},
+                           c_t = exp(b_t) (Section 3.2, below Eq. (10)).
+* ``toeplitz_product``  -- C @ a by plain matrix multiplication: the
+                           "naive" quadratic route that the FFT replaces
+                           (Eqs. (9)-(10)); FFT and direct product agree
+                           exactly up to rounding, so this is the reference.
+* ``attention``         -- Eq. (7): z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j
+                           / phi(q_i) sum_j c_{j-i} phi(k_j)^T, O(n^2).
+* ``attention_rows``    -- the same formula evaluated for selected rows only,
+                           so that outputs of full-size workloads can be
+                           checked one by one.
+
+Conventions (readings of the paper, stated once here):
+* b[h, s] holds b_t for t = s - (n - 1), the ordering of Algorithm 1's
+  argument (b_{-(n-1)}, ..., b_{n-1}).
+* C_ij = c_{j-i} with i the query position and j the key position, as in
+  Eq. (6), Eq. (7) and the matrix printed in Eqs. (9)-(10).
+* Causal masking is expressed through b alone: b_t = -inf gives c_t = 0
+  exactly (Section 3.2, footnote on teacher forcing).
+* phi is applied to q and k as given; any 1/sqrt(d) temperature is the
+  caller's (Eq. (7) and Lemma 2 use the raw kernel exp(x y^T)).
+
+Every function here is pinned by ``tests/test_oracle_pins.py`` against
+brute force, closed forms, the paper's special cases and invariants.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = ["prf_features", "toeplitz_matrix", "toeplitz_product", "attention",
+           "attention_rows"]
+
+
+def _f64(x) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64)
+
+
+def prf_features(x, W) -> np.ndarray:
+    """Positive random features, Eq. (5).
+
+    phi(x)_l = exp(w_l x^T - ||x||^2 / 2) / sqrt(m),  l = 1..m.
+
+    x : [..., H, n, d] (or [n, d]);  W : [H, m, d] (or [m, d]).
+    Returns [..., H, n, m] in float64.
+    """
+    x = _f64(x)
+    W = _f64(W)
+    m = W.shape[-2]
+    proj = x @ np.swapaxes(W, -1, -2)                 # w_l . x for every row
+    half_sq = 0.5 * np.sum(x * x, axis=-1, keepdims=True)
+    return np.exp(proj - half_sq) / np.sqrt(m)
+
+
+def toeplitz_matrix(b_h) -> np.ndarray:
+    """C_ij = exp(b_{j-i}) for one head; b_h has length 2n-1 (index t + n - 1)."""
+    b_h = _f64(b_h)
+    n = (b_h.shape[-1] + 1) // 2
+    i = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    return np.exp(b_h[j - i + n - 1])
+
+
+def toeplitz_product(b, a) -> np.ndarray:
+    """y[beta, h, c, i] = sum_j exp(b[h, j - i + n - 1]) a[beta, h, c, j].
+
+    The direct (quadratic) product C a of Eqs. (9)-(10), per head.
+    b : [H, 2n-1];  a : [B, H, C, n].  Returns [B, H, C, n] float64.
+    """
+    b = _f64(b)
+    a = _f64(a)
+    out = np.empty_like(a)
+    for h in range(b.shape[0]):
+        C = toeplitz_matrix(b[h])
+        out[:, h] = a[:, h] @ C.T
+    return out
+
+
+def attention(q, k, v, b, W, *, row_tile: int = 1024):
+    """Kernelized attention with RPE, Eq. (7), evaluated directly.
+
+    For every (batch, head): Phi_q, Phi_k by Eq. (5); the n x n weight matrix
+    M_ij = c_{j-i} * phi(q_i) phi(k_j)^T; numerator M v, denominator M 1.
+    Rows are processed in tiles to bound memory.
+
+    q, k, v : [B, H, n, d];  b : [H, 2n-1];  W : [H, m, d].
+    Returns (z [B, H, n, d], den [B, H, n]) in float64.
+    """
+    q, k, v, b, W = map(_f64, (q, k, v, b, W))
+    Bn, H, n, d = q.shape
+    z = np.empty((Bn, H, n, d))
+    den = np.empty((Bn, H, n))
+    for h in range(H):
+        for beta in range(Bn):
+            fq = prf_features(q[beta, h], W[h])
+            fk = prf_features(k[beta, h], W[h])
+            for i0 in range(0, n, row_tile):
+                i1 = min(n, i0 + row_tile)
+                rows = np.arange(i0, i1)[:, None]
+                cols = np.arange(n)[None, :]
+                c = np.exp(b[h][cols - rows + n - 1])      # c_{j-i}
+                mt = c * (fq[i0:i1] @ fk.T)
+                num = mt @ v[beta, h]
+                dd = mt.sum(axis=1)
+                z[beta, h, i0:i1] = num / dd[:, None]
+                den[beta, h, i0:i1] = dd
+    return z, den
+
+
+def attention_rows(q, k, v, b, W, rows):
+    """Eq. (7) for selected output rows only.
+
+    rows : iterable of (beta, h, i).  Returns (z [R, d], den [R]) float64 in
+    the order given.  Cost per row is O(n (m + d)) after one O(n m d)
+    feature map per distinct (beta, h).
+    """
+    b = _f64(b)
+    rows = [tuple(int(t) for t in r) for r in rows]
+    n = q.shape[2]
+    d = q.shape[3]
+    z = np.empty((len(rows), d))
+    den = np.empty(len(rows))
+    cache = {}
+    for r, (beta, h, i) in enumerate(rows):
+        if (beta, h) not in cache:
+            cache.clear()
+            cache[(beta, h)] = prf_features(k[beta, h], W[h])
+        fk = cache[(beta, h)]
+        fq = prf_features(_f64(q[beta, h, i])[None, :], W[h])[0]
+        c = np.exp(b[h][np.arange(n) - i + n - 1])
+        w = c * (fk @ fq)
+        den[r] = w.sum()
+        z[r] = (w @ _f64(v[beta, h])) / den[r]
+    return z, den

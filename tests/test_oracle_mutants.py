@@ -1,0 +1,52 @@
+"""Plant plausible mistakes in copies of the oracle and show the pins catch them.
+
+Each mutant is the oracle's own source with one textual change (a flipped
+offset sign, an off-by-one index, a dropped term, a transposed operand, ...),
+executed into a throw-away module on the CPU.  The pins of
+``test_oracle_pins.py`` are re-run on it and at least one must fail.
+"""
+import inspect
+import types
+
+import numpy as np
+import pytest
+
+import oracle.krpe_oracle as ORACLE_SRC
+from test_oracle_pins import ALL_CHECKS
+
+MUTANTS = {
+    "offset_sign_flipped": ("c = np.exp(b[h][cols - rows + n - 1])", "c = np.exp(b[h][rows - cols + n - 1])"),
+    "offset_off_by_one": ("c = np.exp(b[h][cols - rows + n - 1])", "c = np.exp(b[h][(cols - rows + n) % (2 * n - 1)])"),
+    "norm_term_dropped": ("return np.exp(proj - half_sq) / np.sqrt(m)", "return np.exp(proj) / np.sqrt(m)"),
+    "norm_term_not_halved": ("half_sq = 0.5 * np.sum(x * x, axis=-1, keepdims=True)", "half_sq = np.sum(x * x, axis=-1, keepdims=True)"),
+    "sqrt_m_dropped": ("return np.exp(proj - half_sq) / np.sqrt(m)", "return np.exp(proj - half_sq)"),
+    "bias_not_exponentiated": ("c = np.exp(b[h][cols - rows + n - 1])", "c = b[h][cols - rows + n - 1]"),
+    "query_key_swapped": ("mt = c * (fq[i0:i1] @ fk.T)", "mt = c * (fk[i0:i1] @ fq.T)"),
+    "bias_left_out_of_denominator": ("dd = mt.sum(axis=1)", "dd = (fq[i0:i1] @ fk.T).sum(axis=1)"),
+    "values_replaced_by_keys": ("num = mt @ v[beta, h]", "num = mt @ k[beta, h]"),
+    "toeplitz_transposed": ("out[:, h] = a[:, h] @ C.T", "out[:, h] = a[:, h] @ C"),
+    "toeplitz_matrix_sign": ("return np.exp(b_h[j - i + n - 1])", "return np.exp(b_h[i - j + n - 1])"),
+    "rows_offset_sign": ("c = np.exp(b[h][np.arange(n) - i + n - 1])", "c = np.exp(b[h][i - np.arange(n) + n - 1])"),
+    "rows_wrong_head_features": ("cache[(beta, h)] = prf_features(k[beta, h], W[h])", "cache[(beta, h)] = prf_features(k[beta, h], W[0])"),
+}
+
+
+def _mutant(old, new):
+    src = inspect.getsource(ORACLE_SRC)
+    assert src.count(old) == 1, f"mutation anchor not found exactly once: {old!r}"
+    mod = types.ModuleType("oracle_mutant")
+    exec(compile(src.replace(old, new), "<oracle-mutant>", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    mod = _mutant(*MUTANTS[name])
+    caught = []
+    with np.errstate(all="ignore"):
+        for check in ALL_CHECKS:
+            try:
+                check(mod)
+            except Exception:      # AssertionError or a numerical blow-up
+                caught.append(check.__name__)
+    assert caught, f"no pin detects mutant {name}"
