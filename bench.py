@@ -1,0 +1,237 @@
+"""Benchmark of the kernelized-attention-with-RPE forward pass on one GPU.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 4]
+
+A step is one krpe_attention_fwd call over the whole workload (all batches and
+heads): spectrum of c, feature maps of q and k, the FFT convolution +
+contraction kernel and the final division.  Inputs are seeded synthetic data
+already resident in device memory when the timed region starts.  Prints one
+JSON line with whole-job throughput (tokens/s), the roofline position of the
+dominant kernel (timed with HIP events on the library's stream) and the fp64
+oracle's throughput on a bounded sample of the same workload on the host CPU.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tokens/sec and ms/layer for RPE kernelized attn fwd; % HBM/MFMA roofline"
+PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak
+PEAK_HBM_GBS = 8000.0
+
+
+def conv_stage_flops(B: int, H: int, n: int, d: int, m: int) -> float:
+    """Algorithmic flops of the FFT convolution + contraction stage.
+
+    Per channel (m (d+1) channels per head): two real FFTs of length L = 2n at
+    2.5 L log2 L flops each, the pointwise complex product with the spectrum
+    over n + 1 bins (6 flops each), forming the channel (1 multiply per
+    position) and the contraction with phi(q) (1 multiply-add per position).
+    """
+    L = 2 * n
+    per_channel = 5.0 * L * math.log2(L) + 6.0 * (n + 1) + 4.0 * n
+    return B * H * m * (d + 1) * per_channel
+
+
+def conv_stage_bytes(B, H, n, d, m, s_in) -> float:
+    """Algorithmic HBM bytes of the stage: phi(q), phi(k) (fp32), v, the spectrum, partial sums."""
+    return B * H * (2 * n * m * 4 + n * d * s_in + 2 * (d + 1) * n * 4) + H * 2 * n * 8
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (the library records them on its own stream)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self) -> int:
+        e = ctypes.c_void_p()
+        rc = self.lib.hipEventCreate(ctypes.byref(e))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed: {rc}")
+        return e.value
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        self.lib.hipEventSynchronize(ctypes.c_void_p(b))
+        out = ctypes.c_float()
+        rc = self.lib.hipEventElapsedTime(ctypes.byref(out), ctypes.c_void_p(a), ctypes.c_void_p(b))
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return float(out.value)
+
+    def destroy(self, e: int) -> None:
+        self.lib.hipEventDestroy(ctypes.c_void_p(e))
+
+
+def blas_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        nums = [p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+        if nums:
+            return int(max(nums))
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None):
+    """Time the fp64 oracle (Eq. (7), O(n^2) per head) on whole (batch, head) units.
+
+    Runs units until `budget_s` of wall time is spent (at least one), and
+    extrapolates to the full layer.  Also returns the GPU's per-row normwise
+    error on the units the oracle computed.
+    """
+    import oracle
+    wl = d["workload"]
+    B, H, n = wl.B, d["H"], wl.n
+    units = [(beta, h) for h in range(H) for beta in range(B)]
+    rng = np.random.default_rng([2106, 12566, 99])
+    rng.shuffle(units)
+    t0 = time.perf_counter()
+    done = 0
+    worst = 0.0
+    for beta, h in units:
+        z, _ = oracle.attention(d["q"][beta:beta + 1, h:h + 1], d["k"][beta:beta + 1, h:h + 1],
+                                d["v"][beta:beta + 1, h:h + 1], d["b"][h:h + 1], d["W"][h:h + 1])
+        done += 1
+        if z_gpu is not None:
+            num = np.max(np.abs(z_gpu[beta, h] - z[0, 0]), axis=-1)
+            worst = max(worst, float(np.max(num / np.max(np.abs(z[0, 0]), axis=-1))))
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    elapsed = time.perf_counter() - t0
+    per_unit = elapsed / done
+    layer_s = per_unit * B * H
+    tokens_per_s = B * n / layer_s
+    return {
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": f"{done} of {B * H} (batch, head) units of {wl.name}, full Eq. (7) per unit in fp64 "
+                  f"({elapsed:.1f} s), extrapolated to the layer; BLAS threads as cores, elementwise exp "
+                  f"single-threaded",
+        "layer_s": layer_s,
+    }, worst, done
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(heads are independent, so a multi-GPU run would shard (batch, head) with no "
+              "communication; it is not built)", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2106_12566_amd import krpe, synth
+
+    if not os.path.exists(krpe.lib_path()):
+        from paper_2106_12566_amd import build
+        build.build()
+    krpe.load()
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+
+    d = synth.make(args.workload)
+    wl = d["workload"]
+    B, H, n, dd, m = wl.B, d["H"], wl.n, wl.d, wl.m
+    tdt = torch.bfloat16 if wl.qkv_dtype == "bf16" else torch.float32
+    dev = torch.device("cuda", 0)
+    q = torch.from_numpy(d["q"]).to(dev).to(tdt)
+    k = torch.from_numpy(d["k"]).to(dev).to(tdt)
+    v = torch.from_numpy(d["v"]).to(dev).to(tdt)
+    b = torch.from_numpy(d["b"]).to(dev)
+    W = torch.from_numpy(d["W"]).to(dev)
+    out = torch.empty((B, H, n, dd), dtype=torch.float32, device=dev)
+    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m), dtype=torch.uint8, device=dev)
+    print(f"bench: workload {wl.name} B={B} H={H} n={n} d={dd} m={m} {wl.qkv_dtype}", file=sys.stderr,
+          flush=True)
+
+    hip = HipEvents()
+    events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(args.steps)]
+
+    for _ in range(args.warmup):
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws)
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    ms_per_step = 1e3 * elapsed / args.steps
+    stage_names = ["spectrum", "feature_map", "conv_contract", "combine"]
+    stages = {name: float(np.mean([hip.elapsed_ms(ev[i], ev[i + 1]) for ev in events]))
+              for i, name in enumerate(stage_names)}
+    for ev in events:
+        for e in ev:
+            hip.destroy(e)
+    tokens = B * n
+    value = tokens / (ms_per_step * 1e-3)
+
+    flops = conv_stage_flops(B, H, n, dd, m)
+    conv_ms = stages["conv_contract"]
+    achieved_tflops = flops / (conv_ms * 1e-3) / 1e12
+    s_in = 2 if wl.qkv_dtype == "bf16" else 4
+    conv_gbs = conv_stage_bytes(B, H, n, dd, m, s_in) / (conv_ms * 1e-3) / 1e9
+    print(f"bench: {ms_per_step:.3f} ms/step, stages {stages}", file=sys.stderr, flush=True)
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "H": H, "n": n, "d": dd, "m": m,
+                   "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
+                   "causal": wl.causal, "ms_per_layer": ms_per_step, "stages_ms": stages,
+                   "conv_stage_hbm_gbs": conv_gbs},
+        "roofline": {"bound": "alu", "kernel": "k_conv_contract", "achieved": achieved_tflops,
+                     "peak": PEAK_FP32_VECTOR_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        z_gpu = out.cpu().numpy()
+        cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu)
+        result["cpu_baseline"] = {k2: cb[k2] for k2 in ("value", "unit", "cores", "kind", "sample")}
+        result["config"]["parity_rownorm_err"] = err
+        result["config"]["parity_units"] = units
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

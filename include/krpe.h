@@ -1,0 +1,161 @@
+/*
+ * krpe.h -- C ABI of the kernelized-attention-with-RPE library (libkrpe.so).
+ *
+ * The library computes, on one AMD Instinct MI355X (gfx950), the forward pass
+ * of positive-random-feature kernelized attention with a relative positional
+ * bias (Luo et al., "Stable, Fast and Accurate: Kernelized Attention with
+ * Relative Positional Encoding", NeurIPS 2021), in O(n log n) per channel:
+ *
+ *   z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j  /  phi(q_i) sum_j c_{j-i} phi(k_j)^T
+ *                                                        (Section 3.2, Eq. (7))
+ *   phi(x) = exp(W x^T - ||x||^2 / 2) / sqrt(m)          (Section 2.1, Eq. (5))
+ *   c_t    = exp(b_t),  t = j - i in [-(n-1), n-1]       (Section 2.2, Eq. (6))
+ *
+ * The products with the Toeplitz matrix C = {c_{j-i}} of Eqs. (9)-(10) run as
+ * zero-padded FFT convolutions (Section 3.2, the paragraph after Eq. (10)).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every array pointer is a DEVICE pointer (memory from hipMalloc or any
+ *   allocator handing out device memory, e.g. a torch CUDA tensor), holding a
+ *   dense row-major array, 16-byte aligned.  The caller owns all memory: the
+ *   library never allocates, frees or keeps a pointer after returning.
+ * - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *   work is enqueued asynchronously on it; buffers must stay alive until that
+ *   work has completed.  Faults during execution surface at the caller's next
+ *   synchronisation with the stream.
+ * - b[h, s] stores b_t for t = s - (n - 1), i.e. the vector
+ *   (b_{-(n-1)}, ..., b_{n-1}) of Algorithm 1, one vector of length 2n-1 per
+ *   head.  b_t = -inf is allowed and gives c_t = 0 exactly; causal masking
+ *   (Section 3.2, footnote on teacher forcing) is expressed this way, with
+ *   b_t = -inf for t > 0.
+ * - All argument checks run on the host before any HIP call.  A non-OK return
+ *   means nothing was enqueued; krpe_last_error() then describes the problem.
+ *   Launch failures return KRPE_ERR_HIP.  No exception or abort crosses the ABI.
+ * - Inputs are read-only.  Outputs are fully overwritten and must not overlap
+ *   any input or the workspace (KRPE_ERR_ALIAS).  Workspace contents are
+ *   undefined on return.
+ * - Supported sizes: 1 <= n <= 16384 (any n; the FFT length is 2N with N the
+ *   next power of two >= n), 1 <= d <= 128, 1 <= m <= 1024, B, H >= 0, C >= 0.
+ *   B*H == 0 (or C == 0) is a valid empty call that enqueues nothing.
+ * - Precondition (not checked: it would need to read device memory): every
+ *   query row's window of b holds a finite entry (b_0 finite suffices), so
+ *   every denominator of Eq. (7) is > 0.  Otherwise that row of z is NaN.
+ * - Functions are stateless and thread-safe.
+ */
+#ifndef KRPE_H_
+#define KRPE_H_
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of q, k, v and x.  W, b, phi, a, y and z are always fp32. */
+typedef enum {
+  KRPE_F32 = 0,  /* IEEE binary32 */
+  KRPE_BF16 = 1  /* bfloat16 bit patterns (uint16); converted exactly to fp32 */
+} krpe_dtype_t;
+
+typedef enum {
+  KRPE_OK = 0,
+  KRPE_ERR_NULL = 1,        /* a required pointer is NULL */
+  KRPE_ERR_SHAPE = 2,       /* a size is negative or inconsistent */
+  KRPE_ERR_UNSUPPORTED = 3, /* valid per the method, outside the supported sizes */
+  KRPE_ERR_DTYPE = 4,       /* unknown krpe_dtype_t */
+  KRPE_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query says */
+  KRPE_ERR_ALIAS = 6,       /* an output overlaps an input or the workspace */
+  KRPE_ERR_HIP = 7,         /* a HIP runtime call or kernel launch failed */
+  KRPE_ERR_ALIGN = 8        /* a pointer is not 16-byte aligned */
+} krpe_status_t;
+
+/* Version of this ABI (incremented on any incompatible change). */
+int krpe_abi_version(void);
+
+/* Static text for a status code; never NULL. */
+const char* krpe_status_str(int status);
+
+/* Detail of the last non-OK return on the calling thread ("" if none). */
+const char* krpe_last_error(void);
+
+/*
+ * Positive random feature map, Section 2.1, Eq. (5):
+ *   phi[beta, h, i, l] = exp( sum_a W[h, l, a] x[beta, h, i, a]
+ *                             - 0.5 sum_a x[beta, h, i, a]^2 ) / sqrt(m)
+ * x   : [B, H, n, d] in x_dtype        W : [H, m, d] fp32 (rows w_l)
+ * phi : [B, H, n, m] fp32 (output)
+ * Runs as an fp32 MFMA contraction with the exponential fused into its epilogue.
+ */
+krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float* phi,
+                               int B, int H, int n, int d, int m, void* stream);
+
+/*
+ * Bytes of workspace krpe_toeplitz_conv needs for H heads of length n
+ * (0 if the sizes are invalid or unsupported).
+ */
+size_t krpe_toeplitz_conv_workspace(int H, int n);
+
+/*
+ * Product with the Toeplitz matrix C = {c_{j-i}} of Eqs. (9)-(10), per channel:
+ *   y[beta, h, ch, i] = sum_{j<n} exp(b[h, j - i + n - 1]) * a[beta, h, ch, j]
+ * b : [H, 2n-1] fp32     a, y : [B, H, C, n] fp32 (sequence-contiguous channels)
+ * Computed as a zero-padded length-2N FFT convolution (two length-N halves).
+ */
+krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
+                                 int B, int H, int C, int n,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Bytes of workspace krpe_attention_fwd needs (0 if the sizes are invalid or
+ * unsupported).
+ */
+size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m);
+
+/*
+ * Kernelized attention with RPE, Section 3.2, Eq. (7), with phi from Eq. (5)
+ * using W[h] for head h and c = exp(b[h]):
+ * q, k, v : [B, H, n, d] in qkv_dtype (the already-projected x W^Q, x W^K, x W^V)
+ * b       : [H, 2n-1] fp32            W : [H, m, d] fp32
+ * z       : [B, H, n, d] fp32 (output)
+ * ws      : device workspace of at least krpe_attention_fwd_workspace() bytes.
+ * Queries and keys are used as given (no normalisation, no 1/sqrt(d) scale).
+ */
+krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, int qkv_dtype,
+                                 const float* b, const float* W, float* z,
+                                 int B, int H, int n, int d, int m,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * krpe_attention_fwd with per-stage timing: when `events` is not NULL it points
+ * to KRPE_STAGE_EVENTS hipEvent_t handles (as void*), recorded on `stream`
+ * before the spectrum of c, before the feature maps, before the FFT
+ * convolution + contraction kernel, before the final division and after it.
+ * The events are created and owned by the caller.
+ */
+#define KRPE_STAGE_EVENTS 5
+krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const void* v,
+                                          int qkv_dtype, const float* b, const float* W,
+                                          float* z, int B, int H, int n, int d, int m,
+                                          void* ws, size_t ws_bytes, void* stream,
+                                          void* const* events);
+
+/*
+ * Rows of the last krpe_attention_fwd call (with this workspace and these
+ * sizes) that were evaluated exactly instead of through the FFT.
+ *
+ * The FFT path's fp32 rounding error is spread over a whole sequence, so a
+ * row whose denominator of Eq. (7) is small next to the sequence's total
+ * (the first rows under a causal mask, for example) cannot be resolved by it.
+ * krpe_attention_fwd bounds that error for every row and recomputes the rows
+ * it cannot certify directly from Eq. (7) with fp64 accumulation.  This call
+ * waits for `stream`, then copies the number of such rows into *fixed_rows.
+ */
+krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, int H, int n, int d, int m,
+                                       unsigned* fixed_rows, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KRPE_H_ */

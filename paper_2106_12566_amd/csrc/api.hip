@@ -1,0 +1,283 @@
+// C ABI of libkrpe.so (declared in include/krpe.h): argument validation on the
+// host, workspace carving and the launch sequence of each entry point.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <string>
+
+#include "common.hpp"
+#include "krpe.h"
+#include "launch.hpp"
+
+namespace krpe {
+namespace {
+
+thread_local std::string g_last_error;
+
+krpe_status_t fail(krpe_status_t s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+int log2_ceil(int n) {
+  int l = 0;
+  while ((1 << l) < n) ++l;
+  return l;
+}
+
+size_t align_up(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+struct Range {
+  const void* p;
+  size_t bytes;
+};
+bool overlaps(Range a, Range b) {
+  if (a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+size_t dtype_size(int dt) { return dt == KRPE_BF16 ? 2 : 4; }
+
+krpe_status_t hip_check(hipError_t e, const char* what) {
+  if (e == hipSuccess) return KRPE_OK;
+  return fail(KRPE_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm) {
+  if (B < 0 || H < 0 || n < 0 || (need_dm && (d < 0 || m < 0))) return fail(KRPE_ERR_SHAPE, "negative size");
+  if (n < 1) return fail(KRPE_ERR_SHAPE, "n must be >= 1 (b has 2n-1 entries)");
+  if (n > (1 << kMaxLog2N)) return fail(KRPE_ERR_UNSUPPORTED, "n > 16384 is not supported");
+  if (need_dm) {
+    if (d < 1 || m < 1) return fail(KRPE_ERR_SHAPE, "d and m must be >= 1");
+    if (d > kMaxD) return fail(KRPE_ERR_UNSUPPORTED, "d > 128 is not supported");
+    if (m > kMaxM) return fail(KRPE_ERR_UNSUPPORTED, "m > 1024 is not supported");
+  }
+  // Row indices (bh * n + i) are kept in 32 bits and grids in 31 bits.
+  const long long rows = static_cast<long long>(B) * H * n;
+  if (rows >= (1LL << 31)) return fail(KRPE_ERR_UNSUPPORTED, "B * H * n >= 2^31 is not supported");
+  return KRPE_OK;
+}
+
+krpe_status_t record(void* const* events, int i, hipStream_t st) {
+  if (!events || !events[i]) return KRPE_OK;
+  return hip_check(hipEventRecord(static_cast<hipEvent_t>(events[i]), st), "hipEventRecord");
+}
+
+}  // namespace
+
+AttnLayout attn_layout(int B, int H, int n, int d, int m) {
+  AttnLayout L{};
+  L.l2 = log2_ceil(n);
+  const size_t N = static_cast<size_t>(1) << L.l2;
+  const size_t bh = static_cast<size_t>(B) * H;
+  const size_t pairs = static_cast<size_t>(d + 2) / 2;
+  size_t off = 0;
+  auto take = [&off](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.tw = take(2 * N * sizeof(float2));
+  L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
+  L.phiq = take(bh * m * N * sizeof(float));
+  L.phik = take(bh * m * N * sizeof(float));
+  L.part = take(bh * 2 * (d + 1) * n * sizeof(float));
+  L.bnd = take(bh * pairs * n * sizeof(float));
+  L.colmax = take(bh * d * sizeof(float));
+  L.fix = take((1 + bh * n) * sizeof(unsigned));
+  L.total = off;
+  return L;
+}
+
+ConvLayout conv_layout(int H, int n) {
+  ConvLayout L{};
+  L.l2 = log2_ceil(n);
+  const size_t N = static_cast<size_t>(1) << L.l2;
+  L.tw = 0;
+  L.hs = align_up(2 * N * sizeof(float2));
+  L.total = align_up(L.hs + static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  return L;
+}
+
+}  // namespace krpe
+
+using namespace krpe;
+
+extern "C" {
+
+int krpe_abi_version(void) { return 1; }
+
+const char* krpe_status_str(int s) {
+  switch (s) {
+    case KRPE_OK: return "ok";
+    case KRPE_ERR_NULL: return "null pointer";
+    case KRPE_ERR_SHAPE: return "invalid shape";
+    case KRPE_ERR_UNSUPPORTED: return "unsupported size";
+    case KRPE_ERR_DTYPE: return "unknown dtype";
+    case KRPE_ERR_WORKSPACE: return "workspace missing or too small";
+    case KRPE_ERR_ALIAS: return "output overlaps an input or the workspace";
+    case KRPE_ERR_HIP: return "HIP runtime error";
+    case KRPE_ERR_ALIGN: return "pointer not 16-byte aligned";
+    default: return "unknown status";
+  }
+}
+
+const char* krpe_last_error(void) { return g_last_error.c_str(); }
+
+krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float* phi, int B, int H, int n, int d,
+                               int m, void* stream) {
+  g_last_error.clear();
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (x_dtype != KRPE_F32 && x_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "x_dtype must be F32 or BF16");
+  const size_t bh = static_cast<size_t>(B) * H;
+  if (bh == 0) return KRPE_OK;
+  if (!x || !W || !phi) return fail(KRPE_ERR_NULL, "x, W and phi must be non-NULL");
+  if (misaligned(x) || misaligned(W) || misaligned(phi))
+    return fail(KRPE_ERR_ALIGN, "x, W, phi must be 16-byte aligned");
+  const Range rphi{phi, bh * n * m * sizeof(float)};
+  if (overlaps(rphi, {x, bh * n * d * dtype_size(x_dtype)}) ||
+      overlaps(rphi, {W, static_cast<size_t>(H) * m * d * sizeof(float)}))
+    return fail(KRPE_ERR_ALIAS, "phi overlaps x or W");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return hip_check(launch_feature_map(x_dtype == KRPE_BF16, x, x, W, phi, phi, 1, false, m, static_cast<int>(bh),
+                                      H, n, d, m, st),
+                   "feature map launch");
+}
+
+size_t krpe_toeplitz_conv_workspace(int H, int n) {
+  if (H < 0 || n < 1 || n > (1 << kMaxLog2N)) return 0;
+  return conv_layout(H, n).total;
+}
+
+krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B, int H, int C, int n, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (C < 0) return fail(KRPE_ERR_SHAPE, "negative size");
+  if (krpe_status_t s = check_dims(B, H, n, 0, 0, false)) return s;
+  if (static_cast<long long>(B) * H * C * n >= (1LL << 31))
+    return fail(KRPE_ERR_UNSUPPORTED, "B * H * C * n >= 2^31 is not supported");
+  const size_t bh = static_cast<size_t>(B) * H;
+  if (bh == 0 || C == 0) return KRPE_OK;
+  if (!b || !a || !y) return fail(KRPE_ERR_NULL, "b, a and y must be non-NULL");
+  if (misaligned(b) || misaligned(a) || misaligned(y) || misaligned(ws))
+    return fail(KRPE_ERR_ALIGN, "b, a, y, ws must be 16-byte aligned");
+  const ConvLayout L = conv_layout(H, n);
+  if (!ws || ws_bytes < L.total)
+    return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
+  const Range ry{y, bh * C * n * sizeof(float)};
+  const Range rws{ws, ws_bytes};
+  const Range ra{a, bh * C * n * sizeof(float)};
+  const Range rb{b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)};
+  if (overlaps(ry, ra) || overlaps(ry, rb) || overlaps(ry, rws) || overlaps(rws, ra) || overlaps(rws, rb))
+    return fail(KRPE_ERR_ALIAS, "y or the workspace overlaps an input");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  float2* tw = reinterpret_cast<float2*>(w + L.tw);
+  float2* Hs = reinterpret_cast<float2*>(w + L.hs);
+  if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, nullptr, H, n, st), "spectrum launch"))
+    return s;
+  return hip_check(launch_toeplitz(L.l2, a, y, Hs, tw, static_cast<int>(bh), H, C, n, st), "toeplitz launch");
+}
+
+size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
+  if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
+  return attn_layout(B, H, n, d, m).total;
+}
+
+krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
+                                          const float* W, float* z, int B, int H, int n, int d, int m, void* ws,
+                                          size_t ws_bytes, void* stream, void* const* events) {
+  g_last_error.clear();
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
+  const size_t bh = static_cast<size_t>(B) * H;
+  if (bh == 0) return KRPE_OK;
+  if (!q || !k || !v || !b || !W || !z) return fail(KRPE_ERR_NULL, "q, k, v, b, W and z must be non-NULL");
+  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(b) || misaligned(W) || misaligned(z) ||
+      misaligned(ws))
+    return fail(KRPE_ERR_ALIGN, "all pointers must be 16-byte aligned");
+  const AttnLayout L = attn_layout(B, H, n, d, m);
+  if (!ws || ws_bytes < L.total)
+    return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
+  const size_t qkv_bytes = bh * n * d * dtype_size(qkv_dtype);
+  const Range ins[] = {{q, qkv_bytes},
+                       {k, qkv_bytes},
+                       {v, qkv_bytes},
+                       {b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)},
+                       {W, static_cast<size_t>(H) * m * d * sizeof(float)}};
+  const Range rz{z, bh * n * d * sizeof(float)};
+  const Range rws{ws, ws_bytes};
+  if (overlaps(rz, rws)) return fail(KRPE_ERR_ALIAS, "z overlaps the workspace");
+  for (const Range& r : ins)
+    if (overlaps(rz, r) || overlaps(rws, r)) return fail(KRPE_ERR_ALIAS, "z or the workspace overlaps an input");
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  float2* tw = reinterpret_cast<float2*>(w + L.tw);
+  float2* Hs = reinterpret_cast<float2*>(w + L.hs);
+  float2* hnorm = reinterpret_cast<float2*>(w + L.hnorm);
+  float* phiq = reinterpret_cast<float*>(w + L.phiq);
+  float* phik = reinterpret_cast<float*>(w + L.phik);
+  float* part = reinterpret_cast<float*>(w + L.part);
+  float* bnd = reinterpret_cast<float*>(w + L.bnd);
+  float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  unsigned* fix_count = reinterpret_cast<unsigned*>(w + L.fix);
+  unsigned* fix_list = fix_count + 1;
+  const int BHi = static_cast<int>(bh);
+  const int N = 1 << L.l2;
+  const bool bf16 = qkv_dtype == KRPE_BF16;
+
+  if (krpe_status_t s = record(events, 0, st)) return s;
+  if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, fix_count, H, n, st), "spectrum launch"))
+    return s;
+  if (krpe_status_t s = record(events, 1, st)) return s;
+  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, st),
+                                  "feature map launch"))
+    return s;
+  if (krpe_status_t s = record(events, 2, st)) return s;
+  if (krpe_status_t s = hip_check(
+          launch_conv(L.l2, bf16, phiq, phik, v, Hs, tw, part, bnd, colmax, BHi, H, n, d, m, st), "conv launch"))
+    return s;
+  if (krpe_status_t s = record(events, 3, st)) return s;
+  if (krpe_status_t s = hip_check(launch_combine(part, bnd, colmax, hnorm, z, fix_count, fix_list, BHi, H, n, L.l2,
+                                                 d, st),
+                                  "combine launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix_count, fix_list, BHi, H, n, N, d, m,
+                                               st),
+                                  "fixup launch"))
+    return s;
+  return record(events, 4, st);
+}
+
+krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
+                                 const float* W, float* z, int B, int H, int n, int d, int m, void* ws,
+                                 size_t ws_bytes, void* stream) {
+  return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, ws, ws_bytes, stream, nullptr);
+}
+
+krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, int H, int n, int d, int m,
+                                       unsigned* fixed_rows, void* stream) {
+  g_last_error.clear();
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (!fixed_rows) return fail(KRPE_ERR_NULL, "fixed_rows must be non-NULL");
+  *fixed_rows = 0;
+  if (static_cast<size_t>(B) * H == 0) return KRPE_OK;
+  if (!ws) return fail(KRPE_ERR_NULL, "ws must be non-NULL");
+  const AttnLayout L = attn_layout(B, H, n, d, m);
+  if (ws_bytes < L.total) return fail(KRPE_ERR_WORKSPACE, "workspace smaller than these sizes need");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (krpe_status_t s = hip_check(hipStreamSynchronize(st), "hipStreamSynchronize")) return s;
+  return hip_check(
+      hipMemcpy(fixed_rows, static_cast<const char*>(ws) + L.fix, sizeof(unsigned), hipMemcpyDeviceToHost),
+      "hipMemcpy");
+}
+
+}  // extern "C"

@@ -1,0 +1,90 @@
+// Device-side constants and helpers shared by the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "fft.hpp"
+
+namespace krpe {
+
+constexpr int kMaxLog2N = 14;  // n <= 16384 (FFT length 2N <= 32768)
+constexpr int kMaxD = 128;
+constexpr int kMaxM = 1024;
+constexpr int kLog2R = 4;      // 16 complex values per thread
+
+// Launch shape of the transforms of length 2^L2: G transform units of T
+// threads per work-group, enough to fill 256 threads for short transforms.
+template <int L2>
+struct Conf {
+  using F = Fft<L2, kLog2R>;
+  static constexpr int G = F::T >= 256 ? 1 : 256 / F::T;
+  static constexpr int THREADS = G * F::T;
+  static constexpr int WAVES = (THREADS + 63) / 64;
+  static constexpr int LDS_SLOTS = F::P > 1 ? G * F::LDS : 1;
+};
+
+// Work-groups are dispatched round-robin over the 8 XCDs (each with its own
+// L2).  Renumber them so that every XCD runs a contiguous range of logical
+// blocks: units of one head then share an L2.  A bijection on [0, nblocks).
+__device__ __forceinline__ int xcd_block(int b, int nblocks) {
+  constexpr int kXcd = 8;
+  const int per = nblocks / kXcd, rem = nblocks % kXcd;
+  const int xcd = b % kXcd, slot = b / kXcd;
+  return (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+}
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }
+
+// Reduction over the lanes of one wave that belong to the same unit of T
+// threads (T a power of two; units are aligned to T inside the work-group).
+// Every lane of the unit receives the result.
+template <int T, typename Op>
+__device__ __forceinline__ float wave_unit_reduce(float v, Op op) {
+#pragma unroll
+  for (int off = 1; off < (T < 64 ? T : 64); off <<= 1) v = op(v, __shfl_xor(v, off));
+  return v;
+}
+
+// Reduction over all T threads of a unit.  `red` is LDS holding one float per
+// wave of the work-group.  Every thread of the work-group must call it (it
+// contains barriers when T > 64).
+template <int T, typename Op>
+__device__ __forceinline__ float unit_reduce(float v, float* red, Op op) {
+  v = wave_unit_reduce<T>(v, op);
+  if constexpr (T > 64) {
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) red[wave] = v;
+    __syncthreads();
+    const int first = (threadIdx.x / T) * (T / 64);
+    v = red[first];
+#pragma unroll
+    for (int w = 1; w < T / 64; ++w) v = op(v, red[first + w]);
+    __syncthreads();
+  }
+  return v;
+}
+
+struct OpMax {
+  __device__ __forceinline__ float operator()(float a, float b) const { return fmaxf(a, b); }
+};
+struct OpAdd {
+  __device__ __forceinline__ float operator()(float a, float b) const { return a + b; }
+};
+
+// FFT error model.  The rounding error of the zero-padded FFT product
+// y = C a (both spectrum halves, fp32) obeys, at every output i,
+//   |dy_i| <= kGamma * u * log2(L) * ( ||h||_2 ||x||_2 / sqrt(L) * s + |y_i| )
+// for a packed channel pair x = a0/s0 + i a1/s1 and channel scale s in
+// {s0, s1}; L = 2N, u = 2^-24, h the length-L circulant kernel.  The
+// constant is measured on adversarial inputs (heavy-tailed channels of very
+// different scales, causal and spiked kernels) by the GPU test of the model.
+constexpr float kGamma = 8.0f;
+constexpr float kUnitRoundoff = 5.9604645e-8f;
+// A row of Eq. (7) is certified when its bounded normwise relative error is
+// at most kTau; otherwise it is evaluated exactly.
+constexpr float kTau = 1.0e-4f;
+
+}  // namespace krpe

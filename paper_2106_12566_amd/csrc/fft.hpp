@@ -1,0 +1,293 @@
+// Register + LDS resident complex FFT for gfx950.
+//
+// The Toeplitz products of Eqs. (9)-(10) are done as FFT convolutions.  This
+// header holds the transform only; the kernels that use it are in krpe.hip.
+//
+// A transform of length N = 2^LOG2N is owned by T = N / R threads, each
+// holding R = 2^LOG2R complex values in registers.  It is a sequence of P
+// in-place Cooley-Tukey passes.  Pass p splits every sub-problem of length
+// L_p into R_p interleaved sub-sequences: its butterflies read the R_p values
+// at positions  q*L_p + t + S_p*r  (S_p = L_p / R_p, r < R_p), take a length
+// R_p DFT in registers, multiply by the twiddles W_{L_p}^{t*s} and write the
+// R_p results back to the same positions (output s to q*L_p + t + S_p*s).
+// Output s of sub-problem q is the start of sub-problem (q*R_p + s) of pass
+// p+1.  Because every pass writes exactly the positions it read, one barrier
+// per pass boundary is enough, and the inverse transform replays the passes
+// backwards (conjugate twiddles, conjugate DFTs) on the same positions.
+//
+// Data enters pass 0 in registers (thread tau holds positions tau + T*r) and
+// leaves the last pass in registers in digit-reversed order; the inverse takes
+// that order and returns positions tau + T*r.  So per-position data of a
+// thread (loads, twists, accumulators) never has to be exchanged.
+//
+// Positions are padded in LDS by one element per R to spread the strided
+// accesses of late passes over the banks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+namespace krpe {
+
+// ---------------------------------------------------------------- complex --
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 csub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+  return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+// a * conj(b)
+__device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
+  return make_float2(a.x * b.x + a.y * b.y, a.y * b.x - a.x * b.y);
+}
+
+// cos(2*pi*k/64) for k = 0..16 (first quadrant, exact zero at 16).
+__host__ __device__ constexpr float quarter_cos64(int k) {
+  constexpr float q[17] = {1.0f,
+                           0.99518472667219693f, 0.98078528040323043f, 0.95694033573220882f,
+                           0.92387953251128674f, 0.88192126434835505f, 0.83146961230254524f,
+                           0.77301045336273699f, 0.70710678118654757f, 0.63439328416364549f,
+                           0.55557023301960218f, 0.47139673682599781f, 0.38268343236508984f,
+                           0.29028467725446233f, 0.19509032201612833f, 0.098017140329560770f,
+                           0.0f};
+  return q[k];
+}
+// cos(2*pi*k/64) for any k, by quadrant symmetry.
+__host__ __device__ constexpr float cos64(int k) {
+  k = ((k % 64) + 64) % 64;
+  if (k <= 16) return quarter_cos64(k);
+  if (k <= 32) return -quarter_cos64(32 - k);
+  if (k <= 48) return -quarter_cos64(k - 32);
+  return quarter_cos64(64 - k);
+}
+__host__ __device__ constexpr float sin64(int k) { return cos64(k - 16); }
+
+// v * exp(sign * 2*pi*i * K / NN), sign = -1 for the forward transform and +1
+// for the inverse.  NN divides 64.  Quarter turns are exact swaps.
+template <int NN, int K, bool INV>
+__device__ __forceinline__ float2 rot(float2 v) {
+  static_assert(64 % NN == 0, "rot: NN must divide 64");
+  constexpr int k = (((K % NN) + NN) % NN) * (64 / NN);  // angle in units of 2*pi/64
+  constexpr int e = INV ? k : (64 - k) % 64;               // multiply by exp(+i 2*pi e/64)
+  if constexpr (e == 0) {
+    return v;
+  } else if constexpr (e == 16) {
+    return make_float2(-v.y, v.x);
+  } else if constexpr (e == 32) {
+    return make_float2(-v.x, -v.y);
+  } else if constexpr (e == 48) {
+    return make_float2(v.y, -v.x);
+  } else {
+    constexpr float c = cos64(e);
+    constexpr float s = sin64(e);
+    return make_float2(v.x * c - v.y * s, v.x * s + v.y * c);
+  }
+}
+
+// ---------------------------------------------------- in-register DFTs --
+// Dft<R, INV>::run<OFF, ST>(x): X[s] = sum_r x[OFF + ST*r] * W_R^{+-r*s}, in
+// place, natural order at OFF + ST*s.  R = 4^a * 2^b up to 64, built as
+// R = A * 4 with a radix-4 inner DFT over the stride-A sub-sequences, the
+// W_R^{r0*s1} twiddles and a length-A outer DFT.
+template <int R, bool INV>
+struct Dft;
+
+template <bool INV>
+struct Dft<1, INV> {
+  template <int OFF, int ST, int NR>
+  __device__ __forceinline__ static void run(float2 (&)[NR]) {}
+};
+
+template <bool INV>
+struct Dft<2, INV> {
+  template <int OFF, int ST, int NR>
+  __device__ __forceinline__ static void run(float2 (&x)[NR]) {
+    const float2 a = x[OFF], b = x[OFF + ST];
+    x[OFF] = cadd(a, b);
+    x[OFF + ST] = csub(a, b);
+  }
+};
+
+template <bool INV>
+struct Dft<4, INV> {
+  template <int OFF, int ST, int NR>
+  __device__ __forceinline__ static void run(float2 (&x)[NR]) {
+    const float2 a0 = x[OFF], a1 = x[OFF + ST], a2 = x[OFF + 2 * ST], a3 = x[OFF + 3 * ST];
+    const float2 t0 = cadd(a0, a2), t1 = csub(a0, a2);
+    const float2 t2 = cadd(a1, a3), t3 = rot<4, 1, INV>(csub(a1, a3));
+    x[OFF] = cadd(t0, t2);
+    x[OFF + 2 * ST] = csub(t0, t2);
+    x[OFF + ST] = cadd(t1, t3);
+    x[OFF + 3 * ST] = csub(t1, t3);
+  }
+};
+
+template <int R, bool INV>
+struct Dft {
+  static_assert(R % 4 == 0 && R <= 64, "Dft: unsupported radix");
+  static constexpr int A = R / 4;
+
+  template <int R0, int S1, int NR>
+  __device__ __forceinline__ static void twiddle_col(float2 (&y)[NR]) {
+    y[R0 * 4 + S1] = rot<R, R0 * S1, INV>(y[R0 * 4 + S1]);
+    if constexpr (S1 + 1 < 4) twiddle_col<R0, S1 + 1>(y);
+  }
+  template <int R0, int OFF, int ST, int NR>
+  __device__ __forceinline__ static void inner(float2 (&x)[NR], float2 (&y)[R]) {
+    // y[r0*4 + s1] = DFT4 over r1 of x[OFF + ST*(r0 + A*r1)]
+#pragma unroll
+    for (int r1 = 0; r1 < 4; ++r1) y[R0 * 4 + r1] = x[OFF + ST * (R0 + A * r1)];
+    Dft<4, INV>::template run<R0 * 4, 1>(y);
+    twiddle_col<R0, 0>(y);
+    if constexpr (R0 + 1 < A) inner<R0 + 1, OFF, ST>(x, y);
+  }
+  template <int S1, int OFF, int ST, int NR>
+  __device__ __forceinline__ static void outer(float2 (&x)[NR], float2 (&y)[R]) {
+    // X[s1 + 4*s2] = DFT_A over r0 of y[r0*4 + s1]
+    float2 col[A];
+#pragma unroll
+    for (int r0 = 0; r0 < A; ++r0) col[r0] = y[r0 * 4 + S1];
+    Dft<A, INV>::template run<0, 1>(col);
+#pragma unroll
+    for (int s2 = 0; s2 < A; ++s2) x[OFF + ST * (S1 + 4 * s2)] = col[s2];
+    if constexpr (S1 + 1 < 4) outer<S1 + 1, OFF, ST>(x, y);
+  }
+  template <int OFF, int ST, int NR>
+  __device__ __forceinline__ static void run(float2 (&x)[NR]) {
+    float2 y[R];
+    inner<0, OFF, ST>(x, y);
+    outer<0, OFF, ST>(x, y);
+  }
+};
+
+// ------------------------------------------------------------- FFT plan --
+template <int LOG2N_, int LOG2R_>
+struct Fft {
+  static constexpr int LOG2N = LOG2N_;
+  static constexpr int N = 1 << LOG2N;
+  static constexpr int LR = LOG2N < LOG2R_ ? LOG2N : LOG2R_;  // log2 of values per thread
+  static constexpr int R = 1 << LR;
+  static constexpr int T = N / R;                               // threads per transform
+  static constexpr int P = LR == 0 ? 1 : (LOG2N + LR - 1) / LR;  // passes
+  // log2 of the radix of pass p: LR for all passes but the last, which takes the rest.
+  __host__ __device__ static constexpr int lr(int p) { return p + 1 < P ? LR : LOG2N - LR * (P - 1); }
+  __host__ __device__ static constexpr int pad(int a) { return a + (a >> (LR > 0 ? LR : 1)); }
+  static constexpr int LDS = N + (N >> (LR > 0 ? LR : 1)) + 1;  // float2 slots per transform
+
+  // Position (before padding) held by register i of thread tau after the
+  // forward transform (digit-reversed order).
+  __device__ __forceinline__ static int spectrum_pos(int tau, int i) {
+    constexpr int RL = 1 << lr(P - 1);
+    return (tau + T * (i / RL)) * RL + (i % RL);
+  }
+  // Frequency index of the value stored at (unpadded) position a after the
+  // forward transform: a = sum_p s_p * S_p  ->  k = s_0 + R_0 (s_1 + R_1 (s_2 + ...)).
+  __host__ __device__ static int frequency_of(int a) {
+    int k = 0, mul = 1, len = N;
+    for (int p = 0; p < P; ++p) {
+      const int rp = 1 << lr(p);
+      const int sp = len >> lr(p);
+      const int s = (a / sp) % rp;
+      k += s * mul;
+      mul *= rp;
+      len = sp;
+    }
+    return k;
+  }
+
+  // ---- one pass, forward: read (p > 0), DFT, twiddle, write (p < P-1) ----
+  template <int p>
+  __device__ __forceinline__ static void fwd_pass(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+                                                  int tau) {
+    constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
+    constexpr int L = N >> (LR * p), SP = L >> LRP;
+    if constexpr (p > 0) {
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int b = tau + T * u;
+        const int base = (b / SP) * L + (b % SP);
+#pragma unroll
+        for (int r = 0; r < RP; ++r) x[u * RP + r] = lds[pad(base + SP * r)];
+      }
+    }
+    dft_block<p, 0, false>(x);
+    if constexpr (SP > 1) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int t = (tau + T * u) % SP;
+#pragma unroll
+        for (int s = 1; s < RP; ++s) x[u * RP + s] = cmul(x[u * RP + s], tw[(t * s) << (LR * p + 1)]);
+      }
+    }
+    if constexpr (p + 1 < P) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int b = tau + T * u;
+        const int base = (b / SP) * L + (b % SP);
+#pragma unroll
+        for (int s = 0; s < RP; ++s) lds[pad(base + SP * s)] = x[u * RP + s];
+      }
+      fwd_pass<p + 1>(x, lds, tw, tau);
+    }
+  }
+
+  // ---- one pass, inverse: read (p < P-1), conj twiddle, conj DFT, write (p > 0) ----
+  template <int p>
+  __device__ __forceinline__ static void inv_pass(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+                                                  int tau) {
+    constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
+    constexpr int L = N >> (LR * p), SP = L >> LRP;
+    if constexpr (p + 1 < P) {
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int b = tau + T * u;
+        const int base = (b / SP) * L + (b % SP);
+#pragma unroll
+        for (int s = 0; s < RP; ++s) x[u * RP + s] = lds[pad(base + SP * s)];
+      }
+    }
+    if constexpr (SP > 1) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int t = (tau + T * u) % SP;
+#pragma unroll
+        for (int s = 1; s < RP; ++s) x[u * RP + s] = cmulc(x[u * RP + s], tw[(t * s) << (LR * p + 1)]);
+      }
+    }
+    dft_block<p, 0, true>(x);
+    if constexpr (p > 0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int b = tau + T * u;
+        const int base = (b / SP) * L + (b % SP);
+#pragma unroll
+        for (int r = 0; r < RP; ++r) lds[pad(base + SP * r)] = x[u * RP + r];
+      }
+      inv_pass<p - 1>(x, lds, tw, tau);
+    }
+  }
+
+  template <int p, int u, bool INV>
+  __device__ __forceinline__ static void dft_block(float2 (&x)[R]) {
+    constexpr int RP = 1 << lr(p), U = R / RP;
+    Dft<RP, INV>::template run<u * RP, 1>(x);
+    if constexpr (u + 1 < U) dft_block<p, u + 1, INV>(x);
+  }
+
+  // Forward DFT (sign -1), unnormalised.  In: x[r] = position tau + T*r.
+  // Out: x[i] = frequency frequency_of(spectrum_pos(tau, i)).
+  // `lds` is this transform's LDS region (LDS float2 slots); `tw` is the table
+  // W_{2N}^k = exp(-i*pi*k/N), k < 2N.  All T threads of the transform, and
+  // every other thread of the work-group, must call it together (barriers).
+  __device__ __forceinline__ static void forward(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+                                                 int tau) {
+    fwd_pass<0>(x, lds, tw, tau);
+  }
+  // Inverse DFT (sign +1), unnormalised; exact reverse of forward's layout.
+  __device__ __forceinline__ static void inverse(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+                                                 int tau) {
+    inv_pass<P - 1>(x, lds, tw, tau);
+  }
+};
+
+}  // namespace krpe

@@ -1,0 +1,200 @@
+"""Python binding of libkrpe.so: argument marshalling only.
+
+Every function takes torch tensors that live on a GPU, checks that their shapes
+agree with each other, allocates the output (and workspace) with torch, and
+calls the C entry point of the same name on the current torch stream.  All
+arithmetic happens in the library's HIP kernels; there is no CPU path: calling
+any of these without the built library or without a GPU raises.
+
+Names and layouts follow the C header ``include/krpe.h``:
+  q, k, v : [B, H, n, d]  float32 or bfloat16      W : [H, m, d] float32
+  b       : [H, 2n-1] float32, b[h, s] = b_{s-(n-1)} (Algorithm 1's ordering)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = ["KrpeError", "load", "lib_path", "feature_map", "toeplitz_conv", "attention_fwd",
+           "attention_fwd_workspace", "toeplitz_conv_workspace", "attention_fwd_fixed_rows", "DTYPES"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libkrpe.so")
+_lib = None
+
+DTYPES = {torch.float32: 0, torch.bfloat16: 1}
+STAGE_EVENTS = 5
+
+
+class KrpeError(RuntimeError):
+    """A non-OK status returned by the library, or a missing library/GPU."""
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def load(path: str | None = None) -> ctypes.CDLL:
+    """Load libkrpe.so (once).  Raises KrpeError if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or _LIB_PATH
+    if not os.path.exists(p):
+        raise KrpeError(f"{p} is missing: build it with `python -m paper_2106_12566_amd.build`")
+    lib = ctypes.CDLL(p)
+    vp, i, sz, fp = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
+    lib.krpe_abi_version.restype = i
+    lib.krpe_abi_version.argtypes = []
+    lib.krpe_status_str.restype = ctypes.c_char_p
+    lib.krpe_status_str.argtypes = [i]
+    lib.krpe_last_error.restype = ctypes.c_char_p
+    lib.krpe_last_error.argtypes = []
+    lib.krpe_feature_map.restype = i
+    lib.krpe_feature_map.argtypes = [vp, i, fp, fp, i, i, i, i, i, vp]
+    lib.krpe_toeplitz_conv_workspace.restype = sz
+    lib.krpe_toeplitz_conv_workspace.argtypes = [i, i]
+    lib.krpe_toeplitz_conv.restype = i
+    lib.krpe_toeplitz_conv.argtypes = [fp, fp, fp, i, i, i, i, vp, sz, vp]
+    lib.krpe_attention_fwd_workspace.restype = sz
+    lib.krpe_attention_fwd_workspace.argtypes = [i, i, i, i, i]
+    lib.krpe_attention_fwd.restype = i
+    lib.krpe_attention_fwd.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, vp, sz, vp]
+    lib.krpe_attention_fwd_profiled.restype = i
+    lib.krpe_attention_fwd_profiled.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, vp, sz, vp,
+                                                ctypes.POINTER(ctypes.c_void_p)]
+    lib.krpe_attention_fwd_stats.restype = i
+    lib.krpe_attention_fwd_stats.argtypes = [vp, sz, i, i, i, i, i, ctypes.POINTER(ctypes.c_uint), vp]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != 0:
+        lib = load()
+        msg = lib.krpe_status_str(status).decode()
+        detail = lib.krpe_last_error().decode()
+        raise KrpeError(f"{what}: {msg} ({detail})")
+
+
+def _gpu(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise KrpeError(f"{name} must be on a GPU (libkrpe has no CPU path)")
+    return t.contiguous()
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None or t.numel() == 0 else t.data_ptr()
+
+
+def _stream(device: torch.device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dtype_code(t: torch.Tensor, name: str) -> int:
+    if t.dtype not in DTYPES:
+        raise KrpeError(f"{name} must be float32 or bfloat16, got {t.dtype}")
+    return DTYPES[t.dtype]
+
+
+def feature_map(x: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
+    """phi = exp(x W^T - ||x||^2/2) / sqrt(m) (Eq. (5)); x [B,H,n,d], W [H,m,d] -> [B,H,n,m] fp32."""
+    lib = load()
+    x = _gpu(x, "x")
+    W = _gpu(W, "W")
+    if x.dim() != 4 or W.dim() != 3:
+        raise KrpeError("x must be [B,H,n,d] and W [H,m,d]")
+    B, H, n, d = x.shape
+    if W.shape[0] != H or W.shape[2] != d or W.dtype != torch.float32:
+        raise KrpeError("W must be float32 [H, m, d] matching x")
+    m = W.shape[1]
+    phi = torch.empty((B, H, n, m), dtype=torch.float32, device=x.device)
+    st = lib.krpe_feature_map(_ptr(x), _dtype_code(x, "x"), _ptr(W), _ptr(phi), B, H, n, d, m,
+                              _stream(x.device))
+    _check(st, "krpe_feature_map")
+    return phi
+
+
+def toeplitz_conv_workspace(H: int, n: int) -> int:
+    return int(load().krpe_toeplitz_conv_workspace(H, n))
+
+
+def toeplitz_conv(b: torch.Tensor, a: torch.Tensor) -> torch.Tensor:
+    """y[beta,h,c,i] = sum_j exp(b[h, j-i+n-1]) a[beta,h,c,j]; b [H,2n-1], a [B,H,C,n] fp32."""
+    lib = load()
+    b = _gpu(b, "b")
+    a = _gpu(a, "a")
+    if a.dim() != 4 or b.dim() != 2:
+        raise KrpeError("a must be [B,H,C,n] and b [H,2n-1]")
+    B, H, C, n = a.shape
+    if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32 or a.dtype != torch.float32:
+        raise KrpeError("b must be float32 [H, 2n-1] and a float32 [B,H,C,n]")
+    y = torch.empty_like(a)
+    wsb = lib.krpe_toeplitz_conv_workspace(H, n)
+    ws = torch.empty(max(int(wsb), 1), dtype=torch.uint8, device=a.device)
+    st = lib.krpe_toeplitz_conv(_ptr(b), _ptr(a), _ptr(y), B, H, C, n, ws.data_ptr(), ws.numel(),
+                                _stream(a.device))
+    _check(st, "krpe_toeplitz_conv")
+    return y
+
+
+def attention_fwd_workspace(B: int, H: int, n: int, d: int, m: int) -> int:
+    return int(load().krpe_attention_fwd_workspace(B, H, n, d, m))
+
+
+def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d: int, m: int) -> int:
+    """Rows of the last attention_fwd call on `workspace` that were evaluated exactly (waits for the stream)."""
+    lib = load()
+    out = ctypes.c_uint(0)
+    st = lib.krpe_attention_fwd_stats(workspace.data_ptr(), workspace.numel(), B, H, n, d, m,
+                                      ctypes.byref(out), _stream(workspace.device))
+    _check(st, "krpe_attention_fwd_stats")
+    return int(out.value)
+
+
+def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
+                  out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                  events=None) -> torch.Tensor:
+    """Eq. (7): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
+
+    ``out`` and ``workspace`` may be passed to reuse allocations (a uint8 tensor
+    of at least attention_fwd_workspace() bytes).  ``events``: optional list of
+    5 raw hipEvent_t handles recorded around the stages (see the C header).
+    """
+    lib = load()
+    q, k, v = _gpu(q, "q"), _gpu(k, "k"), _gpu(v, "v")
+    b, W = _gpu(b, "b"), _gpu(W, "W")
+    if q.dim() != 4:
+        raise KrpeError("q must be [B,H,n,d]")
+    B, H, n, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise KrpeError("q, k, v must share shape and dtype")
+    if W.dim() != 3 or W.shape[0] != H or W.shape[2] != d or W.dtype != torch.float32:
+        raise KrpeError("W must be float32 [H, m, d]")
+    if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
+        raise KrpeError("b must be float32 [H, 2n-1]")
+    m = W.shape[1]
+    if out is None:
+        out = torch.empty((B, H, n, d), dtype=torch.float32, device=q.device)
+    elif out.shape != (B, H, n, d) or out.dtype != torch.float32 or not out.is_contiguous():
+        raise KrpeError("out must be a contiguous float32 [B,H,n,d] tensor")
+    wsb = int(lib.krpe_attention_fwd_workspace(B, H, n, d, m))
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    dt = _dtype_code(q, "q")
+    args = (_ptr(q), _ptr(k), _ptr(v), dt, _ptr(b), _ptr(W), _ptr(out), B, H, n, d, m,
+            workspace.data_ptr(), workspace.numel(), _stream(q.device))
+    if events is None:
+        st = lib.krpe_attention_fwd(*args)
+    else:
+        if len(events) != STAGE_EVENTS:
+            raise KrpeError(f"events must hold {STAGE_EVENTS} hipEvent_t handles")
+        arr = (ctypes.c_void_p * STAGE_EVENTS)(*events)
+        st = lib.krpe_attention_fwd_profiled(*args, arr)
+    _check(st, "krpe_attention_fwd")
+    return out

@@ -1,0 +1,136 @@
+"""C-ABI checks that need no GPU.
+
+* libkrpe.so loads and exports every function that include/krpe.h declares.
+* Argument validation: every error code is produced on the host, before any
+  HIP call, from invalid arguments.  The pointers passed are never
+  dereferenced: each call below is rejected by validation, which is exactly
+  what is being tested, so no kernel is launched and no device is touched.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2106_12566_amd import krpe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "krpe.h")
+
+OK, NULL, SHAPE, UNSUP, DTYPE, WS, ALIAS, HIP, ALIGN = range(9)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(krpe.lib_path()):
+        from paper_2106_12566_amd import build
+        build.build()
+    return krpe.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(krpe_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("krpe_feature_map", "krpe_toeplitz_conv", "krpe_attention_fwd",
+                     "krpe_toeplitz_conv_workspace", "krpe_attention_fwd_workspace",
+                     "krpe_attention_fwd_profiled", "krpe_status_str", "krpe_last_error",
+                     "krpe_abi_version"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert lib.krpe_abi_version() == 1
+    for s in range(9):
+        assert lib.krpe_status_str(s)
+    assert lib.krpe_status_str(99) == b"unknown status"
+
+
+# Fake, 16-byte aligned, non-overlapping device addresses: only ever seen by
+# the validation code, which rejects every call in this file.
+BASE = 1 << 40
+Q, K, V, BB, W, Z, WSP = (BASE + i * (1 << 36) for i in range(7))
+
+
+def attn(lib, q=Q, k=K, v=V, dt=0, b=BB, w=W, z=Z, B=1, H=1, n=8, d=4, m=4, ws=WSP, wsb=None):
+    if wsb is None:
+        wsb = lib.krpe_attention_fwd_workspace(B, H, n, d, m) if n >= 1 else 0
+    return lib.krpe_attention_fwd(q, k, v, dt, b, w, z, B, H, n, d, m, ws, wsb, None)
+
+
+def test_workspace_queries(lib):
+    small = lib.krpe_attention_fwd_workspace(1, 1, 8, 4, 4)
+    big = lib.krpe_attention_fwd_workspace(2, 3, 100, 64, 64)
+    assert 0 < small < big
+    assert lib.krpe_attention_fwd_workspace(1, 1, 0, 4, 4) == 0
+    assert lib.krpe_attention_fwd_workspace(1, 1, 16385, 4, 4) == 0
+    assert lib.krpe_attention_fwd_workspace(1, 1, 8, 129, 4) == 0
+    assert lib.krpe_toeplitz_conv_workspace(2, 100) > 0
+    assert lib.krpe_toeplitz_conv_workspace(2, 0) == 0
+    # workspace covers phi(q), phi(k) in fp32 at least
+    assert lib.krpe_attention_fwd_workspace(8, 12, 4096, 64, 128) >= 2 * 8 * 12 * 4096 * 128 * 4
+
+
+def test_attention_validation(lib):
+    assert attn(lib, q=None) == NULL
+    assert attn(lib, z=None) == NULL
+    assert attn(lib, n=0) == SHAPE
+    assert attn(lib, B=-1) == SHAPE
+    assert attn(lib, n=16385) == UNSUP
+    assert attn(lib, d=129) == UNSUP
+    assert attn(lib, m=1025) == UNSUP
+    assert attn(lib, m=0) == SHAPE
+    assert attn(lib, dt=7) == DTYPE
+    assert attn(lib, q=Q + 4) == ALIGN
+    assert attn(lib, ws=None) == WS
+    assert attn(lib, wsb=16) == WS
+    assert attn(lib, z=Q) == ALIAS                     # output on top of an input
+    assert attn(lib, ws=V + 64) == ALIAS               # workspace overlapping v
+    assert b"workspace" in lib.krpe_last_error() or lib.krpe_last_error() != b""
+    # empty batch: valid, nothing to do (returns before any HIP call)
+    assert attn(lib, B=0, q=None, k=None, v=None, z=None) == OK
+    assert lib.krpe_last_error() == b""
+
+
+def test_toeplitz_validation(lib):
+    ws = lib.krpe_toeplitz_conv_workspace(2, 10)
+    call = lambda b=BB, a=Q, y=Z, B=1, H=2, C=3, n=10, w=WSP, wb=ws: lib.krpe_toeplitz_conv(
+        b, a, y, B, H, C, n, w, wb, None)
+    assert call(a=None) == NULL
+    assert call(n=0) == SHAPE
+    assert call(C=-1) == SHAPE
+    assert call(n=20000) == UNSUP
+    assert call(wb=8) == WS
+    assert call(y=Q) == ALIAS
+    assert call(y=Z + 8) == ALIGN
+    assert call(C=0, a=None, y=None) == OK
+
+
+def test_feature_map_validation(lib):
+    call = lambda x=Q, dt=0, w=W, phi=Z, B=1, H=1, n=8, d=4, m=4: lib.krpe_feature_map(
+        x, dt, w, phi, B, H, n, d, m, None)
+    assert call(x=None) == NULL
+    assert call(dt=2) == DTYPE
+    assert call(d=0) == SHAPE
+    assert call(m=2000) == UNSUP
+    assert call(phi=Q) == ALIAS
+    assert call(H=0, x=None, w=None, phi=None) == OK
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    x = torch.zeros(1, 1, 8, 4)
+    W = torch.zeros(1, 4, 4)
+    with pytest.raises(krpe.KrpeError):
+        krpe.feature_map(x, W)
+    with pytest.raises(krpe.KrpeError):
+        krpe.attention_fwd(x, x, x, torch.zeros(1, 15), W)

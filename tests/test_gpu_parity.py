@@ -1,0 +1,288 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Every input is seeded and synthetic (paper_2106_12566_amd.synth).  Small cases
+compare every output element; the full-size workloads, run in the same launch
+configuration the benchmark times, compare sampled rows that the oracle
+computes one by one, plus properties of Eq. (7) that hold at any size.
+Tolerances are stated in tests/parity_util.py.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2106_12566_amd import synth
+from parity_util import TOL, inputs_to_gpu, rownorm_err, sample_rows, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+# ------------------------------------------------------------ feature map --
+@pytest.mark.parametrize("B,H,n,d,m,dt", [
+    (1, 1, 128, 64, 64, "f32"),     # one tile each way
+    (2, 3, 100, 64, 96, "f32"),     # ragged n and m tails
+    (1, 2, 1, 5, 3, "f32"),         # degenerate sizes
+    (2, 2, 257, 128, 200, "bf16"),  # d = 128 (four K-chunks), bf16 inputs
+    (1, 1, 70, 33, 130, "f32"),     # ragged d
+])
+def test_feature_map(gpu_lib, B, H, n, d, m, dt):
+    _say(f"feature_map B={B} H={H} n={n} d={d} m={m} {dt}")
+    dd = synth.custom(B, H, n, d, m, seed=11, qkv_dtype=dt)
+    phi = gpu_lib.feature_map(to_gpu(dd["q"], dt), to_gpu(dd["W"])).cpu().numpy()
+    ref = oracle.prf_features(dd["q"], dd["W"])
+    assert phi.shape == ref.shape
+    rel = np.max(np.abs(phi - ref) / ref)
+    assert rel <= 2e-4, rel
+
+
+# ------------------------------------------------------- Toeplitz product --
+@pytest.mark.parametrize("B,H,C,n,sigma", [
+    (1, 1, 2, 1, 0.5),
+    (1, 1, 1, 2, 0.5),
+    (2, 3, 5, 16, 0.5),
+    (1, 2, 3, 17, 1.0),       # ragged n (padded to N = 32), odd channel count
+    (2, 1, 4, 128, 1.0),
+    (1, 2, 2, 300, 0.5),
+    (1, 1, 3, 1000, 1.0),
+    (1, 1, 2, 2048, 1.0),
+    (1, 1, 2, 4096, 1.0),
+    (1, 1, 2, 5000, 1.0),     # ragged at a multi-pass length
+    (1, 1, 2, 16384, 0.5),
+])
+def test_toeplitz_conv_matches_direct_product(gpu_lib, B, H, C, n, sigma):
+    _say(f"toeplitz B={B} H={H} C={C} n={n}")
+    rng = np.random.default_rng([7, B, H, C, n])
+    b = (rng.standard_normal((H, 2 * n - 1)) * sigma).astype(np.float32)
+    a = rng.standard_normal((B, H, C, n)).astype(np.float32)
+    y = gpu_lib.toeplitz_conv(to_gpu(b), to_gpu(a)).cpu().numpy()
+    ref = oracle.toeplitz_product(b, a)
+    err = rownorm_err(y, ref)
+    assert err <= 2e-4, err
+
+
+@pytest.mark.parametrize("n", [5, 64, 1000, 4096])
+def test_toeplitz_special_cases(gpu_lib, n):
+    """Identity, shift, full sum and cumulative sum (textbook routines)."""
+    _say(f"toeplitz special n={n}")
+    rng = np.random.default_rng([8, n])
+    a = rng.standard_normal((1, 1, 2, n)).astype(np.float32)
+    ninf = np.full(2 * n - 1, -np.inf, np.float32)
+    scale = np.max(np.abs(a)) * np.sqrt(n)
+    # identity: only c_0 = 1
+    b = ninf.copy(); b[n - 1] = 0.0
+    y = gpu_lib.toeplitz_conv(to_gpu(b[None]), to_gpu(a)).cpu().numpy()
+    assert np.max(np.abs(y - a)) <= 1e-5 * np.max(np.abs(a))
+    if n > 1:
+        # shift: only c_{-1} = 1 -> y_i = a_{i-1}
+        b = ninf.copy(); b[n - 2] = 0.0
+        y = gpu_lib.toeplitz_conv(to_gpu(b[None]), to_gpu(a)).cpu().numpy()
+        ref = np.concatenate([np.zeros((1, 1, 2, 1)), a[..., :-1]], axis=-1)
+        assert np.max(np.abs(y - ref)) <= 1e-5 * np.max(np.abs(a))
+    # all ones: y_i = sum_j a_j
+    b = np.zeros(2 * n - 1, np.float32)
+    y = gpu_lib.toeplitz_conv(to_gpu(b[None]), to_gpu(a)).cpu().numpy()
+    ref = np.broadcast_to(a.astype(np.float64).sum(-1, keepdims=True), a.shape)
+    assert np.max(np.abs(y - ref)) <= 2e-6 * scale * np.log2(2 * n)
+    # causal ones: cumulative sum
+    b = np.zeros(2 * n - 1, np.float32); b[n:] = -np.inf
+    y = gpu_lib.toeplitz_conv(to_gpu(b[None]), to_gpu(a)).cpu().numpy()
+    ref = np.cumsum(a.astype(np.float64), axis=-1)
+    assert np.max(np.abs(y - ref)) <= 2e-6 * scale * np.log2(2 * n)
+
+
+U32 = 2.0 ** -24
+GAMMA = 8.0   # constant of the FFT error model the library uses to certify rows
+
+
+@pytest.mark.parametrize("n,kind", [(1000, "normal"), (2048, "decay"), (4096, "normal"),
+                                    (4096, "causal"), (4096, "spike"), (3000, "causal")])
+def test_fft_error_model(gpu_lib, n, kind):
+    """The rounding error of the FFT product stays under the model the library relies on.
+
+    For the packed channel pair x = a0/s0 + i a1/s1 (s = max |a|), every
+    output i of channel c must satisfy
+        |y_c,i - y_c,i exact| <= GAMMA u log2(L) (||h||_2 ||x||_2 s_c / sqrt(L) + |y_c,i|),
+    with h the length-L circulant kernel.  Channels are heavy-tailed
+    (lognormal, sigma^2 = 8), of very different scales, or all positive (the
+    denominator's case), the worst cases for a shared complex transform.
+    """
+    rng = np.random.default_rng([9, n, len(kind)])
+    H, C = 2, 6
+    t = np.arange(-(n - 1), n)
+    if kind == "normal":
+        b = rng.standard_normal((H, 2 * n - 1))
+    elif kind == "decay":
+        b = -0.01 * np.abs(t)[None] + 0.3 * rng.standard_normal((H, 2 * n - 1))
+    elif kind == "causal":
+        b = 0.5 * rng.standard_normal((H, 2 * n - 1))
+        b[:, t > 0] = -np.inf
+    else:  # one dominant offset
+        b = 0.3 * rng.standard_normal((H, 2 * n - 1))
+        b[:, n + 3] = 6.0
+    b = b.astype(np.float32)
+    logn = np.exp(np.sqrt(8.0) * rng.standard_normal((1, H, C, n)))
+    a = logn * rng.standard_normal((1, H, C, n))
+    a *= np.array([1.0, 1e-3, 10.0, 1e2, 1.0, 1.0])[None, None, :, None]
+    a[:, :, 4:] = logn[:, :, 4:]                       # positive channels, like the denominator's
+    a = a.astype(np.float32)
+    y = gpu_lib.toeplitz_conv(to_gpu(b), to_gpu(a)).cpu().numpy().astype(np.float64)
+    ref = oracle.toeplitz_product(b, a)
+    N = 1 << int(np.ceil(np.log2(n)))
+    L = 2 * N
+    worst = 0.0
+    for h in range(H):
+        h2 = float(np.sqrt(np.sum(np.exp(2.0 * b[h].astype(np.float64)))))
+        for c0 in range(0, C, 2):
+            s = np.max(np.abs(a[0, h, c0:c0 + 2]), axis=-1)
+            xn = np.sqrt(np.sum((a[0, h, c0:c0 + 2].astype(np.float64) / s[:, None]) ** 2))
+            for k in range(2):
+                model = U32 * np.log2(L) * (h2 * xn * s[k] / np.sqrt(L) + np.abs(ref[0, h, c0 + k]))
+                worst = max(worst, np.max(np.abs(y[0, h, c0 + k] - ref[0, h, c0 + k]) / model))
+    _say(f"fft error model n={n} {kind}: max |error| / model = {worst:.3f}")
+    assert worst <= GAMMA, worst
+
+
+def test_exact_rows_for_causal_prefix(gpu_lib):
+    """Under a causal mask the first rows are recomputed exactly, and meet the fp32 bar."""
+    dd = synth.custom(1, 2, 4096, 64, 64, seed=4, bias="causal")
+    q, k, v, b, W = inputs_to_gpu(dd)
+    import torch
+    ws = torch.empty(gpu_lib.attention_fwd_workspace(1, 2, 4096, 64, 64), dtype=torch.uint8, device="cuda")
+    z = gpu_lib.attention_fwd(q, k, v, b, W, workspace=ws).cpu().numpy()
+    fixed = gpu_lib.attention_fwd_fixed_rows(ws, 1, 2, 4096, 64, 64)
+    rows = [(0, h, i) for h in range(2) for i in list(range(16)) + [100, 1000, 4095]]
+    zr, _ = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], rows)
+    got = np.stack([z[bb, h, i] for bb, h, i in rows])
+    err = rownorm_err(got, zr)
+    _say(f"causal n=4096: {fixed} rows evaluated exactly, err={err:.3e}")
+    assert fixed > 0
+    assert err <= TOL["f32"], err
+
+
+# ----------------------------------------------- attention, small + exact --
+SMALL = [
+    # B, H, n, d, m, dtype, bias
+    (1, 1, 1, 4, 4, "f32", "normal"),
+    (1, 1, 2, 3, 1, "f32", "normal"),      # odd m (single feature)
+    (2, 2, 16, 8, 6, "f32", "normal"),
+    (1, 3, 17, 16, 7, "f32", "causal"),    # ragged n, odd m, causal
+    (2, 1, 100, 64, 64, "f32", "decay"),
+    (1, 2, 333, 64, 32, "bf16", "normal"),
+    (1, 1, 1000, 32, 16, "f32", "causal"),
+    (1, 1, 1025, 64, 8, "f32", "normal"),  # just past a power of two
+    (1, 1, 2048, 64, 4, "f32", "normal"),
+    (1, 1, 4096, 64, 2, "f32", "normal"),
+    (1, 1, 8192, 64, 16, "f32", "causal"),  # early rows need the exact path
+    (1, 1, 16384, 64, 2, "f32", "normal"),
+    (1, 1, 16384, 64, 16, "bf16", "causal"),
+]
+
+
+@pytest.mark.parametrize("B,H,n,d,m,dt,bias", SMALL)
+def test_attention_small_full_compare(gpu_lib, B, H, n, d, m, dt, bias):
+    _say(f"attention B={B} H={H} n={n} d={d} m={m} {dt} {bias}")
+    dd = synth.custom(B, H, n, d, m, seed=n + 7 * m, qkv_dtype=dt, bias=bias)
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd)).cpu().numpy()
+    if n * n * B * H <= 2 ** 24:
+        ref, den = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"])
+    else:
+        rows = sample_rows(B, H, n, 48, seed=n, extra=[(0, 0, i) for i in range(8)])
+        zr, den = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], rows)
+        ref = zr
+        z = np.stack([z[bb, h, i] for bb, h, i in rows])
+    assert np.all(den > 0)
+    assert np.all(np.isfinite(z))
+    err = rownorm_err(z, ref)
+    _say(f"  err={err:.3e}")
+    if err > TOL[dt]:
+        per = np.max(np.abs(z - ref), axis=-1) / np.max(np.abs(ref), axis=-1)
+        _say("  worst rows:", np.argsort(per.reshape(-1))[::-1][:8], np.sort(per.reshape(-1))[::-1][:8])
+    assert err <= TOL[dt], err
+
+
+def test_workload1_full(gpu_lib):
+    """The tiny workload (1 head, n = 128, d = 64, m = 64), every element."""
+    dd = synth.make(1)
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd)).cpu().numpy()
+    ref, _ = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"])
+    err = rownorm_err(z, ref)
+    _say(f"workload 1 err={err:.3e}")
+    assert err <= TOL["f32"], err
+
+
+def test_workload2_two_heads_full(gpu_lib):
+    """The BERT-base-shaped layer with 2 of its 12 heads, every element."""
+    dd = synth.make(2, heads=2)
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd)).cpu().numpy()
+    ref, _ = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"])
+    err = rownorm_err(z, ref)
+    _say(f"workload 2 (2 heads) err={err:.3e}")
+    assert err <= TOL["f32"], err
+
+
+# ------------------------------------------------ attention, full workloads --
+@pytest.mark.parametrize("wid", [2, 3, 4, 5])
+def test_full_workload_sampled_rows(gpu_lib, wid):
+    """Full-size workloads, as benchmarked; rows sampled over every head."""
+    wl = synth.WORKLOADS[wid]
+    _say(f"workload {wid}: {wl}")
+    dd = synth.make(wid)
+    import torch
+    ws = torch.empty(gpu_lib.attention_fwd_workspace(wl.B, wl.H, wl.n, wl.d, wl.m), dtype=torch.uint8,
+                     device="cuda")
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd), workspace=ws).cpu().numpy()
+    fixed = gpu_lib.attention_fwd_fixed_rows(ws, wl.B, wl.H, wl.n, wl.d, wl.m)
+    _say(f"  rows evaluated exactly: {fixed} of {wl.B * wl.H * wl.n}")
+    assert np.all(np.isfinite(z))
+    # first rows matter most under the causal mask (smallest denominators)
+    extra = [(0, h, i) for h in range(min(wl.H, 2)) for i in range(8)]
+    rows = sample_rows(wl.B, wl.H, wl.n, 40 if wl.n >= 4096 else 64, seed=wid, extra=extra)
+    zr, den = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], rows)
+    got = np.stack([z[bb, h, i] for bb, h, i in rows])
+    err = rownorm_err(got, zr)
+    _say(f"  sampled-row err={err:.3e} over {len(rows)} rows")
+    assert np.all(den > 0)
+    assert err <= TOL[wl.qkv_dtype], err
+
+
+@pytest.mark.parametrize("wid", [4, 5])
+def test_full_workload_properties(gpu_lib, wid):
+    """At full size: v == 1 gives z == 1; b + const gives the same z; causality."""
+    wl = synth.WORKLOADS[wid]
+    dd = synth.make(wid)
+    q, k, v, b, W = inputs_to_gpu(dd)
+    import torch
+    tol = TOL[wl.qkv_dtype]
+    z0 = gpu_lib.attention_fwd(q, k, v, b, W)
+    ones = torch.ones_like(v)
+    z1 = gpu_lib.attention_fwd(q, k, ones, b, W)
+    assert torch.max(torch.abs(z1 - 1.0)).item() <= tol
+    zb = gpu_lib.attention_fwd(q, k, v, b + 3.0, W)
+    assert rownorm_err(zb.cpu().numpy(), z0.cpu().numpy()) <= tol
+    # determinism: the same call twice gives bitwise-equal results
+    z0b = gpu_lib.attention_fwd(q, k, v, b, W)
+    assert torch.equal(z0, z0b)
+    if wl.causal:
+        i0 = wl.n // 2
+        v2 = v.clone()
+        v2[:, :, i0 + 1:] += 100.0
+        z2 = gpu_lib.attention_fwd(q, k, v2, b, W)
+        before = z0[:, :, : i0 + 1].cpu().numpy()
+        after = z2[:, :, : i0 + 1].cpu().numpy()
+        # unchanged in exact arithmetic; FFT rounding is global, so allow noise
+        # far below the 100x perturbation of later values
+        assert rownorm_err(after, before) <= 2e-3
+
+
+def test_reuses_output_and_workspace(gpu_lib):
+    import torch
+    dd = synth.custom(2, 2, 200, 64, 16, seed=3)
+    q, k, v, b, W = inputs_to_gpu(dd)
+    ws = torch.empty(gpu_lib.attention_fwd_workspace(2, 2, 200, 64, 16), dtype=torch.uint8, device="cuda")
+    out = torch.full((2, 2, 200, 64), float("nan"), device="cuda")
+    gpu_lib.attention_fwd(q, k, v, b, W, out=out, workspace=ws)
+    ref = gpu_lib.attention_fwd(q, k, v, b, W)
+    assert torch.equal(out, ref)
