@@ -44,8 +44,36 @@ def conv_stage_flops(B: int, H: int, n: int, d: int, m: int) -> float:
 
 
 def conv_stage_bytes(B, H, n, d, m, s_in) -> float:
-    """Algorithmic HBM bytes of the stage: phi(q), phi(k) (fp32), v, the spectrum, partial sums."""
-    return B * H * (2 * n * m * 4 + n * d * s_in + 2 * (d + 1) * n * 4) + H * 2 * n * 8
+    """Algorithmic HBM bytes of the stage: read phi(q), phi(k) (fp32) and v once, the spectrum of c
+    (2n complex bins per head), write the n x (d+1) numerators and denominator once."""
+    return B * H * (2 * n * m * 4 + n * d * s_in + (d + 1) * n * 4) + H * 2 * n * 8
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed profiler record, or None when the
+    record is for another workload or the device sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path)).get(kernel)
+    if not rec or rec.get("workload") != workload:
+        return None
+    return rec["bytes"] if device_source_hash() == rec.get("source_sha256") else None
+
+
+def device_source_hash() -> str:
+    """sha256 of the HIP sources with comments and blank space removed (comment edits keep it)."""
+    import glob
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2106_12566_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+        text = open(f).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update(re.sub(r"\s+", " ", text).encode())
+    return h.hexdigest()
 
 
 class HipEvents:
@@ -89,7 +117,7 @@ def blas_threads() -> int:
 
 
 def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None):
-    """Time the fp64 oracle (Eq. (7), O(n^2) per head) on whole (batch, head) units.
+    """Time the fp64 oracle (Eq. (10), O(n^2) per head) on whole (batch, head) units.
 
     Runs units until `budget_s` of wall time is spent (at least one), and
     extrapolates to the full layer.  Also returns the GPU's per-row normwise
@@ -122,7 +150,7 @@ def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None):
         "unit": "tokens/s",
         "cores": blas_threads(),
         "kind": "oracle",
-        "sample": f"{done} of {B * H} (batch, head) units of {wl.name}, full Eq. (7) per unit in fp64 "
+        "sample": f"{done} of {B * H} (batch, head) units of {wl.name}, full Eq. (10) per unit in fp64 "
                   f"({elapsed:.1f} s), extrapolated to the layer; BLAS threads as cores, elementwise exp "
                   f"single-threaded",
         "layer_s": layer_s,
@@ -137,6 +165,9 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the timed region, copy a buffer of this size (MiB) 3 times, so that "
+                         "profiler byte counters can be scaled by a kernel of known traffic")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -221,8 +252,16 @@ def main() -> int:
                    "conv_stage_hbm_gbs": conv_gbs},
         "roofline": {"bound": "alu", "kernel": "k_conv_contract", "achieved": achieved_tflops,
                      "peak": PEAK_FP32_VECTOR_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS, "traffic": None},
+                     "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
+                     "traffic": measured_traffic("k_conv_contract", wl.name)},
     }
+    if args.copy_calibration_mib > 0:
+        src = torch.ones(args.copy_calibration_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["config"]["copy_calibration_bytes"] = src.numel() * 4
     if not args.no_cpu_baseline:
         z_gpu = out.cpu().numpy()
         cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu)

@@ -7,12 +7,12 @@
  * Relative Positional Encoding", NeurIPS 2021), in O(n log n) per channel:
  *
  *   z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j  /  phi(q_i) sum_j c_{j-i} phi(k_j)^T
- *                                                        (Section 3.2, Eq. (7))
+ *                                                        (Section 3.2, Eq. (10))
  *   phi(x) = exp(W x^T - ||x||^2 / 2) / sqrt(m)          (Section 2.1, Eq. (5))
  *   c_t    = exp(b_t),  t = j - i in [-(n-1), n-1]       (Section 2.2, Eq. (6))
  *
- * The products with the Toeplitz matrix C = {c_{j-i}} of Eqs. (9)-(10) run as
- * zero-padded FFT convolutions (Section 3.2, the paragraph after Eq. (10)).
+ * The products with the Toeplitz matrix C = {c_{j-i}} of Eqs. (12)-(13) run as
+ * zero-padded FFT convolutions (Section 3.2, the paragraph after Eq. (13)).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -40,7 +40,7 @@
  *   B*H == 0 (or C == 0) is a valid empty call that enqueues nothing.
  * - Precondition (not checked: it would need to read device memory): every
  *   query row's window of b holds a finite entry (b_0 finite suffices), so
- *   every denominator of Eq. (7) is > 0.  Otherwise that row of z is NaN.
+ *   every denominator of Eq. (10) is > 0.  Otherwise that row of z is NaN.
  * - Functions are stateless and thread-safe.
  */
 #ifndef KRPE_H_
@@ -97,7 +97,7 @@ krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float
 size_t krpe_toeplitz_conv_workspace(int H, int n);
 
 /*
- * Product with the Toeplitz matrix C = {c_{j-i}} of Eqs. (9)-(10), per channel:
+ * Product with the Toeplitz matrix C = {c_{j-i}} of Eqs. (12)-(13), per channel:
  *   y[beta, h, ch, i] = sum_{j<n} exp(b[h, j - i + n - 1]) * a[beta, h, ch, j]
  * b : [H, 2n-1] fp32     a, y : [B, H, C, n] fp32 (sequence-contiguous channels)
  * Computed as a zero-padded length-2N FFT convolution (two length-N halves).
@@ -113,7 +113,7 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
 size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m);
 
 /*
- * Kernelized attention with RPE, Section 3.2, Eq. (7), with phi from Eq. (5)
+ * Kernelized attention with RPE, Section 3.2, Eq. (10), with phi from Eq. (5)
  * using W[h] for head h and c = exp(b[h]):
  * q, k, v : [B, H, n, d] in qkv_dtype (the already-projected x W^Q, x W^K, x W^V)
  * b       : [H, 2n-1] fp32            W : [H, m, d] fp32
@@ -145,10 +145,10 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
  * sizes) that were evaluated exactly instead of through the FFT.
  *
  * The FFT path's fp32 rounding error is spread over a whole sequence, so a
- * row whose denominator of Eq. (7) is small next to the sequence's total
+ * row whose denominator of Eq. (10) is small next to the sequence's total
  * (the first rows under a causal mask, for example) cannot be resolved by it.
  * krpe_attention_fwd bounds that error for every row and recomputes the rows
- * it cannot certify directly from Eq. (7) with fp64 accumulation.  This call
+ * it cannot certify directly from Eq. (10) with fp64 accumulation.  This call
  * waits for `stream`, then copies the number of such rows into *fixed_rows.
  */
 krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, int H, int n, int d, int m,

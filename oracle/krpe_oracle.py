@@ -9,12 +9,12 @@ float64 (inputs given in fp32 or bf16 are converted exactly):
 
 * ``prf_features``      -- Eq. (5), the positive random feature map.
 * ``toeplitz_matrix``   -- the positional-correlation matrix C = {c_{j-i}},
-                           c_t = exp(b_t) (Section 3.2, below Eq. (10)).
+                           c_t = exp(b_t) (Section 3.2, below Eq. (13)).
 * ``toeplitz_product``  -- C @ a by plain matrix multiplication: the
                            "naive" quadratic route that the FFT replaces
-                           (Eqs. (9)-(10)); FFT and direct product agree
+                           (Eqs. (12)-(13)); FFT and direct product agree
                            exactly up to rounding, so this is the reference.
-* ``attention``         -- Eq. (7): z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j
+* ``attention``         -- Eq. (10): z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j
                            / phi(q_i) sum_j c_{j-i} phi(k_j)^T, O(n^2).
 * ``attention_rows``    -- the same formula evaluated for selected rows only,
                            so that outputs of full-size workloads can be
@@ -24,11 +24,12 @@ Conventions (readings of the paper, stated once here):
 * b[h, s] holds b_t for t = s - (n - 1), the ordering of Algorithm 1's
   argument (b_{-(n-1)}, ..., b_{n-1}).
 * C_ij = c_{j-i} with i the query position and j the key position, as in
-  Eq. (6), Eq. (7) and the matrix printed in Eqs. (9)-(10).
+  Eq. (6), Eq. (10) and the matrix printed in Eqs. (12)-(13).
 * Causal masking is expressed through b alone: b_t = -inf gives c_t = 0
   exactly (Section 3.2, footnote on teacher forcing).
 * phi is applied to q and k as given; any 1/sqrt(d) temperature is the
-  caller's (Eq. (7) and Lemma 2 use the raw kernel exp(x y^T)).
+  caller's (Eq. (10) and the PRF variance lemma of Section 3.3 use the raw
+  kernel exp(x y^T)).
 
 Every function here is pinned by ``tests/test_oracle_pins.py`` against
 brute force, closed forms, the paper's special cases and invariants.
@@ -73,7 +74,7 @@ def toeplitz_matrix(b_h) -> np.ndarray:
 def toeplitz_product(b, a) -> np.ndarray:
     """y[beta, h, c, i] = sum_j exp(b[h, j - i + n - 1]) a[beta, h, c, j].
 
-    The direct (quadratic) product C a of Eqs. (9)-(10), per head.
+    The direct (quadratic) product C a of Eqs. (12)-(13), per head.
     b : [H, 2n-1];  a : [B, H, C, n].  Returns [B, H, C, n] float64.
     """
     b = _f64(b)
@@ -86,7 +87,7 @@ def toeplitz_product(b, a) -> np.ndarray:
 
 
 def attention(q, k, v, b, W, *, row_tile: int = 1024):
-    """Kernelized attention with RPE, Eq. (7), evaluated directly.
+    """Kernelized attention with RPE, Eq. (10), evaluated directly.
 
     For every (batch, head): Phi_q, Phi_k by Eq. (5); the n x n weight matrix
     M_ij = c_{j-i} * phi(q_i) phi(k_j)^T; numerator M v, denominator M 1.
@@ -117,7 +118,7 @@ def attention(q, k, v, b, W, *, row_tile: int = 1024):
 
 
 def attention_rows(q, k, v, b, W, rows):
-    """Eq. (7) for selected output rows only.
+    """Eq. (10) for selected output rows only.
 
     rows : iterable of (beta, h, i).  Returns (z [R, d], den [R]) float64 in
     the order given.  Cost per row is O(n (m + d)) after one O(n m d)

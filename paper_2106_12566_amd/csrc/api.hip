@@ -89,7 +89,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.part = take(bh * 2 * (d + 1) * n * sizeof(float));
   L.bnd = take(bh * pairs * n * sizeof(float));
   L.colmax = take(bh * d * sizeof(float));
-  L.fix = take((1 + bh * n) * sizeof(unsigned));
+  L.fix = take((bh + 1 + bh * n) * sizeof(unsigned));
   L.total = off;
   return L;
 }
@@ -145,7 +145,7 @@ krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float
     return fail(KRPE_ERR_ALIAS, "phi overlaps x or W");
   hipStream_t st = static_cast<hipStream_t>(stream);
   return hip_check(launch_feature_map(x_dtype == KRPE_BF16, x, x, W, phi, phi, 1, false, m, static_cast<int>(bh),
-                                      H, n, d, m, st),
+                                      H, n, d, m, nullptr, st),
                    "feature map launch");
 }
 
@@ -180,7 +180,7 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
   float2* tw = reinterpret_cast<float2*>(w + L.tw);
   float2* Hs = reinterpret_cast<float2*>(w + L.hs);
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
-  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, nullptr, H, n, st), "spectrum launch"))
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch"))
     return s;
   return hip_check(launch_toeplitz(L.l2, a, y, Hs, tw, static_cast<int>(bh), H, C, n, st), "toeplitz launch");
 }
@@ -227,18 +227,17 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   float* part = reinterpret_cast<float*>(w + L.part);
   float* bnd = reinterpret_cast<float*>(w + L.bnd);
   float* colmax = reinterpret_cast<float*>(w + L.colmax);
-  unsigned* fix_count = reinterpret_cast<unsigned*>(w + L.fix);
-  unsigned* fix_list = fix_count + 1;
+  unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
   const int BHi = static_cast<int>(bh);
   const int N = 1 << L.l2;
   const bool bf16 = qkv_dtype == KRPE_BF16;
 
   if (krpe_status_t s = record(events, 0, st)) return s;
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
-  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, fix_count, H, n, st), "spectrum launch"))
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch"))
     return s;
   if (krpe_status_t s = record(events, 1, st)) return s;
-  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, st),
+  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix, st),
                                   "feature map launch"))
     return s;
   if (krpe_status_t s = record(events, 2, st)) return s;
@@ -246,12 +245,10 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
           launch_conv(L.l2, bf16, phiq, phik, v, Hs, tw, part, bnd, colmax, BHi, H, n, d, m, st), "conv launch"))
     return s;
   if (krpe_status_t s = record(events, 3, st)) return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, bnd, colmax, hnorm, z, fix_count, fix_list, BHi, H, n, L.l2,
-                                                 d, st),
+  if (krpe_status_t s = hip_check(launch_combine(part, bnd, colmax, hnorm, z, fix, BHi, H, n, L.l2, d, st),
                                   "combine launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix_count, fix_list, BHi, H, n, N, d, m,
-                                               st),
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, BHi, H, n, N, d, m, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);
@@ -276,7 +273,8 @@ krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, i
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (krpe_status_t s = hip_check(hipStreamSynchronize(st), "hipStreamSynchronize")) return s;
   return hip_check(
-      hipMemcpy(fixed_rows, static_cast<const char*>(ws) + L.fix, sizeof(unsigned), hipMemcpyDeviceToHost),
+      hipMemcpy(fixed_rows, static_cast<const char*>(ws) + L.fix + static_cast<size_t>(B) * H * sizeof(unsigned),
+                sizeof(unsigned), hipMemcpyDeviceToHost),
       "hipMemcpy");
 }
 

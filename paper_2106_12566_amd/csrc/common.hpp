@@ -23,6 +23,12 @@ struct Conf {
   static constexpr int THREADS = G * F::T;
   static constexpr int WAVES = (THREADS + 63) / 64;
   static constexpr int LDS_SLOTS = F::P > 1 ? G * F::LDS : 1;
+  // The convolution kernel runs both halves of the spectrum in one unit (two
+  // interleaved transforms sharing loads, barriers and accumulators) when
+  // their LDS fits next to each other; otherwise one half per unit.
+  static constexpr int KH = (F::T <= 256 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
+  static constexpr int HSPLIT = 2 / KH;  // work units per column pair and head
+  static constexpr int CONV_LDS_SLOTS = F::P > 1 ? G * KH * F::LDS : 1;
 };
 
 // Work-groups are dispatched round-robin over the 8 XCDs (each with its own
@@ -83,7 +89,7 @@ struct OpAdd {
 // different scales, causal and spiked kernels) by the GPU test of the model.
 constexpr float kGamma = 8.0f;
 constexpr float kUnitRoundoff = 5.9604645e-8f;
-// A row of Eq. (7) is certified when its bounded normwise relative error is
+// A row of Eq. (10) is certified when its bounded normwise relative error is
 // at most kTau; otherwise it is evaluated exactly.
 constexpr float kTau = 1.0e-4f;
 

@@ -1,7 +1,7 @@
 // Register + LDS resident complex FFT for gfx950.
 //
-// The Toeplitz products of Eqs. (9)-(10) are done as FFT convolutions.  This
-// header holds the transform only; the kernels that use it are in krpe.hip.
+// The Toeplitz products of Eqs. (12)-(13) are done as FFT convolutions.  This
+// header holds the transform only; the kernels that use it are in kernels.hip.
 //
 // A transform of length N = 2^LOG2N is owned by T = N / R threads, each
 // holding R = 2^LOG2R complex values in registers.  It is a sequence of P
@@ -193,9 +193,12 @@ struct Fft {
     return k;
   }
 
-  // ---- one pass, forward: read (p > 0), DFT, twiddle, write (p < P-1) ----
-  template <int p>
-  __device__ __forceinline__ static void fwd_pass(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+  // ---- one pass, forward, on K independent transforms at once (transform k
+  // in LDS region lds + k * LDS): read (p > 0), DFT, twiddle, write (p < P-1).
+  // The K transforms share the barriers, and their independent instruction
+  // streams interleave.
+  template <int p, int K>
+  __device__ __forceinline__ static void fwd_pass(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
                                                   int tau) {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
@@ -206,16 +209,23 @@ struct Fft {
         const int b = tau + T * u;
         const int base = (b / SP) * L + (b % SP);
 #pragma unroll
-        for (int r = 0; r < RP; ++r) x[u * RP + r] = lds[pad(base + SP * r)];
+        for (int k = 0; k < K; ++k)
+#pragma unroll
+          for (int r = 0; r < RP; ++r) x[k][u * RP + r] = lds[k * LDS + pad(base + SP * r)];
       }
     }
-    dft_block<p, 0, false>(x);
+#pragma unroll
+    for (int k = 0; k < K; ++k) dft_block<p, 0, false>(x[k]);
     if constexpr (SP > 1) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int t = (tau + T * u) % SP;
 #pragma unroll
-        for (int s = 1; s < RP; ++s) x[u * RP + s] = cmul(x[u * RP + s], tw[(t * s) << (LR * p + 1)]);
+        for (int s = 1; s < RP; ++s) {
+          const float2 w = tw[(t * s) << (LR * p + 1)];
+#pragma unroll
+          for (int k = 0; k < K; ++k) x[k][u * RP + s] = cmul(x[k][u * RP + s], w);
+        }
       }
     }
     if constexpr (p + 1 < P) {
@@ -224,15 +234,17 @@ struct Fft {
         const int b = tau + T * u;
         const int base = (b / SP) * L + (b % SP);
 #pragma unroll
-        for (int s = 0; s < RP; ++s) lds[pad(base + SP * s)] = x[u * RP + s];
+        for (int k = 0; k < K; ++k)
+#pragma unroll
+          for (int s = 0; s < RP; ++s) lds[k * LDS + pad(base + SP * s)] = x[k][u * RP + s];
       }
-      fwd_pass<p + 1>(x, lds, tw, tau);
+      fwd_pass<p + 1, K>(x, lds, tw, tau);
     }
   }
 
   // ---- one pass, inverse: read (p < P-1), conj twiddle, conj DFT, write (p > 0) ----
-  template <int p>
-  __device__ __forceinline__ static void inv_pass(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+  template <int p, int K>
+  __device__ __forceinline__ static void inv_pass(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
                                                   int tau) {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
@@ -243,7 +255,9 @@ struct Fft {
         const int b = tau + T * u;
         const int base = (b / SP) * L + (b % SP);
 #pragma unroll
-        for (int s = 0; s < RP; ++s) x[u * RP + s] = lds[pad(base + SP * s)];
+        for (int k = 0; k < K; ++k)
+#pragma unroll
+          for (int s = 0; s < RP; ++s) x[k][u * RP + s] = lds[k * LDS + pad(base + SP * s)];
       }
     }
     if constexpr (SP > 1) {
@@ -251,19 +265,26 @@ struct Fft {
       for (int u = 0; u < U; ++u) {
         const int t = (tau + T * u) % SP;
 #pragma unroll
-        for (int s = 1; s < RP; ++s) x[u * RP + s] = cmulc(x[u * RP + s], tw[(t * s) << (LR * p + 1)]);
+        for (int s = 1; s < RP; ++s) {
+          const float2 w = tw[(t * s) << (LR * p + 1)];
+#pragma unroll
+          for (int k = 0; k < K; ++k) x[k][u * RP + s] = cmulc(x[k][u * RP + s], w);
+        }
       }
     }
-    dft_block<p, 0, true>(x);
+#pragma unroll
+    for (int k = 0; k < K; ++k) dft_block<p, 0, true>(x[k]);
     if constexpr (p > 0) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
         const int base = (b / SP) * L + (b % SP);
 #pragma unroll
-        for (int r = 0; r < RP; ++r) lds[pad(base + SP * r)] = x[u * RP + r];
+        for (int k = 0; k < K; ++k)
+#pragma unroll
+          for (int r = 0; r < RP; ++r) lds[k * LDS + pad(base + SP * r)] = x[k][u * RP + r];
       }
-      inv_pass<p - 1>(x, lds, tw, tau);
+      inv_pass<p - 1, K>(x, lds, tw, tau);
     }
   }
 
@@ -274,19 +295,29 @@ struct Fft {
     if constexpr (u + 1 < U) dft_block<p, u + 1, INV>(x);
   }
 
-  // Forward DFT (sign -1), unnormalised.  In: x[r] = position tau + T*r.
-  // Out: x[i] = frequency frequency_of(spectrum_pos(tau, i)).
-  // `lds` is this transform's LDS region (LDS float2 slots); `tw` is the table
+  // Forward DFT (sign -1), unnormalised, of K transforms.  In: x[k][r] =
+  // position tau + T*r.  Out: x[k][i] = frequency frequency_of(spectrum_pos(tau, i)).
+  // `lds` holds K regions of LDS float2 slots; `tw` is the table
   // W_{2N}^k = exp(-i*pi*k/N), k < 2N.  All T threads of the transform, and
   // every other thread of the work-group, must call it together (barriers).
-  __device__ __forceinline__ static void forward(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+  template <int K>
+  __device__ __forceinline__ static void forward(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
                                                  int tau) {
-    fwd_pass<0>(x, lds, tw, tau);
+    fwd_pass<0, K>(x, lds, tw, tau);
   }
   // Inverse DFT (sign +1), unnormalised; exact reverse of forward's layout.
+  template <int K>
+  __device__ __forceinline__ static void inverse(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
+                                                 int tau) {
+    inv_pass<P - 1, K>(x, lds, tw, tau);
+  }
+  __device__ __forceinline__ static void forward(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
+                                                 int tau) {
+    forward<1>(reinterpret_cast<float2(&)[1][R]>(x), lds, tw, tau);
+  }
   __device__ __forceinline__ static void inverse(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
                                                  int tau) {
-    inv_pass<P - 1>(x, lds, tw, tau);
+    inverse<1>(reinterpret_cast<float2(&)[1][R]>(x), lds, tw, tau);
   }
 };
 

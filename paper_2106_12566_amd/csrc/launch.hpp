@@ -19,7 +19,8 @@ struct AttnLayout {
   size_t part;       // float  [BH][2][d+1][n] per-half numerators / denominator
   size_t bnd;        // float  [BH][pairs][n]  sum_l phi_l(q_i) ||x_{l,pair}||_2
   size_t colmax;     // float  [BH][d]         max_j |v_{j,c}|
-  size_t fix;        // uint   [1 + BH n]      count, then rows to evaluate exactly
+  size_t fix;        // uint   [BH + 1 + BH n] rows queued per head, total; then the
+                     //                        queued row indices of each head
   size_t total;
 };
 AttnLayout attn_layout(int B, int H, int n, int d, int m);
@@ -31,22 +32,22 @@ struct ConvLayout {
 ConvLayout conv_layout(int H, int n);
 
 hipError_t launch_twiddles(float2* tw, int l2, hipStream_t st);
-hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs, float2* hnorm,
-                           unsigned* fix_count, int H, int n, hipStream_t st);
+hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs, float2* hnorm, int H, int n,
+                           hipStream_t st);
 // nsrc sources (1 or 2) x0/x1 -> phi0/phi1.  feature_major: phi[bh][l][ld] for
-// positions < ld (zero beyond n); otherwise phi[bh][i][m].
+// positions < ld (zero beyond n); otherwise phi[bh][i][m].  fix_counts, if not
+// NULL, gets its BH + 1 entries cleared.
 hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const float* W, float* phi0,
                               float* phi1, int nsrc, bool feature_major, int ld, int BH, int H, int n, int d,
-                              int m, hipStream_t st);
+                              int m, unsigned* fix_counts, hipStream_t st);
 hipError_t launch_conv(int l2, bool bf16, const float* phiq, const float* phik, const void* v,
                        const float2* Hs, const float2* tw, float* part, float* bnd, float* colmax, int BH,
                        int H, int n, int d, int m, hipStream_t st);
 hipError_t launch_combine(const float* part, const float* bnd, const float* colmax, const float2* hnorm,
-                          float* z, unsigned* fix_count, unsigned* fix_list, int BH, int H, int n, int l2,
-                          int d, hipStream_t st);
+                          float* z, unsigned* fix, int BH, int H, int n, int l2, int d, hipStream_t st);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
-                        float* z, const unsigned* fix_count, const unsigned* fix_list, int BH, int H, int n,
-                        int ld, int d, int m, hipStream_t st);
+                        float* z, const unsigned* fix, int BH, int H, int n, int ld, int d, int m,
+                        hipStream_t st);
 hipError_t launch_toeplitz(int l2, const float* a, float* y, const float2* Hs, const float2* tw, int BH, int H,
                            int C, int n, hipStream_t st);
 

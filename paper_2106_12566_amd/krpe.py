@@ -160,7 +160,7 @@ def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d:
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
                   out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
                   events=None) -> torch.Tensor:
-    """Eq. (7): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
+    """Eq. (10): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
 
     ``out`` and ``workspace`` may be passed to reuse allocations (a uint8 tensor
     of at least attention_fwd_workspace() bytes).  ``events``: optional list of

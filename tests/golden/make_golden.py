@@ -1,6 +1,6 @@
 """Write the oracle regression fixtures in this folder.
 
-The paper prints no worked numerical example for Eq. (7), so these fixtures
+The paper prints no worked numerical example for Eq. (10), so these fixtures
 are not the paper's numbers: they freeze the fp64 oracle's output on the
 smallest synthetic workload (one head, n = 128, d = 64, m = 64) so that any
 later change to the oracle's arithmetic shows up as a diff.  Only ``oracle``
@@ -25,7 +25,7 @@ def main():
     d = synth.make(1)
     z, den = oracle.attention(d["q"], d["k"], d["v"], d["b"], d["W"])
     out = {
-        "what": "Eq. (7) evaluated by the fp64 oracle on workload 1 (B=1, H=1, n=128, d=64, m=64)",
+        "what": "Eq. (10) evaluated by the fp64 oracle on workload 1 (B=1, H=1, n=128, d=64, m=64)",
         "generator": "paper_2106_12566_amd.synth.make(1)",
         "rows": ROWS,
         "z": [[float(x) for x in z[0, 0, i]] for i in ROWS],

@@ -1,7 +1,7 @@
 """Helpers shared by the GPU parity tests (error metrics and tensor transfer).
 
 Tolerances (stated once):
-* Outputs z of Eq. (7): per-row normwise relative error
+* Outputs z of Eq. (10): per-row normwise relative error
       err = max over (beta, h, i) of ||z_gpu[i] - z_ref[i]||_inf / ||z_ref[i]||_inf
   must be <= 2e-4 when q, k, v are fp32 and <= 2e-2 when they are bf16.
   z entries cross zero, so an elementwise relative error is ill-posed; the

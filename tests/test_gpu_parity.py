@@ -3,7 +3,7 @@
 Every input is seeded and synthetic (paper_2106_12566_amd.synth).  Small cases
 compare every output element; the full-size workloads, run in the same launch
 configuration the benchmark times, compare sampled rows that the oracle
-computes one by one, plus properties of Eq. (7) that hold at any size.
+computes one by one, plus properties of Eq. (10) that hold at any size.
 Tolerances are stated in tests/parity_util.py.
 """
 import numpy as np

@@ -5,15 +5,15 @@ that ``test_oracle_mutants.py`` can re-run the same checks on deliberately
 broken copies of it and show that every planted mistake is caught.
 
 Sources of truth used here (none of them re-types the oracle's formula):
-* brute force with scalar Python loops straight from Eq. (5) and Eq. (7);
+* brute force with scalar Python loops straight from Eq. (5) and Eq. (10);
 * the paper's own factorisation route: vec-stacked A_1, A_2, the Toeplitz
-  matrix of Eqs. (9)-(10) and the final ratio of Algorithm 1;
-* the closed form Eq. (3) (linear attention) that Eq. (7) reduces to when b
+  matrix of Eqs. (12)-(13) and the final ratio of Algorithm 1;
+* the closed form Eq. (3) (linear attention) that Eq. (10) reduces to when b
   is constant, and its prefix-sum form under the causal mask;
-* Lemma 2 (unbiasedness and exact variance of the PRF kernel estimate);
+* the PRF variance lemma of Section 3.3 (unbiasedness and exact variance of the PRF kernel estimate);
 * the softmax-with-RPE limit (Eq. (1) with the bias of Eq. (6)) as m grows;
 * textbook special cases of a Toeplitz product (identity, shift, sum,
-  cumulative sum) and invariants of Eq. (7).
+  cumulative sum) and invariants of Eq. (10).
 """
 import math
 
@@ -58,7 +58,7 @@ def _brute_phi(x_row, W_h):
 
 
 def _brute_attention(q, k, v, b, W):
-    """Eq. (7) with scalar loops; b[h][t + n - 1] = b_t."""
+    """Eq. (10) with scalar loops; b[h][t + n - 1] = b_t."""
     Bn, H, n, d = q.shape
     z = np.zeros((Bn, H, n, d))
     for beta in range(Bn):
@@ -93,7 +93,7 @@ def check_brute_force(impl):
 
 
 def check_algorithm1_route(impl):
-    """Vec-stacked A_1, A_2 (Eq. (8)), D = C A (Eqs. (9)-(10)), then the ratio."""
+    """Vec-stacked A_1, A_2 (Eq. (11)), D = C A (Eqs. (12)-(13)), then the ratio."""
     rng = np.random.default_rng(12)
     n, d, m = 13, 5, 6
     q, k, v, b, W = _rand_case(rng, 1, 1, n, d, m)
@@ -123,7 +123,7 @@ def check_single_position(impl):
 
 
 def check_const_bias_is_linear_attention(impl):
-    """b == kappa makes c a constant, Eq. (7) becomes Eq. (3) (O(n) route)."""
+    """b == kappa makes c a constant, Eq. (10) becomes Eq. (3) (O(n) route)."""
     rng = np.random.default_rng(14)
     n, d, m = 40, 8, 16
     q, k, v, _, W = _rand_case(rng, 2, 2, n, d, m)
@@ -142,7 +142,7 @@ def check_const_bias_is_linear_attention(impl):
 def check_causal_prefix_sums(impl):
     """b_t = kappa for t <= 0, -inf for t > 0: the teacher-forcing mask.
 
-    Query i then sees keys j <= i only and Eq. (7) becomes running sums of
+    Query i then sees keys j <= i only and Eq. (10) becomes running sums of
     phi(k_j)^T v_j and phi(k_j)^T.
     """
     rng = np.random.default_rng(15)
@@ -232,7 +232,7 @@ def check_causality(impl):
     assert not np.allclose(z[:, :, cut:], z2[:, :, cut:])
 
 
-def check_lemma2(impl):
+def check_prf_variance_lemma(impl):
     """E_W[phi(x) phi(y)^T] = exp(x y^T); Var = (exp(|x+y|^2) - 1) exp(x y^T)^2 / m."""
     rng = np.random.default_rng(20)
     d, m, T = 16, 16, 20000
@@ -293,7 +293,7 @@ def check_rows_match_full(impl):
 ALL_CHECKS = [check_brute_force, check_algorithm1_route, check_single_position,
               check_const_bias_is_linear_attention, check_causal_prefix_sums,
               check_only_diagonal, check_shift_kernel, check_invariants,
-              check_causality, check_lemma2, check_toeplitz_special_cases,
+              check_causality, check_prf_variance_lemma, check_toeplitz_special_cases,
               check_rows_match_full]
 
 
@@ -325,7 +325,7 @@ def _sphere(rng, n, d, R):
 
 @pytest.mark.parametrize("R", [0.5, 1.0])
 def test_softmax_limit(R):
-    """As m grows, Eq. (7) with PRF approaches softmax attention with RPE.
+    """As m grows, Eq. (10) with PRF approaches softmax attention with RPE.
 
     Mirrors the paper's simulation for Theorem 3 (queries and keys on a sphere
     of radius R, Gaussian features).  Monte-Carlo error must fall like
@@ -354,7 +354,7 @@ def test_softmax_limit(R):
 
 
 def test_denominator_unbiased():
-    """E_W[den_i] = sum_j c_{j-i} exp(q_i k_j^T) (Lemma 2's unbiasedness, summed)."""
+    """E_W[den_i] = sum_j c_{j-i} exp(q_i k_j^T) (the PRF variance lemma's unbiasedness (Section 3.3), summed)."""
     rng = np.random.default_rng(23)
     n, d, m, T = 12, 8, 64, 400
     q = _sphere(rng, n, d, 0.8)
