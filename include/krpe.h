@@ -91,10 +91,10 @@ krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float
                                int B, int H, int n, int d, int m, void* stream);
 
 /*
- * Bytes of workspace krpe_toeplitz_conv needs for H heads of length n
- * (0 if the sizes are invalid or unsupported).
+ * Bytes of workspace krpe_toeplitz_conv needs for B x H heads of C channels of
+ * length n (0 if the sizes are invalid or unsupported).
  */
-size_t krpe_toeplitz_conv_workspace(int H, int n);
+size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n);
 
 /*
  * Product with the Toeplitz matrix C = {c_{j-i}} of Eqs. (12)-(13), per channel:

@@ -74,7 +74,8 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.l2 = log2_ceil(n);
   const size_t N = static_cast<size_t>(1) << L.l2;
   const size_t bh = static_cast<size_t>(B) * H;
-  const size_t pairs = static_cast<size_t>(d + 2) / 2;
+  const size_t cols = static_cast<size_t>(d) + 1, pairs = (cols + 1) / 2;
+  L.ksplit = gram_splits(static_cast<int>(bh), m, static_cast<int>(N));
   size_t off = 0;
   auto take = [&off](size_t bytes) {
     const size_t at = off;
@@ -86,21 +87,34 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
   L.phiq = take(bh * m * N * sizeof(float));
   L.phik = take(bh * m * N * sizeof(float));
-  L.part = take(bh * 2 * (d + 1) * n * sizeof(float));
-  L.bnd = take(bh * pairs * n * sizeof(float));
-  L.colmax = take(bh * d * sizeof(float));
+  L.vsc = take(bh * pairs * N * sizeof(float2));
+  L.colmax = take(bh * cols * sizeof(float));
+  L.x2 = take(bh * L.ksplit * m * pairs * sizeof(float));
+  L.part = take(bh * conv_splits(L.l2) * cols * n * sizeof(float));
   L.fix = take((bh + 1 + bh * n) * sizeof(unsigned));
   L.total = off;
   return L;
 }
 
-ConvLayout conv_layout(int H, int n) {
+ConvLayout conv_layout(int B, int H, int C, int n) {
   ConvLayout L{};
   L.l2 = log2_ceil(n);
   const size_t N = static_cast<size_t>(1) << L.l2;
-  L.tw = 0;
-  L.hs = align_up(2 * N * sizeof(float2));
-  L.total = align_up(L.hs + static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  const size_t bh = static_cast<size_t>(B) * H;
+  const size_t pairs = (static_cast<size_t>(C) + 1) / 2;
+  size_t off = 0;
+  auto take = [&off](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.tw = take(2 * N * sizeof(float2));
+  L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  L.ones = take(N * sizeof(float));
+  L.vsc = take(bh * pairs * N * sizeof(float2));
+  L.colmax = take(bh * C * sizeof(float));
+  L.part = take(conv_splits(L.l2) > 1 ? bh * conv_splits(L.l2) * C * n * sizeof(float) : 0);
+  L.total = off;
   return L;
 }
 
@@ -110,7 +124,7 @@ using namespace krpe;
 
 extern "C" {
 
-int krpe_abi_version(void) { return 1; }
+int krpe_abi_version(void) { return 2; }
 
 const char* krpe_status_str(int s) {
   switch (s) {
@@ -149,9 +163,9 @@ krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float
                    "feature map launch");
 }
 
-size_t krpe_toeplitz_conv_workspace(int H, int n) {
-  if (H < 0 || n < 1 || n > (1 << kMaxLog2N)) return 0;
-  return conv_layout(H, n).total;
+size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n) {
+  if (B < 0 || H < 0 || C < 0 || n < 1 || n > (1 << kMaxLog2N)) return 0;
+  return conv_layout(B, H, C, n).total;
 }
 
 krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B, int H, int C, int n, void* ws,
@@ -166,7 +180,7 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
   if (!b || !a || !y) return fail(KRPE_ERR_NULL, "b, a and y must be non-NULL");
   if (misaligned(b) || misaligned(a) || misaligned(y) || misaligned(ws))
     return fail(KRPE_ERR_ALIGN, "b, a, y, ws must be 16-byte aligned");
-  const ConvLayout L = conv_layout(H, n);
+  const ConvLayout L = conv_layout(B, H, C, n);
   if (!ws || ws_bytes < L.total)
     return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
   const Range ry{y, bh * C * n * sizeof(float)};
@@ -179,10 +193,28 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
   char* w = static_cast<char*>(ws);
   float2* tw = reinterpret_cast<float2*>(w + L.tw);
   float2* Hs = reinterpret_cast<float2*>(w + L.hs);
+  float* ones = reinterpret_cast<float*>(w + L.ones);
+  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
+  float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* part = reinterpret_cast<float*>(w + L.part);
+  const int BHi = static_cast<int>(bh);
+  const int N = 1 << L.l2;
+  const int splits = conv_splits(L.l2);
+  // The product runs through the attention's convolution kernel with one
+  // feature equal to 1 everywhere: a_c plays the role of the value column c.
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
-  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch"))
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch")) return s;
+  if (krpe_status_t s = hip_check(launch_ones(ones, n, N, st), "ones launch")) return s;
+  if (krpe_status_t s = hip_check(launch_vprep(false, a, 1, n, static_cast<long long>(C) * n, C, false, BHi, n, N,
+                                               colmax, vsc, st),
+                                  "column launch"))
     return s;
-  return hip_check(launch_toeplitz(L.l2, a, y, Hs, tw, static_cast<int>(bh), H, C, n, st), "toeplitz launch");
+  if (krpe_status_t s = hip_check(launch_conv(L.l2, ones, ones, 0, vsc, colmax, Hs, tw, splits > 1 ? part : y, BHi,
+                                              H, n, C, 1, st),
+                                  "conv launch"))
+    return s;
+  if (splits > 1) return hip_check(launch_sum_splits(part, y, BHi, C, n, splits, st), "sum launch");
+  return KRPE_OK;
 }
 
 size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
@@ -224,28 +256,37 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   float2* hnorm = reinterpret_cast<float2*>(w + L.hnorm);
   float* phiq = reinterpret_cast<float*>(w + L.phiq);
   float* phik = reinterpret_cast<float*>(w + L.phik);
-  float* part = reinterpret_cast<float*>(w + L.part);
-  float* bnd = reinterpret_cast<float*>(w + L.bnd);
+  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
   float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* x2 = reinterpret_cast<float*>(w + L.x2);
+  float* part = reinterpret_cast<float*>(w + L.part);
   unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
   const int BHi = static_cast<int>(bh);
   const int N = 1 << L.l2;
   const bool bf16 = qkv_dtype == KRPE_BF16;
+  const int pairs = (d + 2) / 2;
 
   if (krpe_status_t s = record(events, 0, st)) return s;
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
-  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch"))
-    return s;
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch")) return s;
   if (krpe_status_t s = record(events, 1, st)) return s;
   if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix, st),
                                   "feature map launch"))
     return s;
+  if (krpe_status_t s = hip_check(launch_vprep(bf16, v, d, 1, static_cast<long long>(n) * d, d, true, BHi, n, N,
+                                               colmax, vsc, st),
+                                  "column launch"))
+    return s;
   if (krpe_status_t s = record(events, 2, st)) return s;
-  if (krpe_status_t s = hip_check(
-          launch_conv(L.l2, bf16, phiq, phik, v, Hs, tw, part, bnd, colmax, BHi, H, n, d, m, st), "conv launch"))
+  if (krpe_status_t s = hip_check(launch_conv(L.l2, phiq, phik, static_cast<long long>(m) * N, vsc, colmax, Hs, tw,
+                                              part, BHi, H, n, d + 1, m, st),
+                                  "conv launch"))
     return s;
   if (krpe_status_t s = record(events, 3, st)) return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, bnd, colmax, hnorm, z, fix, BHi, H, n, L.l2, d, st),
+  if (krpe_status_t s = hip_check(launch_gram(phik, vsc, x2, BHi, m, N, pairs, L.ksplit, st), "norm launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_combine(part, phiq, x2, colmax, hnorm, z, fix, BHi, H, n, L.l2, d, m,
+                                                 L.ksplit, st),
                                   "combine launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, BHi, H, n, N, d, m, st),

@@ -14,21 +14,41 @@ constexpr int kMaxD = 128;
 constexpr int kMaxM = 1024;
 constexpr int kLog2R = 4;      // 16 complex values per thread
 
-// Launch shape of the transforms of length 2^L2: G transform units of T
-// threads per work-group, enough to fill 256 threads for short transforms.
+// Launch shape of the products of length-2N circular convolutions, N = 2^L2.
+//
+// The 2N frequency bins are split into S = 2 FOLD residue classes
+// k = S k' + r; class r is a length L' = 2N / S transform (L' = N / FOLD) of
+// the input folded FOLD times (Section 3.2 leaves the FFT open; see the
+// convolution kernel for the algebra).  FOLD = 1 up to N = 4096 (the classes
+// are the even and odd bins), FOLD = 2 above, which keeps one transform
+// within 8192 points and the per-thread state within the register file.
+//
+// A transform is owned by T = L' / 16 threads (16 complex values each); a
+// work-group holds G units of T threads (filling 256 threads for short
+// transforms); a unit of the convolution kernel runs KH residue classes as
+// interleaved transforms sharing loads, barriers and accumulators.
 template <int L2>
 struct Conf {
-  using F = Fft<L2, kLog2R>;
+  static constexpr int FOLD = L2 <= 12 ? 1 : 2;
+  static constexpr int S = 2 * FOLD;                 // residue classes
+  static constexpr int L2T = L2 <= 12 ? L2 : L2 - 1;  // log2 of the transform length
+  static constexpr int LOG2R = kLog2R;
+  using F = Fft<L2T, LOG2R, 1 + L2 - L2T>;  // twiddles come from the W_{2N} table
+  static constexpr int N = 1 << L2;
+  static constexpr int LT = F::N;  // transform length 2N / S
   static constexpr int G = F::T >= 256 ? 1 : 256 / F::T;
   static constexpr int THREADS = G * F::T;
   static constexpr int WAVES = (THREADS + 63) / 64;
   static constexpr int LDS_SLOTS = F::P > 1 ? G * F::LDS : 1;
-  // The convolution kernel runs both halves of the spectrum in one unit (two
-  // interleaved transforms sharing loads, barriers and accumulators) when
-  // their LDS fits next to each other; otherwise one half per unit.
-  static constexpr int KH = (F::T <= 256 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
-  static constexpr int HSPLIT = 2 / KH;  // work units per column pair and head
+  static constexpr int KH = (F::T <= 256 && F::R <= 16 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
+  static constexpr int HSPLIT = S / KH;  // work units per column pair and head
   static constexpr int CONV_LDS_SLOTS = F::P > 1 ? G * KH * F::LDS : 1;
+  // Per-position values (v pairs, twists, prefetched phi), the spectrum and
+  // the hoisted twiddles stay in registers only for work-groups of <= 256
+  // threads (512 registers per thread); larger ones re-read them.
+  static constexpr bool VREG = THREADS <= 256 && FOLD == 1;
+  static constexpr bool HREG = THREADS <= 256;
+  static constexpr bool HOIST = THREADS <= 256 && FOLD == 1;
 };
 
 // Work-groups are dispatched round-robin over the 8 XCDs (each with its own

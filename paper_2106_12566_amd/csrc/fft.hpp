@@ -159,7 +159,10 @@ struct Dft {
 };
 
 // ------------------------------------------------------------- FFT plan --
-template <int LOG2N_, int LOG2R_>
+// TWS = log2(table length / N): the twiddle table always holds W_M^k, k < M,
+// for some M = N << TWS (M = 2N for a transform of the full half-length, 4N
+// when the transform is a quarter of the circular length).
+template <int LOG2N_, int LOG2R_, int TWS = 1>
 struct Fft {
   static constexpr int LOG2N = LOG2N_;
   static constexpr int N = 1 << LOG2N;
@@ -222,7 +225,7 @@ struct Fft {
         const int t = (tau + T * u) % SP;
 #pragma unroll
         for (int s = 1; s < RP; ++s) {
-          const float2 w = tw[(t * s) << (LR * p + 1)];
+          const float2 w = tw[(t * s) << (LR * p + TWS)];
 #pragma unroll
           for (int k = 0; k < K; ++k) x[k][u * RP + s] = cmul(x[k][u * RP + s], w);
         }
@@ -266,7 +269,7 @@ struct Fft {
         const int t = (tau + T * u) % SP;
 #pragma unroll
         for (int s = 1; s < RP; ++s) {
-          const float2 w = tw[(t * s) << (LR * p + 1)];
+          const float2 w = tw[(t * s) << (LR * p + TWS)];
 #pragma unroll
           for (int k = 0; k < K; ++k) x[k][u * RP + s] = cmulc(x[k][u * RP + s], w);
         }
@@ -298,7 +301,7 @@ struct Fft {
   // Forward DFT (sign -1), unnormalised, of K transforms.  In: x[k][r] =
   // position tau + T*r.  Out: x[k][i] = frequency frequency_of(spectrum_pos(tau, i)).
   // `lds` holds K regions of LDS float2 slots; `tw` is the table
-  // W_{2N}^k = exp(-i*pi*k/N), k < 2N.  All T threads of the transform, and
+  // W_M^k = exp(-2 i pi k / M), k < M = N << TWS.  All T threads of the transform, and
   // every other thread of the work-group, must call it together (barriers).
   template <int K>
   __device__ __forceinline__ static void forward(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,

@@ -61,8 +61,21 @@ __device__ __forceinline__ float circ_kernel(const float* __restrict__ bh, int s
   return 0.f;
 }
 
-// One transform per (head, half).  Hs[h][half][k] in natural frequency order.
-// Also, when requested: hnorm[h] = (||h||_1, ||h||_2).
+// z * (-i)^e for a real z, e taken mod 4.
+__device__ __forceinline__ float2 real_quarter_turn(float z, int e) {
+  switch (e & 3) {
+    case 0: return make_float2(z, 0.f);
+    case 1: return make_float2(0.f, -z);
+    case 2: return make_float2(-z, 0.f);
+    default: return make_float2(0.f, z);
+  }
+}
+
+// One transform per (head, residue class r < S): the bins k = S k' + r of the
+// length-2N transform of h are DFT_{LT}(g_r) with
+//   g_r[j] = W_{2N}^{r j} sum_{p < S} h[j + p LT] W_S^{p r},   j < LT = 2N / S.
+// Hs[h][r][.] holds them, scaled by 1/(2N), in register order (below).  Also,
+// when requested: hnorm[h] = (||h||_1, ||h||_2).
 template <int L2>
 __global__ __launch_bounds__(Conf<L2>::THREADS) void k_spectrum(const float* __restrict__ b,
                                                                  const float2* __restrict__ tw,
@@ -70,39 +83,47 @@ __global__ __launch_bounds__(Conf<L2>::THREADS) void k_spectrum(const float* __r
                                                                  float2* __restrict__ hnorm, int H, int n) {
   using C = Conf<L2>;
   using F = typename C::F;
+  constexpr int S = C::S;
   __shared__ float2 lds[C::LDS_SLOTS];
   __shared__ float red[C::WAVES];
-  const int g = threadIdx.x / F::T, tau = threadIdx.x % F::T;
-  const int units = 2 * H;
+  // With one unit per work-group the unit index is wave-uniform: say so, so
+  // that per-unit pointers live in scalar registers.
+  const int g = C::G == 1 ? 0 : threadIdx.x / F::T, tau = C::G == 1 ? threadIdx.x : threadIdx.x % F::T;
+  const int units = S * H;
   int unit = blockIdx.x * C::G + g;
   const bool active = unit < units;
   if (!active) unit = units - 1;
-  const int h = unit >> 1, half = unit & 1;
+  const int h = unit / S, r = unit % S;
   const float* bh = b + static_cast<size_t>(h) * (2 * n - 1);
   float2 x[F::R];
   float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-  for (int r = 0; r < F::R; ++r) {
-    const int s = tau + F::T * r;
-    const float lo = circ_kernel(bh, s, n, F::N), hi = circ_kernel(bh, s + F::N, n, F::N);
-    s1 += lo + hi;
-    s2 = fmaf(lo, lo, fmaf(hi, hi, s2));
-    x[r] = half == 0 ? make_float2(lo + hi, 0.f) : make_float2((lo - hi) * tw[s].x, (lo - hi) * tw[s].y);
+  for (int i = 0; i < F::R; ++i) {
+    const int j = tau + F::T * i;
+    float2 acc = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int p = 0; p < S; ++p) {
+      const float hv = circ_kernel(bh, j + p * F::N, n, C::N);
+      s1 += hv;
+      s2 = fmaf(hv, hv, s2);
+      acc = cadd(acc, real_quarter_turn(hv, (4 / S) * p * r));
+    }
+    x[i] = r == 0 ? acc : cmul(acc, tw[r * j]);
   }
   if (hnorm) {
     s1 = unit_reduce<F::T>(s1, red, OpAdd());
     s2 = unit_reduce<F::T>(s2, red, OpAdd());
-    if (active && half == 0 && tau == 0) hnorm[h] = make_float2(s1, sqrtf(s2));
+    if (active && r == 0 && tau == 0) hnorm[h] = make_float2(s1, sqrtf(s2));
   }
   F::forward(x, lds + g * (F::P > 1 ? F::LDS : 0), tw, tau);
   if (active) {
-    const float scale = 1.0f / static_cast<float>(2 * F::N);
+    // Stored in the order the forward transform leaves the bins in registers:
+    // element i * T + tau is register i of thread tau (frequency
+    // F::frequency_of(F::spectrum_pos(tau, i))).
+    const float scale = 1.0f / static_cast<float>(2 * C::N);
     float2* out = Hs + static_cast<size_t>(unit) * F::N;
 #pragma unroll
-    for (int i = 0; i < F::R; ++i) {
-      const int k = F::frequency_of(F::spectrum_pos(tau, i));
-      out[k] = make_float2(x[i].x * scale, x[i].y * scale);
-    }
+    for (int i = 0; i < F::R; ++i) out[i * F::T + tau] = make_float2(x[i].x * scale, x[i].y * scale);
   }
 }
 
@@ -192,109 +213,279 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
   }
 }
 
-// ---------------------------------------------- convolution + contraction --
-// Unit u = ((bh * HSPLIT + hs) * pairs + cp), pairs = ceil((d + 1) / 2).  The
-// unit owns the two columns c0 = 2 cp and c1 = 2 cp + 1 of v' = [v, 1]
-// (column d is the all-ones column of the denominator; c1 > d means none) and
-// the spectrum halves hs*KH .. hs*KH + KH - 1.  For every feature l the two
-// channels phi_l(k_j) v'_{j,c0} and phi_l(k_j) v'_{j,c1} share the envelope
-// phi_l(k), so packing them as the real and imaginary parts of one complex
-// signal keeps their magnitudes alike: the FFT's rounding error, set by the
-// pair's norm, stays proportional to each.  Each column is also scaled by its
-// own max |v| before packing.
-//
-// Writes the partial numerators / denominator of Eq. (10) of its halves
-//   part[bh][hs][c][i] = sum_l phi_l(q_i) (C_hs a_{l,c})_i,   c in {c0, c1},
-// and, from hs = 0, the error-bound weights
-//   bnd[bh][cp][i] = sum_l phi_l(q_i) ||x_l||_2   (x_l the packed signal)
-// and colmax[bh][c] = max_j |v_{j,c}| for its value columns.
-template <typename F, int WAVES, int KH, int HALF0>
-__device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const float* __restrict__ pq,
-                                          const float2* __restrict__ tw, const float (&v0)[F::R],
-                                          const float (&v1)[F::R], const float2 (&Hr)[KH][F::R], float2* lds,
-                                          float (*nslot)[WAVES], int tau, int m, float (&acc0)[F::R],
-                                          float (&acc1)[F::R], float (&bound)[F::R]) {
-  constexpr bool kTwist = HALF0 + KH > 1;   // some half of this unit is the odd one
-  constexpr bool kBound = HALF0 == 0;       // one unit per pair accumulates the bound
-  float2 twist[F::R];
-  if constexpr (kTwist) {
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) twist[r] = tw[tau + F::T * r];
+// ------------------------------------------------------ value columns --
+// Column c of v' (value columns, plus an all-ones column when with_ones: the
+// denominator's channel A2 of Eq. (11)) is scaled by its max |.| and packed
+// with its neighbour as one complex signal per pair p = c / 2:
+//   vsc[bh][p][pos] = (v'_{2p}(pos) / s_{2p}, v'_{2p+1}(pos) / s_{2p+1}),  0 beyond n,
+//   colmax[bh][c] = s_c.
+// v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc].  Block (bh, pb) handles
+// columns 16 pb .. 16 pb + 15.
+template <typename TV>
+__global__ __launch_bounds__(256) void k_vprep(const TV* __restrict__ v, long long sp, long long sc,
+                                               long long bh_stride, int ncols, int with_ones, int n, int N,
+                                               float* __restrict__ colmax, float2* __restrict__ vsc, int pblocks) {
+  __shared__ float part_max[16][17];
+  __shared__ float smax[16];
+  const int bh = blockIdx.x / pblocks, pb = blockIdx.x % pblocks;
+  const int cols = ncols + with_ones, pairs = (cols + 1) / 2;
+  const TV* __restrict__ vb = v + bh * bh_stride;
+  const int tid = threadIdx.x;
+  {
+    const int c = pb * 16 + (tid & 15), lane_row = tid >> 4;
+    float mx = 0.f;
+    if (c < ncols) {
+      for (int pos = lane_row; pos < n; pos += 16) mx = fmaxf(mx, fabsf(to_f32(vb[pos * sp + c * sc])));
+    } else if (c < cols) {
+      mx = 1.f;
+    }
+    part_max[lane_row][tid & 15] = mx;
   }
-  float a_next[F::R];
-#pragma unroll
-  for (int r = 0; r < F::R; ++r) a_next[r] = pk[tau + F::T * r];
-  for (int l = 0; l < m; ++l) {
-    float a[F::R], f[F::R];
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) a[r] = a_next[r];
-    // Loads for later stay in flight across the transform (the barriers only
-    // wait for LDS traffic): phi(q) for this feature, phi(k) for the next.
-    const float* __restrict__ pql = pq + static_cast<size_t>(l) * F::N;
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) f[r] = pql[tau + F::T * r];
-    if (l + 1 < m) {
-      const float* __restrict__ pkn = pk + static_cast<size_t>(l + 1) * F::N;
-#pragma unroll
-      for (int r = 0; r < F::R; ++r) a_next[r] = pkn[tau + F::T * r];
-    }
-    float2 x[KH][F::R];
-    float nx = 0.f;
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) {
-      const float2 xb = make_float2(a[r] * v0[r], a[r] * v1[r]);
-      if constexpr (kBound) nx = fmaf(xb.x, xb.x, fmaf(xb.y, xb.y, nx));
-#pragma unroll
-      for (int k = 0; k < KH; ++k) x[k][r] = (HALF0 + k == 1) ? cmul(xb, twist[r]) : xb;
-    }
-    if constexpr (kBound) {
-      nx = wave_unit_reduce<F::T>(nx, OpAdd());
-      // Cross-wave part of the reduction rides on the FFT's own barriers:
-      // written here, read after the inverse transform; double-buffered on l.
-      if constexpr (F::T > 64) {
-        if ((threadIdx.x & 63) == 0) nslot[l & 1][threadIdx.x >> 6] = nx;
+  __syncthreads();
+  if (tid < 16) {
+    float mx = 0.f;
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, part_max[r][tid]);
+    smax[tid] = mx;
+    const int c = pb * 16 + tid;
+    if (c < cols) colmax[static_cast<size_t>(bh) * cols + c] = mx;
+  }
+  __syncthreads();
+  for (int pl = 0; pl < 8; ++pl) {
+    const int p = pb * 8 + pl;
+    if (p >= pairs) break;
+    const int ca = 2 * p, cb = 2 * p + 1;
+    const float sa = smax[2 * pl] > 0.f ? smax[2 * pl] : 1.f;
+    const float sb = smax[2 * pl + 1] > 0.f ? smax[2 * pl + 1] : 1.f;
+    float2* __restrict__ out = vsc + (static_cast<size_t>(bh) * pairs + p) * N;
+    for (int pos = tid; pos < N; pos += 256) {
+      float a = 0.f, b2 = 0.f;
+      if (pos < n) {
+        a = ca < ncols ? to_f32(vb[pos * sp + ca * sc]) : (ca < cols ? 1.f : 0.f);
+        b2 = cb < ncols ? to_f32(vb[pos * sp + cb * sc]) : (cb < cols ? 1.f : 0.f);
       }
-    }
-    F::template forward<KH>(x, lds, tw, tau);
-#pragma unroll
-    for (int k = 0; k < KH; ++k)
-#pragma unroll
-      for (int i = 0; i < F::R; ++i) x[k][i] = cmul(x[k][i], Hr[k][i]);
-    F::template inverse<KH>(x, lds, tw, tau);
-    float xn = 0.f;
-    if constexpr (kBound) {
-      if constexpr (F::T > 64) {
-        const int first = (threadIdx.x / F::T) * (F::T / 64);
-        nx = nslot[l & 1][first];
-#pragma unroll
-        for (int w = 1; w < F::T / 64; ++w) nx += nslot[l & 1][first + w];
-      }
-      xn = sqrtf(nx);
-    }
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) {
-      float2 y = (HALF0 == 1) ? cmulc(x[0][r], twist[r]) : x[0][r];
-      if constexpr (KH == 2) y = cadd(y, cmulc(x[1][r], twist[r]));
-      acc0[r] = fmaf(f[r], y.x, acc0[r]);
-      acc1[r] = fmaf(f[r], y.y, acc1[r]);
-      if constexpr (kBound) bound[r] = fmaf(f[r], xn, bound[r]);
+      out[pos] = make_float2(a / sa, b2 / sb);
     }
   }
 }
 
-template <int L2, typename TV>
+// ---------------------------------------------- convolution + contraction --
+// z * (-i)^E, E taken mod 4.
+template <int E>
+__device__ __forceinline__ float2 quarter_turn(float2 z) {
+  constexpr int e = ((E % 4) + 4) % 4;
+  if constexpr (e == 0) return z;
+  if constexpr (e == 1) return make_float2(z.y, -z.x);
+  if constexpr (e == 2) return make_float2(-z.x, -z.y);
+  return make_float2(-z.y, z.x);
+}
+
+// Unit u = ((bh * HSPLIT + hs) * pairs + cp).  The unit owns columns
+// c0 = 2 cp, c1 = 2 cp + 1 of v' (packed and scaled by k_vprep) and the
+// residue classes r = hs*KH .. hs*KH + KH - 1 of the length-2N spectrum.  For
+// every feature l the two channels phi_l(k_j) v'_{j,c0} and phi_l(k_j) v'_{j,c1}
+// (columns of A1 / A2, Eq. (11)) share the envelope phi_l(k), so packing them
+// as the real and imaginary parts of one complex signal keeps their
+// magnitudes alike: the FFT's rounding error, set by the pair's norm, stays
+// proportional to each.
+//
+// Residue class r of the circular convolution y = h (*) x of length 2N, with
+// x zero from N on, S = 2 FOLD classes and transforms of length LT = N / FOLD:
+//   u_r[j]      = W_{2N}^{r j} sum_{p < FOLD} x[j + p LT] W_S^{p r}
+//   y[i + q LT] = sum_r W_{2N}^{-r i} W_S^{-q r} IDFT_LT(H_r * DFT_LT(u_r))[i]
+// for j, i < LT and q < FOLD (the outputs below N), H_r as in k_spectrum.
+//
+// Writes the partial numerators / denominator of Eq. (10) of its classes
+//   part[bh][hs][c][i] = s_c sum_l phi_l(q_i) (C_hs a_{l,c})_i,   c in {c0, c1}.
+// phi rows are [m][N] per (batch, head), phi_bh_stride apart (0 broadcasts one
+// set of rows to every head).
+template <typename F, int FOLD, int KH, int R0, bool VREG, bool HREG, bool HOIST>
+__device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const float* __restrict__ pq,
+                                          const float2* __restrict__ vrow, const float2* __restrict__ tw,
+                                          const float2* __restrict__ Hh, float2* lds, int tau, int m,
+                                          float (&acc0)[FOLD][F::R], float (&acc1)[FOLD][F::R]) {
+  constexpr int S = 2 * FOLD;
+  constexpr int NP = FOLD * F::N;  // row length of phi and v
+  // Spectrum classes, register order (see k_spectrum): kept in registers when
+  // the work-group is small enough, else re-read just before the product.
+  float2 Hr[HREG ? KH : 1][F::R];
+  if constexpr (HREG) {
+#pragma unroll
+    for (int k = 0; k < KH; ++k)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i) Hr[k][i] = Hh[k * F::N + i * F::T + tau];
+  }
+  float2 vx[VREG ? FOLD : 1][VREG ? F::R : 1];
+  if constexpr (VREG) {
+#pragma unroll
+    for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i) vx[p][i] = vrow[tau + F::T * i + p * F::N];
+  }
+  // W_{2N}^{r j} of the classes r > 0.
+  float2 twist[VREG ? KH : 1][VREG ? F::R : 1];
+  if constexpr (VREG) {
+#pragma unroll
+    for (int k = 0; k < KH; ++k)
+      if (R0 + k > 0) {
+#pragma unroll
+        for (int i = 0; i < F::R; ++i) twist[k][i] = tw[(R0 + k) * (tau + F::T * i)];
+      }
+  }
+  // With registers to spare, phi(k) of the next feature and phi(q) of this one
+  // are loaded at the top of the iteration and stay in flight across the
+  // transform (the barriers only wait for LDS traffic).
+  float a_next[VREG ? FOLD : 1][VREG ? F::R : 1];
+  if constexpr (VREG) {
+#pragma unroll
+    for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i) a_next[p][i] = pk[tau + F::T * i + p * F::N];
+  }
+  for (int l = 0; l < m; ++l) {
+    const float* __restrict__ pkl = pk + static_cast<size_t>(l) * NP;
+    const float* __restrict__ pql = pq + static_cast<size_t>(l) * NP;
+    // Large work-groups have too few registers to keep the loop-invariant
+    // twiddles: hide the table pointer from loop-invariant code motion so they
+    // are re-read (from L1) inside the transforms instead.
+    const float2* __restrict__ twl = tw;
+    const float2* __restrict__ Hl = Hh;
+    int taul = tau;
+    if constexpr (!HOIST) {
+      asm volatile("" : "+s"(twl));
+      asm volatile("" : "+v"(Hl));
+      asm volatile("" : "+v"(taul));
+    }
+    float a[FOLD][F::R], f[FOLD][F::R];
+#pragma unroll
+    for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i)
+        a[p][i] = VREG ? a_next[VREG ? p : 0][VREG ? i : 0] : pkl[taul + F::T * i + p * F::N];
+    if constexpr (VREG) {
+#pragma unroll
+      for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+        for (int i = 0; i < F::R; ++i) f[p][i] = pql[tau + F::T * i + p * F::N];
+      if (l + 1 < m) {
+#pragma unroll
+        for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+          for (int i = 0; i < F::R; ++i) a_next[p][i] = pkl[NP + tau + F::T * i + p * F::N];
+      }
+    }
+    float2 x[KH][F::R];
+#pragma unroll
+    for (int i = 0; i < F::R; ++i) {
+      float2 xb[FOLD];
+#pragma unroll
+      for (int p = 0; p < FOLD; ++p) {
+        const float2 vv = VREG ? vx[VREG ? p : 0][VREG ? i : 0] : vrow[taul + F::T * i + p * F::N];
+        xb[p] = make_float2(a[p][i] * vv.x, a[p][i] * vv.y);
+      }
+#pragma unroll
+      for (int k = 0; k < KH; ++k) {
+        float2 u = xb[0];
+        if constexpr (FOLD == 2) {
+          // W_4^{r} = (-i)^r on the second fold
+          switch ((R0 + k) & 3) {
+            case 0: u = cadd(u, quarter_turn<0>(xb[1])); break;
+            case 1: u = cadd(u, quarter_turn<1>(xb[1])); break;
+            case 2: u = cadd(u, quarter_turn<2>(xb[1])); break;
+            default: u = cadd(u, quarter_turn<3>(xb[1])); break;
+          }
+        }
+        if (R0 + k > 0) {
+          const float2 w = VREG ? twist[VREG ? k : 0][VREG ? i : 0] : twl[(R0 + k) * (taul + F::T * i)];
+          u = cmul(u, w);
+        }
+        x[k][i] = u;
+      }
+    }
+    F::template forward<KH>(x, lds, twl, taul);
+#pragma unroll
+    for (int k = 0; k < KH; ++k)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i)
+        x[k][i] = cmul(x[k][i], HREG ? Hr[HREG ? k : 0][i] : Hl[k * F::N + i * F::T + taul]);
+    F::template inverse<KH>(x, lds, twl, taul);
+    if constexpr (!HOIST) {
+      // fresh (opaque) copies: the twists are re-read rather than kept live
+      // across both transforms
+      asm volatile("" : "+s"(twl));
+      asm volatile("" : "+v"(taul));
+    }
+    if constexpr (!VREG) {
+#pragma unroll
+      for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+        for (int i = 0; i < F::R; ++i) f[p][i] = pql[taul + F::T * i + p * F::N];
+    }
+#pragma unroll
+    for (int i = 0; i < F::R; ++i) {
+      float2 yk[KH];
+#pragma unroll
+      for (int k = 0; k < KH; ++k) {
+        yk[k] = x[k][i];
+        if (R0 + k > 0) {
+          const float2 w = VREG ? twist[VREG ? k : 0][VREG ? i : 0] : twl[(R0 + k) * (taul + F::T * i)];
+          yk[k] = cmulc(yk[k], w);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < FOLD; ++q) {
+        float2 y = make_float2(0.f, 0.f);
+#pragma unroll
+        for (int k = 0; k < KH; ++k) {
+          // W_S^{-q r} = (-i)^{-(4/S) q r}
+          float2 t = yk[k];
+          if (q > 0) {
+            switch (((4 / S) * q * (R0 + k)) & 3) {
+              case 0: break;
+              case 1: t = quarter_turn<-1>(t); break;
+              case 2: t = quarter_turn<-2>(t); break;
+              default: t = quarter_turn<-3>(t); break;
+            }
+          }
+          y = k == 0 ? t : cadd(y, t);
+        }
+        acc0[q][i] = fmaf(f[q][i], y.x, acc0[q][i]);
+        acc1[q][i] = fmaf(f[q][i], y.y, acc1[q][i]);
+      }
+    }
+  }
+}
+
+// Calls conv_loop with the first class of split hs as a compile-time constant.
+template <typename C, int HS = 0>
+__device__ __forceinline__ void conv_split(int hs, const float* __restrict__ pk, const float* __restrict__ pq,
+                                           const float2* __restrict__ vrow, const float2* __restrict__ tw,
+                                           const float2* __restrict__ Hh, float2* lds, int tau, int m,
+                                           float (&acc0)[C::FOLD][C::F::R], float (&acc1)[C::FOLD][C::F::R]) {
+  if constexpr (HS < C::HSPLIT) {
+    if (HS + 1 == C::HSPLIT || hs == HS) {
+      conv_loop<typename C::F, C::FOLD, C::KH, HS * C::KH, C::VREG, C::HREG, C::HOIST>(pk, pq, vrow, tw, Hh, lds,
+                                                                                       tau, m, acc0, acc1);
+    } else {
+      conv_split<C, HS + 1>(hs, pk, pq, vrow, tw, Hh, lds, tau, m, acc0, acc1);
+    }
+  }
+}
+
+template <int L2>
 __global__ __launch_bounds__(Conf<L2>::THREADS) void k_conv_contract(
-    const float* __restrict__ phiq, const float* __restrict__ phik, const TV* __restrict__ v,
-    const float2* __restrict__ Hs, const float2* __restrict__ tw, float* __restrict__ part,
-    float* __restrict__ bnd, float* __restrict__ colmax, int H, int n, int d, int m, int units) {
+    const float* __restrict__ phiq, const float* __restrict__ phik, long long phi_bh_stride,
+    const float2* __restrict__ vsc, const float* __restrict__ colmax, const float2* __restrict__ Hs,
+    const float2* __restrict__ tw, float* __restrict__ part, int H, int n, int cols, int m, int units) {
   using C = Conf<L2>;
   using F = typename C::F;
-  constexpr int KH = C::KH;
+  constexpr int KH = C::KH, FOLD = C::FOLD;
+  // Units of one work-group must run the same class split (same barriers).
+  static_assert(C::HSPLIT == 1 || C::G == 1, "class splits need one unit per work-group");
   __shared__ float2 lds_all[C::CONV_LDS_SLOTS];
-  __shared__ float red[C::WAVES];
-  __shared__ float nslot[2][C::WAVES];
-  const int g = threadIdx.x / F::T, tau = threadIdx.x % F::T;
-  const int pairs = (d + 2) / 2;
+  // With one unit per work-group the unit index is wave-uniform: say so, so
+  // that per-unit pointers live in scalar registers.
+  const int g = C::G == 1 ? 0 : threadIdx.x / F::T, tau = C::G == 1 ? threadIdx.x : threadIdx.x % F::T;
+  const int pairs = (cols + 1) / 2;
   int unit = xcd_block(blockIdx.x, gridDim.x) * C::G + g;
   const bool active = unit < units;
   if (!active) unit = units - 1;  // keep the barriers uniform; results discarded
@@ -303,113 +494,172 @@ __global__ __launch_bounds__(Conf<L2>::THREADS) void k_conv_contract(
   const int hs = rest % C::HSPLIT, bh = rest / C::HSPLIT, h = bh % H;
   const int c0 = 2 * cp, c1 = 2 * cp + 1;
   float2* lds = lds_all + g * (F::P > 1 ? KH * F::LDS : 0);
+  const float2* __restrict__ vrow = vsc + (static_cast<size_t>(bh) * pairs + cp) * C::N;
 
-  // Value columns at this thread's positions, and their scales.
-  const TV* __restrict__ vb = v + static_cast<size_t>(bh) * n * d;
-  float v0[F::R], v1[F::R];
-  float mx0 = 0.f, mx1 = 0.f;
+  const float2* __restrict__ Hh = Hs + (static_cast<size_t>(h) * C::S + hs * KH) * F::N;
+  float acc0[FOLD][F::R], acc1[FOLD][F::R];
 #pragma unroll
-  for (int r = 0; r < F::R; ++r) {
-    const int pos = tau + F::T * r;
-    const bool in = pos < n;
-    v0[r] = in ? (c0 < d ? to_f32(vb[static_cast<size_t>(pos) * d + c0]) : 1.f) : 0.f;
-    v1[r] = in ? (c1 < d ? to_f32(vb[static_cast<size_t>(pos) * d + c1]) : (c1 == d ? 1.f : 0.f)) : 0.f;
-    mx0 = fmaxf(mx0, fabsf(v0[r]));
-    mx1 = fmaxf(mx1, fabsf(v1[r]));
-  }
-  mx0 = unit_reduce<F::T>(mx0, red, OpMax());
-  mx1 = unit_reduce<F::T>(mx1, red, OpMax());
-  const float s0 = mx0 > 0.f ? mx0 : 1.f, s1 = mx1 > 0.f ? mx1 : 1.f;
-  const float is0 = 1.f / s0, is1 = 1.f / s1;
+  for (int q = 0; q < FOLD; ++q)
 #pragma unroll
-  for (int r = 0; r < F::R; ++r) {
-    v0[r] *= is0;
-    v1[r] *= is1;
-  }
-  if (active && hs == 0 && tau == 0) {
-    if (c0 < d) colmax[static_cast<size_t>(bh) * d + c0] = mx0;
-    if (c1 < d) colmax[static_cast<size_t>(bh) * d + c1] = mx1;
-  }
+    for (int i = 0; i < F::R; ++i) acc0[q][i] = acc1[q][i] = 0.f;
 
-  // Spectrum halves in registers, in the order the forward transform leaves them.
-  float2 Hr[KH][F::R];
-#pragma unroll
-  for (int k = 0; k < KH; ++k) {
-    const float2* __restrict__ Hh = Hs + (static_cast<size_t>(h) * 2 + hs * KH + k) * F::N;
-#pragma unroll
-    for (int i = 0; i < F::R; ++i) Hr[k][i] = Hh[F::frequency_of(F::spectrum_pos(tau, i))];
-  }
-
-  float acc0[F::R], acc1[F::R], bound[F::R];
-#pragma unroll
-  for (int r = 0; r < F::R; ++r) acc0[r] = acc1[r] = bound[r] = 0.f;
-
-  const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * F::N;
-  const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * F::N;
-  if constexpr (KH == 2) {
-    conv_loop<F, C::WAVES, 2, 0>(pk, pq, tw, v0, v1, Hr, lds, nslot, tau, m, acc0, acc1, bound);
-  } else {
-    if (hs)
-      conv_loop<F, C::WAVES, 1, 1>(pk, pq, tw, v0, v1, Hr, lds, nslot, tau, m, acc0, acc1, bound);
-    else
-      conv_loop<F, C::WAVES, 1, 0>(pk, pq, tw, v0, v1, Hr, lds, nslot, tau, m, acc0, acc1, bound);
-  }
+  const float* __restrict__ pk = phik + bh * phi_bh_stride;
+  const float* __restrict__ pq = phiq + bh * phi_bh_stride;
+  conv_split<C>(hs, pk, pq, vrow, tw, Hh, lds, tau, m, acc0, acc1);
 
   if (active) {
-    float* __restrict__ out = part + ((static_cast<size_t>(bh) * C::HSPLIT + hs) * (d + 1) + c0) * n;
-    float* __restrict__ bout = bnd + (static_cast<size_t>(bh) * pairs + cp) * n;
+    const float s0 = colmax[static_cast<size_t>(bh) * cols + c0];
+    const float s1 = c1 < cols ? colmax[static_cast<size_t>(bh) * cols + c1] : 0.f;
+    float* __restrict__ out = part + ((static_cast<size_t>(bh) * C::HSPLIT + hs) * cols + c0) * n;
 #pragma unroll
-    for (int r = 0; r < F::R; ++r) {
-      const int pos = tau + F::T * r;
-      if (pos < n) {
-        out[pos] = acc0[r] * s0;
-        if (c1 <= d) out[n + pos] = acc1[r] * s1;
-        if (hs == 0) bout[pos] = bound[r];
+    for (int q = 0; q < FOLD; ++q)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i) {
+        const int pos = tau + F::T * i + q * F::N;
+        if (pos < n) {
+          out[pos] = acc0[q][i] * (s0 > 0.f ? s0 : 1.f);
+          if (c1 < cols) out[n + pos] = acc1[q][i] * (s1 > 0.f ? s1 : 1.f);
+        }
       }
+  }
+}
+
+// ------------------------------------------------------- channel norms --
+// X2[bh][ks][l][p] = sum over positions of slice ks of phi_l(k_j)^2 |vsc_p(j)|^2
+// = ||x_{l,p}||^2 restricted to the slice, x_{l,p} the packed signal the
+// convolution kernel transforms for feature l and column pair p.  Block
+// (bh, l-tile of 64, slice ks); threads own a feature and every 4th pair.
+constexpr int kMaxPairs = (kMaxD + 2) / 2;
+constexpr int kPairSlots = (kMaxPairs + 3) / 4;
+
+__global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, const float2* __restrict__ vsc,
+                                              float* __restrict__ X2, int m, int N, int pairs, int ltiles,
+                                              int ksplit) {
+  __shared__ float A[64][65];
+  __shared__ float Bq[64][kMaxPairs + 1];
+  int bid = blockIdx.x;
+  const int ks = bid % ksplit;
+  bid /= ksplit;
+  const int lt = bid % ltiles, bh = bid / ltiles;
+  const int tid = threadIdx.x, li = tid & 63, pg = tid >> 6;
+  const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * N;
+  const float2* __restrict__ vb = vsc + static_cast<size_t>(bh) * pairs * N;
+  const int slice = N / ksplit, pos_begin = ks * slice, pos_end = pos_begin + slice;
+  float acc[kPairSlots];
+#pragma unroll
+  for (int k = 0; k < kPairSlots; ++k) acc[k] = 0.f;
+  for (int p0 = pos_begin; p0 < pos_end; p0 += 64) {
+    __syncthreads();
+    for (int e = tid; e < 64 * 64; e += 256) {
+      const int r = e >> 6, x = e & 63;
+      const int l = lt * 64 + r;
+      const float a = (l < m && p0 + x < pos_end) ? pk[static_cast<size_t>(l) * N + p0 + x] : 0.f;
+      A[r][x] = a * a;
+    }
+    for (int e = tid; e < 64 * pairs; e += 256) {
+      const int p = e >> 6, x = e & 63;
+      float q2 = 0.f;
+      if (p0 + x < pos_end) {
+        const float2 w = vb[static_cast<size_t>(p) * N + p0 + x];
+        q2 = w.x * w.x + w.y * w.y;
+      }
+      Bq[x][p] = q2;
+    }
+    __syncthreads();
+    for (int x = 0; x < 64; ++x) {
+      const float a = A[li][x];
+#pragma unroll
+      for (int k = 0; k < kPairSlots; ++k) {
+        const int p = pg + 4 * k;
+        if (p < pairs) acc[k] = fmaf(a, Bq[x][p], acc[k]);
+      }
+    }
+  }
+  const int l = lt * 64 + li;
+  if (l < m) {
+    float* __restrict__ out = X2 + ((static_cast<size_t>(bh) * ksplit + ks) * m + l) * pairs;
+#pragma unroll
+    for (int k = 0; k < kPairSlots; ++k) {
+      const int p = pg + 4 * k;
+      if (p < pairs) out[p] = acc[k];
     }
   }
 }
 
 // -------------------------------------------------------------- combine --
 // z[bh][i][c] = sum_s P_s[c][i] / sum_s P_s[d][i],  P = part[bh], s < nsplit,
-// and the certification of each row.  With K = kGamma u log2(L) ||h||_2 / sqrt(L),
-// the error model of common.hpp bounds the rounding error of numerator c by
-// K bnd[p(c)][i] s_c (+ a part relative to the value itself) and that of the
-// denominator by K bnd[p(d)][i], p(c) = c / 2 the packed pair of column c.  A
-// row whose normwise relative bound exceeds kTau is queued for k_fixup.
-__global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part, const float* __restrict__ bnd,
-                                                 const float* __restrict__ colmax,
+// and the certification of each row.  With K = kGamma u log2(L) ||h||_2 / sqrt(L)
+// and the bound weights B_p(i) = sum_l phi_l(q_i) ||x_{l,p}||_2, the error
+// model of common.hpp bounds the rounding error of numerator c by
+// K B_{c/2}(i) s_c (+ a part relative to the value itself) and that of the
+// denominator by K B_{d/2}(i).  A row whose normwise relative bound exceeds
+// kTau is queued for k_fixup.
+__global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part, const float* __restrict__ phiq,
+                                                 const float* __restrict__ X2, const float* __restrict__ colmax,
                                                  const float2* __restrict__ hnorm, float* __restrict__ z,
-                                                 unsigned* __restrict__ fix, int BH, int H, int n, int log2N,
-                                                 int d, int nsplit, int tiles_n) {
+                                                 unsigned* __restrict__ fix, int BH, int H, int n, int N,
+                                                 int log2N, int d, int m, int nsplit, int ksplit, int tiles_n) {
   __shared__ float tile[kMaxD + 1][65];
-  __shared__ float btile[kMaxD / 2 + 1][65];
+  __shared__ float qc[64][65];
+  __shared__ float xc[64][kMaxPairs + 1];
+  __shared__ float btile[kMaxPairs][65];
   __shared__ float scol[kMaxD + 1];
   __shared__ float zmax[64];
   const int bh = blockIdx.x / tiles_n, i0 = (blockIdx.x % tiles_n) * 64;
   const int h = bh % H;
-  const int pairs = (d + 2) / 2;
-  const float* __restrict__ p0 = part + static_cast<size_t>(bh) * nsplit * (d + 1) * n;
-  const float* __restrict__ bb = bnd + static_cast<size_t>(bh) * pairs * n;
-  for (int e = threadIdx.x; e < (d + 1) * 64; e += 256) {
+  const int cols = d + 1, pairs = (cols + 1) / 2;
+  const int tid = threadIdx.x;
+  const float* __restrict__ p0 = part + static_cast<size_t>(bh) * nsplit * cols * n;
+  for (int e = tid; e < cols * 64; e += 256) {
     const int c = e >> 6, i = e & 63;
     const int pos = i0 + i;
     float t = 1.f;
     if (pos < n) {
       t = p0[static_cast<size_t>(c) * n + pos];
-      for (int sp = 1; sp < nsplit; ++sp) t += p0[(static_cast<size_t>(sp) * (d + 1) + c) * n + pos];
+      for (int sp = 1; sp < nsplit; ++sp) t += p0[(static_cast<size_t>(sp) * cols + c) * n + pos];
     }
     tile[c][i] = t;
   }
-  for (int e = threadIdx.x; e < pairs * 64; e += 256) {
-    const int p = e >> 6, i = e & 63;
-    const int pos = i0 + i;
-    btile[p][i] = pos < n ? bb[static_cast<size_t>(p) * n + pos] : 0.f;
+  for (int c = tid; c < cols; c += 256) scol[c] = colmax[static_cast<size_t>(bh) * cols + c];
+  // bound weights for the 64 rows: thread (row li, pairs pg + 4k)
+  const int li = tid & 63, pg = tid >> 6;
+  float bacc[kPairSlots];
+#pragma unroll
+  for (int k = 0; k < kPairSlots; ++k) bacc[k] = 0.f;
+  const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * N;
+  const float* __restrict__ xb = X2 + static_cast<size_t>(bh) * ksplit * m * pairs;
+  for (int l0 = 0; l0 < m; l0 += 64) {
+    __syncthreads();
+    for (int e = tid; e < 64 * 64; e += 256) {
+      const int r = e >> 6, x = e & 63;
+      qc[r][x] = (l0 + r < m && i0 + x < n) ? pq[static_cast<size_t>(l0 + r) * N + i0 + x] : 0.f;
+    }
+    for (int e = tid; e < 64 * pairs; e += 256) {
+      const int r = e / pairs, p = e % pairs;
+      float s2 = 0.f;
+      if (l0 + r < m)
+        for (int ks = 0; ks < ksplit; ++ks) s2 += xb[(static_cast<size_t>(ks) * m + l0 + r) * pairs + p];
+      xc[r][p] = sqrtf(s2);
+    }
+    __syncthreads();
+    const int lmax = min(64, m - l0);
+    for (int r = 0; r < lmax; ++r) {
+      const float q = qc[r][li];
+#pragma unroll
+      for (int k = 0; k < kPairSlots; ++k) {
+        const int p = pg + 4 * k;
+        if (p < pairs) bacc[k] = fmaf(q, xc[r][p], bacc[k]);
+      }
+    }
   }
-  for (int c = threadIdx.x; c <= d; c += 256) scol[c] = c < d ? colmax[static_cast<size_t>(bh) * d + c] : 1.f;
+#pragma unroll
+  for (int k = 0; k < kPairSlots; ++k) {
+    const int p = pg + 4 * k;
+    if (p < pairs) btile[p][li] = bacc[k];
+  }
   __syncthreads();
-  if (threadIdx.x < 64) {
-    const int i = threadIdx.x;
+  if (tid < 64) {
+    const int i = tid;
     float zm = 0.f;
     const float den = tile[d][i];
     for (int c = 0; c < d; ++c) zm = fmaxf(zm, fabsf(tile[c][i] / den));
@@ -417,13 +667,13 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
   }
   __syncthreads();
   float* __restrict__ zb = z + static_cast<size_t>(bh) * n * d;
-  for (int e = threadIdx.x; e < 64 * d; e += 256) {
+  for (int e = tid; e < 64 * d; e += 256) {
     const int i = e / d, c = e % d;
     const int pos = i0 + i;
     if (pos < n) zb[static_cast<size_t>(pos) * d + c] = tile[c][i] / tile[d][i];
   }
-  if (threadIdx.x < 64) {
-    const int i = threadIdx.x, pos = i0 + i;
+  if (tid < 64) {
+    const int i = tid, pos = i0 + i;
     bool flag = false;
     if (pos < n) {
       const float L = static_cast<float>(2 << log2N);
@@ -646,79 +896,24 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
   }
 }
 
-// ------------------------------------------------------ Toeplitz product --
-// Unit u = bh * ceil(C/2) + pair: channels (2 pair, 2 pair + 1) as one complex
-// signal, each scaled by its own max |a| so that neither's rounding error is
-// set by the other's magnitude; both spectrum halves in turn, summed in
-// registers.
-template <int L2>
-__global__ __launch_bounds__(Conf<L2>::THREADS) void k_toeplitz(const float* __restrict__ a,
-                                                                 float* __restrict__ y,
-                                                                 const float2* __restrict__ Hs,
-                                                                 const float2* __restrict__ tw, int H, int Cch,
-                                                                 int n, int units) {
-  using Cf = Conf<L2>;
-  using F = typename Cf::F;
-  __shared__ float2 lds_all[Cf::LDS_SLOTS];
-  __shared__ float red[Cf::WAVES];
-  const int g = threadIdx.x / F::T, tau = threadIdx.x % F::T;
-  int unit = blockIdx.x * Cf::G + g;
-  const bool active = unit < units;
-  if (!active) unit = units - 1;
-  const int pairs = (Cch + 1) / 2;
-  const int bh = unit / pairs, pr = unit % pairs, h = bh % H;
-  const int c0 = 2 * pr;
-  const bool two = c0 + 1 < Cch;
-  float2* lds = lds_all + g * (F::P > 1 ? F::LDS : 0);
-  const float* __restrict__ a0 = a + (static_cast<size_t>(bh) * Cch + c0) * n;
-  float u0[F::R], u1[F::R];
-  float mx0 = 0.f, mx1 = 0.f;
-#pragma unroll
-  for (int r = 0; r < F::R; ++r) {
-    const int pos = tau + F::T * r;
-    u0[r] = pos < n ? a0[pos] : 0.f;
-    u1[r] = (pos < n && two) ? a0[n + pos] : 0.f;
-    mx0 = fmaxf(mx0, fabsf(u0[r]));
-    mx1 = fmaxf(mx1, fabsf(u1[r]));
-  }
-  mx0 = unit_reduce<F::T>(mx0, red, OpMax());
-  mx1 = unit_reduce<F::T>(mx1, red, OpMax());
-  const float s0 = mx0 > 0.f ? mx0 : 1.f, s1 = mx1 > 0.f ? mx1 : 1.f;
-  const float is0 = 1.f / s0, is1 = 1.f / s1;
-  float2 acc[F::R];
-#pragma unroll
-  for (int r = 0; r < F::R; ++r) acc[r] = make_float2(0.f, 0.f);
-  for (int half = 0; half < 2; ++half) {
-    const float2* __restrict__ Hh = Hs + (static_cast<size_t>(h) * 2 + half) * F::N;
-    float2 x[F::R];
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) {
-      const int pos = tau + F::T * r;
-      x[r] = make_float2(u0[r] * is0, u1[r] * is1);
-      if (half) x[r] = cmul(x[r], tw[pos]);
-    }
-    F::forward(x, lds, tw, tau);
-#pragma unroll
-    for (int i = 0; i < F::R; ++i) x[i] = cmul(x[i], Hh[F::frequency_of(F::spectrum_pos(tau, i))]);
-    F::inverse(x, lds, tw, tau);
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) {
-      const int pos = tau + F::T * r;
-      const float2 t = half ? cmulc(x[r], tw[pos]) : x[r];
-      acc[r] = cadd(acc[r], t);
-    }
-  }
-  if (active) {
-    float* __restrict__ y0 = y + (static_cast<size_t>(bh) * Cch + c0) * n;
-#pragma unroll
-    for (int r = 0; r < F::R; ++r) {
-      const int pos = tau + F::T * r;
-      if (pos < n) {
-        y0[pos] = acc[r].x * s0;
-        if (two) y0[n + pos] = acc[r].y * s1;
-      }
-    }
-  }
+// ------------------------------------------------------ Toeplitz helpers --
+// ones[pos] = 1 for pos < n, 0 below N: the broadcast "feature" with which the
+// convolution kernel computes plain Toeplitz products (m = 1, phi = 1).
+__global__ void k_ones(float* __restrict__ ones, int n, int N) {
+  const int pos = blockIdx.x * blockDim.x + threadIdx.x;
+  if (pos < N) ones[pos] = pos < n ? 1.f : 0.f;
+}
+
+// y[bh][c][i] = sum_s part[bh][s][c][i]
+__global__ void k_sum_splits(const float* __restrict__ part, float* __restrict__ y, int C, int n, int nsplit,
+                             long long total) {
+  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= total) return;
+  const long long per = static_cast<long long>(C) * n;
+  const long long bh = e / per, r = e % per;
+  float s = 0.f;
+  for (int sp = 0; sp < nsplit; ++sp) s += part[(bh * nsplit + sp) * per + r];
+  y[e] = s;
 }
 
 // ============================================================ launchers ==
@@ -727,29 +922,20 @@ namespace {
 template <int L2>
 hipError_t spectrum_l2(const float* b, const float2* tw, float2* Hs, float2* hnorm, int H, int n, hipStream_t st) {
   using C = Conf<L2>;
-  const int blocks = (2 * H + C::G - 1) / C::G;
+  const int blocks = (C::S * H + C::G - 1) / C::G;
   hipLaunchKernelGGL(k_spectrum<L2>, dim3(blocks), dim3(C::THREADS), 0, st, b, tw, Hs, hnorm, H, n);
   return hipGetLastError();
 }
 
-template <int L2, typename TV>
-hipError_t conv_l2(const float* phiq, const float* phik, const TV* v, const float2* Hs, const float2* tw,
-                   float* part, float* bnd, float* colmax, int BH, int H, int n, int d, int m, hipStream_t st) {
-  using C = Conf<L2>;
-  const int units = BH * C::HSPLIT * ((d + 2) / 2);
-  const int blocks = (units + C::G - 1) / C::G;
-  hipLaunchKernelGGL((k_conv_contract<L2, TV>), dim3(blocks), dim3(C::THREADS), 0, st, phiq, phik, v, Hs, tw,
-                     part, bnd, colmax, H, n, d, m, units);
-  return hipGetLastError();
-}
-
 template <int L2>
-hipError_t toeplitz_l2(const float* a, float* y, const float2* Hs, const float2* tw, int BH, int H, int Cch, int n,
-                       hipStream_t st) {
+hipError_t conv_l2(const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
+                   const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
+                   int cols, int m, hipStream_t st) {
   using C = Conf<L2>;
-  const int units = BH * ((Cch + 1) / 2);
-  const int blocks = (units + C::G - 1) / C::G;
-  hipLaunchKernelGGL(k_toeplitz<L2>, dim3(blocks), dim3(C::THREADS), 0, st, a, y, Hs, tw, H, Cch, n, units);
+  const long long units = static_cast<long long>(BH) * C::HSPLIT * ((cols + 1) / 2);
+  const long long blocks = (units + C::G - 1) / C::G;
+  hipLaunchKernelGGL(k_conv_contract<L2>, dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0, st, phiq, phik,
+                     phi_bh_stride, vsc, colmax, Hs, tw, part, H, n, cols, m, static_cast<int>(units));
   return hipGetLastError();
 }
 
@@ -769,22 +955,33 @@ struct SpectrumFn {
   static hipError_t run(A... a) { return spectrum_l2<L2>(a...); }
 };
 template <int L2>
-struct ConvF32Fn {
+struct ConvFn {
   template <typename... A>
-  static hipError_t run(A... a) { return conv_l2<L2, float>(a...); }
+  static hipError_t run(A... a) { return conv_l2<L2>(a...); }
 };
 template <int L2>
-struct ConvBf16Fn {
-  template <typename... A>
-  static hipError_t run(A... a) { return conv_l2<L2, uint16_t>(a...); }
-};
-template <int L2>
-struct ToeplitzFn {
-  template <typename... A>
-  static hipError_t run(A... a) { return toeplitz_l2<L2>(a...); }
+struct SplitFn {
+  static hipError_t run(int* out) {
+    *out = Conf<L2>::HSPLIT;
+    return hipSuccess;
+  }
 };
 
 }  // namespace
+
+int conv_splits(int l2) {
+  int s = 2;
+  dispatch<SplitFn>(l2, &s);
+  return s;
+}
+
+int gram_splits(int BH, int m, int N) {
+  // enough blocks to fill the GPU, slices of at least 1024 positions
+  const int ltiles = (m + 63) / 64;
+  int ks = 1;
+  while (ks < 16 && static_cast<long long>(BH) * ltiles * ks < 1024 && N / (2 * ks) >= 1024) ks *= 2;
+  return ks;
+}
 
 hipError_t launch_twiddles(float2* tw, int l2, hipStream_t st) {
   const int count = 2 << l2;
@@ -827,35 +1024,42 @@ hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const f
   return hipGetLastError();
 }
 
-hipError_t launch_conv(int l2, bool bf16, const float* phiq, const float* phik, const void* v, const float2* Hs,
-                       const float2* tw, float* part, float* bnd, float* colmax, int BH, int H, int n, int d,
-                       int m, hipStream_t st) {
+hipError_t launch_vprep(bool bf16, const void* v, long long sp, long long sc, long long bh_stride, int ncols,
+                        bool with_ones, int BH, int n, int N, float* colmax, float2* vsc, hipStream_t st) {
+  const int cols = ncols + (with_ones ? 1 : 0);
+  const int pblocks = (cols + 15) / 16;
+  const dim3 grid(static_cast<unsigned>(static_cast<long long>(BH) * pblocks)), block(256);
   if (bf16)
-    return dispatch<ConvBf16Fn>(l2, phiq, phik, static_cast<const uint16_t*>(v), Hs, tw, part, bnd, colmax, BH, H,
-                                n, d, m, st);
-  return dispatch<ConvF32Fn>(l2, phiq, phik, static_cast<const float*>(v), Hs, tw, part, bnd, colmax, BH, H, n, d,
-                             m, st);
+    hipLaunchKernelGGL(k_vprep<uint16_t>, grid, block, 0, st, static_cast<const uint16_t*>(v), sp, sc, bh_stride,
+                       ncols, with_ones ? 1 : 0, n, N, colmax, vsc, pblocks);
+  else
+    hipLaunchKernelGGL(k_vprep<float>, grid, block, 0, st, static_cast<const float*>(v), sp, sc, bh_stride, ncols,
+                       with_ones ? 1 : 0, n, N, colmax, vsc, pblocks);
+  return hipGetLastError();
 }
 
-template <int L2>
-struct SplitFn {
-  static hipError_t run(int* out) {
-    *out = Conf<L2>::HSPLIT;
-    return hipSuccess;
-  }
-};
-
-int conv_split(int l2) {
-  int s = 2;
-  dispatch<SplitFn>(l2, &s);
-  return s;
+hipError_t launch_conv(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
+                       const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
+                       int cols, int m, hipStream_t st) {
+  return dispatch<ConvFn>(l2, phiq, phik, phi_bh_stride, vsc, colmax, Hs, tw, part, BH, H, n, cols, m, st);
 }
 
-hipError_t launch_combine(const float* part, const float* bnd, const float* colmax, const float2* hnorm, float* z,
-                          unsigned* fix, int BH, int H, int n, int l2, int d, hipStream_t st) {
+hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, int m, int N, int pairs,
+                       int ksplit, hipStream_t st) {
+  const int ltiles = (m + 63) / 64;
+  const long long blocks = static_cast<long long>(BH) * ltiles * ksplit;
+  hipLaunchKernelGGL(k_gram, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, phik, vsc, X2, m, N, pairs,
+                     ltiles, ksplit);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const float* part, const float* phiq, const float* X2, const float* colmax,
+                          const float2* hnorm, float* z, unsigned* fix, int BH, int H, int n, int l2, int d, int m,
+                          int ksplit, hipStream_t st) {
   const int tiles_n = (n + 63) / 64;
-  hipLaunchKernelGGL(k_combine, dim3(BH * tiles_n), dim3(256), 0, st, part, bnd, colmax, hnorm, z, fix, BH, H, n,
-                     l2, d, conv_split(l2), tiles_n);
+  hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), 0, st,
+                     part, phiq, X2, colmax, hnorm, z, fix, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2), ksplit,
+                     tiles_n);
   return hipGetLastError();
 }
 
@@ -868,9 +1072,16 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
   return hipGetLastError();
 }
 
-hipError_t launch_toeplitz(int l2, const float* a, float* y, const float2* Hs, const float2* tw, int BH, int H,
-                           int C, int n, hipStream_t st) {
-  return dispatch<ToeplitzFn>(l2, a, y, Hs, tw, BH, H, C, n, st);
+hipError_t launch_ones(float* ones, int n, int N, hipStream_t st) {
+  hipLaunchKernelGGL(k_ones, dim3((N + 255) / 256), dim3(256), 0, st, ones, n, N);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st) {
+  const long long total = static_cast<long long>(BH) * C * n;
+  hipLaunchKernelGGL(k_sum_splits, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, st, part, y, C,
+                     n, nsplit, total);
+  return hipGetLastError();
 }
 
 }  // namespace krpe

@@ -11,25 +11,31 @@ namespace krpe {
 // Workspace of krpe_attention_fwd (byte offsets, 256-aligned).
 struct AttnLayout {
   int l2;            // log2 N, N = next power of two >= n
-  size_t tw;         // float2 [2N]            W_{2N}^k
-  size_t hs;         // float2 [H][2][N]       spectrum halves of c, / 2N
-  size_t hnorm;      // float2 [H]             (||h||_1, ||h||_2)
-  size_t phiq;       // float  [BH][m][N]      phi(q), feature-major, zero beyond n
-  size_t phik;       // float  [BH][m][N]      phi(k)
-  size_t part;       // float  [BH][2][d+1][n] per-half numerators / denominator
-  size_t bnd;        // float  [BH][pairs][n]  sum_l phi_l(q_i) ||x_{l,pair}||_2
-  size_t colmax;     // float  [BH][d]         max_j |v_{j,c}|
-  size_t fix;        // uint   [BH + 1 + BH n] rows queued per head, total; then the
-                     //                        queued row indices of each head
+  int ksplit;        // position slices of the channel-norm products
+  size_t tw;         // float2 [2N]              W_{2N}^k
+  size_t hs;         // float2 [H][S][2N/S]      spectrum of c by residue class, / 2N
+  size_t hnorm;      // float2 [H]               (||h||_1, ||h||_2)
+  size_t phiq;       // float  [BH][m][N]        phi(q), feature-major, zero beyond n
+  size_t phik;       // float  [BH][m][N]        phi(k)
+  size_t vsc;        // float2 [BH][pairs][N]    scaled column pairs of v' = [v, 1]
+  size_t colmax;     // float  [BH][d+1]         column scales of v'
+  size_t x2;         // float  [BH][ks][m][pairs] squared norms of the packed channels
+  size_t part;       // float  [BH][splits][d+1][n] numerators / denominator per class split
+  size_t fix;        // uint   [BH + 1 + BH n]   rows queued per head, total; then the
+                     //                          queued row indices of each head
   size_t total;
 };
 AttnLayout attn_layout(int B, int H, int n, int d, int m);
 
+// Workspace of krpe_toeplitz_conv.
 struct ConvLayout {
   int l2;
-  size_t tw, hs, total;
+  size_t tw, hs, ones, vsc, colmax, part, total;
 };
-ConvLayout conv_layout(int H, int n);
+ConvLayout conv_layout(int B, int H, int C, int n);
+
+int conv_splits(int l2);
+int gram_splits(int BH, int m, int N);
 
 hipError_t launch_twiddles(float2* tw, int l2, hipStream_t st);
 hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs, float2* hnorm, int H, int n,
@@ -40,15 +46,21 @@ hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs,
 hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const float* W, float* phi0,
                               float* phi1, int nsrc, bool feature_major, int ld, int BH, int H, int n, int d,
                               int m, unsigned* fix_counts, hipStream_t st);
-hipError_t launch_conv(int l2, bool bf16, const float* phiq, const float* phik, const void* v,
-                       const float2* Hs, const float2* tw, float* part, float* bnd, float* colmax, int BH,
-                       int H, int n, int d, int m, hipStream_t st);
-hipError_t launch_combine(const float* part, const float* bnd, const float* colmax, const float2* hnorm,
-                          float* z, unsigned* fix, int BH, int H, int n, int l2, int d, hipStream_t st);
+// v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc] for c < ncols, 1 for c == ncols if with_ones.
+hipError_t launch_vprep(bool bf16, const void* v, long long sp, long long sc, long long bh_stride, int ncols,
+                        bool with_ones, int BH, int n, int N, float* colmax, float2* vsc, hipStream_t st);
+hipError_t launch_conv(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
+                       const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
+                       int cols, int m, hipStream_t st);
+hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, int m, int N, int pairs,
+                       int ksplit, hipStream_t st);
+hipError_t launch_combine(const float* part, const float* phiq, const float* X2, const float* colmax,
+                          const float2* hnorm, float* z, unsigned* fix, int BH, int H, int n, int l2, int d, int m,
+                          int ksplit, hipStream_t st);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
                         float* z, const unsigned* fix, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
-hipError_t launch_toeplitz(int l2, const float* a, float* y, const float2* Hs, const float2* tw, int BH, int H,
-                           int C, int n, hipStream_t st);
+hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
+hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st);
 
 }  // namespace krpe

@@ -55,7 +55,7 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_feature_map.restype = i
     lib.krpe_feature_map.argtypes = [vp, i, fp, fp, i, i, i, i, i, vp]
     lib.krpe_toeplitz_conv_workspace.restype = sz
-    lib.krpe_toeplitz_conv_workspace.argtypes = [i, i]
+    lib.krpe_toeplitz_conv_workspace.argtypes = [i, i, i, i]
     lib.krpe_toeplitz_conv.restype = i
     lib.krpe_toeplitz_conv.argtypes = [fp, fp, fp, i, i, i, i, vp, sz, vp]
     lib.krpe_attention_fwd_workspace.restype = sz
@@ -120,8 +120,8 @@ def feature_map(x: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
     return phi
 
 
-def toeplitz_conv_workspace(H: int, n: int) -> int:
-    return int(load().krpe_toeplitz_conv_workspace(H, n))
+def toeplitz_conv_workspace(B: int, H: int, C: int, n: int) -> int:
+    return int(load().krpe_toeplitz_conv_workspace(B, H, C, n))
 
 
 def toeplitz_conv(b: torch.Tensor, a: torch.Tensor) -> torch.Tensor:
@@ -135,7 +135,7 @@ def toeplitz_conv(b: torch.Tensor, a: torch.Tensor) -> torch.Tensor:
     if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32 or a.dtype != torch.float32:
         raise KrpeError("b must be float32 [H, 2n-1] and a float32 [B,H,C,n]")
     y = torch.empty_like(a)
-    wsb = lib.krpe_toeplitz_conv_workspace(H, n)
+    wsb = lib.krpe_toeplitz_conv_workspace(B, H, C, n)
     ws = torch.empty(max(int(wsb), 1), dtype=torch.uint8, device=a.device)
     st = lib.krpe_toeplitz_conv(_ptr(b), _ptr(a), _ptr(y), B, H, C, n, ws.data_ptr(), ws.numel(),
                                 _stream(a.device))

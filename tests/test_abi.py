@@ -49,7 +49,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.krpe_abi_version() == 1
+    assert lib.krpe_abi_version() == 2
     for s in range(9):
         assert lib.krpe_status_str(s)
     assert lib.krpe_status_str(99) == b"unknown status"
@@ -74,8 +74,9 @@ def test_workspace_queries(lib):
     assert lib.krpe_attention_fwd_workspace(1, 1, 0, 4, 4) == 0
     assert lib.krpe_attention_fwd_workspace(1, 1, 16385, 4, 4) == 0
     assert lib.krpe_attention_fwd_workspace(1, 1, 8, 129, 4) == 0
-    assert lib.krpe_toeplitz_conv_workspace(2, 100) > 0
-    assert lib.krpe_toeplitz_conv_workspace(2, 0) == 0
+    assert lib.krpe_toeplitz_conv_workspace(1, 2, 3, 100) > 0
+    assert lib.krpe_toeplitz_conv_workspace(1, 2, 3, 0) == 0
+    assert lib.krpe_toeplitz_conv_workspace(2, 2, 3, 100) > lib.krpe_toeplitz_conv_workspace(1, 2, 3, 100)
     # workspace covers phi(q), phi(k) in fp32 at least
     assert lib.krpe_attention_fwd_workspace(8, 12, 4096, 64, 128) >= 2 * 8 * 12 * 4096 * 128 * 4
 
@@ -102,7 +103,7 @@ def test_attention_validation(lib):
 
 
 def test_toeplitz_validation(lib):
-    ws = lib.krpe_toeplitz_conv_workspace(2, 10)
+    ws = lib.krpe_toeplitz_conv_workspace(1, 2, 3, 10)
     call = lambda b=BB, a=Q, y=Z, B=1, H=2, C=3, n=10, w=WSP, wb=ws: lib.krpe_toeplitz_conv(
         b, a, y, B, H, C, n, w, wb, None)
     assert call(a=None) == NULL
