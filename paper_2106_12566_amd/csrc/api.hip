@@ -89,7 +89,9 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.phik = take(bh * m * N * sizeof(float));
   L.vsc = take(bh * pairs * N * sizeof(float2));
   L.colmax = take(bh * cols * sizeof(float));
+  L.vmax = take(bh * vmax_chunks(n) * static_cast<size_t>(d) * sizeof(float));
   L.x2 = take(bh * L.ksplit * m * pairs * sizeof(float));
+  L.wb = take(bh * (static_cast<size_t>(m) + 1) * sizeof(float2));
   L.part = take(bh * conv_splits(L.l2) * cols * n * sizeof(float));
   L.fix = take((bh + 1 + bh * n) * sizeof(unsigned));
   L.total = off;
@@ -113,6 +115,7 @@ ConvLayout conv_layout(int B, int H, int C, int n) {
   L.ones = take(N * sizeof(float));
   L.vsc = take(bh * pairs * N * sizeof(float2));
   L.colmax = take(bh * C * sizeof(float));
+  L.vmax = take(bh * vmax_chunks(n) * static_cast<size_t>(C) * sizeof(float));
   L.part = take(conv_splits(L.l2) > 1 ? bh * conv_splits(L.l2) * C * n * sizeof(float) : 0);
   L.total = off;
   return L;
@@ -196,6 +199,7 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
   float* ones = reinterpret_cast<float*>(w + L.ones);
   float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
   float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* vmax = reinterpret_cast<float*>(w + L.vmax);
   float* part = reinterpret_cast<float*>(w + L.part);
   const int BHi = static_cast<int>(bh);
   const int N = 1 << L.l2;
@@ -206,7 +210,7 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
   if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch")) return s;
   if (krpe_status_t s = hip_check(launch_ones(ones, n, N, st), "ones launch")) return s;
   if (krpe_status_t s = hip_check(launch_vprep(false, a, 1, n, static_cast<long long>(C) * n, C, false, BHi, n, N,
-                                               colmax, vsc, st),
+                                               vmax, colmax, vsc, st),
                                   "column launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_conv(L.l2, ones, ones, 0, vsc, colmax, Hs, tw, splits > 1 ? part : y, BHi,
@@ -258,7 +262,9 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   float* phik = reinterpret_cast<float*>(w + L.phik);
   float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
   float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* vmax = reinterpret_cast<float*>(w + L.vmax);
   float* x2 = reinterpret_cast<float*>(w + L.x2);
+  float2* wb = reinterpret_cast<float2*>(w + L.wb);
   float* part = reinterpret_cast<float*>(w + L.part);
   unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
   const int BHi = static_cast<int>(bh);
@@ -274,7 +280,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                                   "feature map launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_vprep(bf16, v, d, 1, static_cast<long long>(n) * d, d, true, BHi, n, N,
-                                               colmax, vsc, st),
+                                               vmax, colmax, vsc, st),
                                   "column launch"))
     return s;
   if (krpe_status_t s = record(events, 2, st)) return s;
@@ -285,8 +291,9 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   if (krpe_status_t s = record(events, 3, st)) return s;
   if (krpe_status_t s = hip_check(launch_gram(phik, vsc, x2, BHi, m, N, pairs, L.ksplit, st), "norm launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, phiq, x2, colmax, hnorm, z, fix, BHi, H, n, L.l2, d, m,
-                                                 L.ksplit, st),
+  if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, m, d, L.ksplit, st), "bound launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, BHi, H, n, L.l2, d, m, st),
                                   "combine launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, BHi, H, n, N, d, m, st),

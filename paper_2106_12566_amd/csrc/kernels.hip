@@ -213,58 +213,103 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
   }
 }
 
-// ------------------------------------------------------ value columns --
-// Column c of v' (value columns, plus an all-ones column when with_ones: the
-// denominator's channel A2 of Eq. (11)) is scaled by its max |.| and packed
-// with its neighbour as one complex signal per pair p = c / 2:
-//   vsc[bh][p][pos] = (v'_{2p}(pos) / s_{2p}, v'_{2p+1}(pos) / s_{2p+1}),  0 beyond n,
-//   colmax[bh][c] = s_c.
-// v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc].  Block (bh, pb) handles
-// columns 16 pb .. 16 pb + 15.
+// ------------------------------------------------------------ v prep --
+// The value columns v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc]
+// (c < ncols; column ncols is all ones when with_ones: the denominator's
+// channel A2 of Eq. (11)), scaled per column by
+// s_c = max_pos |v'(pos, c)| and packed as column pairs:
+//   vsc[bh][p][pos] = (v'(pos, 2p) / s_2p, v'(pos, 2p+1) / s_2p+1)  for pos < n,
+//   0 for n <= pos < N;  colmax[bh][c] = s_c.
+// Two passes, both reading v along its contiguous index (columns when
+// sc == 1, positions otherwise): k_vmax takes per-chunk column maxima of
+// 256 positions x 64 columns, k_vscale reduces them and writes 64 positions x
+// 32 pairs per block through an LDS transpose.
+constexpr int kVmaxChunk = 256;
+
 template <typename TV>
-__global__ __launch_bounds__(256) void k_vprep(const TV* __restrict__ v, long long sp, long long sc,
-                                               long long bh_stride, int ncols, int with_ones, int n, int N,
-                                               float* __restrict__ colmax, float2* __restrict__ vsc, int pblocks) {
-  __shared__ float part_max[16][17];
-  __shared__ float smax[16];
-  const int bh = blockIdx.x / pblocks, pb = blockIdx.x % pblocks;
+__global__ __launch_bounds__(256) void k_vmax(const TV* __restrict__ v, long long sp, long long sc,
+                                              long long bh_stride, int ncols, int n, int nchunk, int cgroups,
+                                              float* __restrict__ pmax) {
+  __shared__ unsigned cm[64];
+  int bid = blockIdx.x;
+  const int cg = bid % cgroups;
+  bid /= cgroups;
+  const int ch = bid % nchunk, bh = bid / nchunk;
+  const TV* __restrict__ vb = v + bh * bh_stride;
+  const int tid = threadIdx.x;
+  const int c0 = cg * 64, nc = min(64, ncols - c0);
+  const int pos0 = ch * kVmaxChunk, np = min(kVmaxChunk, n - pos0);
+  if (tid < 64) cm[tid] = 0u;
+  __syncthreads();
+  const int total = np * nc;
+  for (int e = tid; e < total; e += 256) {
+    int r, c;
+    if (sc == 1) {
+      r = e / nc;
+      c = e - r * nc;
+    } else {
+      c = e / np;
+      r = e - c * np;
+    }
+    const float x = fabsf(to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]));
+    atomicMax(&cm[c], __float_as_uint(x));  // x >= 0: bit patterns order like the values
+  }
+  __syncthreads();
+  if (tid < nc) pmax[(static_cast<size_t>(bh) * nchunk + ch) * ncols + c0 + tid] = __uint_as_float(cm[tid]);
+}
+
+template <typename TV>
+__global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long long sp, long long sc,
+                                                long long bh_stride, int ncols, int with_ones, int n, int N,
+                                                int nchunk, int cgroups, const float* __restrict__ pmax,
+                                                float* __restrict__ colmax, float2* __restrict__ vsc) {
+  __shared__ float tile[64][65];  // [column][position]
+  __shared__ float scale[64];
+  int bid = blockIdx.x;
+  const int cg = bid % cgroups;
+  bid /= cgroups;
+  const int ptiles = (N + 63) / 64;
+  const int pt = bid % ptiles, bh = bid / ptiles;
   const int cols = ncols + with_ones, pairs = (cols + 1) / 2;
   const TV* __restrict__ vb = v + bh * bh_stride;
   const int tid = threadIdx.x;
-  {
-    const int c = pb * 16 + (tid & 15), lane_row = tid >> 4;
-    float mx = 0.f;
+  const int c0 = cg * 64, nc = min(64, cols - c0);
+  const int pos0 = pt * 64;
+  if (tid < nc) {
+    const int c = c0 + tid;
+    float sv = 1.f;  // the ones column
     if (c < ncols) {
-      for (int pos = lane_row; pos < n; pos += 16) mx = fmaxf(mx, fabsf(to_f32(vb[pos * sp + c * sc])));
-    } else if (c < cols) {
-      mx = 1.f;
+      sv = 0.f;
+      for (int ch = 0; ch < nchunk; ++ch) sv = fmaxf(sv, pmax[(static_cast<size_t>(bh) * nchunk + ch) * ncols + c]);
     }
-    part_max[lane_row][tid & 15] = mx;
+    if (pt == 0) colmax[static_cast<size_t>(bh) * cols + c] = sv;
+    scale[tid] = sv > 0.f ? sv : 1.f;
+  }
+  const int np = max(0, min(64, n - pos0));
+  const int nv = max(0, min(nc, ncols - c0));  // value columns of this group
+  const int total = np * nv;
+  for (int e = tid; e < total; e += 256) {
+    int r, c;
+    if (sc == 1) {
+      r = e / nv;
+      c = e - r * nv;
+    } else {
+      c = e / np;
+      r = e - c * np;
+    }
+    tile[c][r] = to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]);
   }
   __syncthreads();
-  if (tid < 16) {
-    float mx = 0.f;
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, part_max[r][tid]);
-    smax[tid] = mx;
-    const int c = pb * 16 + tid;
-    if (c < cols) colmax[static_cast<size_t>(bh) * cols + c] = mx;
-  }
-  __syncthreads();
-  for (int pl = 0; pl < 8; ++pl) {
-    const int p = pb * 8 + pl;
-    if (p >= pairs) break;
-    const int ca = 2 * p, cb = 2 * p + 1;
-    const float sa = smax[2 * pl] > 0.f ? smax[2 * pl] : 1.f;
-    const float sb = smax[2 * pl + 1] > 0.f ? smax[2 * pl + 1] : 1.f;
-    float2* __restrict__ out = vsc + (static_cast<size_t>(bh) * pairs + p) * N;
-    for (int pos = tid; pos < N; pos += 256) {
-      float a = 0.f, b2 = 0.f;
-      if (pos < n) {
-        a = ca < ncols ? to_f32(vb[pos * sp + ca * sc]) : (ca < cols ? 1.f : 0.f);
-        b2 = cb < ncols ? to_f32(vb[pos * sp + cb * sc]) : (cb < cols ? 1.f : 0.f);
-      }
-      out[pos] = make_float2(a / sa, b2 / sb);
+  const int npairs = (nc + 1) / 2;
+  for (int e = tid; e < npairs * 64; e += 256) {
+    const int pl = e >> 6, r = e & 63;
+    const int ca = 2 * pl, cb = 2 * pl + 1;
+    float a = 0.f, b2 = 0.f;
+    if (r < np) {
+      a = ca < nv ? tile[ca][r] / scale[ca] : (ca < nc ? 1.f : 0.f);
+      b2 = cb < nv ? tile[cb][r] / scale[cb] : (cb < nc ? 1.f : 0.f);
     }
+    if (pos0 + r < N) vsc[(static_cast<size_t>(bh) * pairs + c0 / 2 + pl) * N + pos0 + r] = make_float2(a, b2);
   }
 }
 
@@ -528,33 +573,42 @@ __global__ __launch_bounds__(Conf<L2>::THREADS) void k_conv_contract(
 // X2[bh][ks][l][p] = sum over positions of slice ks of phi_l(k_j)^2 |vsc_p(j)|^2
 // = ||x_{l,p}||^2 restricted to the slice, x_{l,p} the packed signal the
 // convolution kernel transforms for feature l and column pair p.  Block
-// (bh, l-tile of 64, slice ks); threads own a feature and every 4th pair.
+// (bh, l-tile of 64, slice ks), positions staged through LDS 64 at a time;
+// thread t accumulates a 4 x kGramPK register tile: features 4 (t % 16) + j
+// and pairs t / 16 + 16 k.
 constexpr int kMaxPairs = (kMaxD + 2) / 2;
-constexpr int kPairSlots = (kMaxPairs + 3) / 4;
+constexpr int kGramPK = (kMaxPairs + 15) / 16;
 
 __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, const float2* __restrict__ vsc,
                                               float* __restrict__ X2, int m, int N, int pairs, int ltiles,
                                               int ksplit) {
-  __shared__ float A[64][65];
-  __shared__ float Bq[64][kMaxPairs + 1];
+  __shared__ float4 A4[64][17];           // phi^2, [position][feature quad]
+  __shared__ float Bq[64][kMaxPairs | 1];  // |vsc|^2, [position][pair]
   int bid = blockIdx.x;
   const int ks = bid % ksplit;
   bid /= ksplit;
   const int lt = bid % ltiles, bh = bid / ltiles;
-  const int tid = threadIdx.x, li = tid & 63, pg = tid >> 6;
+  const int tid = threadIdx.x, lg = tid & 15, pg = tid >> 4;
+  const int l0 = lt * 64;
   const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * N;
   const float2* __restrict__ vb = vsc + static_cast<size_t>(bh) * pairs * N;
   const int slice = N / ksplit, pos_begin = ks * slice, pos_end = pos_begin + slice;
-  float acc[kPairSlots];
+  float acc[kGramPK][4];
 #pragma unroll
-  for (int k = 0; k < kPairSlots; ++k) acc[k] = 0.f;
+  for (int k = 0; k < kGramPK; ++k)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[k][j] = 0.f;
   for (int p0 = pos_begin; p0 < pos_end; p0 += 64) {
     __syncthreads();
-    for (int e = tid; e < 64 * 64; e += 256) {
-      const int r = e >> 6, x = e & 63;
-      const int l = lt * 64 + r;
-      const float a = (l < m && p0 + x < pos_end) ? pk[static_cast<size_t>(l) * N + p0 + x] : 0.f;
-      A[r][x] = a * a;
+    for (int e = tid; e < 64 * 16; e += 256) {
+      const int x = e & 63, q = e >> 6;
+      float a[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int l = l0 + 4 * q + j;
+        a[j] = (l < m && p0 + x < pos_end) ? pk[static_cast<size_t>(l) * N + p0 + x] : 0.f;
+      }
+      A4[x][q] = make_float4(a[0] * a[0], a[1] * a[1], a[2] * a[2], a[3] * a[3]);
     }
     for (int e = tid; e < 64 * pairs; e += 256) {
       const int p = e >> 6, x = e & 63;
@@ -566,49 +620,90 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
       Bq[x][p] = q2;
     }
     __syncthreads();
+#pragma unroll 4
     for (int x = 0; x < 64; ++x) {
-      const float a = A[li][x];
+      const float4 a = A4[x][lg];
 #pragma unroll
-      for (int k = 0; k < kPairSlots; ++k) {
-        const int p = pg + 4 * k;
-        if (p < pairs) acc[k] = fmaf(a, Bq[x][p], acc[k]);
+      for (int k = 0; k < kGramPK; ++k) {
+        const int p = pg + 16 * k;
+        if (p < pairs) {
+          const float bq = Bq[x][p];
+          acc[k][0] = fmaf(a.x, bq, acc[k][0]);
+          acc[k][1] = fmaf(a.y, bq, acc[k][1]);
+          acc[k][2] = fmaf(a.z, bq, acc[k][2]);
+          acc[k][3] = fmaf(a.w, bq, acc[k][3]);
+        }
       }
     }
   }
-  const int l = lt * 64 + li;
-  if (l < m) {
-    float* __restrict__ out = X2 + ((static_cast<size_t>(bh) * ksplit + ks) * m + l) * pairs;
+  float* __restrict__ out = X2 + (static_cast<size_t>(bh) * ksplit + ks) * m * pairs;
 #pragma unroll
-    for (int k = 0; k < kPairSlots; ++k) {
-      const int p = pg + 4 * k;
-      if (p < pairs) out[p] = acc[k];
+  for (int j = 0; j < 4; ++j) {
+    const int l = l0 + 4 * lg + j;
+    if (l < m) {
+#pragma unroll
+      for (int k = 0; k < kGramPK; ++k) {
+        const int p = pg + 16 * k;
+        if (p < pairs) out[static_cast<size_t>(l) * pairs + p] = acc[k][j];
+      }
     }
   }
+}
+
+// Bound weights of k_combine, per (bh, feature l):
+//   Wb[bh][l] = (A_l, D_l),  A_l = max_{c < d} s_c ||x_{l,c/2}||,  D_l = ||x_{l,d/2}||
+// (column d is the all-ones column of the denominator, scale 1), and
+//   Wb[bh][m] = (max_{c < d} s_c, 0).
+__global__ __launch_bounds__(256) void k_bound_weights(const float* __restrict__ X2, const float* __restrict__ colmax,
+                                                       float2* __restrict__ Wb, int BH, int m, int d, int pairs,
+                                                       int ksplit) {
+  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e >= static_cast<long long>(BH) * (m + 1)) return;
+  const int bh = static_cast<int>(e / (m + 1)), l = static_cast<int>(e % (m + 1));
+  const float* __restrict__ s = colmax + static_cast<size_t>(bh) * (d + 1);
+  if (l == m) {
+    float smax = 0.f;
+    for (int c = 0; c < d; ++c) smax = fmaxf(smax, s[c]);
+    Wb[e] = make_float2(smax, 0.f);
+    return;
+  }
+  float A = 0.f, D = 0.f;
+  for (int p = 0; p < pairs; ++p) {
+    float x2 = 0.f;
+    for (int ks = 0; ks < ksplit; ++ks) x2 += X2[((static_cast<size_t>(bh) * ksplit + ks) * m + l) * pairs + p];
+    const float nrm = sqrtf(x2);
+    const int c0 = 2 * p, c1 = 2 * p + 1;
+    if (c0 < d) A = fmaxf(A, nrm * s[c0]);
+    if (c1 < d) A = fmaxf(A, nrm * s[c1]);
+    if (c0 == d || c1 == d) D = nrm;
+  }
+  Wb[e] = make_float2(A, D);
 }
 
 // -------------------------------------------------------------- combine --
 // z[bh][i][c] = sum_s P_s[c][i] / sum_s P_s[d][i],  P = part[bh], s < nsplit,
 // and the certification of each row.  With K = kGamma u log2(L) ||h||_2 / sqrt(L)
-// and the bound weights B_p(i) = sum_l phi_l(q_i) ||x_{l,p}||_2, the error
-// model of common.hpp bounds the rounding error of numerator c by
-// K B_{c/2}(i) s_c (+ a part relative to the value itself) and that of the
-// denominator by K B_{d/2}(i).  A row whose normwise relative bound exceeds
-// kTau is queued for k_fixup.
+// the error model of common.hpp bounds the rounding error of numerator c by
+// K s_c sum_l phi_l(q_i) ||x_{l,c/2}||_2 <= K sum_l phi_l(q_i) A_l (+ a part
+// relative to the value itself) and that of the denominator by
+// K sum_l phi_l(q_i) D_l (weights of k_bound_weights).  A row whose normwise
+// relative bound exceeds kTau is queued for k_fixup.  Block: 64 rows of one
+// (batch, head); dynamic LDS holds the (d + 1) x 64 tile of sums and the
+// m + 1 weights.
 __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part, const float* __restrict__ phiq,
-                                                 const float* __restrict__ X2, const float* __restrict__ colmax,
-                                                 const float2* __restrict__ hnorm, float* __restrict__ z,
-                                                 unsigned* __restrict__ fix, int BH, int H, int n, int N,
-                                                 int log2N, int d, int m, int nsplit, int ksplit, int tiles_n) {
-  __shared__ float tile[kMaxD + 1][65];
-  __shared__ float qc[64][65];
-  __shared__ float xc[64][kMaxPairs + 1];
-  __shared__ float btile[kMaxPairs][65];
-  __shared__ float scol[kMaxD + 1];
-  __shared__ float zmax[64];
+                                                 const float2* __restrict__ Wb, const float2* __restrict__ hnorm,
+                                                 float* __restrict__ z, unsigned* __restrict__ fix, int BH, int H,
+                                                 int n, int N, int log2N, int d, int m, int nsplit, int tiles_n) {
+  extern __shared__ float dyn[];
+  const int cols = d + 1;
+  float* tile = dyn;                                                  // [cols][65]
+  float2* wl = reinterpret_cast<float2*>(dyn + ((cols * 65 + 1) & ~1));  // [m + 1]
+  __shared__ float2 bsum[4][64];
+  __shared__ float zpart[4][64];
+  __shared__ float rden[64];
   const int bh = blockIdx.x / tiles_n, i0 = (blockIdx.x % tiles_n) * 64;
   const int h = bh % H;
-  const int cols = d + 1, pairs = (cols + 1) / 2;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, li = tid & 63, qg = tid >> 6;
   const float* __restrict__ p0 = part + static_cast<size_t>(bh) * nsplit * cols * n;
   for (int e = tid; e < cols * 64; e += 256) {
     const int c = e >> 6, i = e & 63;
@@ -618,76 +713,50 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
       t = p0[static_cast<size_t>(c) * n + pos];
       for (int sp = 1; sp < nsplit; ++sp) t += p0[(static_cast<size_t>(sp) * cols + c) * n + pos];
     }
-    tile[c][i] = t;
+    tile[c * 65 + i] = t;
   }
-  for (int c = tid; c < cols; c += 256) scol[c] = colmax[static_cast<size_t>(bh) * cols + c];
-  // bound weights for the 64 rows: thread (row li, pairs pg + 4k)
-  const int li = tid & 63, pg = tid >> 6;
-  float bacc[kPairSlots];
-#pragma unroll
-  for (int k = 0; k < kPairSlots; ++k) bacc[k] = 0.f;
-  const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * N;
-  const float* __restrict__ xb = X2 + static_cast<size_t>(bh) * ksplit * m * pairs;
-  for (int l0 = 0; l0 < m; l0 += 64) {
-    __syncthreads();
-    for (int e = tid; e < 64 * 64; e += 256) {
-      const int r = e >> 6, x = e & 63;
-      qc[r][x] = (l0 + r < m && i0 + x < n) ? pq[static_cast<size_t>(l0 + r) * N + i0 + x] : 0.f;
-    }
-    for (int e = tid; e < 64 * pairs; e += 256) {
-      const int r = e / pairs, p = e % pairs;
-      float s2 = 0.f;
-      if (l0 + r < m)
-        for (int ks = 0; ks < ksplit; ++ks) s2 += xb[(static_cast<size_t>(ks) * m + l0 + r) * pairs + p];
-      xc[r][p] = sqrtf(s2);
-    }
-    __syncthreads();
-    const int lmax = min(64, m - l0);
-    for (int r = 0; r < lmax; ++r) {
-      const float q = qc[r][li];
-#pragma unroll
-      for (int k = 0; k < kPairSlots; ++k) {
-        const int p = pg + 4 * k;
-        if (p < pairs) bacc[k] = fmaf(q, xc[r][p], bacc[k]);
+  for (int l = tid; l <= m; l += 256) wl[l] = Wb[static_cast<size_t>(bh) * (m + 1) + l];
+  __syncthreads();
+  // bound sums (features qg, qg + 4, ...) and the largest numerator magnitude
+  // (columns qg, qg + 4, ...) of row li
+  {
+    const int pos = i0 + li;
+    float bA = 0.f, bD = 0.f;
+    if (pos < n) {
+      const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * N + pos;
+      for (int l = qg; l < m; l += 4) {
+        const float f = pq[static_cast<size_t>(l) * N];
+        const float2 w = wl[l];
+        bA = fmaf(f, w.x, bA);
+        bD = fmaf(f, w.y, bD);
       }
     }
-  }
-#pragma unroll
-  for (int k = 0; k < kPairSlots; ++k) {
-    const int p = pg + 4 * k;
-    if (p < pairs) btile[p][li] = bacc[k];
-  }
-  __syncthreads();
-  if (tid < 64) {
-    const int i = tid;
     float zm = 0.f;
-    const float den = tile[d][i];
-    for (int c = 0; c < d; ++c) zm = fmaxf(zm, fabsf(tile[c][i] / den));
-    zmax[i] = zm;
+    for (int c = qg; c < d; c += 4) zm = fmaxf(zm, fabsf(tile[c * 65 + li]));
+    bsum[qg][li] = make_float2(bA, bD);
+    zpart[qg][li] = zm;
   }
   __syncthreads();
-  float* __restrict__ zb = z + static_cast<size_t>(bh) * n * d;
-  for (int e = tid; e < 64 * d; e += 256) {
-    const int i = e / d, c = e % d;
-    const int pos = i0 + i;
-    if (pos < n) zb[static_cast<size_t>(pos) * d + c] = tile[c][i] / tile[d][i];
-  }
   if (tid < 64) {
     const int i = tid, pos = i0 + i;
+    const float den = tile[d * 65 + i];
+    const float inv = 1.0f / den;
+    rden[i] = inv;
     bool flag = false;
     if (pos < n) {
       const float L = static_cast<float>(2 << log2N);
       const float lg = static_cast<float>(log2N + 1);
       const float K = kGamma * kUnitRoundoff * lg * hnorm[h].y * rsqrtf(L);
-      float errN = 0.f, vmax = 0.f;
-      for (int c = 0; c < d; ++c) {
-        errN = fmaxf(errN, btile[c >> 1][i] * scol[c]);
-        vmax = fmaxf(vmax, scol[c]);
+      float bA = 0.f, bD = 0.f, num = 0.f;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        bA += bsum[g][i].x;
+        bD += bsum[g][i].y;
+        num = fmaxf(num, zpart[g][i]);
       }
-      const float den = tile[d][i];
-      const float zm = zmax[i];
-      const float errD = K * btile[d >> 1][i];
-      const float err = K * errN + zm * errD;
+      const float zm = num * inv;  // max_c |z_c| when den > 0
+      const float vmax = wl[m].x;
+      const float err = K * bA + zm * (K * bD);
       const float scale = fmaxf(zm, 1e-6f * vmax);
       const float rel_floor = 2.f * kGamma * kUnitRoundoff * lg;
       const bool ok = isfinite(den) && den > 0.f && isfinite(zm) && err <= (kTau - rel_floor) * scale * den;
@@ -710,6 +779,13 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
         fix[BH + 1 + static_cast<size_t>(bh) * n + base + rank] = static_cast<unsigned>(pos);
       }
     }
+  }
+  __syncthreads();
+  float* __restrict__ zb = z + static_cast<size_t>(bh) * n * d;
+  for (int e = tid; e < 64 * d; e += 256) {
+    const int i = e / d, c = e - i * d;
+    const int pos = i0 + i;
+    if (pos < n) zb[static_cast<size_t>(pos) * d + c] = tile[c * 65 + i] * rden[i];
   }
 }
 
@@ -1025,18 +1101,33 @@ hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const f
 }
 
 hipError_t launch_vprep(bool bf16, const void* v, long long sp, long long sc, long long bh_stride, int ncols,
-                        bool with_ones, int BH, int n, int N, float* colmax, float2* vsc, hipStream_t st) {
+                        bool with_ones, int BH, int n, int N, float* pmax, float* colmax, float2* vsc,
+                        hipStream_t st) {
   const int cols = ncols + (with_ones ? 1 : 0);
-  const int pblocks = (cols + 15) / 16;
-  const dim3 grid(static_cast<unsigned>(static_cast<long long>(BH) * pblocks)), block(256);
-  if (bf16)
-    hipLaunchKernelGGL(k_vprep<uint16_t>, grid, block, 0, st, static_cast<const uint16_t*>(v), sp, sc, bh_stride,
-                       ncols, with_ones ? 1 : 0, n, N, colmax, vsc, pblocks);
-  else
-    hipLaunchKernelGGL(k_vprep<float>, grid, block, 0, st, static_cast<const float*>(v), sp, sc, bh_stride, ncols,
-                       with_ones ? 1 : 0, n, N, colmax, vsc, pblocks);
+  const int nchunk = vmax_chunks(n);
+  const int vgroups = (ncols + 63) / 64, sgroups = (cols + 63) / 64;
+  const dim3 block(256);
+  const dim3 grid_max(static_cast<unsigned>(static_cast<long long>(BH) * nchunk * vgroups));
+  const dim3 grid_scale(static_cast<unsigned>(static_cast<long long>(BH) * ((N + 63) / 64) * sgroups));
+  if (bf16) {
+    const uint16_t* vv = static_cast<const uint16_t*>(v);
+    if (ncols > 0)
+      hipLaunchKernelGGL(k_vmax<uint16_t>, grid_max, block, 0, st, vv, sp, sc, bh_stride, ncols, n, nchunk, vgroups,
+                         pmax);
+    hipLaunchKernelGGL(k_vscale<uint16_t>, grid_scale, block, 0, st, vv, sp, sc, bh_stride, ncols,
+                       with_ones ? 1 : 0, n, N, nchunk, sgroups, pmax, colmax, vsc);
+  } else {
+    const float* vv = static_cast<const float*>(v);
+    if (ncols > 0)
+      hipLaunchKernelGGL(k_vmax<float>, grid_max, block, 0, st, vv, sp, sc, bh_stride, ncols, n, nchunk, vgroups,
+                         pmax);
+    hipLaunchKernelGGL(k_vscale<float>, grid_scale, block, 0, st, vv, sp, sc, bh_stride, ncols, with_ones ? 1 : 0, n,
+                       N, nchunk, sgroups, pmax, colmax, vsc);
+  }
   return hipGetLastError();
 }
+
+int vmax_chunks(int n) { return (n + kVmaxChunk - 1) / kVmaxChunk; }
 
 hipError_t launch_conv(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
                        const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
@@ -1053,13 +1144,21 @@ hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, 
   return hipGetLastError();
 }
 
-hipError_t launch_combine(const float* part, const float* phiq, const float* X2, const float* colmax,
-                          const float2* hnorm, float* z, unsigned* fix, int BH, int H, int n, int l2, int d, int m,
-                          int ksplit, hipStream_t st) {
+hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb, int BH, int m, int d,
+                                int ksplit, hipStream_t st) {
+  const long long total = static_cast<long long>(BH) * (m + 1);
+  hipLaunchKernelGGL(k_bound_weights, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, st, X2, colmax,
+                     Wb, BH, m, d, (d + 2) / 2, ksplit);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
+                          unsigned* fix, int BH, int H, int n, int l2, int d, int m, hipStream_t st) {
   const int tiles_n = (n + 63) / 64;
-  hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), 0, st,
-                     part, phiq, X2, colmax, hnorm, z, fix, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2), ksplit,
-                     tiles_n);
+  const size_t lds = (static_cast<size_t>((d + 1) * 65 + 1) & ~static_cast<size_t>(1)) * sizeof(float) +
+                     static_cast<size_t>(m + 1) * sizeof(float2);
+  hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), lds, st,
+                     part, phiq, Wb, hnorm, z, fix, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2), tiles_n);
   return hipGetLastError();
 }
 

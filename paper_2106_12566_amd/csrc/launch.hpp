@@ -19,7 +19,9 @@ struct AttnLayout {
   size_t phik;       // float  [BH][m][N]        phi(k)
   size_t vsc;        // float2 [BH][pairs][N]    scaled column pairs of v' = [v, 1]
   size_t colmax;     // float  [BH][d+1]         column scales of v'
+  size_t vmax;       // float  [BH][chunks][d]   column maxima per chunk of positions
   size_t x2;         // float  [BH][ks][m][pairs] squared norms of the packed channels
+  size_t wb;         // float2 [BH][m+1]         bound weights of the certification
   size_t part;       // float  [BH][splits][d+1][n] numerators / denominator per class split
   size_t fix;        // uint   [BH + 1 + BH n]   rows queued per head, total; then the
                      //                          queued row indices of each head
@@ -30,7 +32,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m);
 // Workspace of krpe_toeplitz_conv.
 struct ConvLayout {
   int l2;
-  size_t tw, hs, ones, vsc, colmax, part, total;
+  size_t tw, hs, ones, vsc, colmax, vmax, part, total;
 };
 ConvLayout conv_layout(int B, int H, int C, int n);
 
@@ -46,17 +48,22 @@ hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs,
 hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const float* W, float* phi0,
                               float* phi1, int nsrc, bool feature_major, int ld, int BH, int H, int n, int d,
                               int m, unsigned* fix_counts, hipStream_t st);
-// v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc] for c < ncols, 1 for c == ncols if with_ones.
+// v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc] for c < ncols, 1 for c == ncols if with_ones;
+// pmax: scratch of BH * vmax_chunks(n) * ncols floats.
+int vmax_chunks(int n);
 hipError_t launch_vprep(bool bf16, const void* v, long long sp, long long sc, long long bh_stride, int ncols,
-                        bool with_ones, int BH, int n, int N, float* colmax, float2* vsc, hipStream_t st);
+                        bool with_ones, int BH, int n, int N, float* pmax, float* colmax, float2* vsc,
+                        hipStream_t st);
 hipError_t launch_conv(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
                        const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
                        int cols, int m, hipStream_t st);
 hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, int m, int N, int pairs,
                        int ksplit, hipStream_t st);
-hipError_t launch_combine(const float* part, const float* phiq, const float* X2, const float* colmax,
-                          const float2* hnorm, float* z, unsigned* fix, int BH, int H, int n, int l2, int d, int m,
-                          int ksplit, hipStream_t st);
+// Wb[bh][l] = (A_l, D_l) for l < m, Wb[bh][m] = (max column scale, 0) from the channel norms.
+hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb, int BH, int m, int d, int ksplit,
+                                hipStream_t st);
+hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
+                          unsigned* fix, int BH, int H, int n, int l2, int d, int m, hipStream_t st);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
                         float* z, const unsigned* fix, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
