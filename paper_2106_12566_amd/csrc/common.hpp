@@ -40,13 +40,18 @@ struct Conf {
   static constexpr int THREADS = G * F::T;
   static constexpr int WAVES = (THREADS + 63) / 64;
   static constexpr int LDS_SLOTS = F::P > 1 ? G * F::LDS : 1;
-  static constexpr int KH = (F::T <= 256 && F::R <= 16 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
+  // Two work-groups per CU (register budget 256 per thread) for the
+  // mid-size transforms: one runs while the other waits at a barrier.
+  static constexpr int WPE = (L2 >= 9 && L2 <= 12) ? 2 : 1;
+  static constexpr int KH =
+      (WPE == 1 && F::T <= 256 && F::R <= 16 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
   static constexpr int HSPLIT = S / KH;  // work units per column pair and head
   static constexpr int CONV_LDS_SLOTS = F::P > 1 ? G * KH * F::LDS : 1;
-  // Per-position values (v pairs, twists, prefetched phi), the spectrum and
-  // the hoisted twiddles stay in registers only for work-groups of <= 256
+  // Per-position values (v pairs, prefetched phi), the spectrum and the
+  // hoisted twiddles stay in registers only for work-groups of <= 256
   // threads (512 registers per thread); larger ones re-read them.
   static constexpr bool VREG = THREADS <= 256 && FOLD == 1;
+  static constexpr bool PREF = VREG && WPE == 1;
   static constexpr bool HREG = THREADS <= 256;
   static constexpr bool HOIST = THREADS <= 256 && FOLD == 1;
 };

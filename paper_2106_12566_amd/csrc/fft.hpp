@@ -200,9 +200,11 @@ struct Fft {
   // in LDS region lds + k * LDS): read (p > 0), DFT, twiddle, write (p < P-1).
   // The K transforms share the barriers, and their independent instruction
   // streams interleave.
-  template <int p, int K>
+  // W0: pass 0 takes its twiddles for every s (s = 0 included) from w0[k][s]
+  // instead of the table (see forward_w0).
+  template <int p, int K, bool W0 = false>
   __device__ __forceinline__ static void fwd_pass(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
-                                                  int tau) {
+                                                  int tau, const float2 (&w0)[K][R]) {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
     if constexpr (p > 0) {
@@ -219,7 +221,12 @@ struct Fft {
     }
 #pragma unroll
     for (int k = 0; k < K; ++k) dft_block<p, 0, false>(x[k]);
-    if constexpr (SP > 1) {
+    if constexpr (W0 && p == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int s = 0; s < RP; ++s) x[k][s] = cmul(x[k][s], w0[k][s]);
+    } else if constexpr (SP > 1) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int t = (tau + T * u) % SP;
@@ -241,14 +248,14 @@ struct Fft {
 #pragma unroll
           for (int s = 0; s < RP; ++s) lds[k * LDS + pad(base + SP * s)] = x[k][u * RP + s];
       }
-      fwd_pass<p + 1, K>(x, lds, tw, tau);
+      fwd_pass<p + 1, K, W0>(x, lds, tw, tau, w0);
     }
   }
 
   // ---- one pass, inverse: read (p < P-1), conj twiddle, conj DFT, write (p > 0) ----
-  template <int p, int K>
+  template <int p, int K, bool W0 = false>
   __device__ __forceinline__ static void inv_pass(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
-                                                  int tau) {
+                                                  int tau, const float2 (&w0)[K][R]) {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
     if constexpr (p + 1 < P) {
@@ -263,7 +270,12 @@ struct Fft {
           for (int s = 0; s < RP; ++s) x[k][u * RP + s] = lds[k * LDS + pad(base + SP * s)];
       }
     }
-    if constexpr (SP > 1) {
+    if constexpr (W0 && p == 0) {
+#pragma unroll
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int s = 0; s < RP; ++s) x[k][s] = cmulc(x[k][s], w0[k][s]);
+    } else if constexpr (SP > 1) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int t = (tau + T * u) % SP;
@@ -287,7 +299,7 @@ struct Fft {
 #pragma unroll
           for (int r = 0; r < RP; ++r) lds[k * LDS + pad(base + SP * r)] = x[k][u * RP + r];
       }
-      inv_pass<p - 1, K>(x, lds, tw, tau);
+      inv_pass<p - 1, K, W0>(x, lds, tw, tau, w0);
     }
   }
 
@@ -306,13 +318,33 @@ struct Fft {
   template <int K>
   __device__ __forceinline__ static void forward(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
                                                  int tau) {
-    fwd_pass<0, K>(x, lds, tw, tau);
+    float2 none[K][R];
+    fwd_pass<0, K, false>(x, lds, tw, tau, none);
   }
   // Inverse DFT (sign +1), unnormalised; exact reverse of forward's layout.
   template <int K>
   __device__ __forceinline__ static void inverse(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
                                                  int tau) {
-    inv_pass<P - 1, K>(x, lds, tw, tau);
+    float2 none[K][R];
+    inv_pass<P - 1, K, false>(x, lds, tw, tau, none);
+  }
+  // As forward / inverse, with the output twiddles of pass 0 given per
+  // transform: output s of pass 0 is multiplied by w0[k][s] (inverse: its
+  // input by conj(w0[k][s])) in place of W_N^{tau s}.  A diagonal factor
+  // d_tau on the input positions tau + T r of the thread can so be folded into
+  // the transform: w0[k][s] = d_tau W_N^{tau s}, after multiplying register r
+  // by whatever part of the factor depends on r alone.  Needs P > 1.
+  template <int K>
+  __device__ __forceinline__ static void forward_w0(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
+                                                    int tau, const float2 (&w0)[K][R]) {
+    static_assert(P > 1, "forward_w0: needs a pass with twiddles");
+    fwd_pass<0, K, true>(x, lds, tw, tau, w0);
+  }
+  template <int K>
+  __device__ __forceinline__ static void inverse_w0(float2 (&x)[K][R], float2* lds, const float2* __restrict__ tw,
+                                                    int tau, const float2 (&w0)[K][R]) {
+    static_assert(P > 1, "inverse_w0: needs a pass with twiddles");
+    inv_pass<P - 1, K, true>(x, lds, tw, tau, w0);
   }
   __device__ __forceinline__ static void forward(float2 (&x)[R], float2* lds, const float2* __restrict__ tw,
                                                  int tau) {

@@ -36,6 +36,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -314,6 +315,30 @@ __global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long l
 }
 
 // ---------------------------------------------- convolution + contraction --
+// fn(std::integral_constant<int, I>) for I = 0 .. N-1.
+template <int N, int I = 0, typename Fn>
+__device__ __forceinline__ void constexpr_for(Fn&& fn) {
+  if constexpr (I < N) {
+    fn(std::integral_constant<int, I>{});
+    constexpr_for<N, I + 1>(fn);
+  }
+}
+
+// v * exp(-+2 pi i K / NN) (rot of fft.hpp) for a K that is a constant once
+// the loops around the call are unrolled.
+template <int NN, bool INV>
+__device__ __forceinline__ float2 rot_dyn(float2 v, int K) {
+  static_assert(64 % NN == 0, "rot_dyn: NN must divide 64");
+  const int k = (((K % NN) + NN) % NN) * (64 / NN);
+  const int e = INV ? k : (64 - k) % 64;
+  if (e == 0) return v;
+  if (e == 16) return make_float2(-v.y, v.x);
+  if (e == 32) return make_float2(-v.x, -v.y);
+  if (e == 48) return make_float2(v.y, -v.x);
+  const float c = cos64(e), sn = sin64(e);
+  return make_float2(v.x * c - v.y * sn, v.x * sn + v.y * c);
+}
+
 // z * (-i)^E, E taken mod 4.
 template <int E>
 __device__ __forceinline__ float2 quarter_turn(float2 z) {
@@ -343,12 +368,21 @@ __device__ __forceinline__ float2 quarter_turn(float2 z) {
 //   part[bh][hs][c][i] = s_c sum_l phi_l(q_i) (C_hs a_{l,c})_i,   c in {c0, c1}.
 // phi rows are [m][N] per (batch, head), phi_bh_stride apart (0 broadcasts one
 // set of rows to every head).
-template <typename F, int FOLD, int KH, int R0, bool VREG, bool HREG, bool HOIST>
+//
+// The twist W_{2N}^{r j} of class r at position j = tau + T i splits as
+// W_{2N}^{r tau} W_{16S}^{r i}: the second factor is a compile-time constant
+// per register, the first is folded into the twiddles of the first pass
+// (Fft::forward_w0: w0[s] = W_{2N}^{tau (r + S s)}); the inverse undoes both
+// the same way.
+template <typename C, int R0>
 __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const float* __restrict__ pq,
                                           const float2* __restrict__ vrow, const float2* __restrict__ tw,
                                           const float2* __restrict__ Hh, float2* lds, int tau, int m,
-                                          float (&acc0)[FOLD][F::R], float (&acc1)[FOLD][F::R]) {
-  constexpr int S = 2 * FOLD;
+                                          float (&acc0)[C::FOLD][C::F::R], float (&acc1)[C::FOLD][C::F::R]) {
+  using F = typename C::F;
+  constexpr int FOLD = C::FOLD, KH = C::KH, S = C::S;
+  constexpr bool VREG = C::VREG, PREF = C::PREF, HREG = C::HREG, HOIST = C::HOIST;
+  constexpr bool MERGE = F::P > 1;
   constexpr int NP = FOLD * F::N;  // row length of phi and v
   // Spectrum classes, register order (see k_spectrum): kept in registers when
   // the work-group is small enough, else re-read just before the product.
@@ -366,21 +400,22 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
 #pragma unroll
       for (int i = 0; i < F::R; ++i) vx[p][i] = vrow[tau + F::T * i + p * F::N];
   }
-  // W_{2N}^{r j} of the classes r > 0.
-  float2 twist[VREG ? KH : 1][VREG ? F::R : 1];
-  if constexpr (VREG) {
+  // Merged first-pass twiddles (MERGE), or the plain twists W_{2N}^{r j}
+  // (single-pass transforms), of every class of the unit.
+  float2 w0[KH][F::R];
+  auto load_w0 = [&](const float2* __restrict__ t, int ta) {
 #pragma unroll
     for (int k = 0; k < KH; ++k)
-      if (R0 + k > 0) {
 #pragma unroll
-        for (int i = 0; i < F::R; ++i) twist[k][i] = tw[(R0 + k) * (tau + F::T * i)];
-      }
-  }
-  // With registers to spare, phi(k) of the next feature and phi(q) of this one
-  // are loaded at the top of the iteration and stay in flight across the
-  // transform (the barriers only wait for LDS traffic).
-  float a_next[VREG ? FOLD : 1][VREG ? F::R : 1];
-  if constexpr (VREG) {
+      for (int i = 0; i < F::R; ++i)
+        w0[k][i] = MERGE ? t[ta * (R0 + k + S * i)] : t[(R0 + k) * (ta + F::T * i)];
+  };
+  if constexpr (HOIST) load_w0(tw, tau);
+  // With registers to spare, phi(k) of the next feature is loaded at the top
+  // of the iteration and stays in flight across the transform (the barriers
+  // only wait for LDS traffic).
+  float a_next[PREF ? FOLD : 1][PREF ? F::R : 1];
+  if constexpr (PREF) {
 #pragma unroll
     for (int p = 0; p < FOLD; ++p)
 #pragma unroll
@@ -399,14 +434,15 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       asm volatile("" : "+s"(twl));
       asm volatile("" : "+v"(Hl));
       asm volatile("" : "+v"(taul));
+      load_w0(twl, taul);
     }
     float a[FOLD][F::R], f[FOLD][F::R];
 #pragma unroll
     for (int p = 0; p < FOLD; ++p)
 #pragma unroll
       for (int i = 0; i < F::R; ++i)
-        a[p][i] = VREG ? a_next[VREG ? p : 0][VREG ? i : 0] : pkl[taul + F::T * i + p * F::N];
-    if constexpr (VREG) {
+        a[p][i] = PREF ? a_next[PREF ? p : 0][PREF ? i : 0] : pkl[taul + F::T * i + p * F::N];
+    if constexpr (PREF) {
 #pragma unroll
       for (int p = 0; p < FOLD; ++p)
 #pragma unroll
@@ -427,39 +463,51 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         const float2 vv = VREG ? vx[VREG ? p : 0][VREG ? i : 0] : vrow[taul + F::T * i + p * F::N];
         xb[p] = make_float2(a[p][i] * vv.x, a[p][i] * vv.y);
       }
-#pragma unroll
-      for (int k = 0; k < KH; ++k) {
-        float2 u = xb[0];
-        if constexpr (FOLD == 2) {
-          // W_4^{r} = (-i)^r on the second fold
-          switch ((R0 + k) & 3) {
-            case 0: u = cadd(u, quarter_turn<0>(xb[1])); break;
-            case 1: u = cadd(u, quarter_turn<1>(xb[1])); break;
-            case 2: u = cadd(u, quarter_turn<2>(xb[1])); break;
-            default: u = cadd(u, quarter_turn<3>(xb[1])); break;
-          }
-        }
-        if (R0 + k > 0) {
-          const float2 w = VREG ? twist[VREG ? k : 0][VREG ? i : 0] : twl[(R0 + k) * (taul + F::T * i)];
-          u = cmul(u, w);
-        }
-        x[k][i] = u;
+      float2 u0[4];  // folded input of class R0 + k, k < KH <= 2 (indexed by class mod 4)
+      if constexpr (FOLD == 2) {
+        // W_4^{r} = (-i)^r on the second fold
+        u0[0] = cadd(xb[0], xb[1]);
+        u0[1] = cadd(xb[0], quarter_turn<1>(xb[1]));
+        u0[2] = csub(xb[0], xb[1]);
+        u0[3] = cadd(xb[0], quarter_turn<3>(xb[1]));
+      } else {
+        u0[0] = u0[1] = u0[2] = u0[3] = xb[0];
       }
+      constexpr_for<KH>([&](auto kc) {
+        constexpr int k = decltype(kc)::value, r = R0 + k;
+        const float2 u = u0[r & 3];
+        if constexpr (r == 0) {
+          x[k][i] = u;
+        } else if constexpr (MERGE) {
+          x[k][i] = rot_dyn<16 * S, false>(u, r * i);
+        } else {
+          x[k][i] = cmul(u, w0[k][i]);
+        }
+      });
     }
-    F::template forward<KH>(x, lds, twl, taul);
+    if constexpr (MERGE) {
+      F::template forward_w0<KH>(x, lds, twl, taul, w0);
+    } else {
+      F::template forward<KH>(x, lds, twl, taul);
+    }
 #pragma unroll
     for (int k = 0; k < KH; ++k)
 #pragma unroll
       for (int i = 0; i < F::R; ++i)
         x[k][i] = cmul(x[k][i], HREG ? Hr[HREG ? k : 0][i] : Hl[k * F::N + i * F::T + taul]);
-    F::template inverse<KH>(x, lds, twl, taul);
     if constexpr (!HOIST) {
-      // fresh (opaque) copies: the twists are re-read rather than kept live
+      // fresh (opaque) copies: the twiddles are re-read rather than kept live
       // across both transforms
       asm volatile("" : "+s"(twl));
       asm volatile("" : "+v"(taul));
+      load_w0(twl, taul);
     }
-    if constexpr (!VREG) {
+    if constexpr (MERGE) {
+      F::template inverse_w0<KH>(x, lds, twl, taul, w0);
+    } else {
+      F::template inverse<KH>(x, lds, twl, taul);
+    }
+    if constexpr (!PREF) {
 #pragma unroll
       for (int p = 0; p < FOLD; ++p)
 #pragma unroll
@@ -468,14 +516,16 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
 #pragma unroll
     for (int i = 0; i < F::R; ++i) {
       float2 yk[KH];
-#pragma unroll
-      for (int k = 0; k < KH; ++k) {
-        yk[k] = x[k][i];
-        if (R0 + k > 0) {
-          const float2 w = VREG ? twist[VREG ? k : 0][VREG ? i : 0] : twl[(R0 + k) * (taul + F::T * i)];
-          yk[k] = cmulc(yk[k], w);
+      constexpr_for<KH>([&](auto kc) {
+        constexpr int k = decltype(kc)::value, r = R0 + k;
+        if constexpr (r == 0) {
+          yk[k] = x[k][i];
+        } else if constexpr (MERGE) {
+          yk[k] = rot_dyn<16 * S, true>(x[k][i], r * i);
+        } else {
+          yk[k] = cmulc(x[k][i], w0[k][i]);
         }
-      }
+      });
 #pragma unroll
       for (int q = 0; q < FOLD; ++q) {
         float2 y = make_float2(0.f, 0.f);
@@ -508,8 +558,7 @@ __device__ __forceinline__ void conv_split(int hs, const float* __restrict__ pk,
                                            float (&acc0)[C::FOLD][C::F::R], float (&acc1)[C::FOLD][C::F::R]) {
   if constexpr (HS < C::HSPLIT) {
     if (HS + 1 == C::HSPLIT || hs == HS) {
-      conv_loop<typename C::F, C::FOLD, C::KH, HS * C::KH, C::VREG, C::HREG, C::HOIST>(pk, pq, vrow, tw, Hh, lds,
-                                                                                       tau, m, acc0, acc1);
+      conv_loop<C, HS * C::KH>(pk, pq, vrow, tw, Hh, lds, tau, m, acc0, acc1);
     } else {
       conv_split<C, HS + 1>(hs, pk, pq, vrow, tw, Hh, lds, tau, m, acc0, acc1);
     }
@@ -517,25 +566,27 @@ __device__ __forceinline__ void conv_split(int hs, const float* __restrict__ pk,
 }
 
 template <int L2>
-__global__ __launch_bounds__(Conf<L2>::THREADS) void k_conv_contract(
+__global__ __launch_bounds__(Conf<L2>::THREADS) __attribute__((amdgpu_waves_per_eu(Conf<L2>::WPE))) void
+k_conv_contract(
     const float* __restrict__ phiq, const float* __restrict__ phik, long long phi_bh_stride,
     const float2* __restrict__ vsc, const float* __restrict__ colmax, const float2* __restrict__ Hs,
     const float2* __restrict__ tw, float* __restrict__ part, int H, int n, int cols, int m, int units) {
   using C = Conf<L2>;
   using F = typename C::F;
   constexpr int KH = C::KH, FOLD = C::FOLD;
-  // Units of one work-group must run the same class split (same barriers).
-  static_assert(C::HSPLIT == 1 || C::G == 1, "class splits need one unit per work-group");
   __shared__ float2 lds_all[C::CONV_LDS_SLOTS];
   // With one unit per work-group the unit index is wave-uniform: say so, so
   // that per-unit pointers live in scalar registers.
   const int g = C::G == 1 ? 0 : threadIdx.x / F::T, tau = C::G == 1 ? threadIdx.x : threadIdx.x % F::T;
   const int pairs = (cols + 1) / 2;
-  int unit = xcd_block(blockIdx.x, gridDim.x) * C::G + g;
-  const bool active = unit < units;
-  if (!active) unit = units - 1;  // keep the barriers uniform; results discarded
-  const int cp = unit % pairs;
-  const int rest = unit / pairs;
+  // Column pairs are padded to a multiple of G, so that the units of one
+  // work-group share (bh, hs): they run the same class split (same barriers).
+  const int pairs_p = (pairs + C::G - 1) / C::G * C::G;
+  const int unit = xcd_block(blockIdx.x, gridDim.x) * C::G + g;
+  int cp = unit % pairs_p;
+  const int rest = unit / pairs_p;
+  const bool active = unit < units && cp < pairs;
+  if (cp >= pairs) cp = pairs - 1;  // padding unit: keeps the barriers uniform, results discarded
   const int hs = rest % C::HSPLIT, bh = rest / C::HSPLIT, h = bh % H;
   const int c0 = 2 * cp, c1 = 2 * cp + 1;
   float2* lds = lds_all + g * (F::P > 1 ? KH * F::LDS : 0);
@@ -1008,8 +1059,9 @@ hipError_t conv_l2(const float* phiq, const float* phik, long long phi_bh_stride
                    const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
                    int cols, int m, hipStream_t st) {
   using C = Conf<L2>;
-  const long long units = static_cast<long long>(BH) * C::HSPLIT * ((cols + 1) / 2);
-  const long long blocks = (units + C::G - 1) / C::G;
+  const int pairs_p = ((cols + 1) / 2 + C::G - 1) / C::G * C::G;
+  const long long units = static_cast<long long>(BH) * C::HSPLIT * pairs_p;
+  const long long blocks = units / C::G;
   hipLaunchKernelGGL(k_conv_contract<L2>, dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0, st, phiq, phik,
                      phi_bh_stride, vsc, colmax, Hs, tw, part, H, n, cols, m, static_cast<int>(units));
   return hipGetLastError();
@@ -1047,7 +1099,7 @@ struct SplitFn {
 
 int conv_splits(int l2) {
   int s = 2;
-  dispatch<SplitFn>(l2, &s);
+  (void)dispatch<SplitFn>(l2, &s);
   return s;
 }
 
