@@ -249,7 +249,8 @@ def main() -> int:
         "config": {"workload": wl.name, "B": B, "H": H, "n": n, "d": dd, "m": m,
                    "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
                    "causal": wl.causal, "ms_per_layer": ms_per_step, "stages_ms": stages,
-                   "conv_stage_hbm_gbs": conv_gbs},
+                   "conv_stage_hbm_gbs": conv_gbs,
+                   "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)},
         "roofline": {"bound": "alu", "kernel": "k_conv_contract", "achieved": achieved_tflops,
                      "peak": PEAK_FP32_VECTOR_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,

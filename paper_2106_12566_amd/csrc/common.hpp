@@ -20,8 +20,8 @@ constexpr int kLog2R = 4;      // 16 complex values per thread
 // k = S k' + r; class r is a length L' = 2N / S transform (L' = N / FOLD) of
 // the input folded FOLD times (Section 3.2 leaves the FFT open; see the
 // convolution kernel for the algebra).  FOLD = 1 up to N = 4096 (the classes
-// are the even and odd bins), FOLD = 2 above, which keeps one transform
-// within 8192 points and the per-thread state within the register file.
+// are the even and odd bins), 2 at N = 8192 and 4 at N = 16384: transforms
+// never exceed 4096 points, which keeps their state in the register file.
 //
 // A transform is owned by T = L' / 16 threads (16 complex values each); a
 // work-group holds G units of T threads (filling 256 threads for short
@@ -29,10 +29,12 @@ constexpr int kLog2R = 4;      // 16 complex values per thread
 // interleaved transforms sharing loads, barriers and accumulators.
 template <int L2>
 struct Conf {
-  static constexpr int FOLD = L2 <= 12 ? 1 : 2;
-  static constexpr int S = 2 * FOLD;                 // residue classes
-  static constexpr int L2T = L2 <= 12 ? L2 : L2 - 1;  // log2 of the transform length
-  static constexpr int LOG2R = kLog2R;
+  static constexpr int FOLD = L2 <= 12 ? 1 : (L2 == 13 ? 2 : 4);
+  static constexpr int S = 2 * FOLD;                  // residue classes
+  static constexpr int L2T = L2 <= 12 ? L2 : 12;       // log2 of the transform length
+  // 8 values per thread at N = 16384: 512 threads share the 64 positions x
+  // 2 columns of accumulators a 256-thread group could not hold
+  static constexpr int LOG2R = L2 == 14 ? 3 : kLog2R;
   using F = Fft<L2T, LOG2R, 1 + L2 - L2T>;  // twiddles come from the W_{2N} table
   static constexpr int N = 1 << L2;
   static constexpr int LT = F::N;  // transform length 2N / S
@@ -44,7 +46,7 @@ struct Conf {
   // mid-size transforms: one runs while the other waits at a barrier.
   static constexpr int WPE = (L2 >= 9 && L2 <= 12) ? 2 : 1;
   static constexpr int KH =
-      (WPE == 1 && F::T <= 256 && F::R <= 16 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
+      (WPE == 1 && FOLD <= 2 && F::T <= 256 && F::R <= 16 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
   static constexpr int HSPLIT = S / KH;  // work units per column pair and head
   static constexpr int CONV_LDS_SLOTS = F::P > 1 ? G * KH * F::LDS : 1;
   // Per-position values (v pairs, prefetched phi), the spectrum and the
@@ -52,8 +54,8 @@ struct Conf {
   // threads (512 registers per thread); larger ones re-read them.
   static constexpr bool VREG = THREADS <= 256 && FOLD == 1;
   static constexpr bool PREF = VREG && WPE == 1;
-  static constexpr bool HREG = THREADS <= 256;
-  static constexpr bool HOIST = THREADS <= 256 && FOLD == 1;
+  static constexpr bool HREG = THREADS <= 256 || L2 == 14;
+  static constexpr bool HOIST = (THREADS <= 256 && FOLD != 2) || L2 == 14;
 };
 
 // Work-groups are dispatched round-robin over the 8 XCDs (each with its own

@@ -26,6 +26,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 namespace krpe {
 
 // ---------------------------------------------------------------- complex --
@@ -39,26 +41,33 @@ __device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
   return make_float2(a.x * b.x + a.y * b.y, a.y * b.x - a.x * b.y);
 }
 
-// cos(2*pi*k/64) for k = 0..16 (first quadrant, exact zero at 16).
-__host__ __device__ constexpr float quarter_cos64(int k) {
-  constexpr float q[17] = {1.0f,
-                           0.99518472667219693f, 0.98078528040323043f, 0.95694033573220882f,
-                           0.92387953251128674f, 0.88192126434835505f, 0.83146961230254524f,
-                           0.77301045336273699f, 0.70710678118654757f, 0.63439328416364549f,
-                           0.55557023301960218f, 0.47139673682599781f, 0.38268343236508984f,
-                           0.29028467725446233f, 0.19509032201612833f, 0.098017140329560770f,
-                           0.0f};
+// cos(2*pi*k/128) for k = 0..32 (first quadrant, exact zero at 32).
+__host__ __device__ constexpr float quarter_cos128(int k) {
+  constexpr float q[33] = {
+                            1.0f, 0.99879545620517241f, 0.99518472667219693f,
+                            0.98917650996478101f, 0.98078528040323043f, 0.97003125319454397f,
+                            0.95694033573220882f, 0.94154406518302081f, 0.92387953251128674f,
+                            0.90398929312344334f, 0.88192126434835505f, 0.85772861000027212f,
+                            0.83146961230254524f, 0.80320753148064494f, 0.77301045336273699f,
+                            0.74095112535495911f, 0.70710678118654757f, 0.67155895484701833f,
+                            0.63439328416364549f, 0.59569930449243347f, 0.55557023301960229f,
+                            0.51410274419322166f, 0.47139673682599781f, 0.4275550934302822f,
+                            0.38268343236508984f, 0.33688985339222005f, 0.29028467725446233f,
+                            0.24298017990326398f, 0.19509032201612833f, 0.14673047445536175f,
+                            0.09801714032956077f, 0.049067674327418126f, 0.0f};
   return q[k];
 }
-// cos(2*pi*k/64) for any k, by quadrant symmetry.
-__host__ __device__ constexpr float cos64(int k) {
-  k = ((k % 64) + 64) % 64;
-  if (k <= 16) return quarter_cos64(k);
-  if (k <= 32) return -quarter_cos64(32 - k);
-  if (k <= 48) return -quarter_cos64(k - 32);
-  return quarter_cos64(64 - k);
+// cos(2*pi*k/128) for any k, by quadrant symmetry.
+__host__ __device__ constexpr float cos128(int k) {
+  k = ((k % 128) + 128) % 128;
+  if (k <= 32) return quarter_cos128(k);
+  if (k <= 64) return -quarter_cos128(64 - k);
+  if (k <= 96) return -quarter_cos128(k - 64);
+  return quarter_cos128(128 - k);
 }
-__host__ __device__ constexpr float sin64(int k) { return cos64(k - 16); }
+__host__ __device__ constexpr float sin128(int k) { return cos128(k - 32); }
+__host__ __device__ constexpr float cos64(int k) { return cos128(2 * k); }
+__host__ __device__ constexpr float sin64(int k) { return sin128(2 * k); }
 
 // v * exp(sign * 2*pi*i * K / NN), sign = -1 for the forward transform and +1
 // for the inverse.  NN divides 64.  Quarter turns are exact swaps.
@@ -80,6 +89,30 @@ __device__ __forceinline__ float2 rot(float2 v) {
     constexpr float s = sin64(e);
     return make_float2(v.x * c - v.y * s, v.x * s + v.y * c);
   }
+}
+
+// fn(std::integral_constant<int, I>) for I = 0 .. N-1.
+template <int N, int I = 0, typename Fn>
+__device__ __forceinline__ void constexpr_for(Fn&& fn) {
+  if constexpr (I < N) {
+    fn(std::integral_constant<int, I>{});
+    constexpr_for<N, I + 1>(fn);
+  }
+}
+
+// v * exp(-+2 pi i K / NN), as rot below, for a K that is a constant once the
+// loops around the call are unrolled; NN divides 128.
+template <int NN, bool INV>
+__device__ __forceinline__ float2 rot_dyn(float2 v, int K) {
+  static_assert(128 % NN == 0, "rot_dyn: NN must divide 128");
+  const int k = (((K % NN) + NN) % NN) * (128 / NN);
+  const int e = INV ? k : (128 - k) % 128;  // multiply by exp(+2 pi i e / 128)
+  if (e == 0) return v;
+  if (e == 32) return make_float2(-v.y, v.x);
+  if (e == 64) return make_float2(-v.x, -v.y);
+  if (e == 96) return make_float2(v.y, -v.x);
+  const float c = cos128(e), sn = sin128(e);
+  return make_float2(v.x * c - v.y * sn, v.x * sn + v.y * c);
 }
 
 // ---------------------------------------------------- in-register DFTs --

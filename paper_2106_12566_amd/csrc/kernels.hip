@@ -36,7 +36,6 @@
 
 #include <cmath>
 #include <cstdint>
-#include <type_traits>
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -60,16 +59,6 @@ __device__ __forceinline__ float circ_kernel(const float* __restrict__ bh, int s
   if (s < n) return expf(bh[n - 1 - s]);
   if (s > 2 * N - n) return expf(bh[2 * N - s + n - 1]);
   return 0.f;
-}
-
-// z * (-i)^e for a real z, e taken mod 4.
-__device__ __forceinline__ float2 real_quarter_turn(float z, int e) {
-  switch (e & 3) {
-    case 0: return make_float2(z, 0.f);
-    case 1: return make_float2(0.f, -z);
-    case 2: return make_float2(-z, 0.f);
-    default: return make_float2(0.f, z);
-  }
 }
 
 // One transform per (head, residue class r < S): the bins k = S k' + r of the
@@ -107,7 +96,7 @@ __global__ __launch_bounds__(Conf<L2>::THREADS) void k_spectrum(const float* __r
       const float hv = circ_kernel(bh, j + p * F::N, n, C::N);
       s1 += hv;
       s2 = fmaf(hv, hv, s2);
-      acc = cadd(acc, real_quarter_turn(hv, (4 / S) * p * r));
+      acc = cadd(acc, rot_dyn<S, false>(make_float2(hv, 0.f), p * r));
     }
     x[i] = r == 0 ? acc : cmul(acc, tw[r * j]);
   }
@@ -315,40 +304,6 @@ __global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long l
 }
 
 // ---------------------------------------------- convolution + contraction --
-// fn(std::integral_constant<int, I>) for I = 0 .. N-1.
-template <int N, int I = 0, typename Fn>
-__device__ __forceinline__ void constexpr_for(Fn&& fn) {
-  if constexpr (I < N) {
-    fn(std::integral_constant<int, I>{});
-    constexpr_for<N, I + 1>(fn);
-  }
-}
-
-// v * exp(-+2 pi i K / NN) (rot of fft.hpp) for a K that is a constant once
-// the loops around the call are unrolled.
-template <int NN, bool INV>
-__device__ __forceinline__ float2 rot_dyn(float2 v, int K) {
-  static_assert(64 % NN == 0, "rot_dyn: NN must divide 64");
-  const int k = (((K % NN) + NN) % NN) * (64 / NN);
-  const int e = INV ? k : (64 - k) % 64;
-  if (e == 0) return v;
-  if (e == 16) return make_float2(-v.y, v.x);
-  if (e == 32) return make_float2(-v.x, -v.y);
-  if (e == 48) return make_float2(v.y, -v.x);
-  const float c = cos64(e), sn = sin64(e);
-  return make_float2(v.x * c - v.y * sn, v.x * sn + v.y * c);
-}
-
-// z * (-i)^E, E taken mod 4.
-template <int E>
-__device__ __forceinline__ float2 quarter_turn(float2 z) {
-  constexpr int e = ((E % 4) + 4) % 4;
-  if constexpr (e == 0) return z;
-  if constexpr (e == 1) return make_float2(z.y, -z.x);
-  if constexpr (e == 2) return make_float2(-z.x, -z.y);
-  return make_float2(-z.y, z.x);
-}
-
 // Unit u = ((bh * HSPLIT + hs) * pairs + cp).  The unit owns columns
 // c0 = 2 cp, c1 = 2 cp + 1 of v' (packed and scaled by k_vprep) and the
 // residue classes r = hs*KH .. hs*KH + KH - 1 of the length-2N spectrum.  For
@@ -370,7 +325,7 @@ __device__ __forceinline__ float2 quarter_turn(float2 z) {
 // set of rows to every head).
 //
 // The twist W_{2N}^{r j} of class r at position j = tau + T i splits as
-// W_{2N}^{r tau} W_{16S}^{r i}: the second factor is a compile-time constant
+// W_{2N}^{r tau} W_{RS}^{r i} (2N = R S T): the second factor is a compile-time constant
 // per register, the first is folded into the twiddles of the first pass
 // (Fft::forward_w0: w0[s] = W_{2N}^{tau (r + S s)}); the inverse undoes both
 // the same way.
@@ -463,23 +418,16 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         const float2 vv = VREG ? vx[VREG ? p : 0][VREG ? i : 0] : vrow[taul + F::T * i + p * F::N];
         xb[p] = make_float2(a[p][i] * vv.x, a[p][i] * vv.y);
       }
-      float2 u0[4];  // folded input of class R0 + k, k < KH <= 2 (indexed by class mod 4)
-      if constexpr (FOLD == 2) {
-        // W_4^{r} = (-i)^r on the second fold
-        u0[0] = cadd(xb[0], xb[1]);
-        u0[1] = cadd(xb[0], quarter_turn<1>(xb[1]));
-        u0[2] = csub(xb[0], xb[1]);
-        u0[3] = cadd(xb[0], quarter_turn<3>(xb[1]));
-      } else {
-        u0[0] = u0[1] = u0[2] = u0[3] = xb[0];
-      }
       constexpr_for<KH>([&](auto kc) {
         constexpr int k = decltype(kc)::value, r = R0 + k;
-        const float2 u = u0[r & 3];
+        // fold: u = sum_p xb[p] W_S^{p r}
+        float2 u = xb[0];
+#pragma unroll
+        for (int p = 1; p < FOLD; ++p) u = cadd(u, rot_dyn<S, false>(xb[p], p * r));
         if constexpr (r == 0) {
           x[k][i] = u;
         } else if constexpr (MERGE) {
-          x[k][i] = rot_dyn<16 * S, false>(u, r * i);
+          x[k][i] = rot_dyn<F::R * S, false>(u, r * i);
         } else {
           x[k][i] = cmul(u, w0[k][i]);
         }
@@ -521,7 +469,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         if constexpr (r == 0) {
           yk[k] = x[k][i];
         } else if constexpr (MERGE) {
-          yk[k] = rot_dyn<16 * S, true>(x[k][i], r * i);
+          yk[k] = rot_dyn<F::R * S, true>(x[k][i], r * i);
         } else {
           yk[k] = cmulc(x[k][i], w0[k][i]);
         }
@@ -531,16 +479,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         float2 y = make_float2(0.f, 0.f);
 #pragma unroll
         for (int k = 0; k < KH; ++k) {
-          // W_S^{-q r} = (-i)^{-(4/S) q r}
-          float2 t = yk[k];
-          if (q > 0) {
-            switch (((4 / S) * q * (R0 + k)) & 3) {
-              case 0: break;
-              case 1: t = quarter_turn<-1>(t); break;
-              case 2: t = quarter_turn<-2>(t); break;
-              default: t = quarter_turn<-3>(t); break;
-            }
-          }
+          const float2 t = rot_dyn<S, true>(yk[k], q * (R0 + k));  // W_S^{-q r}
           y = k == 0 ? t : cadd(y, t);
         }
         acc0[q][i] = fmaf(f[q][i], y.x, acc0[q][i]);
