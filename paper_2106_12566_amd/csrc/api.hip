@@ -93,7 +93,8 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.x2 = take(bh * L.ksplit * m * pairs * sizeof(float));
   L.wb = take(bh * (static_cast<size_t>(m) + 1) * sizeof(float2));
   L.part = take(bh * conv_splits(L.l2) * cols * n * sizeof(float));
-  L.fix = take((bh + 1 + bh * n) * sizeof(unsigned));
+  L.fix = take((bh + 1) * sizeof(unsigned));
+  L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.total = off;
   return L;
 }
@@ -267,6 +268,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   float2* wb = reinterpret_cast<float2*>(w + L.wb);
   float* part = reinterpret_cast<float*>(w + L.part);
   unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
+  unsigned long long* fixmask = reinterpret_cast<unsigned long long*>(w + L.fixmask);
   const int BHi = static_cast<int>(bh);
   const int N = 1 << L.l2;
   const bool bf16 = qkv_dtype == KRPE_BF16;
@@ -293,10 +295,10 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
     return s;
   if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, m, d, L.ksplit, st), "bound launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, BHi, H, n, L.l2, d, m, st),
+  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, fixmask, BHi, H, n, L.l2, d, m, st),
                                   "combine launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, BHi, H, n, N, d, m, st),
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, fixmask, BHi, H, n, N, d, m, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);

@@ -682,8 +682,9 @@ __global__ __launch_bounds__(256) void k_bound_weights(const float* __restrict__
 // m + 1 weights.
 __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part, const float* __restrict__ phiq,
                                                  const float2* __restrict__ Wb, const float2* __restrict__ hnorm,
-                                                 float* __restrict__ z, unsigned* __restrict__ fix, int BH, int H,
-                                                 int n, int N, int log2N, int d, int m, int nsplit, int tiles_n) {
+                                                 float* __restrict__ z, unsigned* __restrict__ fix,
+                                                 unsigned long long* __restrict__ fixmask, int BH, int H, int n, int N,
+                                                 int log2N, int d, int m, int nsplit, int tiles_n) {
   extern __shared__ float dyn[];
   const int cols = d + 1;
   float* tile = dyn;                                                  // [cols][65]
@@ -752,21 +753,15 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
       const bool ok = isfinite(den) && den > 0.f && isfinite(zm) && err <= (kTau - rel_floor) * scale * den;
       flag = !ok;
     }
-    // One wave holds the tile's 64 rows: append its uncertified rows, in
-    // order, to the head's queue (fix[0..BH) counts, fix[BH] total, then the
-    // lists fix[BH + 1 + bh * n + slot]).
+    // One wave holds the tile's 64 rows: its uncertified rows as one mask
+    // word, counted per head (fix[0..BH)) and in total (fix[BH]).
     const unsigned long long mask = __ballot(flag);
-    if (mask != 0ull) {
-      const int nflag = __popcll(mask);
-      unsigned base = 0;
-      if (threadIdx.x == 0) {
-        base = atomicAdd(&fix[bh], static_cast<unsigned>(nflag));
-        atomicAdd(&fix[BH], static_cast<unsigned>(nflag));
-      }
-      base = __shfl(base, 0);
-      if (flag) {
-        const int rank = __popcll(mask & ((1ull << threadIdx.x) - 1ull));
-        fix[BH + 1 + static_cast<size_t>(bh) * n + base + rank] = static_cast<unsigned>(pos);
+    if (threadIdx.x == 0) {
+      fixmask[static_cast<size_t>(bh) * tiles_n + blockIdx.x % tiles_n] = mask;
+      if (mask != 0ull) {
+        const unsigned nflag = static_cast<unsigned>(__popcll(mask));
+        atomicAdd(&fix[bh], nflag);
+        atomicAdd(&fix[BH], nflag);
       }
     }
   }
@@ -780,57 +775,83 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
 }
 
 // ---------------------------------------------------------------- fixup --
-// Exact evaluation of Eq. (10) for the rows k_combine could not certify.  Work
-// group (bh, k) of a fixed grid takes groups k, k + kFixPerHead, ... of 8
-// queued rows of head bh:
-//   P_rj = c_{j-i_r} phi(q_{i_r}) . phi(k_j)    (only keys with a finite b_{j-i_r})
-//   z_r  = sum_j P_rj v_j / sum_j P_rj          (chunk sums in fp32, totals in fp64)
-// Keys go in chunks of 1024 aligned to multiples of 1024 (so a row's sums do
-// not depend on which rows share its group: the result is deterministic):
-// each thread forms P for 4 keys x 8 rows (one load of phi(k) feeds 8 rows),
-// then threads split by value column and key subset accumulate P v'.  Rows
-// not queued keep the FFT result.  Every work-group exits when its head's
-// queue is done.
-constexpr int kFixRows = 8;
-constexpr int kFixChunk = 1024;
-constexpr int kFixPerHead = 32;
+// Exact evaluation of Eq. (10) for the rows k_combine could not certify, on
+// the matrix cores.  Work-group (bh, k) of a fixed grid takes groups k,
+// k + kFixPerHead, ... of 32 queued rows of head bh and walks the keys in
+// chunks of 128 aligned to multiples of 128:
+//   S = phi(q_rows) phi(k_chunk)^T      32 x 128, fp32 MFMA over the m features
+//   P = S * c_{j-i}                     0 where b_{j-i} = -inf or j >= n
+//   Z += P [v, 1]                       fp32 MFMA per chunk, totals in fp64
+// A row's sums depend only on its own values and the fixed chunking (chunks
+// that are outside its range add exact zeros), so results do not depend on
+// which rows share a group.  Waves: S takes one 32-key tile each; P V takes
+// the ceil(d / 32) column tiles, the spare waves splitting the chunk's keys.
+// Every work-group exits when its head's queue is done.
+constexpr int kFixRows = 32;
+constexpr int kFixKeys = 128;
+constexpr int kFixL = 32;                 // features staged per step
+constexpr int kFixStride = kFixKeys + 1;  // LDS row stride (odd: column reads hit distinct banks)
+constexpr int kFixPerHead = 64;
+constexpr int kFixMaxTiles = (1 << kMaxLog2N) / 64;
 
 __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, const float* __restrict__ phik,
                                                const void* __restrict__ vraw, int v_bf16,
                                                const float* __restrict__ b, float* __restrict__ z,
-                                               const unsigned* __restrict__ fix, int BH, int H, int n, int ld,
-                                               int d, int m) {
-  // P chunk, reused after the key loop for the per-thread partial sums of P v'
-  __shared__ __align__(16) float sp[kFixRows][kFixChunk];
-  static_assert(sizeof(float) * kFixRows * kFixChunk >= sizeof(double) * 256 * kFixRows, "red fits in sp");
-  double (*red)[kFixRows] = reinterpret_cast<double (*)[kFixRows]>(&sp[0][0]);
-  extern __shared__ __align__(16) float sq_dyn[];  // phi(q) of the group's rows, [l][r], m * 8 floats
-  float (*sq)[kFixRows] = reinterpret_cast<float (*)[kFixRows]>(sq_dyn);
+                                               const unsigned* __restrict__ fix,
+                                               const unsigned long long* __restrict__ fixmask, int BH, int H, int n,
+                                               int ld, int d, int m) {
+  extern __shared__ __align__(16) float sq[];   // phi(q) of the group's rows, [l][32]
+  __shared__ __align__(16) float sk[kFixL * kFixStride];  // phi(k) chunk [l][key]; then P [row][key]
+  __shared__ double dsum[8][kFixRows];
+  __shared__ double sden[kFixRows];
+  __shared__ int srows[kFixRows];
   __shared__ int smin, smax;
-  const int tid = threadIdx.x;
-  const int cols = d + 1;
-  const int nsub = 256 / cols;                 // key subsets in the accumulation
-  const int col = tid % cols, sub = tid / cols;
+  __shared__ unsigned long long smask[kFixMaxTiles];
+  __shared__ unsigned spre[kFixMaxTiles + 1];
+  double* red = reinterpret_cast<double*>(sk);  // after the key loop: partial numerators
+  static_assert(sizeof(float) * kFixL * kFixStride >= 2 * 1024 * sizeof(double), "red fits in sk");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lk = lane >> 5;
   // slot-major order: the first group of every head is dispatched first
   const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
-  if (bh >= BH) return;
   const unsigned count = fix[bh];
-  const unsigned* __restrict__ list = fix + BH + 1 + static_cast<size_t>(bh) * n;
   const int ngroups = static_cast<int>((count + kFixRows - 1) / kFixRows);
-  if (kslot >= ngroups) return;                // uniform per work-group
-  {
-    const int h = bh % H;
-    const float* __restrict__ bhv = b + static_cast<size_t>(h) * (2 * n - 1);
-    const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * ld;
-    const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * ld;
-    const size_t vbase = static_cast<size_t>(bh) * n * d;
+  if (kslot >= ngroups) return;  // uniform per work-group
+  const int h = bh % H;
+  const float* __restrict__ bhv = b + static_cast<size_t>(h) * (2 * n - 1);
+  const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * ld;
+  const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * ld;
+  const size_t vbase = static_cast<size_t>(bh) * n * d;
+  // column tiles of P V and the waves that share one (key split)
+  const int tiles = (d + 31) / 32;
+  const int wpt = tiles == 3 ? 1 : 4 / tiles;
+  const int my_tile = wave / wpt, my_part = wave % wpt;
+  const bool pv_wave = wave < tiles * wpt;
+  const int pv_keys = kFixKeys / wpt;
+  auto vload = [&](int j, int c) -> float {
+    const size_t idx = vbase + static_cast<size_t>(j) * d + c;
+    return v_bf16 ? to_f32(static_cast<const uint16_t*>(vraw)[idx]) : static_cast<const float*>(vraw)[idx];
+  };
 
-    // Range of s = t + n - 1 where b_t is finite.
-    if (tid == 0) {
-      smin = 2 * n;
-      smax = -1;
+  // Queued rows in row order: group g takes the ranks 32 g .. 32 g + 31 of
+  // the set bits of the head's mask words (prefix counts in spre).
+  const int tiles_n = (n + 63) / 64;
+  for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
+  // Range of s = t + n - 1 where b_t is finite.
+  if (tid == 0) {
+    smin = 2 * n;
+    smax = -1;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    unsigned acc = 0;
+    for (int t = 0; t < tiles_n; ++t) {
+      spre[t] = acc;
+      acc += static_cast<unsigned>(__popcll(smask[t]));
     }
-    __syncthreads();
+    spre[tiles_n] = acc;
+  }
+  {
     int lo = 2 * n, hi = -1;
     for (int sidx = tid; sidx < 2 * n - 1; sidx += 256)
       if (bhv[sidx] != -INFINITY) {
@@ -839,124 +860,174 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
       }
     atomicMin(&smin, lo);
     atomicMax(&smax, hi);
+  }
+
+  for (int grp = kslot; grp < ngroups; grp += kFixPerHead) {
+    __syncthreads();  // previous group's srows / sq / red consumed
+    if (tid < kFixRows) {
+      const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
+      int row = -1;
+      if (rank < count) {
+        int lo = 0, hi = tiles_n;  // last word with spre <= rank: it holds the bit
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (spre[mid] <= rank) lo = mid; else hi = mid;
+        }
+        unsigned long long w = smask[lo];
+        for (unsigned c = spre[lo]; c < rank; ++c) w &= w - 1ull;
+        row = lo * 64 + __ffsll(static_cast<long long>(w)) - 1;
+      }
+      srows[tid] = row;
+    }
     __syncthreads();
-    const int s_lo = smin, s_hi = smax;
-
-    for (int grp = kslot; grp < ngroups; grp += kFixPerHead) {
-      int rows[kFixRows];
-      int first = n, last = -1;
-#pragma unroll
-      for (int r = 0; r < kFixRows; ++r) {
-        const unsigned slot = static_cast<unsigned>(grp * kFixRows + r);
-        rows[r] = slot < count ? static_cast<int>(list[slot]) : -1;
-        if (rows[r] >= 0) {
-          first = min(first, rows[r]);
-          last = max(last, rows[r]);
-        }
+    int first = n, last = -1;
+    for (int r = 0; r < kFixRows; ++r) {
+      const int i = srows[r];
+      if (i >= 0) {
+        first = min(first, i);
+        last = max(last, i);
       }
-      const int jlo = max(0, first + s_lo - (n - 1));
-      const int jhi = min(n - 1, last + s_hi - (n - 1));
+    }
+    const int jlo = max(0, first + smin - (n - 1));
+    const int jhi = min(n - 1, last + smax - (n - 1));
+    for (int e = tid; e < m * kFixRows; e += 256) {
+      const int l = e / kFixRows, r = e % kFixRows;
+      const int i = srows[r];
+      sq[e] = i >= 0 ? pq[static_cast<size_t>(l) * ld + i] : 0.f;
+    }
+    double zt[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) zt[v] = 0.0;
+    double dacc = 0.0;
 
-      __syncthreads();
-      for (int e2 = tid; e2 < m * kFixRows; e2 += 256) {
-        const int l = e2 / kFixRows, r = e2 % kFixRows;
-        sq[l][r] = rows[r] >= 0 ? pq[static_cast<size_t>(l) * ld + rows[r]] : 0.f;
-      }
-      double acc[kFixRows];
+    for (int jc = (jlo / kFixKeys) * kFixKeys; jc <= jhi; jc += kFixKeys) {
+      // ---- S = phi(q_rows) phi(k_chunk)^T: wave w holds keys jc + 32 w ...
+      floatx16 sacc;
 #pragma unroll
-      for (int r = 0; r < kFixRows; ++r) acc[r] = 0.0;
-
-      for (int jc = (jlo / kFixChunk) * kFixChunk; jc <= jhi; jc += kFixChunk) {
-        __syncthreads();  // sq staged / previous chunk's sp consumed
-        float kk[kFixRows][4];
+      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
+      // phi(k) of the chunk, kFixL features at a time; the next step's values
+      // are loaded into registers while the matrix cores work on this one
+      float kn[kFixL * kFixKeys / 256];
+      auto load_step = [&](int l0) {
 #pragma unroll
-        for (int r = 0; r < kFixRows; ++r)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) kk[r][q] = 0.f;
-        int jj[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) jj[q] = min(jc + tid + 256 * q, n - 1);
-#pragma unroll 8
-        for (int l = 0; l < m; ++l) {
-          float kv[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) kv[q] = pk[static_cast<size_t>(l) * ld + jj[q]];
-          const float4 qa = *reinterpret_cast<const float4*>(&sq[l][0]);
-          const float4 qb = *reinterpret_cast<const float4*>(&sq[l][4]);
-          const float qr[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
-#pragma unroll
-          for (int r = 0; r < kFixRows; ++r)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) kk[r][q] = fmaf(qr[r], kv[q], kk[r][q]);
+        for (int q = 0; q < kFixL * kFixKeys / 256; ++q) {
+          const int e = tid + 256 * q;
+          const int l = l0 + e / kFixKeys, j = jc + e % kFixKeys;
+          kn[q] = (l < m && j < n) ? pk[static_cast<size_t>(l) * ld + j] : 0.f;
         }
+      };
+      load_step(0);
+      for (int l0 = 0; l0 < m; l0 += kFixL) {
+        __syncthreads();  // sq staged / sk free
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int j = jc + tid + 256 * q;
-#pragma unroll
-          for (int r = 0; r < kFixRows; ++r) {
-            float p = 0.f;
-            if (rows[r] >= 0 && j >= jlo && j <= jhi) {
-              const float bj = bhv[j - rows[r] + n - 1];
-              if (bj != -INFINITY) p = kk[r][q] * expf(bj);
-            }
-            sp[r][tid + 256 * q] = p;
-          }
+        for (int q = 0; q < kFixL * kFixKeys / 256; ++q) {
+          const int e = tid + 256 * q;
+          sk[(e / kFixKeys) * kFixStride + e % kFixKeys] = kn[q];
         }
         __syncthreads();
-        if (sub < nsub) {
-          float part[kFixRows];
+        if (l0 + kFixL < m) load_step(l0 + kFixL);
+        const int lend = min(kFixL, m - l0);
+        if (lend == kFixL) {
+          // full step: all operands read first, then the matrix ops back to back
+          float qa[kFixL / 2], kb[kFixL / 2];
 #pragma unroll
-          for (int r = 0; r < kFixRows; ++r) part[r] = 0.f;
-          const int jend = min(kFixChunk, jhi - jc + 1);
-          auto vload = [&](int j) -> float {
-            if (col == d) return 1.f;
-            const size_t idx = vbase + static_cast<size_t>(jc + j) * d + col;
-            return v_bf16 ? to_f32(static_cast<const uint16_t*>(vraw)[idx]) : static_cast<const float*>(vraw)[idx];
-          };
-          // 8 keys per step so that 8 loads of v are in flight at once
-          int j = sub;
-          for (; j + 7 * nsub < jend; j += 8 * nsub) {
-            float vv[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) vv[u] = vload(j + u * nsub);
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-#pragma unroll
-              for (int r = 0; r < kFixRows; ++r) part[r] = fmaf(sp[r][j + u * nsub], vv[u], part[r]);
-          }
-          for (; j < jend; j += nsub) {
-            const float vv = vload(j);
-#pragma unroll
-            for (int r = 0; r < kFixRows; ++r) part[r] = fmaf(sp[r][j], vv, part[r]);
+          for (int q = 0; q < kFixL / 2; ++q) {
+            qa[q] = sq[(l0 + 2 * q + lk) * kFixRows + lr];
+            kb[q] = sk[(2 * q + lk) * kFixStride + wave * 32 + lr];
           }
 #pragma unroll
-          for (int r = 0; r < kFixRows; ++r) acc[r] += static_cast<double>(part[r]);
+          for (int q = 0; q < kFixL / 2; ++q) sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[q], kb[q], sacc, 0, 0, 0);
+        } else {
+          for (int kk = 0; kk < lend; kk += 2) {
+            const int l = kk + lk;
+            const float qa = l < lend ? sq[(l0 + l) * kFixRows + lr] : 0.f;
+            const float kb = sk[l * kFixStride + wave * 32 + lr];
+            sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa, kb, sacc, 0, 0, 0);
+          }
         }
       }
-      // sum the key subsets: thread (col, sub) -> red, then thread col < cols adds them up
-      __syncthreads();  // red aliases sp
+      __syncthreads();  // sk reads done: it now holds P
+      // ---- P = S * c_{j-i}; lane holds key wave*32 + lr, rows 8(v/4) + 4 lk + v%4
 #pragma unroll
-      for (int r = 0; r < kFixRows; ++r) red[tid][r] = acc[r];
-      __syncthreads();
-      if (tid < cols) {
-#pragma unroll
-        for (int r = 0; r < kFixRows; ++r) {
-          double s2 = red[tid][r];
-          for (int sb = 1; sb < nsub; ++sb) s2 += red[sb * cols + tid][r];
-          acc[r] = s2;
+      for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
+        const int key = wave * 32 + lr, j = jc + key, i = srows[row];
+        float pv = 0.f;
+        if (i >= 0 && j < n) {
+          const float bj = bhv[j - i + n - 1];
+          if (bj != -INFINITY) pv = sacc[v] * expf(bj);
         }
+        sk[row * kFixStride + key] = pv;
       }
       __syncthreads();
-      if (tid < cols) {
+      // ---- denominators: thread (row tid % 32, keys 16 (tid / 32) ...)
+      {
+        const int row = tid & 31, seg = tid >> 5;
+        float ds = 0.f;
 #pragma unroll
-        for (int r = 0; r < kFixRows; ++r) red[tid][r] = acc[r];
+        for (int k2 = 0; k2 < 16; ++k2) ds += sk[row * kFixStride + seg * 16 + k2];
+        dacc += static_cast<double>(ds);
+      }
+      // ---- numerators: Z[row][c] += sum_key P[row][key] v[key][c]
+      if (pv_wave) {
+        floatx16 zc;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) zc[v] = 0.f;
+        const int col = my_tile * 32 + lr;
+        const int kb0 = my_part * pv_keys;
+        // v rows in blocks of 32 keys, the next block in flight during the
+        // matrix ops of this one
+        float vb[16], vn[16];
+        auto load_v = [&](int k0) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const int j = jc + k0 + 2 * q + lk;
+            vn[q] = (col < d && j < n) ? vload(j, col) : 0.f;
+          }
+        };
+        load_v(kb0);
+        for (int k0 = kb0; k0 < kb0 + pv_keys; k0 += 32) {
+#pragma unroll
+          for (int q = 0; q < 16; ++q) vb[q] = vn[q];
+          if (k0 + 32 < kb0 + pv_keys) load_v(k0 + 32);
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            const float pa = sk[lr * kFixStride + k0 + 2 * q + lk];
+            zc = __builtin_amdgcn_mfma_f32_32x32x2f32(pa, vb[q], zc, 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) zt[v] += static_cast<double>(zc[v]);
+      }
+    }
+    // ---- reduce the key splits, the denominators, and write the rows
+    dsum[tid >> 5][tid & 31] = dacc;
+    for (int part = 1; part < wpt; ++part) {
+      __syncthreads();
+      if (pv_wave && my_part == part) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) red[my_tile * 1024 + v * 64 + lane] = zt[v];
       }
       __syncthreads();
-      if (tid < d) {
+      if (pv_wave && my_part == 0) {
 #pragma unroll
-        for (int r = 0; r < kFixRows; ++r)
-          if (rows[r] >= 0)
-            z[(static_cast<size_t>(bh) * n + rows[r]) * d + tid] = static_cast<float>(red[tid][r] / red[d][r]);
+        for (int v = 0; v < 16; ++v) zt[v] += red[my_tile * 1024 + v * 64 + lane];
+      }
+    }
+    __syncthreads();
+    if (tid < kFixRows) {
+      double den = 0.0;
+      for (int sg = 0; sg < 8; ++sg) den += dsum[sg][tid];
+      sden[tid] = den;
+    }
+    __syncthreads();
+    if (pv_wave && my_part == 0) {
+      const int col = my_tile * 32 + lr;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
+        const int i = srows[row];
+        if (i >= 0 && col < d) z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[v] / sden[row]);
       }
     }
   }
@@ -1144,21 +1215,30 @@ hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb
 }
 
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
-                          unsigned* fix, int BH, int H, int n, int l2, int d, int m, hipStream_t st) {
+                          unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2, int d, int m,
+                          hipStream_t st) {
   const int tiles_n = (n + 63) / 64;
   const size_t lds = (static_cast<size_t>((d + 1) * 65 + 1) & ~static_cast<size_t>(1)) * sizeof(float) +
                      static_cast<size_t>(m + 1) * sizeof(float2);
   hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), lds, st,
-                     part, phiq, Wb, hnorm, z, fix, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2), tiles_n);
+                     part, phiq, Wb, hnorm, z, fix, fixmask, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2), tiles_n);
   return hipGetLastError();
 }
 
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b, float* z,
-                        const unsigned* fix, int BH, int H, int n, int ld, int d, int m, hipStream_t st) {
+                        const unsigned* fix, const unsigned long long* fixmask, int BH, int H, int n, int ld, int d,
+                        int m, hipStream_t st) {
   const long long blocks = static_cast<long long>(BH) * kFixPerHead;
   const size_t lds = static_cast<size_t>(m) * kFixRows * sizeof(float);
+  if (lds > 64 * 1024) {
+    // phi(q) of a group exceeds the default dynamic LDS limit for m > 512
+    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fixup),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                       static_cast<int>(kMaxM * kFixRows * sizeof(float)));
+    if (once != hipSuccess) return once;
+  }
   hipLaunchKernelGGL(k_fixup, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik, v, bf16 ? 1 : 0,
-                     b, z, fix, BH, H, n, ld, d, m);
+                     b, z, fix, fixmask, BH, H, n, ld, d, m);
   return hipGetLastError();
 }
 

@@ -23,8 +23,8 @@ struct AttnLayout {
   size_t x2;         // float  [BH][ks][m][pairs] squared norms of the packed channels
   size_t wb;         // float2 [BH][m+1]         bound weights of the certification
   size_t part;       // float  [BH][splits][d+1][n] numerators / denominator per class split
-  size_t fix;        // uint   [BH + 1 + BH n]   rows queued per head, total; then the
-                     //                          queued row indices of each head
+  size_t fix;        // uint   [BH + 1]          rows queued per head, then their total
+  size_t fixmask;    // uint64 [BH][ceil(n/64)]  queued rows: bit i % 64 of word i / 64
   size_t total;
 };
 AttnLayout attn_layout(int B, int H, int n, int d, int m);
@@ -63,9 +63,11 @@ hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, 
 hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb, int BH, int m, int d, int ksplit,
                                 hipStream_t st);
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
-                          unsigned* fix, int BH, int H, int n, int l2, int d, int m, hipStream_t st);
+                          unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2, int d, int m,
+                          hipStream_t st);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
-                        float* z, const unsigned* fix, int BH, int H, int n, int ld, int d, int m,
+                        float* z, const unsigned* fix, const unsigned long long* fixmask, int BH, int H, int n, int ld,
+                        int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
 hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st);
