@@ -23,10 +23,11 @@ constexpr int kLog2R = 4;      // 16 complex values per thread
 // are the even and odd bins), 2 at N = 8192 and 4 at N = 16384: transforms
 // never exceed 4096 points, which keeps their state in the register file.
 //
-// A transform is owned by T = L' / 16 threads (16 complex values each); a
-// work-group holds G units of T threads (filling 256 threads for short
-// transforms); a unit of the convolution kernel runs KH residue classes as
-// interleaved transforms sharing loads, barriers and accumulators.
+// A transform is owned by T = L' / R threads (R complex values each); a
+// work-group holds G units of T threads (G > 1 only for transforms of fewer
+// than 128 threads, filling 256); a unit of the convolution kernel runs KH
+// residue classes as interleaved transforms sharing loads, barriers and
+// accumulators.
 template <int L2>
 struct Conf {
   static constexpr int FOLD = L2 <= 12 ? 1 : (L2 == 13 ? 2 : 4);
@@ -38,7 +39,7 @@ struct Conf {
   using F = Fft<L2T, LOG2R, 1 + L2 - L2T>;  // twiddles come from the W_{2N} table
   static constexpr int N = 1 << L2;
   static constexpr int LT = F::N;  // transform length 2N / S
-  static constexpr int G = F::T >= 256 ? 1 : 256 / F::T;
+  static constexpr int G = F::T >= 128 ? 1 : 256 / F::T;  // units per work-group
   static constexpr int THREADS = G * F::T;
   static constexpr int WAVES = (THREADS + 63) / 64;
   static constexpr int LDS_SLOTS = F::P > 1 ? G * F::LDS : 1;

@@ -205,6 +205,18 @@ struct Fft {
   static constexpr int P = LR == 0 ? 1 : (LOG2N + LR - 1) / LR;  // passes
   // log2 of the radix of pass p: LR for all passes but the last, which takes the rest.
   __host__ __device__ static constexpr int lr(int p) { return p + 1 < P ? LR : LOG2N - LR * (P - 1); }
+  // LDS hand-over between passes.  A transform of at most 64 threads lives in
+  // one wave, whose LDS operations are performed in order: a compiler-level
+  // wave barrier suffices and the other waves of the work-group run on.
+  __device__ __forceinline__ static void unit_sync() {
+    if constexpr (T <= 64) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    } else {
+      __syncthreads();
+    }
+  }
   __host__ __device__ static constexpr int pad(int a) { return a + (a >> (LR > 0 ? LR : 1)); }
   static constexpr int LDS = N + (N >> (LR > 0 ? LR : 1)) + 1;  // float2 slots per transform
 
@@ -241,7 +253,7 @@ struct Fft {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
     if constexpr (p > 0) {
-      __syncthreads();
+      unit_sync();
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
@@ -292,7 +304,7 @@ struct Fft {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
     if constexpr (p + 1 < P) {
-      __syncthreads();
+      unit_sync();
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
