@@ -205,11 +205,31 @@ struct Fft {
   static constexpr int P = LR == 0 ? 1 : (LOG2N + LR - 1) / LR;  // passes
   // log2 of the radix of pass p: LR for all passes but the last, which takes the rest.
   __host__ __device__ static constexpr int lr(int p) { return p + 1 < P ? LR : LOG2N - LR * (P - 1); }
-  // LDS hand-over between passes.  A transform of at most 64 threads lives in
-  // one wave, whose LDS operations are performed in order: a compiler-level
-  // wave barrier suffices and the other waves of the work-group run on.
-  __device__ __forceinline__ static void unit_sync() {
-    if constexpr (T <= 64) {
+  // Whether the LDS hand-over between passes p and p + 1 stays inside 64-lane
+  // waves: every position a thread reads in pass p + 1 was written in pass p
+  // by a thread of its own wave (the same pairs exchange data, in reverse,
+  // in the inverse transform).
+  __host__ __device__ static constexpr bool wave_local(int p) {
+    if (T <= 64) return true;
+    const int la = lr(p), lena = N >> (LR * p), spa = lena >> la;
+    const int lb = lr(p + 1), rpb = 1 << lb, ub = R / rpb, lenb = N >> (LR * (p + 1)), spb = lenb >> lb;
+    for (int tau = 0; tau < T; ++tau)
+      for (int u = 0; u < ub; ++u) {
+        const int bb = tau + T * u, base = (bb / spb) * lenb + bb % spb;
+        for (int r = 0; r < rpb; ++r) {
+          const int pos = base + spb * r;
+          const int writer = ((pos / lena) * spa + pos % spa) % T;
+          if (writer / 64 != tau / 64) return false;
+        }
+      }
+    return true;
+  }
+  // LDS hand-over across boundary p.  Inside a wave, LDS operations are
+  // performed in order: a compiler-level wave barrier suffices and the other
+  // waves of the work-group run on.  Otherwise a work-group barrier.
+  template <int p>
+  __device__ __forceinline__ static void boundary_sync() {
+    if constexpr (wave_local(p)) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -253,7 +273,7 @@ struct Fft {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
     if constexpr (p > 0) {
-      unit_sync();
+      boundary_sync<p - 1>();
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
@@ -304,7 +324,7 @@ struct Fft {
     constexpr int LRP = lr(p), RP = 1 << LRP, U = R / RP;
     constexpr int L = N >> (LR * p), SP = L >> LRP;
     if constexpr (p + 1 < P) {
-      unit_sync();
+      boundary_sync<p>();
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
