@@ -178,6 +178,12 @@ SMALL = [
     (1, 1, 8192, 64, 16, "f32", "causal"),  # early rows need the exact path
     (1, 1, 16384, 64, 2, "f32", "normal"),
     (1, 1, 16384, 64, 16, "bf16", "causal"),
+    # exact-row path at every column-tile count and past 512 features
+    # (dynamic LDS above 64 KiB), odd m
+    (1, 1, 2048, 96, 40, "f32", "causal"),
+    (1, 1, 1024, 128, 601, "f32", "causal"),
+    (1, 2, 512, 128, 1024, "bf16", "causal"),
+    (1, 1, 700, 20, 33, "f32", "causal"),
 ]
 
 
