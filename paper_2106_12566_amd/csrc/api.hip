@@ -95,6 +95,8 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.part = take(bh * conv_splits(L.l2) * cols * n * sizeof(float));
   L.fix = take((bh + 1) * sizeof(unsigned));
   L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
+  L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
+  L.brange = take(static_cast<size_t>(H) * sizeof(int2));
   L.total = off;
   return L;
 }
@@ -269,6 +271,8 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   float* part = reinterpret_cast<float*>(w + L.part);
   unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
   unsigned long long* fixmask = reinterpret_cast<unsigned long long*>(w + L.fixmask);
+  double* fixpart = reinterpret_cast<double*>(w + L.fixpart);
+  int2* brange = reinterpret_cast<int2*>(w + L.brange);
   const int BHi = static_cast<int>(bh);
   const int N = 1 << L.l2;
   const bool bf16 = qkv_dtype == KRPE_BF16;
@@ -298,7 +302,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, fixmask, BHi, H, n, L.l2, d, m, st),
                                   "combine launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, fixmask, BHi, H, n, N, d, m, st),
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, fixmask, fixpart, brange, BHi, H, n, N, d, m, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);

@@ -776,30 +776,66 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
 
 // ---------------------------------------------------------------- fixup --
 // Exact evaluation of Eq. (10) for the rows k_combine could not certify, on
-// the matrix cores.  Work-group (bh, k) of a fixed grid takes groups k,
-// k + kFixPerHead, ... of 32 queued rows of head bh and walks the keys in
-// chunks of 128 aligned to multiples of 128:
+// the matrix cores.  The queued rows of head bh form groups of 32 in row
+// order; a group's keys (with a finite b_{j-i}) are walked in chunks of 128
+// aligned to multiples of 128, and when the head has fewer groups than
+// work-group slots each group's chunks are split into contiguous shares
+// (fix_key_parts).  Work-group (bh, k) takes items k, k + slots, ...:
 //   S = phi(q_rows) phi(k_chunk)^T      32 x 128, fp32 MFMA over the m features
 //   P = S * c_{j-i}                     0 where b_{j-i} = -inf or j >= n
 //   Z += P [v, 1]                       fp32 MFMA per chunk, totals in fp64
-// A row's sums depend only on its own values and the fixed chunking (chunks
-// that are outside its range add exact zeros), so results do not depend on
-// which rows share a group.  Waves: S takes one 32-key tile each; P V takes
-// the ceil(d / 32) column tiles, the spare waves splitting the chunk's keys.
-// Every work-group exits when its head's queue is done.
+// An unsplit group writes its rows; shares go to fixpart and k_fixup_combine
+// adds them in share order.  Chunks outside a row's range add exact zeros, so
+// a row's result depends only on its values and the share boundaries.  Waves:
+// S takes one 32-key tile each; P V takes the ceil(d / 32) column tiles, the
+// spare waves splitting the chunk's keys.
 constexpr int kFixRows = 32;
 constexpr int kFixKeys = 128;
 constexpr int kFixL = 32;                 // features staged per step
 constexpr int kFixStride = kFixKeys + 1;  // LDS row stride (odd: column reads hit distinct banks)
-constexpr int kFixPerHead = 64;
 constexpr int kFixMaxTiles = (1 << kMaxLog2N) / 64;
+constexpr int kFixMaxParts = 16;
 
-__global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, const float* __restrict__ phik,
-                                               const void* __restrict__ vraw, int v_bf16,
+// Work items of a head: every group of 32 rows, each split into kparts shares
+// of its key chunks when the head has fewer groups than work-group slots.
+// A share keeps at least 4 of the n / 128 chunks.
+__host__ __device__ inline int fix_key_parts(int ngroups, int slots, int n) {
+  if (ngroups <= 0) return 1;
+  int k = slots / ngroups;
+  const int by_len = (n + 4 * kFixKeys - 1) / (4 * kFixKeys);
+  if (k > by_len) k = by_len;
+  return k < 1 ? 1 : (k > kFixMaxParts ? kFixMaxParts : k);
+}
+
+// Range [lo, hi] of s = t + n - 1 where b_t is finite, per head (lo > hi if none).
+__global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int2* __restrict__ brange, int n) {
+  __shared__ int smin, smax;
+  const float* __restrict__ bh = b + static_cast<size_t>(blockIdx.x) * (2 * n - 1);
+  if (threadIdx.x == 0) {
+    smin = 2 * n;
+    smax = -1;
+  }
+  __syncthreads();
+  int lo = 2 * n, hi = -1;
+  for (int sidx = threadIdx.x; sidx < 2 * n - 1; sidx += 256)
+    if (bh[sidx] != -INFINITY) {
+      lo = min(lo, sidx);
+      hi = max(hi, sidx);
+    }
+  atomicMin(&smin, lo);
+  atomicMax(&smax, hi);
+  __syncthreads();
+  if (threadIdx.x == 0) brange[blockIdx.x] = make_int2(smin, smax);
+}
+
+template <typename TV>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_fixup(const float* __restrict__ phiq, const float* __restrict__ phik,
+                                               const TV* __restrict__ vv,
                                                const float* __restrict__ b, float* __restrict__ z,
                                                const unsigned* __restrict__ fix,
-                                               const unsigned long long* __restrict__ fixmask, int BH, int H, int n,
-                                               int ld, int d, int m) {
+                                               const unsigned long long* __restrict__ fixmask,
+                                               double* __restrict__ fixpart, const int2* __restrict__ brange,
+                                               int BH, int H, int n, int ld, int d, int m, int slots) {
   extern __shared__ __align__(16) float sq[];   // phi(q) of the group's rows, [l][32]
   __shared__ __align__(16) float sk[kFixL * kFixStride];  // phi(k) chunk [l][key]; then P [row][key]
   __shared__ double dsum[8][kFixRows];
@@ -812,11 +848,13 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
   static_assert(sizeof(float) * kFixL * kFixStride >= 2 * 1024 * sizeof(double), "red fits in sk");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lk = lane >> 5;
-  // slot-major order: the first group of every head is dispatched first
+  // slot-major order: the first item of every head is dispatched first
   const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
   const unsigned count = fix[bh];
   const int ngroups = static_cast<int>((count + kFixRows - 1) / kFixRows);
-  if (kslot >= ngroups) return;  // uniform per work-group
+  const int kparts = fix_key_parts(ngroups, slots, n);
+  const int items = ngroups * kparts;
+  if (kslot >= items) return;  // uniform per work-group
   const int h = bh % H;
   const float* __restrict__ bhv = b + static_cast<size_t>(h) * (2 * n - 1);
   const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * ld;
@@ -828,10 +866,7 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
   const int my_tile = wave / wpt, my_part = wave % wpt;
   const bool pv_wave = wave < tiles * wpt;
   const int pv_keys = kFixKeys / wpt;
-  auto vload = [&](int j, int c) -> float {
-    const size_t idx = vbase + static_cast<size_t>(j) * d + c;
-    return v_bf16 ? to_f32(static_cast<const uint16_t*>(vraw)[idx]) : static_cast<const float*>(vraw)[idx];
-  };
+  auto vload = [&](int j, int c) -> float { return to_f32(vv[vbase + static_cast<size_t>(j) * d + c]); };
 
   // Queued rows in row order: group g takes the ranks 32 g .. 32 g + 31 of
   // the set bits of the head's mask words (prefix counts in spre).
@@ -839,8 +874,9 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
   for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
   // Range of s = t + n - 1 where b_t is finite.
   if (tid == 0) {
-    smin = 2 * n;
-    smax = -1;
+    const int2 br = brange[h];
+    smin = br.x;
+    smax = br.y;
   }
   __syncthreads();
   if (tid == 0) {
@@ -851,18 +887,8 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
     }
     spre[tiles_n] = acc;
   }
-  {
-    int lo = 2 * n, hi = -1;
-    for (int sidx = tid; sidx < 2 * n - 1; sidx += 256)
-      if (bhv[sidx] != -INFINITY) {
-        lo = min(lo, sidx);
-        hi = max(hi, sidx);
-      }
-    atomicMin(&smin, lo);
-    atomicMax(&smax, hi);
-  }
-
-  for (int grp = kslot; grp < ngroups; grp += kFixPerHead) {
+  for (int item = kslot; item < items; item += slots) {
+    const int grp = item / kparts, kpart = item % kparts;
     __syncthreads();  // previous group's srows / sq / red consumed
     if (tid < kFixRows) {
       const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
@@ -900,7 +926,11 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
     for (int v = 0; v < 16; ++v) zt[v] = 0.0;
     double dacc = 0.0;
 
-    for (int jc = (jlo / kFixKeys) * kFixKeys; jc <= jhi; jc += kFixKeys) {
+    // this item's share of the group's key chunks (contiguous, chunk-aligned)
+    const int c0 = jlo / kFixKeys, nch = jhi >= jlo ? jhi / kFixKeys - c0 + 1 : 0;
+    const int cb = c0 + static_cast<int>(static_cast<long long>(nch) * kpart / kparts);
+    const int ce = c0 + static_cast<int>(static_cast<long long>(nch) * (kpart + 1) / kparts);
+    for (int jc = cb * kFixKeys; jc < ce * kFixKeys; jc += kFixKeys) {
       // ---- S = phi(q_rows) phi(k_chunk)^T: wave w holds keys jc + 32 w ...
       floatx16 sacc;
 #pragma unroll
@@ -1021,14 +1051,90 @@ __global__ __launch_bounds__(256) void k_fixup(const float* __restrict__ phiq, c
       sden[tid] = den;
     }
     __syncthreads();
-    if (pv_wave && my_part == 0) {
-      const int col = my_tile * 32 + lr;
+    if (kparts == 1) {
+      if (pv_wave && my_part == 0) {
+        const int col = my_tile * 32 + lr;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
-        const int i = srows[row];
-        if (i >= 0 && col < d) z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[v] / sden[row]);
+        for (int v = 0; v < 16; ++v) {
+          const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
+          const int i = srows[row];
+          if (i >= 0 && col < d)
+            z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[v] / sden[row]);
+        }
       }
+    } else {
+      // partial sums of this key share: fixpart[bh][item][row][c], c = d the denominator
+      double* __restrict__ out = fixpart + (static_cast<size_t>(bh) * slots + item) * kFixRows * (d + 1);
+      if (pv_wave && my_part == 0) {
+        const int col = my_tile * 32 + lr;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
+          if (col < d) out[row * (d + 1) + col] = zt[v];
+        }
+      }
+      if (tid < kFixRows) out[tid * (d + 1) + d] = sden[tid];
+    }
+  }
+}
+
+// Sums the key shares of every group k_fixup split (in share order, so the
+// result is deterministic) and writes the rows.  Work-group (bh, slot) takes
+// groups slot, slot + slots, ...
+__global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restrict__ fix,
+                                                       const unsigned long long* __restrict__ fixmask,
+                                                       const double* __restrict__ fixpart, float* __restrict__ z,
+                                                       int BH, int n, int d, int slots) {
+  __shared__ unsigned long long smask[kFixMaxTiles];
+  __shared__ unsigned spre[kFixMaxTiles + 1];
+  __shared__ int srows[kFixRows];
+  const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
+  const unsigned count = fix[bh];
+  const int ngroups = static_cast<int>((count + kFixRows - 1) / kFixRows);
+  const int kparts = fix_key_parts(ngroups, slots, n);
+  if (kparts == 1 || kslot >= ngroups) return;
+  const int tid = threadIdx.x;
+  const int tiles_n = (n + 63) / 64;
+  for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
+  __syncthreads();
+  if (tid == 0) {
+    unsigned acc = 0;
+    for (int t = 0; t < tiles_n; ++t) {
+      spre[t] = acc;
+      acc += static_cast<unsigned>(__popcll(smask[t]));
+    }
+    spre[tiles_n] = acc;
+  }
+  for (int grp = kslot; grp < ngroups; grp += slots) {
+    __syncthreads();
+    if (tid < kFixRows) {
+      const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
+      int row = -1;
+      if (rank < count) {
+        int lo = 0, hi = tiles_n;
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (spre[mid] <= rank) lo = mid; else hi = mid;
+        }
+        unsigned long long w = smask[lo];
+        for (unsigned c = spre[lo]; c < rank; ++c) w &= w - 1ull;
+        row = lo * 64 + __ffsll(static_cast<long long>(w)) - 1;
+      }
+      srows[tid] = row;
+    }
+    __syncthreads();
+    const double* __restrict__ base = fixpart + (static_cast<size_t>(bh) * slots + grp * kparts) * kFixRows * (d + 1);
+    for (int e = tid; e < kFixRows * d; e += 256) {
+      const int row = e / d, c = e % d;
+      const int i = srows[row];
+      if (i < 0) continue;
+      double num = 0.0, den = 0.0;
+      for (int p = 0; p < kparts; ++p) {
+        const double* part = base + static_cast<size_t>(p) * kFixRows * (d + 1) + row * (d + 1);
+        num += part[c];
+        den += part[d];
+      }
+      z[(static_cast<size_t>(bh) * n + i) * d + c] = static_cast<float>(num / den);
     }
   }
 }
@@ -1225,20 +1331,41 @@ hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb
   return hipGetLastError();
 }
 
+int fix_slots(int BH) {
+  const int s = 4096 / (BH > 0 ? BH : 1);
+  return s < 32 ? 32 : (s > 512 ? 512 : s);
+}
+
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b, float* z,
-                        const unsigned* fix, const unsigned long long* fixmask, int BH, int H, int n, int ld, int d,
-                        int m, hipStream_t st) {
-  const long long blocks = static_cast<long long>(BH) * kFixPerHead;
+                        const unsigned* fix, const unsigned long long* fixmask, double* fixpart, int2* brange, int BH,
+                        int H, int n, int ld, int d, int m, hipStream_t st) {
+  const int slots = fix_slots(BH);
+  hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, n);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  const long long blocks = static_cast<long long>(BH) * slots;
   const size_t lds = static_cast<size_t>(m) * kFixRows * sizeof(float);
   if (lds > 64 * 1024) {
     // phi(q) of a group exceeds the default dynamic LDS limit for m > 512
-    static const hipError_t once = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fixup),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                       static_cast<int>(kMaxM * kFixRows * sizeof(float)));
+    static const hipError_t once = [] {
+      const int bytes = static_cast<int>(kMaxM * kFixRows * sizeof(float));
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fixup<float>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+      if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fixup<uint16_t>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+      return e;
+    }();
     if (once != hipSuccess) return once;
   }
-  hipLaunchKernelGGL(k_fixup, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik, v, bf16 ? 1 : 0,
-                     b, z, fix, fixmask, BH, H, n, ld, d, m);
+  if (bf16)
+    hipLaunchKernelGGL(k_fixup<uint16_t>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
+                       static_cast<const uint16_t*>(v), b, z, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m, slots);
+  else
+    hipLaunchKernelGGL(k_fixup<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
+                       static_cast<const float*>(v), b, z, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m, slots);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, fixmask, fixpart, z,
+                     BH, n, d, slots);
   return hipGetLastError();
 }
 

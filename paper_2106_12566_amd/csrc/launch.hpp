@@ -25,6 +25,8 @@ struct AttnLayout {
   size_t part;       // float  [BH][splits][d+1][n] numerators / denominator per class split
   size_t fix;        // uint   [BH + 1]          rows queued per head, then their total
   size_t fixmask;    // uint64 [BH][ceil(n/64)]  queued rows: bit i % 64 of word i / 64
+  size_t fixpart;    // double [BH][slots][32][d+1] key-share partial sums of the exact rows
+  size_t brange;     // int2   [H]               range of finite b per head
   size_t total;
 };
 AttnLayout attn_layout(int B, int H, int n, int d, int m);
@@ -65,9 +67,12 @@ hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
                           unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2, int d, int m,
                           hipStream_t st);
+// Work-group slots per head of the exact-row kernels, and their partial sums:
+// fixpart holds BH * fix_slots(BH) * 32 * (d + 1) doubles.
+int fix_slots(int BH);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
-                        float* z, const unsigned* fix, const unsigned long long* fixmask, int BH, int H, int n, int ld,
-                        int d, int m,
+                        float* z, const unsigned* fix, const unsigned long long* fixmask, double* fixpart,
+                        int2* brange, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
 hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st);
