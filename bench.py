@@ -116,7 +116,7 @@ def blas_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
-def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None):
+def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool = False):
     """Time the fp64 oracle (Eq. (10), O(n^2) per head) on whole (batch, head) units.
 
     Runs units until `budget_s` of wall time is spent (at least one), and
@@ -134,7 +134,7 @@ def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None):
     worst = 0.0
     for beta, h in units:
         z, _ = oracle.attention(d["q"][beta:beta + 1, h:h + 1], d["k"][beta:beta + 1, h:h + 1],
-                                d["v"][beta:beta + 1, h:h + 1], d["b"][h:h + 1], d["W"][h:h + 1])
+                                d["v"][beta:beta + 1, h:h + 1], d["b"][h:h + 1], d["W"][h:h + 1], nprf=nprf)
         done += 1
         if z_gpu is not None:
             num = np.max(np.abs(z_gpu[beta, h] - z[0, 0]), axis=-1)
@@ -165,6 +165,8 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--nprf", action="store_true",
+                    help="normalise the rows of q and k first (Algorithm 1's NPRF attention)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, copy a buffer of this size (MiB) 3 times, so that "
                          "profiler byte counters can be scaled by a kernel of known traffic")
@@ -207,12 +209,12 @@ def main() -> int:
     events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(args.steps)]
 
     for _ in range(args.warmup):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf)
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
     for s in range(args.steps):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s])
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], nprf=args.nprf)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
@@ -248,7 +250,7 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "B": B, "H": H, "n": n, "d": dd, "m": m,
                    "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
-                   "causal": wl.causal, "ms_per_layer": ms_per_step, "stages_ms": stages,
+                   "causal": wl.causal, "nprf": args.nprf, "ms_per_layer": ms_per_step, "stages_ms": stages,
                    "conv_stage_hbm_gbs": conv_gbs,
                    "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)},
         "roofline": {"bound": "alu", "kernel": "k_conv_contract", "achieved": achieved_tflops,
@@ -265,7 +267,7 @@ def main() -> int:
         result["config"]["copy_calibration_bytes"] = src.numel() * 4
     if not args.no_cpu_baseline:
         z_gpu = out.cpu().numpy()
-        cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu)
+        cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu, nprf=args.nprf)
         result["cpu_baseline"] = {k2: cb[k2] for k2 in ("value", "unit", "cores", "kind", "sample")}
         result["config"]["parity_rownorm_err"] = err
         result["config"]["parity_units"] = units

@@ -70,6 +70,14 @@ typedef enum {
   KRPE_ERR_ALIGN = 8        /* a pointer is not 16-byte aligned */
 } krpe_status_t;
 
+/*
+ * Option bits of the _ex entry points (other bits: KRPE_ERR_UNSUPPORTED).
+ * KRPE_NPRF: divide every row of q and k (of x for the feature map) by its l2
+ * norm before the feature map -- the first step of Algorithm 1, "Normalized
+ * Kernelized Attention with RPE" (Section 3.3).  A zero row stays zero.
+ */
+#define KRPE_NPRF 1u
+
 /* Version of this ABI (incremented on any incompatible change). */
 int krpe_abi_version(void);
 
@@ -89,6 +97,9 @@ const char* krpe_last_error(void);
  */
 krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float* phi,
                                int B, int H, int n, int d, int m, void* stream);
+/* krpe_feature_map with option bits (KRPE_NPRF: phi of x / ||x||). */
+krpe_status_t krpe_feature_map_ex(const void* x, int x_dtype, const float* W, float* phi,
+                                  int B, int H, int n, int d, int m, unsigned flags, void* stream);
 
 /*
  * Bytes of workspace krpe_toeplitz_conv needs for B x H heads of C channels of
@@ -100,7 +111,8 @@ size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n);
  * Product with the Toeplitz matrix C = {c_{j-i}} of Eqs. (12)-(13), per channel:
  *   y[beta, h, ch, i] = sum_{j<n} exp(b[h, j - i + n - 1]) * a[beta, h, ch, j]
  * b : [H, 2n-1] fp32     a, y : [B, H, C, n] fp32 (sequence-contiguous channels)
- * Computed as a zero-padded length-2N FFT convolution (two length-N halves).
+ * Computed as a zero-padded length-2N FFT convolution (split into residue
+ * classes of its frequency bins, each a transform of at most 4096 points).
  */
 krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
                                  int B, int H, int C, int n,
@@ -127,7 +139,16 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
                                  void* ws, size_t ws_bytes, void* stream);
 
 /*
- * krpe_attention_fwd with per-stage timing: when `events` is not NULL it points
+ * krpe_attention_fwd with option bits: KRPE_NPRF normalises the rows of q
+ * and k first (Algorithm 1's NPRF attention).  The same workspace size.
+ */
+krpe_status_t krpe_attention_fwd_ex(const void* q, const void* k, const void* v, int qkv_dtype,
+                                    const float* b, const float* W, float* z,
+                                    int B, int H, int n, int d, int m, unsigned flags,
+                                    void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * krpe_attention_fwd_ex with per-stage timing: when `events` is not NULL it points
  * to KRPE_STAGE_EVENTS hipEvent_t handles (as void*), recorded on `stream`
  * before the spectrum of c, before the feature maps, before the FFT
  * convolution + contraction kernel, before the final division and after it.
@@ -137,7 +158,7 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
 krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const void* v,
                                           int qkv_dtype, const float* b, const float* W,
                                           float* z, int B, int H, int n, int d, int m,
-                                          void* ws, size_t ws_bytes, void* stream,
+                                          unsigned flags, void* ws, size_t ws_bytes, void* stream,
                                           void* const* events);
 
 /*

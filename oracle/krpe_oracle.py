@@ -19,6 +19,9 @@ float64 (inputs given in fp32 or bf16 are converted exactly):
 * ``attention_rows``    -- the same formula evaluated for selected rows only,
                            so that outputs of full-size workloads can be
                            checked one by one.
+* ``normalize_rows``    -- the first step of Algorithm 1 (NPRF attention,
+                           Section 3.3): every query and key divided by its
+                           l2 norm; ``attention(..., nprf=True)`` applies it.
 
 Conventions (readings of the paper, stated once here):
 * b[h, s] holds b_t for t = s - (n - 1), the ordering of Algorithm 1's
@@ -39,7 +42,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = ["prf_features", "toeplitz_matrix", "toeplitz_product", "attention",
-           "attention_rows"]
+           "attention_rows", "normalize_rows"]
 
 
 def _f64(x) -> np.ndarray:
@@ -60,6 +63,13 @@ def prf_features(x, W) -> np.ndarray:
     proj = x @ np.swapaxes(W, -1, -2)                 # w_l . x for every row
     half_sq = 0.5 * np.sum(x * x, axis=-1, keepdims=True)
     return np.exp(proj - half_sq) / np.sqrt(m)
+
+
+def normalize_rows(x) -> np.ndarray:
+    """x_i / ||x_i||_2 for every row (last axis), Algorithm 1's first step; zero rows stay zero."""
+    x = _f64(x)
+    norm = np.sqrt(np.sum(x * x, axis=-1, keepdims=True))
+    return np.divide(x, norm, out=np.zeros_like(x), where=norm > 0)
 
 
 def toeplitz_matrix(b_h) -> np.ndarray:
@@ -86,7 +96,7 @@ def toeplitz_product(b, a) -> np.ndarray:
     return out
 
 
-def attention(q, k, v, b, W, *, row_tile: int = 1024):
+def attention(q, k, v, b, W, *, row_tile: int = 1024, nprf: bool = False):
     """Kernelized attention with RPE, Eq. (10), evaluated directly.
 
     For every (batch, head): Phi_q, Phi_k by Eq. (5); the n x n weight matrix
@@ -94,9 +104,12 @@ def attention(q, k, v, b, W, *, row_tile: int = 1024):
     Rows are processed in tiles to bound memory.
 
     q, k, v : [B, H, n, d];  b : [H, 2n-1];  W : [H, m, d].
+    nprf: q and k rows normalised first (Algorithm 1).
     Returns (z [B, H, n, d], den [B, H, n]) in float64.
     """
     q, k, v, b, W = map(_f64, (q, k, v, b, W))
+    if nprf:
+        q, k = normalize_rows(q), normalize_rows(k)
     Bn, H, n, d = q.shape
     z = np.empty((Bn, H, n, d))
     den = np.empty((Bn, H, n))
@@ -117,7 +130,7 @@ def attention(q, k, v, b, W, *, row_tile: int = 1024):
     return z, den
 
 
-def attention_rows(q, k, v, b, W, rows):
+def attention_rows(q, k, v, b, W, rows, *, nprf: bool = False):
     """Eq. (10) for selected output rows only.
 
     rows : iterable of (beta, h, i).  Returns (z [R, d], den [R]) float64 in
@@ -125,6 +138,8 @@ def attention_rows(q, k, v, b, W, rows):
     feature map per distinct (beta, h).
     """
     b = _f64(b)
+    if nprf:
+        q, k = normalize_rows(q), normalize_rows(k)
     rows = [tuple(int(t) for t in r) for r in rows]
     n = q.shape[2]
     d = q.shape[3]

@@ -130,7 +130,7 @@ using namespace krpe;
 
 extern "C" {
 
-int krpe_abi_version(void) { return 2; }
+int krpe_abi_version(void) { return 3; }
 
 const char* krpe_status_str(int s) {
   switch (s) {
@@ -149,10 +149,11 @@ const char* krpe_status_str(int s) {
 
 const char* krpe_last_error(void) { return g_last_error.c_str(); }
 
-krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float* phi, int B, int H, int n, int d,
-                               int m, void* stream) {
+krpe_status_t krpe_feature_map_ex(const void* x, int x_dtype, const float* W, float* phi, int B, int H, int n,
+                                  int d, int m, unsigned flags, void* stream) {
   g_last_error.clear();
   if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (flags & ~static_cast<unsigned>(KRPE_NPRF)) return fail(KRPE_ERR_UNSUPPORTED, "unknown flag bits");
   if (x_dtype != KRPE_F32 && x_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "x_dtype must be F32 or BF16");
   const size_t bh = static_cast<size_t>(B) * H;
   if (bh == 0) return KRPE_OK;
@@ -165,8 +166,13 @@ krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float
     return fail(KRPE_ERR_ALIAS, "phi overlaps x or W");
   hipStream_t st = static_cast<hipStream_t>(stream);
   return hip_check(launch_feature_map(x_dtype == KRPE_BF16, x, x, W, phi, phi, 1, false, m, static_cast<int>(bh),
-                                      H, n, d, m, nullptr, st),
+                                      H, n, d, m, nullptr, (flags & KRPE_NPRF) != 0, st),
                    "feature map launch");
+}
+
+krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float* phi, int B, int H, int n, int d,
+                               int m, void* stream) {
+  return krpe_feature_map_ex(x, x_dtype, W, phi, B, H, n, d, m, 0u, stream);
 }
 
 size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n) {
@@ -230,10 +236,11 @@ size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
 }
 
 krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
-                                          const float* W, float* z, int B, int H, int n, int d, int m, void* ws,
-                                          size_t ws_bytes, void* stream, void* const* events) {
+                                          const float* W, float* z, int B, int H, int n, int d, int m, unsigned flags,
+                                          void* ws, size_t ws_bytes, void* stream, void* const* events) {
   g_last_error.clear();
   if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (flags & ~static_cast<unsigned>(KRPE_NPRF)) return fail(KRPE_ERR_UNSUPPORTED, "unknown flag bits");
   if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
   const size_t bh = static_cast<size_t>(B) * H;
   if (bh == 0) return KRPE_OK;
@@ -282,7 +289,8 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
   if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch")) return s;
   if (krpe_status_t s = record(events, 1, st)) return s;
-  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix, st),
+  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix,
+                                                     (flags & KRPE_NPRF) != 0, st),
                                   "feature map launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_vprep(bf16, v, d, 1, static_cast<long long>(n) * d, d, true, BHi, n, N,
@@ -308,10 +316,17 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   return record(events, 4, st);
 }
 
+krpe_status_t krpe_attention_fwd_ex(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
+                                    const float* W, float* z, int B, int H, int n, int d, int m, unsigned flags,
+                                    void* ws, size_t ws_bytes, void* stream) {
+  return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, flags, ws, ws_bytes, stream,
+                                     nullptr);
+}
+
 krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
                                  const float* W, float* z, int B, int H, int n, int d, int m, void* ws,
                                  size_t ws_bytes, void* stream) {
-  return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, ws, ws_bytes, stream, nullptr);
+  return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, 0u, ws, ws_bytes, stream, nullptr);
 }
 
 krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, int H, int n, int d, int m,

@@ -132,12 +132,13 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
                                                      const float* __restrict__ W, float* __restrict__ phi0,
                                                      float* __restrict__ phi1, int H, int n, int ld, int d,
                                                      int m, float inv_sqrt_m, int tiles_n, int tiles_m,
-                                                     int BH, unsigned* __restrict__ fix_counts) {
+                                                     int BH, unsigned* __restrict__ fix_counts, int nprf) {
   // Clear the exact-evaluation queue counters (fix_counts[0..BH]) for k_combine.
   if (fix_counts && threadIdx.x == 0 && blockIdx.x <= static_cast<unsigned>(BH)) fix_counts[blockIdx.x] = 0u;
   __shared__ float xs[64][33];
   __shared__ float wsm[64][33];
   __shared__ float half_sq[64];
+  __shared__ float row_scale[64];
   int bid = blockIdx.x;
   const int tn = bid % tiles_n;
   bid /= tiles_n;
@@ -182,7 +183,14 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
     }
     __syncthreads();
   }
-  if (threadIdx.x < 64) half_sq[threadIdx.x] = 0.5f * sq;
+  if (threadIdx.x < 64) {
+    // phi of x / ||x|| when normalising (Algorithm 1, first step): the
+    // projections scale by 1 / ||x|| and ||x||^2 / 2 becomes 1/2 (a zero row
+    // stays zero)
+    const bool nz = sq > 0.f;
+    half_sq[threadIdx.x] = nprf ? (nz ? 0.5f : 0.f) : 0.5f * sq;
+    row_scale[threadIdx.x] = nprf ? (nz ? rsqrtf(sq) : 0.f) : 1.f;
+  }
   __syncthreads();
   const int n_store = FEATURE_MAJOR ? ld : n;
 #pragma unroll
@@ -194,7 +202,7 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
     const int ii = FEATURE_MAJOR ? wi + col : wi + row;  // position within tile
     const int l = l0 + li, i = i0 + ii;
     if (i < n_store && l < m) {
-      const float val = i < n ? expf(acc[v] - half_sq[ii]) * inv_sqrt_m : 0.f;
+      const float val = i < n ? expf(fmaf(acc[v], row_scale[ii], -half_sq[ii])) * inv_sqrt_m : 0.f;
       if constexpr (FEATURE_MAJOR)
         phi[(static_cast<size_t>(bh) * m + l) * ld + i] = val;
       else
@@ -1240,7 +1248,7 @@ hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs,
 
 hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const float* W, float* phi0, float* phi1,
                               int nsrc, bool feature_major, int ld, int BH, int H, int n, int d, int m,
-                              unsigned* fix_counts, hipStream_t st) {
+                              unsigned* fix_counts, bool nprf, hipStream_t st) {
   const int rows = feature_major ? ld : n;
   const int tiles_n = (rows + 63) / 64, tiles_m = (m + 63) / 64;
   const long long blocks = static_cast<long long>(tiles_n) * tiles_m * BH * nsrc;
@@ -1251,19 +1259,19 @@ hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const f
     const uint16_t* c = static_cast<const uint16_t*>(x1);
     if (feature_major)
       hipLaunchKernelGGL((k_feature_map<uint16_t, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d, m,
-                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts);
+                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
     else
       hipLaunchKernelGGL((k_feature_map<uint16_t, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d,
-                         m, inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts);
+                         m, inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
   } else {
     const float* a = static_cast<const float*>(x0);
     const float* c = static_cast<const float*>(x1);
     if (feature_major)
       hipLaunchKernelGGL((k_feature_map<float, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d, m,
-                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts);
+                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
     else
       hipLaunchKernelGGL((k_feature_map<float, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d, m,
-                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts);
+                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
   }
   return hipGetLastError();
 }

@@ -26,6 +26,7 @@ _lib = None
 
 DTYPES = {torch.float32: 0, torch.bfloat16: 1}
 STAGE_EVENTS = 5
+NPRF = 1  # option bit: l2-normalise the rows of q and k (x) before the feature map
 
 
 class KrpeError(RuntimeError):
@@ -54,6 +55,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_last_error.argtypes = []
     lib.krpe_feature_map.restype = i
     lib.krpe_feature_map.argtypes = [vp, i, fp, fp, i, i, i, i, i, vp]
+    lib.krpe_feature_map_ex.restype = i
+    lib.krpe_feature_map_ex.argtypes = [vp, i, fp, fp, i, i, i, i, i, ctypes.c_uint, vp]
     lib.krpe_toeplitz_conv_workspace.restype = sz
     lib.krpe_toeplitz_conv_workspace.argtypes = [i, i, i, i]
     lib.krpe_toeplitz_conv.restype = i
@@ -62,9 +65,11 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_attention_fwd_workspace.argtypes = [i, i, i, i, i]
     lib.krpe_attention_fwd.restype = i
     lib.krpe_attention_fwd.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, vp, sz, vp]
+    lib.krpe_attention_fwd_ex.restype = i
+    lib.krpe_attention_fwd_ex.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, ctypes.c_uint, vp, sz, vp]
     lib.krpe_attention_fwd_profiled.restype = i
-    lib.krpe_attention_fwd_profiled.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, vp, sz, vp,
-                                                ctypes.POINTER(ctypes.c_void_p)]
+    lib.krpe_attention_fwd_profiled.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, ctypes.c_uint, vp, sz,
+                                                vp, ctypes.POINTER(ctypes.c_void_p)]
     lib.krpe_attention_fwd_stats.restype = i
     lib.krpe_attention_fwd_stats.argtypes = [vp, sz, i, i, i, i, i, ctypes.POINTER(ctypes.c_uint), vp]
     if path is None:
@@ -102,8 +107,10 @@ def _dtype_code(t: torch.Tensor, name: str) -> int:
     return DTYPES[t.dtype]
 
 
-def feature_map(x: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
-    """phi = exp(x W^T - ||x||^2/2) / sqrt(m) (Eq. (5)); x [B,H,n,d], W [H,m,d] -> [B,H,n,m] fp32."""
+def feature_map(x: torch.Tensor, W: torch.Tensor, nprf: bool = False) -> torch.Tensor:
+    """phi = exp(x W^T - ||x||^2/2) / sqrt(m) (Eq. (5)); x [B,H,n,d], W [H,m,d] -> [B,H,n,m] fp32.
+
+    nprf: phi of x / ||x|| (rows normalised first, Algorithm 1)."""
     lib = load()
     x = _gpu(x, "x")
     W = _gpu(W, "W")
@@ -114,9 +121,9 @@ def feature_map(x: torch.Tensor, W: torch.Tensor) -> torch.Tensor:
         raise KrpeError("W must be float32 [H, m, d] matching x")
     m = W.shape[1]
     phi = torch.empty((B, H, n, m), dtype=torch.float32, device=x.device)
-    st = lib.krpe_feature_map(_ptr(x), _dtype_code(x, "x"), _ptr(W), _ptr(phi), B, H, n, d, m,
-                              _stream(x.device))
-    _check(st, "krpe_feature_map")
+    st = lib.krpe_feature_map_ex(_ptr(x), _dtype_code(x, "x"), _ptr(W), _ptr(phi), B, H, n, d, m,
+                                 NPRF if nprf else 0, _stream(x.device))
+    _check(st, "krpe_feature_map_ex")
     return phi
 
 
@@ -159,8 +166,10 @@ def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d:
 
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
                   out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                  events=None) -> torch.Tensor:
+                  events=None, nprf: bool = False) -> torch.Tensor:
     """Eq. (10): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
+
+    ``nprf``: normalise the rows of q and k first (Algorithm 1's NPRF attention).
 
     ``out`` and ``workspace`` may be passed to reuse allocations (a uint8 tensor
     of at least attention_fwd_workspace() bytes).  ``events``: optional list of
@@ -187,10 +196,10 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     if workspace is None:
         workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
     dt = _dtype_code(q, "q")
-    args = (_ptr(q), _ptr(k), _ptr(v), dt, _ptr(b), _ptr(W), _ptr(out), B, H, n, d, m,
+    args = (_ptr(q), _ptr(k), _ptr(v), dt, _ptr(b), _ptr(W), _ptr(out), B, H, n, d, m, NPRF if nprf else 0,
             workspace.data_ptr(), workspace.numel(), _stream(q.device))
     if events is None:
-        st = lib.krpe_attention_fwd(*args)
+        st = lib.krpe_attention_fwd_ex(*args)
     else:
         if len(events) != STAGE_EVENTS:
             raise KrpeError(f"events must hold {STAGE_EVENTS} hipEvent_t handles")

@@ -39,7 +39,7 @@ def test_header_declares_the_boundary():
     for required in ("krpe_feature_map", "krpe_toeplitz_conv", "krpe_attention_fwd",
                      "krpe_toeplitz_conv_workspace", "krpe_attention_fwd_workspace",
                      "krpe_attention_fwd_profiled", "krpe_status_str", "krpe_last_error",
-                     "krpe_abi_version"):
+                     "krpe_abi_version", "krpe_feature_map_ex", "krpe_attention_fwd_ex"):
         assert required in names
 
 
@@ -49,7 +49,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.krpe_abi_version() == 2
+    assert lib.krpe_abi_version() == 3
     for s in range(9):
         assert lib.krpe_status_str(s)
     assert lib.krpe_status_str(99) == b"unknown status"
@@ -100,6 +100,18 @@ def test_attention_validation(lib):
     # empty batch: valid, nothing to do (returns before any HIP call)
     assert attn(lib, B=0, q=None, k=None, v=None, z=None) == OK
     assert lib.krpe_last_error() == b""
+
+
+def test_option_bits_validation(lib):
+    wsb = lib.krpe_attention_fwd_workspace(1, 1, 8, 4, 4)
+    ex = lambda flags: lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, flags, WSP, wsb, None)
+    assert ex(2) == UNSUP                    # unknown option bit
+    assert ex(1 | 8) == UNSUP
+    assert lib.krpe_attention_fwd_ex(None, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, WSP, wsb, None) == NULL
+    assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, None, wsb, None) == WS
+    fm = lambda flags: lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 4, flags, None)
+    assert fm(4) == UNSUP
+    assert lib.krpe_feature_map_ex(None, 0, W, Z, 1, 1, 8, 4, 4, 1, None) == NULL
 
 
 def test_toeplitz_validation(lib):

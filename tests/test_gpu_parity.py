@@ -38,6 +38,22 @@ def test_feature_map(gpu_lib, B, H, n, d, m, dt):
     assert rel <= 2e-4, rel
 
 
+@pytest.mark.parametrize("B,H,n,d,m,dt", [
+    (1, 2, 130, 64, 64, "f32"),
+    (2, 1, 77, 128, 33, "bf16"),
+])
+def test_feature_map_normalised(gpu_lib, B, H, n, d, m, dt):
+    """KRPE_NPRF: phi of x / ||x|| (Algorithm 1), a zero row staying zero."""
+    dd = synth.custom(B, H, n, d, m, seed=12, qkv_dtype=dt)
+    x = dd["q"] * 2.0                      # rows far from unit norm (still bf16-exact)
+    x[0, 0, 5] = 0.0
+    phi = gpu_lib.feature_map(to_gpu(x, dt), to_gpu(dd["W"]), nprf=True).cpu().numpy()
+    ref = oracle.prf_features(oracle.normalize_rows(x), dd["W"])
+    rel = np.max(np.abs(phi - ref) / ref)
+    _say(f"feature_map nprf B={B} H={H} n={n} d={d} m={m} {dt}: rel={rel:.3e}")
+    assert rel <= 2e-4, rel
+
+
 # ------------------------------------------------------- Toeplitz product --
 @pytest.mark.parametrize("B,H,C,n,sigma", [
     (1, 1, 2, 1, 0.5),
@@ -207,6 +223,32 @@ def test_attention_small_full_compare(gpu_lib, B, H, n, d, m, dt, bias):
         per = np.max(np.abs(z - ref), axis=-1) / np.max(np.abs(ref), axis=-1)
         _say("  worst rows:", np.argsort(per.reshape(-1))[::-1][:8], np.sort(per.reshape(-1))[::-1][:8])
     assert err <= TOL[dt], err
+
+
+NPRF_CASES = [
+    # B, H, n, d, m, dtype, bias
+    (2, 2, 256, 64, 32, "f32", "normal"),
+    (1, 2, 1000, 64, 64, "bf16", "causal"),
+    (1, 1, 4096, 64, 128, "f32", "normal"),
+]
+
+
+@pytest.mark.parametrize("B,H,n,d,m,dt,bias", NPRF_CASES)
+def test_attention_normalised(gpu_lib, B, H, n, d, m, dt, bias):
+    """NPRF attention (Algorithm 1): q, k rows normalised, then Eq. (10)."""
+    dd = synth.custom(B, H, n, d, m, seed=31 + n, qkv_dtype=dt, bias=bias)
+    q, k, v, b, W = inputs_to_gpu(dd)
+    z = gpu_lib.attention_fwd(q, k, v, b, W, nprf=True).cpu().numpy()
+    rows = sample_rows(B, H, n, 48, seed=n, extra=[(0, 0, i) for i in range(4)])
+    zr, den = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], rows, nprf=True)
+    got = np.stack([z[bb, h, i] for bb, h, i in rows])
+    err = rownorm_err(got, zr)
+    _say(f"attention nprf B={B} H={H} n={n} d={d} m={m} {dt} {bias}: err={err:.3e}")
+    assert np.all(den > 0)
+    assert err <= TOL[dt], err
+    # the option changes the result (the inputs are not unit rows)
+    z0 = gpu_lib.attention_fwd(q, k, v, b, W).cpu().numpy()
+    assert rownorm_err(z0, z) > 1e-4
 
 
 def test_workload1_full(gpu_lib):

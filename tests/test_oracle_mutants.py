@@ -28,6 +28,9 @@ MUTANTS = {
     "toeplitz_matrix_sign": ("return np.exp(b_h[j - i + n - 1])", "return np.exp(b_h[i - j + n - 1])"),
     "rows_offset_sign": ("c = np.exp(b[h][np.arange(n) - i + n - 1])", "c = np.exp(b[h][i - np.arange(n) + n - 1])"),
     "rows_wrong_head_features": ("cache[(beta, h)] = prf_features(k[beta, h], W[h])", "cache[(beta, h)] = prf_features(k[beta, h], W[0])"),
+    "nprf_keys_not_normalised": ("        q, k = normalize_rows(q), normalize_rows(k)\n    Bn", "        q = normalize_rows(q)\n    Bn"),
+    "nprf_squared_norm": ("return np.divide(x, norm, out=np.zeros_like(x), where=norm > 0)", "return np.divide(x, norm * norm, out=np.zeros_like(x), where=norm > 0)"),
+    "nprf_ignored": ("    if nprf:\n        q, k = normalize_rows(q), normalize_rows(k)\n    Bn", "    Bn"),
 }
 
 

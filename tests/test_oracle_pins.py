@@ -279,6 +279,49 @@ def check_toeplitz_special_cases(impl):
     assert np.allclose(y, ref, rtol=1e-13, atol=1e-13)
 
 
+def _brute_normalize(x_row):
+    """x / ||x||_2 with scalar arithmetic (Algorithm 1, first step); zero stays zero."""
+    nrm = math.sqrt(sum(t * t for t in x_row))
+    return [t / nrm for t in x_row] if nrm > 0 else [0.0 for _ in x_row]
+
+
+def check_nprf_brute_force(impl):
+    """NPRF attention (Algorithm 1): normalise q and k rows, then Eq. (10), scalar loops."""
+    rng = np.random.default_rng(21)
+    for (n, d, m) in [(1, 3, 2), (6, 4, 5), (11, 7, 3)]:
+        q, k, v, b, W = _rand_case(rng, 2, 2, n, d, m, scale=1.7)
+        q[0, 1, 0] = 0.0                      # a zero row stays zero
+        qn = np.array([[[_brute_normalize(q[a, h, i].tolist()) for i in range(n)] for h in range(2)]
+                       for a in range(2)])
+        kn = np.array([[[_brute_normalize(k[a, h, i].tolist()) for i in range(n)] for h in range(2)]
+                       for a in range(2)])
+        z, _ = impl.attention(q, k, v, b, W, nprf=True)
+        assert _rownorm_err(z, _brute_attention(qn, kn, v, b, W)) < 1e-12, (n, d, m)
+        rows = [(1, 0, n - 1), (0, 1, 0)]
+        zr, _ = impl.attention_rows(q, k, v, b, W, rows, nprf=True)
+        for r, (a, h, i) in enumerate(rows):
+            assert np.allclose(zr[r], z[a, h, i], rtol=1e-12, atol=1e-14)
+
+
+def check_nprf_scale_invariance(impl):
+    """Under NPRF, rescaling each query and key by a positive factor changes nothing;
+    inputs that are already unit rows give the plain Eq. (10) result."""
+    rng = np.random.default_rng(22)
+    q, k, v, b, W = _rand_case(rng, 1, 2, 12, 6, 9)
+    z0, _ = impl.attention(q, k, v, b, W, nprf=True)
+    sq = rng.uniform(0.1, 5.0, size=q.shape[:-1] + (1,))
+    sk = rng.uniform(0.1, 5.0, size=k.shape[:-1] + (1,))
+    z1, _ = impl.attention(q * sq, k * sk, v, b, W, nprf=True)
+    assert _rownorm_err(z1, z0) < 1e-12
+    qu = q / np.linalg.norm(q, axis=-1, keepdims=True)
+    ku = k / np.linalg.norm(k, axis=-1, keepdims=True)
+    z2, _ = impl.attention(qu, ku, v, b, W)
+    assert _rownorm_err(z2, z0) < 1e-12
+    # and the normalisation does matter for inputs that are not unit rows
+    z3, _ = impl.attention(q * sq, k * sk, v, b, W)
+    assert _rownorm_err(z3, z0) > 1e-6
+
+
 def check_rows_match_full(impl):
     d = synth.custom(2, 3, 64, 16, 8, seed=5)
     q, k, v, b, W = d["q"], d["k"], d["v"], d["b"], d["W"]
@@ -294,7 +337,7 @@ ALL_CHECKS = [check_brute_force, check_algorithm1_route, check_single_position,
               check_const_bias_is_linear_attention, check_causal_prefix_sums,
               check_only_diagonal, check_shift_kernel, check_invariants,
               check_causality, check_prf_variance_lemma, check_toeplitz_special_cases,
-              check_rows_match_full]
+              check_rows_match_full, check_nprf_brute_force, check_nprf_scale_invariance]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda f: f.__name__)
