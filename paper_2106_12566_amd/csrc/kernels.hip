@@ -346,6 +346,11 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
   constexpr int FOLD = C::FOLD, KH = C::KH, S = C::S;
   constexpr bool VREG = C::VREG, PREF = C::PREF, HREG = C::HREG, HOIST = C::HOIST;
   constexpr bool MERGE = F::P > 1;
+  // One class and no fold (the classes of a length-N transform): the
+  // per-register twist factor W_{RS}^{r i} of the input is applied to v once,
+  // phi_l(k) being real, and that of the output to the accumulators after the
+  // loop, phi_l(q) being real and the rotation linear.
+  constexpr bool PRETWIST = MERGE && KH == 1 && FOLD == 1 && VREG && R0 != 0;
   constexpr int NP = FOLD * F::N;  // row length of phi and v
   // Spectrum classes, register order (see k_spectrum): kept in registers when
   // the work-group is small enough, else re-read just before the product.
@@ -361,7 +366,10 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
 #pragma unroll
     for (int p = 0; p < FOLD; ++p)
 #pragma unroll
-      for (int i = 0; i < F::R; ++i) vx[p][i] = vrow[tau + F::T * i + p * F::N];
+      for (int i = 0; i < F::R; ++i) {
+        const float2 vv = vrow[tau + F::T * i + p * F::N];
+        vx[p][i] = PRETWIST ? rot_dyn<F::R * S, false>(vv, R0 * i) : vv;
+      }
   }
   // Merged first-pass twiddles (MERGE), or the plain twists W_{2N}^{r j}
   // (single-pass transforms), of every class of the unit.
@@ -432,7 +440,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         float2 u = xb[0];
 #pragma unroll
         for (int p = 1; p < FOLD; ++p) u = cadd(u, rot_dyn<S, false>(xb[p], p * r));
-        if constexpr (r == 0) {
+        if constexpr (r == 0 || PRETWIST) {
           x[k][i] = u;
         } else if constexpr (MERGE) {
           x[k][i] = rot_dyn<F::R * S, false>(u, r * i);
@@ -474,7 +482,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       float2 yk[KH];
       constexpr_for<KH>([&](auto kc) {
         constexpr int k = decltype(kc)::value, r = R0 + k;
-        if constexpr (r == 0) {
+        if constexpr (r == 0 || PRETWIST) {
           yk[k] = x[k][i];
         } else if constexpr (MERGE) {
           yk[k] = rot_dyn<F::R * S, true>(x[k][i], r * i);
@@ -493,6 +501,14 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         acc0[q][i] = fmaf(f[q][i], y.x, acc0[q][i]);
         acc1[q][i] = fmaf(f[q][i], y.y, acc1[q][i]);
       }
+    }
+  }
+  if constexpr (PRETWIST) {
+#pragma unroll
+    for (int i = 0; i < F::R; ++i) {
+      const float2 y = rot_dyn<F::R * S, true>(make_float2(acc0[0][i], acc1[0][i]), R0 * i);
+      acc0[0][i] = y.x;
+      acc1[0][i] = y.y;
     }
   }
 }
