@@ -116,7 +116,7 @@ def blas_threads() -> int:
     return len(os.sched_getaffinity(0))
 
 
-def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool = False):
+def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool = False, kind: str = "prf"):
     """Time the fp64 oracle (Eq. (10), O(n^2) per head) on whole (batch, head) units.
 
     Runs units until `budget_s` of wall time is spent (at least one), and
@@ -134,7 +134,8 @@ def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool 
     worst = 0.0
     for beta, h in units:
         z, _ = oracle.attention(d["q"][beta:beta + 1, h:h + 1], d["k"][beta:beta + 1, h:h + 1],
-                                d["v"][beta:beta + 1, h:h + 1], d["b"][h:h + 1], d["W"][h:h + 1], nprf=nprf)
+                                d["v"][beta:beta + 1, h:h + 1], d["b"][h:h + 1],
+                                None if kind == "elu" else d["W"][h:h + 1], nprf=nprf, kind=kind)
         done += 1
         if z_gpu is not None:
             num = np.max(np.abs(z_gpu[beta, h] - z[0, 0]), axis=-1)
@@ -165,6 +166,8 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
+                    help="feature map of Section 2: PRF (Eq. (5)), trigonometric (2m features) or elu + 1 (m = d)")
     ap.add_argument("--nprf", action="store_true",
                     help="normalise the rows of q and k first (Algorithm 1's NPRF attention)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -201,7 +204,12 @@ def main() -> int:
     b = torch.from_numpy(d["b"]).to(dev)
     W = torch.from_numpy(d["W"]).to(dev)
     out = torch.empty((B, H, n, dd), dtype=torch.float32, device=dev)
-    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m), dtype=torch.uint8, device=dev)
+    fm = args.feature_map
+    if fm == "elu":
+        m = dd                       # elu + 1 has one feature per coordinate
+    M = 2 * m if fm == "trf" else m  # features per position
+    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, nprf=args.nprf, features=fm), dtype=torch.uint8,
+                     device=dev)
     print(f"bench: workload {wl.name} B={B} H={H} n={n} d={dd} m={m} {wl.qkv_dtype}", file=sys.stderr,
           flush=True)
 
@@ -209,12 +217,12 @@ def main() -> int:
     events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(args.steps)]
 
     for _ in range(args.warmup):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf, features=fm)
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
     for s in range(args.steps):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], nprf=args.nprf)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], nprf=args.nprf, features=fm)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
@@ -228,11 +236,11 @@ def main() -> int:
     tokens = B * n
     value = tokens / (ms_per_step * 1e-3)
 
-    flops = conv_stage_flops(B, H, n, dd, m)
+    flops = conv_stage_flops(B, H, n, dd, M)
     conv_ms = stages["conv_contract"]
     achieved_tflops = flops / (conv_ms * 1e-3) / 1e12
     s_in = 2 if wl.qkv_dtype == "bf16" else 4
-    conv_gbs = conv_stage_bytes(B, H, n, dd, m, s_in) / (conv_ms * 1e-3) / 1e9
+    conv_gbs = conv_stage_bytes(B, H, n, dd, M, s_in) / (conv_ms * 1e-3) / 1e9
     print(f"bench: {ms_per_step:.3f} ms/step, stages {stages}", file=sys.stderr, flush=True)
 
     result = {
@@ -250,13 +258,14 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": wl.name, "B": B, "H": H, "n": n, "d": dd, "m": m,
                    "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
-                   "causal": wl.causal, "nprf": args.nprf, "ms_per_layer": ms_per_step, "stages_ms": stages,
+                   "causal": wl.causal, "nprf": args.nprf, "feature_map": fm, "features_per_position": M,
+                   "ms_per_layer": ms_per_step, "stages_ms": stages,
                    "conv_stage_hbm_gbs": conv_gbs,
                    "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)},
         "roofline": {"bound": "alu", "kernel": "k_conv_contract", "achieved": achieved_tflops,
                      "peak": PEAK_FP32_VECTOR_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
-                     "traffic": measured_traffic("k_conv_contract", wl.name)},
+                     "traffic": measured_traffic("k_conv_contract", wl.name) if fm == "prf" else None},
     }
     if args.copy_calibration_mib > 0:
         src = torch.ones(args.copy_calibration_mib << 18, dtype=torch.float32, device=dev)
@@ -267,7 +276,7 @@ def main() -> int:
         result["config"]["copy_calibration_bytes"] = src.numel() * 4
     if not args.no_cpu_baseline:
         z_gpu = out.cpu().numpy()
-        cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu, nprf=args.nprf)
+        cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu, nprf=args.nprf, kind=fm)
         result["cpu_baseline"] = {k2: cb[k2] for k2 in ("value", "unit", "cores", "kind", "sample")}
         result["config"]["parity_rownorm_err"] = err
         result["config"]["parity_units"] = units

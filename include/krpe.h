@@ -77,6 +77,26 @@ typedef enum {
  * Kernelized Attention with RPE" (Section 3.3).  A zero row stays zero.
  */
 #define KRPE_NPRF 1u
+/*
+ * Feature map options (Section 2; at most one of them; PRF of Eq. (5) when
+ * neither is set).  The method is the same for every feature map: only phi
+ * changes, and with it the number M of features per position.
+ * KRPE_FEAT_TRF: the trigonometric random features of Section 2,
+ *   phi(x) = exp(||x||^2/2) / sqrt(m) [sin(w_1 x), .., sin(w_m x),
+ *                                      cos(w_1 x), .., cos(w_m x)],
+ *   M = 2m signed features from the m rows of W (so m <= 512).  The
+ *   denominator of Eq. (10) can then be small or negative: rows whose FFT
+ *   result cannot be certified to 1e-4 (a vanishing denominator among them)
+ *   are evaluated directly, and a zero denominator gives inf / nan as the
+ *   formula does.
+ * KRPE_FEAT_ELU: elu(x) + 1 elementwise, the linear transformer's map the
+ *   paper compares with; M = d, m must equal d, W is not read (may be NULL).
+ * Sphere-PRF and ORF (the paper's appendix comparison) are PRF with W drawn
+ * from the sphere of radius sqrt(d) or with orthogonal rows: no option, the
+ * caller passes that W.
+ */
+#define KRPE_FEAT_TRF 2u
+#define KRPE_FEAT_ELU 4u
 
 /* Version of this ABI (incremented on any incompatible change). */
 int krpe_abi_version(void);
@@ -97,7 +117,11 @@ const char* krpe_last_error(void);
  */
 krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float* phi,
                                int B, int H, int n, int d, int m, void* stream);
-/* krpe_feature_map with option bits (KRPE_NPRF: phi of x / ||x||). */
+/*
+ * krpe_feature_map with option bits: KRPE_NPRF (phi of x / ||x||), one of
+ * KRPE_FEAT_TRF / KRPE_FEAT_ELU.  phi is then [B, H, n, M] with M = 2m (TRF,
+ * sin features first) or d (elu + 1; W not read).
+ */
 krpe_status_t krpe_feature_map_ex(const void* x, int x_dtype, const float* W, float* phi,
                                   int B, int H, int n, int d, int m, unsigned flags, void* stream);
 
@@ -123,6 +147,8 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
  * unsupported).
  */
 size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m);
+/* The same for krpe_attention_fwd_ex with option bits (TRF needs more). */
+size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsigned flags);
 
 /*
  * Kernelized attention with RPE, Section 3.2, Eq. (10), with phi from Eq. (5)
@@ -140,7 +166,9 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
 
 /*
  * krpe_attention_fwd with option bits: KRPE_NPRF normalises the rows of q
- * and k first (Algorithm 1's NPRF attention).  The same workspace size.
+ * and k first (Algorithm 1's NPRF attention); KRPE_FEAT_TRF / KRPE_FEAT_ELU
+ * select the feature map (W [H, m, d] as above; not read for elu + 1, where
+ * m == d).  Workspace: krpe_attention_fwd_workspace_ex with the same flags.
  */
 krpe_status_t krpe_attention_fwd_ex(const void* q, const void* k, const void* v, int qkv_dtype,
                                     const float* b, const float* W, float* z,
@@ -162,8 +190,9 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                                           void* const* events);
 
 /*
- * Rows of the last krpe_attention_fwd call (with this workspace and these
- * sizes) that were evaluated exactly instead of through the FFT.
+ * Rows of the last krpe_attention_fwd / _ex call (with this workspace and
+ * these sizes, whatever its option bits) that were evaluated exactly instead
+ * of through the FFT.
  *
  * The FFT path's fp32 rounding error is spread over a whole sequence, so a
  * row whose denominator of Eq. (10) is small next to the sequence's total

@@ -8,6 +8,11 @@ It computes the *definitions* written in the paper, directly and slowly, in
 float64 (inputs given in fp32 or bf16 are converted exactly):
 
 * ``prf_features``      -- Eq. (5), the positive random feature map.
+* ``trf_features``      -- the trigonometric random feature map of Section 2
+                           (sin features, then cos features).
+* ``elu_features``      -- elu(x) + 1, the linear transformer's map that
+                           Section 2 names.
+* ``features``          -- one of the three by name.
 * ``toeplitz_matrix``   -- the positional-correlation matrix C = {c_{j-i}},
                            c_t = exp(b_t) (Section 3.2, below Eq. (13)).
 * ``toeplitz_product``  -- C @ a by plain matrix multiplication: the
@@ -15,7 +20,8 @@ float64 (inputs given in fp32 or bf16 are converted exactly):
                            (Eqs. (12)-(13)); FFT and direct product agree
                            exactly up to rounding, so this is the reference.
 * ``attention``         -- Eq. (10): z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j
-                           / phi(q_i) sum_j c_{j-i} phi(k_j)^T, O(n^2).
+                           / phi(q_i) sum_j c_{j-i} phi(k_j)^T, O(n^2), for
+                           any of the three feature maps.
 * ``attention_rows``    -- the same formula evaluated for selected rows only,
                            so that outputs of full-size workloads can be
                            checked one by one.
@@ -41,8 +47,8 @@ from __future__ import annotations
 
 import numpy as np
 
-__all__ = ["prf_features", "toeplitz_matrix", "toeplitz_product", "attention",
-           "attention_rows", "normalize_rows"]
+__all__ = ["prf_features", "trf_features", "elu_features", "features", "toeplitz_matrix",
+           "toeplitz_product", "attention", "attention_rows", "normalize_rows"]
 
 
 def _f64(x) -> np.ndarray:
@@ -63,6 +69,40 @@ def prf_features(x, W) -> np.ndarray:
     proj = x @ np.swapaxes(W, -1, -2)                 # w_l . x for every row
     half_sq = 0.5 * np.sum(x * x, axis=-1, keepdims=True)
     return np.exp(proj - half_sq) / np.sqrt(m)
+
+
+def trf_features(x, W) -> np.ndarray:
+    """Trigonometric random features (Section 2, the map of Peng et al.).
+
+    phi(x) = exp(||x||^2 / 2) / sqrt(m) [sin(w_1 x^T), ..., sin(w_m x^T),
+                                         cos(w_1 x^T), ..., cos(w_m x^T)].
+
+    x : [..., H, n, d] (or [n, d]);  W : [H, m, d] (or [m, d]).
+    Returns [..., H, n, 2m] in float64 (signed values).
+    """
+    x = _f64(x)
+    W = _f64(W)
+    m = W.shape[-2]
+    proj = x @ np.swapaxes(W, -1, -2)
+    amp = np.exp(0.5 * np.sum(x * x, axis=-1, keepdims=True)) / np.sqrt(m)
+    return np.concatenate([amp * np.sin(proj), amp * np.cos(proj)], axis=-1)
+
+
+def elu_features(x, W=None) -> np.ndarray:
+    """elu(x) + 1 elementwise (the linear transformer's map, Section 2): x + 1 for x > 0, exp(x) otherwise.
+
+    d features; W is not used.  Returns [..., n, d] in float64.
+    """
+    x = _f64(x)
+    return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+_MAPS = {"prf": prf_features, "trf": trf_features, "elu": elu_features}
+
+
+def features(x, W, kind: str = "prf") -> np.ndarray:
+    """phi(x) for kind in {"prf", "trf", "elu"} (W unused for "elu")."""
+    return _MAPS[kind](x, W)
 
 
 def normalize_rows(x) -> np.ndarray:
@@ -96,18 +136,21 @@ def toeplitz_product(b, a) -> np.ndarray:
     return out
 
 
-def attention(q, k, v, b, W, *, row_tile: int = 1024, nprf: bool = False):
+def attention(q, k, v, b, W, *, row_tile: int = 1024, nprf: bool = False, kind: str = "prf"):
     """Kernelized attention with RPE, Eq. (10), evaluated directly.
 
-    For every (batch, head): Phi_q, Phi_k by Eq. (5); the n x n weight matrix
-    M_ij = c_{j-i} * phi(q_i) phi(k_j)^T; numerator M v, denominator M 1.
-    Rows are processed in tiles to bound memory.
+    For every (batch, head): Phi_q, Phi_k by the feature map `kind` (Eq. (5)
+    for "prf"); the n x n weight matrix M_ij = c_{j-i} * phi(q_i) phi(k_j)^T;
+    numerator M v, denominator M 1.  Rows are processed in tiles to bound
+    memory.
 
-    q, k, v : [B, H, n, d];  b : [H, 2n-1];  W : [H, m, d].
+    q, k, v : [B, H, n, d];  b : [H, 2n-1];  W : [H, m, d] (None for "elu").
     nprf: q and k rows normalised first (Algorithm 1).
     Returns (z [B, H, n, d], den [B, H, n]) in float64.
     """
-    q, k, v, b, W = map(_f64, (q, k, v, b, W))
+    q, k, v, b = map(_f64, (q, k, v, b))
+    W = _f64(W) if W is not None else [None] * q.shape[1]
+    fmap = _MAPS[kind]
     if nprf:
         q, k = normalize_rows(q), normalize_rows(k)
     Bn, H, n, d = q.shape
@@ -115,8 +158,8 @@ def attention(q, k, v, b, W, *, row_tile: int = 1024, nprf: bool = False):
     den = np.empty((Bn, H, n))
     for h in range(H):
         for beta in range(Bn):
-            fq = prf_features(q[beta, h], W[h])
-            fk = prf_features(k[beta, h], W[h])
+            fq = fmap(q[beta, h], W[h])
+            fk = fmap(k[beta, h], W[h])
             for i0 in range(0, n, row_tile):
                 i1 = min(n, i0 + row_tile)
                 rows = np.arange(i0, i1)[:, None]
@@ -130,7 +173,7 @@ def attention(q, k, v, b, W, *, row_tile: int = 1024, nprf: bool = False):
     return z, den
 
 
-def attention_rows(q, k, v, b, W, rows, *, nprf: bool = False):
+def attention_rows(q, k, v, b, W, rows, *, nprf: bool = False, kind: str = "prf"):
     """Eq. (10) for selected output rows only.
 
     rows : iterable of (beta, h, i).  Returns (z [R, d], den [R]) float64 in
@@ -140,6 +183,9 @@ def attention_rows(q, k, v, b, W, rows, *, nprf: bool = False):
     b = _f64(b)
     if nprf:
         q, k = normalize_rows(q), normalize_rows(k)
+    fmap = _MAPS[kind]
+    if W is None:
+        W = [None] * q.shape[1]
     rows = [tuple(int(t) for t in r) for r in rows]
     n = q.shape[2]
     d = q.shape[3]
@@ -149,9 +195,9 @@ def attention_rows(q, k, v, b, W, rows, *, nprf: bool = False):
     for r, (beta, h, i) in enumerate(rows):
         if (beta, h) not in cache:
             cache.clear()
-            cache[(beta, h)] = prf_features(k[beta, h], W[h])
+            cache[(beta, h)] = fmap(k[beta, h], W[h])
         fk = cache[(beta, h)]
-        fq = prf_features(_f64(q[beta, h, i])[None, :], W[h])[0]
+        fq = fmap(_f64(q[beta, h, i])[None, :], W[h])[0]
         c = np.exp(b[h][np.arange(n) - i + n - 1])
         w = c * (fk @ fq)
         den[r] = w.sum()

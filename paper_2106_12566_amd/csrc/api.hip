@@ -62,6 +62,22 @@ krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm) {
   return KRPE_OK;
 }
 
+constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU;
+
+// Feature map selected by the option bits, and its number of features M
+// (the row count of phi): m for PRF, 2m for TRF, d for elu + 1 (which needs
+// m == d).
+krpe_status_t feature_kind(unsigned flags, int d, int m, int* kind, int* M) {
+  if (flags & ~kKnownFlags) return fail(KRPE_ERR_UNSUPPORTED, "unknown flag bits");
+  if ((flags & KRPE_FEAT_TRF) && (flags & KRPE_FEAT_ELU))
+    return fail(KRPE_ERR_UNSUPPORTED, "KRPE_FEAT_TRF and KRPE_FEAT_ELU are exclusive");
+  *kind = (flags & KRPE_FEAT_TRF) ? kFeatTrf : (flags & KRPE_FEAT_ELU) ? kFeatElu : kFeatPrf;
+  *M = *kind == kFeatTrf ? 2 * m : (*kind == kFeatElu ? d : m);
+  if (*kind == kFeatElu && m != d) return fail(KRPE_ERR_SHAPE, "KRPE_FEAT_ELU needs m == d");
+  if (*M > kMaxM) return fail(KRPE_ERR_UNSUPPORTED, "more than 1024 features is not supported");
+  return KRPE_OK;
+}
+
 krpe_status_t record(void* const* events, int i, hipStream_t st) {
   if (!events || !events[i]) return KRPE_OK;
   return hip_check(hipEventRecord(static_cast<hipEvent_t>(events[i]), st), "hipEventRecord");
@@ -82,6 +98,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
     off = align_up(off + bytes);
     return at;
   };
+  L.fix = take((bh + 1) * sizeof(unsigned));  // first: its offset does not depend on the sizes
   L.tw = take(2 * N * sizeof(float2));
   L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
   L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
@@ -93,7 +110,6 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.x2 = take(bh * L.ksplit * m * pairs * sizeof(float));
   L.wb = take(bh * (static_cast<size_t>(m) + 1) * sizeof(float2));
   L.part = take(bh * conv_splits(L.l2) * cols * n * sizeof(float));
-  L.fix = take((bh + 1) * sizeof(unsigned));
   L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
@@ -130,7 +146,7 @@ using namespace krpe;
 
 extern "C" {
 
-int krpe_abi_version(void) { return 3; }
+int krpe_abi_version(void) { return 4; }
 
 const char* krpe_status_str(int s) {
   switch (s) {
@@ -153,20 +169,22 @@ krpe_status_t krpe_feature_map_ex(const void* x, int x_dtype, const float* W, fl
                                   int d, int m, unsigned flags, void* stream) {
   g_last_error.clear();
   if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
-  if (flags & ~static_cast<unsigned>(KRPE_NPRF)) return fail(KRPE_ERR_UNSUPPORTED, "unknown flag bits");
+  int kind = kFeatPrf, M = m;
+  if (krpe_status_t s = feature_kind(flags, d, m, &kind, &M)) return s;
   if (x_dtype != KRPE_F32 && x_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "x_dtype must be F32 or BF16");
   const size_t bh = static_cast<size_t>(B) * H;
   if (bh == 0) return KRPE_OK;
-  if (!x || !W || !phi) return fail(KRPE_ERR_NULL, "x, W and phi must be non-NULL");
-  if (misaligned(x) || misaligned(W) || misaligned(phi))
+  const bool needW = kind != kFeatElu;
+  if (!x || (needW && !W) || !phi) return fail(KRPE_ERR_NULL, "x, W (but for elu + 1) and phi must be non-NULL");
+  if (misaligned(x) || (needW && misaligned(W)) || misaligned(phi))
     return fail(KRPE_ERR_ALIGN, "x, W, phi must be 16-byte aligned");
-  const Range rphi{phi, bh * n * m * sizeof(float)};
+  const Range rphi{phi, bh * n * M * sizeof(float)};
   if (overlaps(rphi, {x, bh * n * d * dtype_size(x_dtype)}) ||
-      overlaps(rphi, {W, static_cast<size_t>(H) * m * d * sizeof(float)}))
+      (needW && overlaps(rphi, {W, static_cast<size_t>(H) * m * d * sizeof(float)})))
     return fail(KRPE_ERR_ALIAS, "phi overlaps x or W");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  return hip_check(launch_feature_map(x_dtype == KRPE_BF16, x, x, W, phi, phi, 1, false, m, static_cast<int>(bh),
-                                      H, n, d, m, nullptr, (flags & KRPE_NPRF) != 0, st),
+  return hip_check(launch_feature_map(x_dtype == KRPE_BF16, x, x, W, phi, phi, 1, false, M, static_cast<int>(bh),
+                                      H, n, d, m, nullptr, (flags & KRPE_NPRF) != 0, kind, st),
                    "feature map launch");
 }
 
@@ -230,9 +248,15 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
   return KRPE_OK;
 }
 
-size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
+size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsigned flags) {
   if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
-  return attn_layout(B, H, n, d, m).total;
+  int kind = kFeatPrf, M = m;
+  if (feature_kind(flags, d, m, &kind, &M) != KRPE_OK) return 0;
+  return attn_layout(B, H, n, d, M).total;
+}
+
+size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
+  return krpe_attention_fwd_workspace_ex(B, H, n, d, m, 0u);
 }
 
 krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
@@ -240,15 +264,18 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                                           void* ws, size_t ws_bytes, void* stream, void* const* events) {
   g_last_error.clear();
   if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
-  if (flags & ~static_cast<unsigned>(KRPE_NPRF)) return fail(KRPE_ERR_UNSUPPORTED, "unknown flag bits");
+  int kind = kFeatPrf, M = m;
+  if (krpe_status_t s = feature_kind(flags, d, m, &kind, &M)) return s;
   if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
   const size_t bh = static_cast<size_t>(B) * H;
   if (bh == 0) return KRPE_OK;
-  if (!q || !k || !v || !b || !W || !z) return fail(KRPE_ERR_NULL, "q, k, v, b, W and z must be non-NULL");
-  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(b) || misaligned(W) || misaligned(z) ||
-      misaligned(ws))
+  const bool needW = kind != kFeatElu;
+  if (!q || !k || !v || !b || (needW && !W) || !z)
+    return fail(KRPE_ERR_NULL, "q, k, v, b, W (but for elu + 1) and z must be non-NULL");
+  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(b) || (needW && misaligned(W)) ||
+      misaligned(z) || misaligned(ws))
     return fail(KRPE_ERR_ALIGN, "all pointers must be 16-byte aligned");
-  const AttnLayout L = attn_layout(B, H, n, d, m);
+  const AttnLayout L = attn_layout(B, H, n, d, M);
   if (!ws || ws_bytes < L.total)
     return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
   const size_t qkv_bytes = bh * n * d * dtype_size(qkv_dtype);
@@ -256,7 +283,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                        {k, qkv_bytes},
                        {v, qkv_bytes},
                        {b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)},
-                       {W, static_cast<size_t>(H) * m * d * sizeof(float)}};
+                       {W, needW ? static_cast<size_t>(H) * m * d * sizeof(float) : 0}};
   const Range rz{z, bh * n * d * sizeof(float)};
   const Range rws{ws, ws_bytes};
   if (overlaps(rz, rws)) return fail(KRPE_ERR_ALIAS, "z overlaps the workspace");
@@ -290,7 +317,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch")) return s;
   if (krpe_status_t s = record(events, 1, st)) return s;
   if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix,
-                                                     (flags & KRPE_NPRF) != 0, st),
+                                                     (flags & KRPE_NPRF) != 0, kind, st),
                                   "feature map launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_vprep(bf16, v, d, 1, static_cast<long long>(n) * d, d, true, BHi, n, N,
@@ -298,19 +325,19 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                                   "column launch"))
     return s;
   if (krpe_status_t s = record(events, 2, st)) return s;
-  if (krpe_status_t s = hip_check(launch_conv(L.l2, phiq, phik, static_cast<long long>(m) * N, vsc, colmax, Hs, tw,
-                                              part, BHi, H, n, d + 1, m, st),
+  if (krpe_status_t s = hip_check(launch_conv(L.l2, phiq, phik, static_cast<long long>(M) * N, vsc, colmax, Hs, tw,
+                                              part, BHi, H, n, d + 1, M, st),
                                   "conv launch"))
     return s;
   if (krpe_status_t s = record(events, 3, st)) return s;
-  if (krpe_status_t s = hip_check(launch_gram(phik, vsc, x2, BHi, m, N, pairs, L.ksplit, st), "norm launch"))
+  if (krpe_status_t s = hip_check(launch_gram(phik, vsc, x2, BHi, M, N, pairs, L.ksplit, st), "norm launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, m, d, L.ksplit, st), "bound launch"))
+  if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, M, d, L.ksplit, st), "bound launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, fixmask, BHi, H, n, L.l2, d, m, st),
+  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, fixmask, BHi, H, n, L.l2, d, M, st),
                                   "combine launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, fixmask, fixpart, brange, BHi, H, n, N, d, m, st),
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, fixmask, fixpart, brange, BHi, H, n, N, d, M, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);
@@ -337,8 +364,10 @@ krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, i
   *fixed_rows = 0;
   if (static_cast<size_t>(B) * H == 0) return KRPE_OK;
   if (!ws) return fail(KRPE_ERR_NULL, "ws must be non-NULL");
+  // The counters sit at the start of the workspace whatever the feature map.
   const AttnLayout L = attn_layout(B, H, n, d, m);
-  if (ws_bytes < L.total) return fail(KRPE_ERR_WORKSPACE, "workspace smaller than these sizes need");
+  if (ws_bytes < L.fix + (static_cast<size_t>(B) * H + 1) * sizeof(unsigned))
+    return fail(KRPE_ERR_WORKSPACE, "workspace smaller than these sizes need");
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (krpe_status_t s = hip_check(hipStreamSynchronize(st), "hipStreamSynchronize")) return s;
   return hip_check(

@@ -14,6 +14,12 @@ constexpr int kMaxD = 128;
 constexpr int kMaxM = 1024;
 constexpr int kLog2R = 4;      // 16 complex values per thread
 
+// Feature maps (Sec. 2): PRF of Eq. (5), the trigonometric map TRF (2m signed
+// features), elu + 1 (d features, no projections).
+constexpr int kFeatPrf = 0;
+constexpr int kFeatTrf = 1;
+constexpr int kFeatElu = 2;
+
 // Launch shape of the products of length-2N circular convolutions, N = 2^L2.
 //
 // The 2N frequency bins are split into S = 2 FOLD residue classes

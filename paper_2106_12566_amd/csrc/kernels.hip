@@ -120,25 +120,30 @@ __global__ __launch_bounds__(Conf<L2>::THREADS) void k_spectrum(const float* __r
 // --------------------------------------------------------- feature map --
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-// phi = exp(x W^T - ||x||^2/2) / sqrt(m) for up to two sources (q and k) in
-// one launch.  Tile: 64 positions x 64 features per work-group, four waves of
-// 32 x 32 v_mfma_f32_32x32x2f32 tiles; K (= d) staged through LDS in chunks of
-// 32.  FEATURE_MAJOR writes phi[bh][l][i] for i < ld (zeros for n <= i < ld;
-// lanes run along positions), otherwise phi[bh][i][l] (lanes run along
-// features): stores stay coalesced either way because the operand roles are
-// swapped.
+// Feature maps of the projections s = x W^T (Sec. 2): PRF, Eq. (5),
+// phi_l = exp(s_l - ||x||^2/2) / sqrt(m) (m features); TRF, the trigonometric
+// map, phi_l = exp(||x||^2/2) sin(s_l) / sqrt(m) and phi_{m+l} = exp(||x||^2/2)
+// cos(s_l) / sqrt(m) (2m signed features).  Up to two sources (q and k) in
+// one launch.  Tile: 64 positions x 64 projections per work-group, four waves
+// of 32 x 32 v_mfma_f32_32x32x2f32 tiles; K (= d) staged through LDS in chunks
+// of 32.  FEATURE_MAJOR writes phi[bh][l][i] for i < ld (zeros for
+// n <= i < ld; lanes run along positions), otherwise phi[bh][i][l] (lanes run
+// along features): stores stay coalesced either way because the operand
+// roles are swapped.  M = m (PRF) or 2m (TRF) is the row length of phi.
 template <typename TX, bool FEATURE_MAJOR>
 __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, const TX* __restrict__ x1,
                                                      const float* __restrict__ W, float* __restrict__ phi0,
                                                      float* __restrict__ phi1, int H, int n, int ld, int d,
                                                      int m, float inv_sqrt_m, int tiles_n, int tiles_m,
-                                                     int BH, unsigned* __restrict__ fix_counts, int nprf) {
+                                                     int BH, unsigned* __restrict__ fix_counts, int nprf,
+                                                     int trf) {
   // Clear the exact-evaluation queue counters (fix_counts[0..BH]) for k_combine.
   if (fix_counts && threadIdx.x == 0 && blockIdx.x <= static_cast<unsigned>(BH)) fix_counts[blockIdx.x] = 0u;
   __shared__ float xs[64][33];
   __shared__ float wsm[64][33];
   __shared__ float half_sq[64];
   __shared__ float row_scale[64];
+  __shared__ float trf_amp[64];
   int bid = blockIdx.x;
   const int tn = bid % tiles_n;
   bid /= tiles_n;
@@ -190,9 +195,11 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
     const bool nz = sq > 0.f;
     half_sq[threadIdx.x] = nprf ? (nz ? 0.5f : 0.f) : 0.5f * sq;
     row_scale[threadIdx.x] = nprf ? (nz ? rsqrtf(sq) : 0.f) : 1.f;
+    trf_amp[threadIdx.x] = expf(half_sq[threadIdx.x]) * inv_sqrt_m;
   }
   __syncthreads();
   const int n_store = FEATURE_MAJOR ? ld : n;
+  const int M = trf ? 2 * m : m;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     // 32x32 MFMA result layout: lane holds column lane%32, rows 8(v/4) + 4(lane/32) + v%4
@@ -202,12 +209,77 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
     const int ii = FEATURE_MAJOR ? wi + col : wi + row;  // position within tile
     const int l = l0 + li, i = i0 + ii;
     if (i < n_store && l < m) {
-      const float val = i < n ? expf(fmaf(acc[v], row_scale[ii], -half_sq[ii])) * inv_sqrt_m : 0.f;
-      if constexpr (FEATURE_MAJOR)
-        phi[(static_cast<size_t>(bh) * m + l) * ld + i] = val;
-      else
-        phi[(static_cast<size_t>(bh) * n + i) * m + l] = val;
+      if (trf) {
+        float sv = 0.f, cv = 0.f;
+        if (i < n) {
+          sincosf(acc[v] * row_scale[ii], &sv, &cv);
+          sv *= trf_amp[ii];
+          cv *= trf_amp[ii];
+        }
+        if constexpr (FEATURE_MAJOR) {
+          phi[(static_cast<size_t>(bh) * M + l) * ld + i] = sv;
+          phi[(static_cast<size_t>(bh) * M + m + l) * ld + i] = cv;
+        } else {
+          phi[(static_cast<size_t>(bh) * n + i) * M + l] = sv;
+          phi[(static_cast<size_t>(bh) * n + i) * M + m + l] = cv;
+        }
+      } else {
+        const float val = i < n ? expf(fmaf(acc[v], row_scale[ii], -half_sq[ii])) * inv_sqrt_m : 0.f;
+        if constexpr (FEATURE_MAJOR)
+          phi[(static_cast<size_t>(bh) * M + l) * ld + i] = val;
+        else
+          phi[(static_cast<size_t>(bh) * n + i) * M + l] = val;
+      }
     }
+  }
+}
+
+// The elu + 1 map of the linear transformer the paper compares with (Sec. 2):
+// phi_l(x) = x_l + 1 for x_l > 0, exp(x_l) otherwise, d features, no
+// projections (of x / ||x|| when normalising; a zero row stays zero before
+// the map).  Block: 64 positions of one (source, batch-head), x staged through
+// LDS; same output layouts and queue-counter duty as k_feature_map.
+template <typename TX, bool FEATURE_MAJOR>
+__global__ __launch_bounds__(256) void k_feature_elu(const TX* __restrict__ x0, const TX* __restrict__ x1,
+                                                     float* __restrict__ phi0, float* __restrict__ phi1, int n,
+                                                     int ld, int d, int tiles_n, int BH,
+                                                     unsigned* __restrict__ fix_counts, int nprf) {
+  if (fix_counts && threadIdx.x == 0 && blockIdx.x <= static_cast<unsigned>(BH)) fix_counts[blockIdx.x] = 0u;
+  __shared__ float xs[64][kMaxD + 1];
+  __shared__ float scale[64];
+  int bid = blockIdx.x;
+  const int tn = bid % tiles_n;
+  bid /= tiles_n;
+  const int bh = bid % BH, src = bid / BH;
+  const TX* __restrict__ xb = (src == 0 ? x0 : x1) + static_cast<size_t>(bh) * n * d;
+  float* __restrict__ phi = src == 0 ? phi0 : phi1;
+  const int i0 = tn * 64;
+  for (int e = threadIdx.x; e < 64 * d; e += 256) {
+    const int r = e / d, c = e - r * d;
+    xs[r][c] = i0 + r < n ? to_f32(xb[static_cast<size_t>(i0 + r) * d + c]) : 0.f;
+  }
+  __syncthreads();
+  if (threadIdx.x < 64) {
+    float sq = 0.f;
+    for (int c = 0; c < d; ++c) sq = fmaf(xs[threadIdx.x][c], xs[threadIdx.x][c], sq);
+    scale[threadIdx.x] = nprf ? (sq > 0.f ? rsqrtf(sq) : 0.f) : 1.f;
+  }
+  __syncthreads();
+  const int rows = FEATURE_MAJOR ? ld : n;
+  for (int e = threadIdx.x; e < 64 * d; e += 256) {
+    // feature-major: lanes along positions; position-major: lanes along features
+    const int r = FEATURE_MAJOR ? (e & 63) : e / d, l = FEATURE_MAJOR ? (e >> 6) : e - (e / d) * d;
+    const int i = i0 + r;
+    if (i >= rows) continue;
+    float val = 0.f;
+    if (i < n) {
+      const float t = xs[r][l] * scale[r];
+      val = t > 0.f ? t + 1.f : expf(t);
+    }
+    if constexpr (FEATURE_MAJOR)
+      phi[(static_cast<size_t>(bh) * d + l) * ld + i] = val;
+    else
+      phi[(static_cast<size_t>(bh) * n + i) * d + l] = val;
   }
 }
 
@@ -740,7 +812,7 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
     if (pos < n) {
       const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * N + pos;
       for (int l = qg; l < m; l += 4) {
-        const float f = pq[static_cast<size_t>(l) * N];
+        const float f = fabsf(pq[static_cast<size_t>(l) * N]);  // signed features (TRF)
         const float2 w = wl[l];
         bA = fmaf(f, w.x, bA);
         bD = fmaf(f, w.y, bD);
@@ -769,12 +841,12 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
         bD += bsum[g][i].y;
         num = fmaxf(num, zpart[g][i]);
       }
-      const float zm = num * inv;  // max_c |z_c| when den > 0
+      const float zm = num * fabsf(inv);  // max_c |z_c|
       const float vmax = wl[m].x;
       const float err = K * bA + zm * (K * bD);
       const float scale = fmaxf(zm, 1e-6f * vmax);
       const float rel_floor = 2.f * kGamma * kUnitRoundoff * lg;
-      const bool ok = isfinite(den) && den > 0.f && isfinite(zm) && err <= (kTau - rel_floor) * scale * den;
+      const bool ok = isfinite(den) && den != 0.f && isfinite(zm) && err <= (kTau - rel_floor) * scale * fabsf(den);
       flag = !ok;
     }
     // One wave holds the tile's 64 rows: its uncertified rows as one mask
@@ -1264,30 +1336,57 @@ hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs,
 
 hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const float* W, float* phi0, float* phi1,
                               int nsrc, bool feature_major, int ld, int BH, int H, int n, int d, int m,
-                              unsigned* fix_counts, bool nprf, hipStream_t st) {
+                              unsigned* fix_counts, bool nprf, int kind, hipStream_t st) {
   const int rows = feature_major ? ld : n;
-  const int tiles_n = (rows + 63) / 64, tiles_m = (m + 63) / 64;
+  const int tiles_n = (rows + 63) / 64;
+  const dim3 block(256);
+  if (kind == kFeatElu) {
+    const dim3 grid(static_cast<unsigned>(static_cast<long long>(tiles_n) * BH * nsrc));
+    const int np = nprf ? 1 : 0;
+    if (bf16) {
+      const uint16_t* a = static_cast<const uint16_t*>(x0);
+      const uint16_t* c = static_cast<const uint16_t*>(x1);
+      if (feature_major)
+        hipLaunchKernelGGL((k_feature_elu<uint16_t, true>), grid, block, 0, st, a, c, phi0, phi1, n, ld, d, tiles_n,
+                           BH, fix_counts, np);
+      else
+        hipLaunchKernelGGL((k_feature_elu<uint16_t, false>), grid, block, 0, st, a, c, phi0, phi1, n, ld, d, tiles_n,
+                           BH, fix_counts, np);
+    } else {
+      const float* a = static_cast<const float*>(x0);
+      const float* c = static_cast<const float*>(x1);
+      if (feature_major)
+        hipLaunchKernelGGL((k_feature_elu<float, true>), grid, block, 0, st, a, c, phi0, phi1, n, ld, d, tiles_n, BH,
+                           fix_counts, np);
+      else
+        hipLaunchKernelGGL((k_feature_elu<float, false>), grid, block, 0, st, a, c, phi0, phi1, n, ld, d, tiles_n,
+                           BH, fix_counts, np);
+    }
+    return hipGetLastError();
+  }
+  const int tiles_m = (m + 63) / 64;
   const long long blocks = static_cast<long long>(tiles_n) * tiles_m * BH * nsrc;
   const float inv_sqrt_m = static_cast<float>(1.0 / std::sqrt(static_cast<double>(m)));
-  const dim3 grid(static_cast<unsigned>(blocks)), block(256);
+  const dim3 grid(static_cast<unsigned>(blocks));
+  const int np = nprf ? 1 : 0, trf = kind == kFeatTrf ? 1 : 0;
   if (bf16) {
     const uint16_t* a = static_cast<const uint16_t*>(x0);
     const uint16_t* c = static_cast<const uint16_t*>(x1);
     if (feature_major)
       hipLaunchKernelGGL((k_feature_map<uint16_t, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d, m,
-                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
+                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
     else
       hipLaunchKernelGGL((k_feature_map<uint16_t, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d,
-                         m, inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
+                         m, inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
   } else {
     const float* a = static_cast<const float*>(x0);
     const float* c = static_cast<const float*>(x1);
     if (feature_major)
       hipLaunchKernelGGL((k_feature_map<float, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d, m,
-                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
+                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
     else
       hipLaunchKernelGGL((k_feature_map<float, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, d, m,
-                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, nprf ? 1 : 0);
+                         inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
   }
   return hipGetLastError();
 }

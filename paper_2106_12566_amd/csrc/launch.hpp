@@ -50,7 +50,7 @@ hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs,
 // l2 norm first.
 hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const float* W, float* phi0,
                               float* phi1, int nsrc, bool feature_major, int ld, int BH, int H, int n, int d,
-                              int m, unsigned* fix_counts, bool nprf, hipStream_t st);
+                              int m, unsigned* fix_counts, bool nprf, int kind, hipStream_t st);
 // v'(pos, c) = v[bh * bh_stride + pos * sp + c * sc] for c < ncols, 1 for c == ncols if with_ones;
 // pmax: scratch of BH * vmax_chunks(n) * ncols floats.
 int vmax_chunks(int n);

@@ -27,6 +27,9 @@ _lib = None
 DTYPES = {torch.float32: 0, torch.bfloat16: 1}
 STAGE_EVENTS = 5
 NPRF = 1  # option bit: l2-normalise the rows of q and k (x) before the feature map
+FEAT_TRF = 2  # option bit: trigonometric random features (2m signed features)
+FEAT_ELU = 4  # option bit: elu(x) + 1 (d features, W not read)
+FEATURES = {"prf": 0, "trf": FEAT_TRF, "elu": FEAT_ELU}
 
 
 class KrpeError(RuntimeError):
@@ -63,6 +66,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_toeplitz_conv.argtypes = [fp, fp, fp, i, i, i, i, vp, sz, vp]
     lib.krpe_attention_fwd_workspace.restype = sz
     lib.krpe_attention_fwd_workspace.argtypes = [i, i, i, i, i]
+    lib.krpe_attention_fwd_workspace_ex.restype = sz
+    lib.krpe_attention_fwd_workspace_ex.argtypes = [i, i, i, i, i, ctypes.c_uint]
     lib.krpe_attention_fwd.restype = i
     lib.krpe_attention_fwd.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, vp, sz, vp]
     lib.krpe_attention_fwd_ex.restype = i
@@ -107,22 +112,40 @@ def _dtype_code(t: torch.Tensor, name: str) -> int:
     return DTYPES[t.dtype]
 
 
-def feature_map(x: torch.Tensor, W: torch.Tensor, nprf: bool = False) -> torch.Tensor:
-    """phi = exp(x W^T - ||x||^2/2) / sqrt(m) (Eq. (5)); x [B,H,n,d], W [H,m,d] -> [B,H,n,m] fp32.
+def _flags(nprf: bool, features: str) -> int:
+    if features not in FEATURES:
+        raise KrpeError(f"features must be one of {sorted(FEATURES)}, got {features!r}")
+    return (NPRF if nprf else 0) | FEATURES[features]
 
-    nprf: phi of x / ||x|| (rows normalised first, Algorithm 1)."""
+
+def _proj(W: torch.Tensor | None, H: int, d: int, features: str) -> tuple[torch.Tensor | None, int]:
+    """W (None allowed for elu + 1) and the m the C call takes."""
+    if features == "elu":
+        return None, d
+    if W is None:
+        raise KrpeError("W is required for the prf and trf feature maps")
+    W = _gpu(W, "W")
+    if W.dim() != 3 or W.shape[0] != H or W.shape[2] != d or W.dtype != torch.float32:
+        raise KrpeError("W must be float32 [H, m, d]")
+    return W, W.shape[1]
+
+
+def feature_map(x: torch.Tensor, W: torch.Tensor | None, nprf: bool = False, features: str = "prf") -> torch.Tensor:
+    """phi of x [B,H,n,d] -> [B,H,n,M] fp32 with the projections W [H,m,d].
+
+    features: "prf" (Eq. (5), M = m), "trf" (sin then cos features, M = 2m),
+    "elu" (elu(x) + 1, M = d, W unused).  nprf: phi of x / ||x|| (Algorithm 1)."""
     lib = load()
     x = _gpu(x, "x")
-    W = _gpu(W, "W")
-    if x.dim() != 4 or W.dim() != 3:
-        raise KrpeError("x must be [B,H,n,d] and W [H,m,d]")
+    if x.dim() != 4:
+        raise KrpeError("x must be [B,H,n,d]")
     B, H, n, d = x.shape
-    if W.shape[0] != H or W.shape[2] != d or W.dtype != torch.float32:
-        raise KrpeError("W must be float32 [H, m, d] matching x")
-    m = W.shape[1]
-    phi = torch.empty((B, H, n, m), dtype=torch.float32, device=x.device)
-    st = lib.krpe_feature_map_ex(_ptr(x), _dtype_code(x, "x"), _ptr(W), _ptr(phi), B, H, n, d, m,
-                                 NPRF if nprf else 0, _stream(x.device))
+    flags = _flags(nprf, features)
+    W, m = _proj(W, H, d, features)
+    M = 2 * m if features == "trf" else m
+    phi = torch.empty((B, H, n, M), dtype=torch.float32, device=x.device)
+    st = lib.krpe_feature_map_ex(_ptr(x), _dtype_code(x, "x"), _ptr(W), _ptr(phi), B, H, n, d, m, flags,
+                                 _stream(x.device))
     _check(st, "krpe_feature_map_ex")
     return phi
 
@@ -150,8 +173,9 @@ def toeplitz_conv(b: torch.Tensor, a: torch.Tensor) -> torch.Tensor:
     return y
 
 
-def attention_fwd_workspace(B: int, H: int, n: int, d: int, m: int) -> int:
-    return int(load().krpe_attention_fwd_workspace(B, H, n, d, m))
+def attention_fwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool = False,
+                            features: str = "prf") -> int:
+    return int(load().krpe_attention_fwd_workspace_ex(B, H, n, d, m, _flags(nprf, features)))
 
 
 def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d: int, m: int) -> int:
@@ -164,12 +188,14 @@ def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d:
     return int(out.value)
 
 
-def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
+def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor | None,
                   out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                  events=None, nprf: bool = False) -> torch.Tensor:
+                  events=None, nprf: bool = False, features: str = "prf") -> torch.Tensor:
     """Eq. (10): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
 
     ``nprf``: normalise the rows of q and k first (Algorithm 1's NPRF attention).
+    ``features``: "prf" (Eq. (5)), "trf" (trigonometric, 2m features) or "elu"
+    (elu + 1, W unused and may be None).
 
     ``out`` and ``workspace`` may be passed to reuse allocations (a uint8 tensor
     of at least attention_fwd_workspace() bytes).  ``events``: optional list of
@@ -177,26 +203,27 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     """
     lib = load()
     q, k, v = _gpu(q, "q"), _gpu(k, "k"), _gpu(v, "v")
-    b, W = _gpu(b, "b"), _gpu(W, "W")
+    b = _gpu(b, "b")
     if q.dim() != 4:
         raise KrpeError("q must be [B,H,n,d]")
     B, H, n, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
         raise KrpeError("q, k, v must share shape and dtype")
-    if W.dim() != 3 or W.shape[0] != H or W.shape[2] != d or W.dtype != torch.float32:
-        raise KrpeError("W must be float32 [H, m, d]")
+    flags = _flags(nprf, features)
+    W, m = _proj(W, H, d, features)
     if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
         raise KrpeError("b must be float32 [H, 2n-1]")
-    m = W.shape[1]
     if out is None:
         out = torch.empty((B, H, n, d), dtype=torch.float32, device=q.device)
     elif out.shape != (B, H, n, d) or out.dtype != torch.float32 or not out.is_contiguous():
         raise KrpeError("out must be a contiguous float32 [B,H,n,d] tensor")
-    wsb = int(lib.krpe_attention_fwd_workspace(B, H, n, d, m))
+    wsb = int(lib.krpe_attention_fwd_workspace_ex(B, H, n, d, m, flags))
     if workspace is None:
         workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
     dt = _dtype_code(q, "q")
-    args = (_ptr(q), _ptr(k), _ptr(v), dt, _ptr(b), _ptr(W), _ptr(out), B, H, n, d, m, NPRF if nprf else 0,
+    if workspace.numel() < wsb:
+        raise KrpeError(f"workspace must hold at least {wsb} bytes")
+    args = (_ptr(q), _ptr(k), _ptr(v), dt, _ptr(b), _ptr(W), _ptr(out), B, H, n, d, m, flags,
             workspace.data_ptr(), workspace.numel(), _stream(q.device))
     if events is None:
         st = lib.krpe_attention_fwd_ex(*args)

@@ -101,6 +101,16 @@ def orthogonal_features(rng: np.random.Generator, m: int, d: int) -> np.ndarray:
     return w * norms[:, None]
 
 
+def sphere_features(rng: np.random.Generator, m: int, d: int) -> np.ndarray:
+    """Sphere-PRF rows (the appendix comparison of feature maps): i.i.d. uniform on the
+    sphere of radius sqrt(d), drawn as normalised Gaussian vectors."""
+    g = rng.standard_normal((m, d))
+    return g / np.linalg.norm(g, axis=1, keepdims=True) * np.sqrt(d)
+
+
+_FEATURE_DRAWS = {"gaussian": gaussian_features, "orthogonal": orthogonal_features, "sphere": sphere_features}
+
+
 def _bias(rng: np.random.Generator, wl: Workload) -> np.ndarray:
     n = wl.n
     t = np.arange(-(n - 1), n, dtype=np.float64)
@@ -137,7 +147,7 @@ def make(wid: int | Workload, seed: int | None = None, *, heads: int | None = No
     v = (rng.standard_normal(shape) * scale).astype(np.float32)
     if wl.qkv_dtype == "bf16":
         q, k, v = bf16_round(q), bf16_round(k), bf16_round(v)
-    feat = gaussian_features if wl.features == "gaussian" else orthogonal_features
+    feat = _FEATURE_DRAWS[wl.features]
     W = np.stack([feat(rng, wl.m, wl.d) for _ in range(H)]).astype(np.float32)
     b = np.stack([_bias(rng, wl) for _ in range(H)]).astype(np.float32)
     return {"q": q, "k": k, "v": v, "W": W, "b": b, "workload": wl, "H": H}
@@ -146,7 +156,9 @@ def make(wid: int | Workload, seed: int | None = None, *, heads: int | None = No
 def custom(B: int, H: int, n: int, d: int, m: int, *, seed: int = 0,
            qkv_dtype: str = "f32", features: str = "gaussian", bias: str = "normal",
            bias_sigma: float = 0.5, qk_scale: float | None = None) -> dict:
-    """Inputs with arbitrary shapes and the same distributions (for edge cases)."""
+    """Inputs with arbitrary shapes and the same distributions (for edge cases).
+
+    features: how the rows of W are drawn, "gaussian", "orthogonal" or "sphere"."""
     wl = Workload(0, f"custom-{B}x{H}x{n}x{d}x{m}", B, H, n, d, m, qkv_dtype,
                   features, bias, bias_sigma, bias == "causal")
     rng = np.random.default_rng([2106, 12566, 0, seed])
@@ -157,7 +169,7 @@ def custom(B: int, H: int, n: int, d: int, m: int, *, seed: int = 0,
     v = (rng.standard_normal(shape) * d ** -0.25).astype(np.float32)
     if qkv_dtype == "bf16":
         q, k, v = bf16_round(q), bf16_round(k), bf16_round(v)
-    feat = gaussian_features if features == "gaussian" else orthogonal_features
+    feat = _FEATURE_DRAWS[features]
     W = np.stack([feat(rng, m, d) for _ in range(H)]).astype(np.float32)
     b = np.stack([_bias(rng, wl) for _ in range(H)]).astype(np.float32)
     return {"q": q, "k": k, "v": v, "W": W, "b": b, "workload": wl, "H": H}

@@ -39,7 +39,8 @@ def test_header_declares_the_boundary():
     for required in ("krpe_feature_map", "krpe_toeplitz_conv", "krpe_attention_fwd",
                      "krpe_toeplitz_conv_workspace", "krpe_attention_fwd_workspace",
                      "krpe_attention_fwd_profiled", "krpe_status_str", "krpe_last_error",
-                     "krpe_abi_version", "krpe_feature_map_ex", "krpe_attention_fwd_ex"):
+                     "krpe_abi_version", "krpe_feature_map_ex", "krpe_attention_fwd_ex",
+                     "krpe_attention_fwd_workspace_ex"):
         assert required in names
 
 
@@ -49,7 +50,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.krpe_abi_version() == 3
+    assert lib.krpe_abi_version() == 4
     for s in range(9):
         assert lib.krpe_status_str(s)
     assert lib.krpe_status_str(99) == b"unknown status"
@@ -105,12 +106,28 @@ def test_attention_validation(lib):
 def test_option_bits_validation(lib):
     wsb = lib.krpe_attention_fwd_workspace(1, 1, 8, 4, 4)
     ex = lambda flags: lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, flags, WSP, wsb, None)
-    assert ex(2) == UNSUP                    # unknown option bit
+    assert ex(8) == UNSUP                    # unknown option bit
     assert ex(1 | 8) == UNSUP
+    assert ex(2 | 4) == UNSUP                # TRF and elu + 1 together
+    # elu + 1 needs m == d (here d = 4, m = 3); TRF doubles the features (2m <= 1024)
+    assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 3, 4, WSP, wsb, None) == SHAPE
+    assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 600, 2, WSP, wsb, None) == UNSUP
+    assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, None, Z, 1, 1, 8, 4, 4, 2, WSP, wsb, None) == NULL
+    assert lib.krpe_attention_fwd_ex(None, K, V, 0, BB, None, Z, 1, 1, 8, 4, 4, 4, WSP, wsb, None) == NULL
+    wse = lambda flags, m=4: lib.krpe_attention_fwd_workspace_ex(2, 3, 100, 4, m, flags)
+    assert wse(0) == lib.krpe_attention_fwd_workspace(2, 3, 100, 4, 4)
+    assert wse(1) == wse(0)                  # normalisation needs no space
+    assert wse(2) > wse(0)                   # 2m trigonometric features
+    assert wse(4) == wse(0)                  # elu + 1: M = d = m
+    assert wse(4, m=3) == 0 and wse(6) == 0 and wse(8) == 0
+    assert wse(2, m=513) == 0
     assert lib.krpe_attention_fwd_ex(None, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, WSP, wsb, None) == NULL
     assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, None, wsb, None) == WS
     fm = lambda flags: lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 4, flags, None)
-    assert fm(4) == UNSUP
+    assert fm(8) == UNSUP
+    assert fm(6) == UNSUP
+    assert lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 3, 4, None) == SHAPE
+    assert lib.krpe_feature_map_ex(Q, 0, None, Z, 1, 1, 8, 4, 4, 2, None) == NULL
     assert lib.krpe_feature_map_ex(None, 0, W, Z, 1, 1, 8, 4, 4, 1, None) == NULL
 
 

@@ -27,10 +27,20 @@ MUTANTS = {
     "toeplitz_transposed": ("out[:, h] = a[:, h] @ C.T", "out[:, h] = a[:, h] @ C"),
     "toeplitz_matrix_sign": ("return np.exp(b_h[j - i + n - 1])", "return np.exp(b_h[i - j + n - 1])"),
     "rows_offset_sign": ("c = np.exp(b[h][np.arange(n) - i + n - 1])", "c = np.exp(b[h][i - np.arange(n) + n - 1])"),
-    "rows_wrong_head_features": ("cache[(beta, h)] = prf_features(k[beta, h], W[h])", "cache[(beta, h)] = prf_features(k[beta, h], W[0])"),
+    "rows_wrong_head_features": ("cache[(beta, h)] = fmap(k[beta, h], W[h])", "cache[(beta, h)] = fmap(k[beta, h], W[0])"),
     "nprf_keys_not_normalised": ("        q, k = normalize_rows(q), normalize_rows(k)\n    Bn", "        q = normalize_rows(q)\n    Bn"),
     "nprf_squared_norm": ("return np.divide(x, norm, out=np.zeros_like(x), where=norm > 0)", "return np.divide(x, norm * norm, out=np.zeros_like(x), where=norm > 0)"),
     "nprf_ignored": ("    if nprf:\n        q, k = normalize_rows(q), normalize_rows(k)\n    Bn", "    Bn"),
+    "trf_norm_sign": ("amp = np.exp(0.5 * np.sum(x * x, axis=-1, keepdims=True)) / np.sqrt(m)",
+                      "amp = np.exp(-0.5 * np.sum(x * x, axis=-1, keepdims=True)) / np.sqrt(m)"),
+    "trf_cos_twice": ("return np.concatenate([amp * np.sin(proj), amp * np.cos(proj)], axis=-1)",
+                      "return np.concatenate([amp * np.cos(proj), amp * np.cos(proj)], axis=-1)"),
+    "trf_sqrt_2m": ("amp = np.exp(0.5 * np.sum(x * x, axis=-1, keepdims=True)) / np.sqrt(m)",
+                    "amp = np.exp(0.5 * np.sum(x * x, axis=-1, keepdims=True)) / np.sqrt(2 * m)"),
+    "elu_plus_one_dropped": ("return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))",
+                             "return np.where(x > 0, x, np.exp(np.minimum(x, 0.0)) - 1.0)"),
+    "elu_branch_flipped": ("return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))",
+                           "return np.where(x >= 0, np.exp(np.minimum(x, 0.0)), x + 1.0)"),
 }
 
 

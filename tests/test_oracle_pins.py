@@ -11,6 +11,9 @@ Sources of truth used here (none of them re-types the oracle's formula):
 * the closed form Eq. (3) (linear attention) that Eq. (10) reduces to when b
   is constant, and its prefix-sum form under the causal mask;
 * the PRF variance lemma of Section 3.3 (unbiasedness and exact variance of the PRF kernel estimate);
+* for the other feature maps of Section 2: scalar loops, the product-to-sum
+  identity of the trigonometric map, its unbiasedness for the softmax kernel
+  (E cos(w u) = exp(-|u|^2/2) for Gaussian w), and the linear-attention route;
 * the softmax-with-RPE limit (Eq. (1) with the bias of Eq. (6)) as m grows;
 * textbook special cases of a Toeplitz product (identity, shift, sum,
   cumulative sum) and invariants of Eq. (10).
@@ -333,11 +336,132 @@ def check_rows_match_full(impl):
         assert np.isclose(dr[r], den[beta, h, i], rtol=1e-12)
 
 
+def _brute_trf(x_row, W_h):
+    """The trigonometric map of Section 2 for one vector, scalar loops: sin features, then cos."""
+    m = len(W_h)
+    amp = math.exp(sum(t * t for t in x_row) / 2.0) / math.sqrt(m)
+    dots = [sum(W_h[l][a] * x_row[a] for a in range(len(x_row))) for l in range(m)]
+    return [amp * math.sin(t) for t in dots] + [amp * math.cos(t) for t in dots]
+
+
+def _brute_elu(x_row, W_h=None):
+    """elu(x) + 1 for one vector, scalar branches."""
+    return [t + 1.0 if t > 0 else math.exp(t) for t in x_row]
+
+
+def _brute_attention_map(q, k, v, b, W, phi):
+    """Eq. (10) with scalar loops for any feature map phi(row, W_h)."""
+    Bn, H, n, d = q.shape
+    z = np.zeros((Bn, H, n, d))
+    for beta in range(Bn):
+        for h in range(H):
+            Wh = None if W is None else W[h].tolist()
+            fq = [phi(q[beta, h, i].tolist(), Wh) for i in range(n)]
+            fk = [phi(k[beta, h, j].tolist(), Wh) for j in range(n)]
+            for i in range(n):
+                num = [0.0] * d
+                den = 0.0
+                for j in range(n):
+                    w = math.exp(b[h][j - i + n - 1]) * sum(a * c for a, c in zip(fq[i], fk[j]))
+                    den += w
+                    for c in range(d):
+                        num[c] += w * v[beta, h, j, c]
+                for c in range(d):
+                    z[beta, h, i, c] = num[c] / den
+    return z
+
+
+def check_trf_brute_force(impl):
+    """TRF features and Eq. (10) with them against scalar loops (values near 1, so the
+    signed denominator stays away from zero)."""
+    rng = np.random.default_rng(31)
+    for (n, d, m) in [(1, 3, 2), (5, 4, 3), (9, 6, 5)]:
+        q, k, v, b, W = _rand_case(rng, 2, 2, n, d, m, scale=0.15)
+        W *= 0.3
+        ref_phi = np.array([[[_brute_trf(q[a, h, i].tolist(), W[h].tolist()) for i in range(n)]
+                             for h in range(2)] for a in range(2)])
+        assert np.max(np.abs(impl.trf_features(q, W) - ref_phi)) < 1e-13
+        assert np.max(np.abs(impl.features(q, W, "trf") - ref_phi)) < 1e-13
+        z, _ = impl.attention(q, k, v, b, W, kind="trf")
+        assert _rownorm_err(z, _brute_attention_map(q, k, v, b, W, _brute_trf)) < 1e-11, (n, d, m)
+        rows = [(1, 0, n - 1), (0, 1, 0)]
+        zr, _ = impl.attention_rows(q, k, v, b, W, rows, kind="trf")
+        for r, (a, h, i) in enumerate(rows):
+            assert np.allclose(zr[r], z[a, h, i], rtol=1e-12, atol=1e-14)
+
+
+def check_trf_kernel_identity(impl):
+    """sin a sin b + cos a cos b = cos(a - b): phi(x).phi(y) equals
+    exp((|x|^2 + |y|^2)/2) / m * sum_l cos(w_l (x - y)), a form with no sin/cos split."""
+    rng = np.random.default_rng(32)
+    x = rng.standard_normal((7, 5)) * 0.6
+    y = rng.standard_normal((9, 5)) * 0.6
+    W = rng.standard_normal((11, 5))
+    fx, fy = impl.trf_features(x, W), impl.trf_features(y, W)
+    assert fx.shape == (7, 22)
+    for i in range(7):
+        for j in range(9):
+            u = x[i] - y[j]
+            ref = math.exp((x[i] @ x[i] + y[j] @ y[j]) / 2.0) / 11.0 * sum(math.cos(W[l] @ u) for l in range(11))
+            assert abs(fx[i] @ fy[j] - ref) < 1e-12 * max(1.0, abs(ref))
+
+
+def check_trf_unbiased(impl):
+    """With w ~ N(0, I), E[cos(w u)] = exp(-|u|^2/2), so phi(x).phi(y) estimates exp(x y^T)
+    (the softmax kernel); the m-term mean of cosines is within 6/sqrt(m) of its expectation."""
+    rng = np.random.default_rng(33)
+    d, m = 6, 40000
+    x = rng.standard_normal(d) * 0.3
+    y = rng.standard_normal(d) * 0.3
+    W = rng.standard_normal((m, d))
+    est = impl.trf_features(x[None], W)[0] @ impl.trf_features(y[None], W)[0]
+    amp = math.exp((x @ x + y @ y) / 2.0)
+    assert abs(est / amp - math.exp(-((x - y) @ (x - y)) / 2.0)) < 6.0 / math.sqrt(m)
+    assert abs(est / math.exp(x @ y) - 1.0) < 6.0 * amp / math.sqrt(m) / math.exp(x @ y)
+
+
+def check_elu_brute_force(impl):
+    """elu + 1 features and Eq. (10) with them against scalar loops, W not used."""
+    rng = np.random.default_rng(34)
+    for (n, d) in [(1, 3), (6, 4), (10, 7)]:
+        q, k, v, b, _ = _rand_case(rng, 2, 2, n, d, 1, scale=1.0)
+        q[0, 0, 0, 0] = 0.0
+        ref_phi = np.array([[[_brute_elu(q[a, h, i].tolist()) for i in range(n)] for h in range(2)]
+                            for a in range(2)])
+        assert np.max(np.abs(impl.elu_features(q) - ref_phi)) < 1e-15
+        z, _ = impl.attention(q, k, v, b, None, kind="elu")
+        assert _rownorm_err(z, _brute_attention_map(q, k, v, b, None, _brute_elu)) < 1e-12, (n, d)
+        rows = [(1, 1, n - 1), (0, 0, 0)]
+        zr, _ = impl.attention_rows(q, k, v, b, None, rows, kind="elu")
+        for r, (a, h, i) in enumerate(rows):
+            assert np.allclose(zr[r], z[a, h, i], rtol=1e-12, atol=1e-14)
+
+
+def check_feature_maps_linear_route(impl):
+    """Constant b: Eq. (10) is linear attention, Eq. (3), whatever the feature map;
+    computed through the d x M summary sum_j phi(k_j)^T v_j (the O(n) route)."""
+    rng = np.random.default_rng(35)
+    n, d, m = 30, 6, 8
+    q, k, v, _, W = _rand_case(rng, 1, 2, n, d, m, scale=0.3)
+    b = np.full((2, 2 * n - 1), -0.21)
+    maps = {"trf": lambda x, Wh: [_brute_trf(r, Wh) for r in x.tolist()],
+            "elu": lambda x, Wh: [_brute_elu(r) for r in x.tolist()]}
+    for kind, phi in maps.items():
+        z, _ = impl.attention(q, k, v, b, W if kind == "trf" else None, kind=kind)
+        for h in range(2):
+            fq = np.array(phi(q[0, h], W[h].tolist()))
+            fk = np.array(phi(k[0, h], W[h].tolist()))
+            ref = (fq @ (fk.T @ v[0, h])) / (fq @ fk.sum(axis=0))[:, None]
+            assert _rownorm_err(z[0, h], ref) < 1e-11, kind
+
+
 ALL_CHECKS = [check_brute_force, check_algorithm1_route, check_single_position,
               check_const_bias_is_linear_attention, check_causal_prefix_sums,
               check_only_diagonal, check_shift_kernel, check_invariants,
               check_causality, check_prf_variance_lemma, check_toeplitz_special_cases,
-              check_rows_match_full, check_nprf_brute_force, check_nprf_scale_invariance]
+              check_rows_match_full, check_nprf_brute_force, check_nprf_scale_invariance,
+              check_trf_brute_force, check_trf_kernel_identity, check_trf_unbiased,
+              check_elu_brute_force, check_feature_maps_linear_route]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda f: f.__name__)
