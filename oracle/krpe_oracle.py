@@ -25,6 +25,12 @@ float64 (inputs given in fp32 or bf16 are converted exactly):
 * ``attention_rows``    -- the same formula evaluated for selected rows only,
                            so that outputs of full-size workloads can be
                            checked one by one.
+* ``attention_grad``    -- gradients of <G, z> with respect to q, k, v and b
+                           (W fixed), by the chain rule through Eq. (10),
+                           Eq. (5), c = exp(b) and the row normalisation;
+                           the paper states no backward pass, so this is the
+                           derivative of its forward definition, pinned by
+                           finite differences.
 * ``normalize_rows``    -- the first step of Algorithm 1 (NPRF attention,
                            Section 3.3): every query and key divided by its
                            l2 norm; ``attention(..., nprf=True)`` applies it.
@@ -48,7 +54,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = ["prf_features", "trf_features", "elu_features", "features", "toeplitz_matrix",
-           "toeplitz_product", "attention", "attention_rows", "normalize_rows"]
+           "toeplitz_product", "attention", "attention_rows", "attention_grad", "normalize_rows"]
 
 
 def _f64(x) -> np.ndarray:
@@ -203,3 +209,62 @@ def attention_rows(q, k, v, b, W, rows, *, nprf: bool = False, kind: str = "prf"
         den[r] = w.sum()
         z[r] = (w @ _f64(v[beta, h])) / den[r]
     return z, den
+
+
+def attention_grad(q, k, v, b, W, G, *, nprf: bool = False):
+    """Gradients of L = sum z * G through Eq. (10) with PRF features, W fixed.
+
+    Per (batch, head), with Phi_q, Phi_k from Eq. (5), K = Phi_q Phi_k^T,
+    C_ij = c_{j-i} = exp(b_{j-i}), A = C * K (elementwise), z = (A v) / (A 1):
+      dN_i = G_i / den_i,  dden_i = -(G_i . z_i) / den_i,
+      dA = dN v^T + dden 1^T,
+      dv = A^T dN,
+      dK = dA * C,   dPhi_q = dK Phi_k,   dPhi_k = dK^T Phi_q,
+      dC = dA * K,   dc_t = sum over the diagonal j - i = t of dC,  db_t = dc_t c_t,
+      dx = (dPhi * Phi) W - x * rowsum(dPhi * Phi)     (d phi_l / dx = phi_l (w_l - x)),
+    and with nprf, x = u / ||u|| gives du = (dx - x (x . dx)) / ||u|| (0 for a zero row).
+    db is summed over the batch (b is per head); entries with b_t = -inf get 0.
+
+    q, k, v, G : [B, H, n, d];  b : [H, 2n-1];  W : [H, m, d].
+    Returns (dq, dk, dv [B, H, n, d], db [H, 2n-1]) in float64.
+    """
+    q, k, v, b, W, G = map(_f64, (q, k, v, b, W, G))
+    Bn, H, n, d = q.shape
+    qs, ks = (normalize_rows(q), normalize_rows(k)) if nprf else (q, k)
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    db = np.zeros_like(b)
+    i = np.arange(n)[:, None]
+    j = np.arange(n)[None, :]
+    for h in range(H):
+        C = np.exp(b[h][j - i + n - 1])
+        for beta in range(Bn):
+            fq = prf_features(qs[beta, h], W[h])
+            fk = prf_features(ks[beta, h], W[h])
+            K = fq @ fk.T
+            A = C * K
+            den = A.sum(axis=1)
+            z = (A @ v[beta, h]) / den[:, None]
+            dN = G[beta, h] / den[:, None]
+            dden = -np.sum(G[beta, h] * z, axis=1) / den
+            dA = dN @ v[beta, h].T + dden[:, None]
+            dv[beta, h] = A.T @ dN
+            dK = dA * C
+            dfq = dK @ fk
+            dfk = dK.T @ fq
+            dC = dA * K
+            for t in range(-(n - 1), n):
+                db[h, t + n - 1] += np.trace(dC, offset=t)
+            for x, dphi, phi, out, raw in ((qs[beta, h], dfq, fq, dq, q[beta, h]),
+                                           (ks[beta, h], dfk, fk, dk, k[beta, h])):
+                P = dphi * phi
+                dx = P @ W[h] - x * P.sum(axis=1, keepdims=True)
+                if nprf:
+                    nrm = np.sqrt(np.sum(raw * raw, axis=1, keepdims=True))
+                    dx = np.divide(dx - x * np.sum(x * dx, axis=1, keepdims=True), nrm,
+                                   out=np.zeros_like(dx), where=nrm > 0)
+                out[beta, h] = dx
+    cfin = np.isfinite(b)
+    db = np.where(cfin, db * np.exp(np.where(cfin, b, 0.0)), 0.0)
+    return dq, dk, dv, db

@@ -39,6 +39,14 @@ MUTANTS = {
                     "amp = np.exp(0.5 * np.sum(x * x, axis=-1, keepdims=True)) / np.sqrt(2 * m)"),
     "elu_plus_one_dropped": ("return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))",
                              "return np.where(x > 0, x, np.exp(np.minimum(x, 0.0)) - 1.0)"),
+    "grad_den_term_dropped": ("dA = dN @ v[beta, h].T + dden[:, None]", "dA = dN @ v[beta, h].T"),
+    "grad_keys_not_transposed": ("dfk = dK.T @ fq", "dfk = dK @ fq"),
+    "grad_db_chain_missing": ("db = np.where(cfin, db * np.exp(np.where(cfin, b, 0.0)), 0.0)",
+                              "db = np.where(cfin, db, 0.0)"),
+    "grad_diagonal_sign": ("db[h, t + n - 1] += np.trace(dC, offset=t)", "db[h, t + n - 1] += np.trace(dC, offset=-t)"),
+    "grad_norm_term_dropped": ("dx = P @ W[h] - x * P.sum(axis=1, keepdims=True)", "dx = P @ W[h]"),
+    "grad_nprf_projection_dropped": ("dx = np.divide(dx - x * np.sum(x * dx, axis=1, keepdims=True), nrm,",
+                                     "dx = np.divide(dx, nrm,"),
     "elu_branch_flipped": ("return np.where(x > 0, x + 1.0, np.exp(np.minimum(x, 0.0)))",
                            "return np.where(x >= 0, np.exp(np.minimum(x, 0.0)), x + 1.0)"),
 }

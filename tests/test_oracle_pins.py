@@ -14,6 +14,9 @@ Sources of truth used here (none of them re-types the oracle's formula):
 * for the other feature maps of Section 2: scalar loops, the product-to-sum
   identity of the trigonometric map, its unbiasedness for the softmax kernel
   (E cos(w u) = exp(-|u|^2/2) for Gaussian w), and the linear-attention route;
+* for the gradients (the paper states no backward pass): central finite
+  differences of the forward definition, and invariances (constant shift of
+  b, constant shift of a value column, scale of normalised queries/keys);
 * the softmax-with-RPE limit (Eq. (1) with the bias of Eq. (6)) as m grows;
 * textbook special cases of a Toeplitz product (identity, shift, sum,
   cumulative sum) and invariants of Eq. (10).
@@ -455,13 +458,72 @@ def check_feature_maps_linear_route(impl):
             assert _rownorm_err(z[0, h], ref) < 1e-11, kind
 
 
+def _fd_grads(impl, q, k, v, b, W, G, nprf, eps=1e-6):
+    """Central differences of L = sum(z * G) in every entry of q, k, v and every finite entry of b."""
+    def loss(q_, k_, v_, b_):
+        z, _ = impl.attention(q_, k_, v_, b_, W, nprf=nprf)
+        return float(np.sum(z * G))
+    out = []
+    for which in range(4):
+        args = [q.copy(), k.copy(), v.copy(), b.copy()]
+        base = args[which]
+        g = np.zeros_like(base)
+        for idx in np.ndindex(base.shape):
+            if not np.isfinite(base[idx]):
+                continue
+            keep = base[idx]
+            base[idx] = keep + eps
+            lp = loss(*args)
+            base[idx] = keep - eps
+            lm = loss(*args)
+            base[idx] = keep
+            g[idx] = (lp - lm) / (2 * eps)
+        out.append(g)
+    return out
+
+
+def check_grad_finite_differences(impl):
+    """attention_grad against central differences of the forward definition (tiny cases,
+    plain and normalised, one with a causal b)."""
+    rng = np.random.default_rng(51)
+    for (n, d, m, nprf, causal) in [(5, 3, 4, False, False), (4, 2, 3, True, False), (6, 3, 5, False, True)]:
+        q, k, v, b, W = _rand_case(rng, 1, 2, n, d, m, scale=0.7)
+        if causal:
+            b[:, n:] = -np.inf
+        G = rng.standard_normal(q.shape)
+        got = impl.attention_grad(q, k, v, b, W, G, nprf=nprf)
+        ref = _fd_grads(impl, q, k, v, b, W, G, nprf)
+        for name, a_, r_ in zip("qkvb", got, ref):
+            assert a_.shape == r_.shape, name
+            scale = max(np.max(np.abs(r_)), 1e-3)
+            assert np.max(np.abs(a_ - r_)) <= 1e-6 * scale, (name, n, nprf, causal, np.max(np.abs(a_ - r_)))
+        if causal:
+            assert np.all(got[3][:, n:] == 0.0)
+
+
+def check_grad_invariants(impl):
+    """A constant shift of b leaves z unchanged (sum_t db_t = 0); adding a to every value of
+    column c shifts z[., c] by a (sum_j dv[j, c] = sum_i G[i, c]); under NPRF, scaling a query
+    or key changes nothing (dq_i . q_i = dk_j . k_j = 0)."""
+    rng = np.random.default_rng(52)
+    q, k, v, b, W = _rand_case(rng, 2, 2, 12, 5, 7)
+    G = rng.standard_normal(q.shape)
+    dq, dk, dv, db = impl.attention_grad(q, k, v, b, W, G)
+    assert np.max(np.abs(db.sum(axis=1))) < 1e-10 * np.max(np.abs(db))
+    assert np.allclose(dv.sum(axis=2), G.sum(axis=2), rtol=1e-10, atol=1e-12)
+    dq, dk, dv, db = impl.attention_grad(q * 2.0, k * 0.5, v, b, W, G, nprf=True)
+    assert np.max(np.abs(np.sum(dq * q, axis=-1))) < 1e-10 * np.max(np.abs(dq)) * np.max(np.abs(q))
+    assert np.max(np.abs(np.sum(dk * k, axis=-1))) < 1e-10 * np.max(np.abs(dk)) * np.max(np.abs(k))
+
+
 ALL_CHECKS = [check_brute_force, check_algorithm1_route, check_single_position,
               check_const_bias_is_linear_attention, check_causal_prefix_sums,
               check_only_diagonal, check_shift_kernel, check_invariants,
               check_causality, check_prf_variance_lemma, check_toeplitz_special_cases,
               check_rows_match_full, check_nprf_brute_force, check_nprf_scale_invariance,
               check_trf_brute_force, check_trf_kernel_identity, check_trf_unbiased,
-              check_elu_brute_force, check_feature_maps_linear_route]
+              check_elu_brute_force, check_feature_maps_linear_route,
+              check_grad_finite_differences, check_grad_invariants]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda f: f.__name__)
