@@ -190,6 +190,36 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                                           void* const* events);
 
 /*
+ * Bytes of workspace krpe_attention_bwd needs (0 if the sizes or flags are
+ * invalid or unsupported).
+ */
+size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned flags);
+
+/*
+ * Backward pass of krpe_attention_fwd_ex (PRF features of Eq. (5), optional
+ * KRPE_NPRF; W fixed): the gradients of L = sum(dz * z) with respect to q, k
+ * and v, z from Eq. (10).  The paper states no backward pass; these are the
+ * derivatives of its forward definition.  With A = C o (phi(Q) phi(K)^T),
+ * den = A 1 and Gh = [dz / den, -(dz . z) / den] per row:
+ *   dv = A^T Gh[:, :d],  dphi(Q) = ((Gh [v, 1]^T) o C) phi(K),
+ *   dphi(K) = ((Gh [v, 1]^T) o C)^T phi(Q),  dx = (dphi o phi) W - x rowsum(dphi o phi)
+ * (through the row normalisation when KRPE_NPRF).  Each of the three
+ * products is one run of the forward's FFT convolution kernel, with the
+ * transposed Toeplitz matrix (the reversed b) where C^T appears; the forward
+ * pass is recomputed inside (its exact-row evaluation included).
+ * q, k, v : [B, H, n, d] in qkv_dtype    b : [H, 2n-1]    W : [H, m, d]
+ * dz      : [B, H, n, d] fp32             dq, dk, dv : [B, H, n, d] fp32 (outputs)
+ * db      : must be NULL (the gradient of b is not computed: KRPE_ERR_UNSUPPORTED).
+ * ws      : device workspace of at least krpe_attention_bwd_workspace() bytes.
+ * Outputs must not overlap each other, an input or the workspace.
+ */
+krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, int qkv_dtype,
+                                 const float* b, const float* W, const float* dz,
+                                 float* dq, float* dk, float* dv, float* db,
+                                 int B, int H, int n, int d, int m, unsigned flags,
+                                 void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Rows of the last krpe_attention_fwd / _ex call (with this workspace and
  * these sizes, whatever its option bits) that were evaluated exactly instead
  * of through the FFT.

@@ -117,6 +117,32 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   return L;
 }
 
+BwdLayout bwd_layout(int B, int H, int n, int d, int M) {
+  BwdLayout L{};
+  L.f = attn_layout(B, H, n, d, M);
+  const size_t N = static_cast<size_t>(1) << L.f.l2;
+  const size_t bh = static_cast<size_t>(B) * H;
+  const size_t cmax = static_cast<size_t>(M > d + 1 ? M : d + 1), pairs = (cmax + 1) / 2;
+  size_t off = L.f.total;
+  auto take = [&off](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.zf = take(bh * n * d * sizeof(float));
+  L.den = take(bh * n * sizeof(float));
+  L.brev = take(static_cast<size_t>(H) * (2 * n - 1) * sizeof(float));
+  L.hsr = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  L.gh = take(bh * (d + 1) * N * sizeof(float));
+  L.vh = take(bh * (d + 1) * N * sizeof(float));
+  L.vsc = take(bh * pairs * N * sizeof(float2));
+  L.colmax = take(bh * cmax * sizeof(float));
+  L.vmax = take(bh * vmax_chunks(n) * cmax * sizeof(float));
+  L.part = take(bh * conv_splits(L.f.l2) * cmax * n * sizeof(float));
+  L.total = off;
+  return L;
+}
+
 ConvLayout conv_layout(int B, int H, int C, int n) {
   ConvLayout L{};
   L.l2 = log2_ceil(n);
@@ -140,13 +166,67 @@ ConvLayout conv_layout(int B, int H, int C, int n) {
   return L;
 }
 
+// The forward launch sequence of Eq. (10) on a carved workspace: z, and the
+// row denominators into den_out when not NULL (the backward pass needs them).
+krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const void* k, const void* v, bool bf16,
+                          const float* b, const float* W, float* z, float* den_out, int BHi, int H, int n, int d,
+                          int m, int M, int kind, bool nprf, hipStream_t st, void* const* events) {
+  float2* tw = reinterpret_cast<float2*>(w + L.tw);
+  float2* Hs = reinterpret_cast<float2*>(w + L.hs);
+  float2* hnorm = reinterpret_cast<float2*>(w + L.hnorm);
+  float* phiq = reinterpret_cast<float*>(w + L.phiq);
+  float* phik = reinterpret_cast<float*>(w + L.phik);
+  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
+  float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* vmax = reinterpret_cast<float*>(w + L.vmax);
+  float* x2 = reinterpret_cast<float*>(w + L.x2);
+  float2* wb = reinterpret_cast<float2*>(w + L.wb);
+  float* part = reinterpret_cast<float*>(w + L.part);
+  unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
+  unsigned long long* fixmask = reinterpret_cast<unsigned long long*>(w + L.fixmask);
+  double* fixpart = reinterpret_cast<double*>(w + L.fixpart);
+  int2* brange = reinterpret_cast<int2*>(w + L.brange);
+  const int N = 1 << L.l2;
+  const int pairs = (d + 2) / 2;
+
+  if (krpe_status_t s = record(events, 0, st)) return s;
+  if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch")) return s;
+  if (krpe_status_t s = record(events, 1, st)) return s;
+  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix,
+                                                     nprf, kind, st),
+                                  "feature map launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_vprep(bf16, v, d, 1, static_cast<long long>(n) * d, d, true, BHi, n, N,
+                                               vmax, colmax, vsc, st),
+                                  "column launch"))
+    return s;
+  if (krpe_status_t s = record(events, 2, st)) return s;
+  if (krpe_status_t s = hip_check(launch_conv(L.l2, phiq, phik, static_cast<long long>(M) * N, vsc, colmax, Hs, tw,
+                                              part, BHi, H, n, d + 1, M, st),
+                                  "conv launch"))
+    return s;
+  if (krpe_status_t s = record(events, 3, st)) return s;
+  if (krpe_status_t s = hip_check(launch_gram(phik, vsc, x2, BHi, M, N, pairs, L.ksplit, st), "norm launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, M, d, L.ksplit, st), "bound launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, den_out, fix, fixmask, BHi, H, n, L.l2, d, M, st),
+                                  "combine launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, den_out, fix, fixmask, fixpart, brange, BHi, H, n, N, d, M, st),
+                                  "fixup launch"))
+    return s;
+  return record(events, 4, st);
+}
+
 }  // namespace krpe
 
 using namespace krpe;
 
 extern "C" {
 
-int krpe_abi_version(void) { return 4; }
+int krpe_abi_version(void) { return 5; }
 
 const char* krpe_status_str(int s) {
   switch (s) {
@@ -290,57 +370,9 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   for (const Range& r : ins)
     if (overlaps(rz, r) || overlaps(rws, r)) return fail(KRPE_ERR_ALIAS, "z or the workspace overlaps an input");
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  char* w = static_cast<char*>(ws);
-  float2* tw = reinterpret_cast<float2*>(w + L.tw);
-  float2* Hs = reinterpret_cast<float2*>(w + L.hs);
-  float2* hnorm = reinterpret_cast<float2*>(w + L.hnorm);
-  float* phiq = reinterpret_cast<float*>(w + L.phiq);
-  float* phik = reinterpret_cast<float*>(w + L.phik);
-  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
-  float* colmax = reinterpret_cast<float*>(w + L.colmax);
-  float* vmax = reinterpret_cast<float*>(w + L.vmax);
-  float* x2 = reinterpret_cast<float*>(w + L.x2);
-  float2* wb = reinterpret_cast<float2*>(w + L.wb);
-  float* part = reinterpret_cast<float*>(w + L.part);
-  unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
-  unsigned long long* fixmask = reinterpret_cast<unsigned long long*>(w + L.fixmask);
-  double* fixpart = reinterpret_cast<double*>(w + L.fixpart);
-  int2* brange = reinterpret_cast<int2*>(w + L.brange);
-  const int BHi = static_cast<int>(bh);
-  const int N = 1 << L.l2;
-  const bool bf16 = qkv_dtype == KRPE_BF16;
-  const int pairs = (d + 2) / 2;
-
-  if (krpe_status_t s = record(events, 0, st)) return s;
-  if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
-  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch")) return s;
-  if (krpe_status_t s = record(events, 1, st)) return s;
-  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m, fix,
-                                                     (flags & KRPE_NPRF) != 0, kind, st),
-                                  "feature map launch"))
-    return s;
-  if (krpe_status_t s = hip_check(launch_vprep(bf16, v, d, 1, static_cast<long long>(n) * d, d, true, BHi, n, N,
-                                               vmax, colmax, vsc, st),
-                                  "column launch"))
-    return s;
-  if (krpe_status_t s = record(events, 2, st)) return s;
-  if (krpe_status_t s = hip_check(launch_conv(L.l2, phiq, phik, static_cast<long long>(M) * N, vsc, colmax, Hs, tw,
-                                              part, BHi, H, n, d + 1, M, st),
-                                  "conv launch"))
-    return s;
-  if (krpe_status_t s = record(events, 3, st)) return s;
-  if (krpe_status_t s = hip_check(launch_gram(phik, vsc, x2, BHi, M, N, pairs, L.ksplit, st), "norm launch"))
-    return s;
-  if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, M, d, L.ksplit, st), "bound launch"))
-    return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, fix, fixmask, BHi, H, n, L.l2, d, M, st),
-                                  "combine launch"))
-    return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, fix, fixmask, fixpart, brange, BHi, H, n, N, d, M, st),
-                                  "fixup launch"))
-    return s;
-  return record(events, 4, st);
+  return run_forward(L, static_cast<char*>(ws), q, k, v, qkv_dtype == KRPE_BF16, b, W, z, nullptr,
+                     static_cast<int>(bh), H, n, d, m, M, kind, (flags & KRPE_NPRF) != 0,
+                     static_cast<hipStream_t>(stream), events);
 }
 
 krpe_status_t krpe_attention_fwd_ex(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
@@ -354,6 +386,113 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
                                  const float* W, float* z, int B, int H, int n, int d, int m, void* ws,
                                  size_t ws_bytes, void* stream) {
   return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, 0u, ws, ws_bytes, stream, nullptr);
+}
+
+size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned flags) {
+  if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
+  if (flags & ~static_cast<unsigned>(KRPE_NPRF)) return 0;
+  return bwd_layout(B, H, n, d, m).total;
+}
+
+krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, int qkv_dtype, const float* b,
+                                 const float* W, const float* dz, float* dq, float* dk, float* dv, float* db, int B,
+                                 int H, int n, int d, int m, unsigned flags, void* ws, size_t ws_bytes,
+                                 void* stream) {
+  g_last_error.clear();
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (flags & ~static_cast<unsigned>(KRPE_NPRF))
+    return fail(KRPE_ERR_UNSUPPORTED, "the backward pass takes only KRPE_NPRF (PRF features)");
+  if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
+  if (db) return fail(KRPE_ERR_UNSUPPORTED, "the gradient of b is not computed (pass db = NULL)");
+  const size_t bh = static_cast<size_t>(B) * H;
+  if (bh == 0) return KRPE_OK;
+  if (!q || !k || !v || !b || !W || !dz || !dq || !dk || !dv)
+    return fail(KRPE_ERR_NULL, "q, k, v, b, W, dz, dq, dk and dv must be non-NULL");
+  const void* ptrs[] = {q, k, v, b, W, dz, dq, dk, dv, ws};
+  for (const void* p : ptrs)
+    if (misaligned(p)) return fail(KRPE_ERR_ALIGN, "all pointers must be 16-byte aligned");
+  const BwdLayout L = bwd_layout(B, H, n, d, m);
+  if (!ws || ws_bytes < L.total)
+    return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
+  const size_t qkv_bytes = bh * n * d * dtype_size(qkv_dtype), g_bytes = bh * n * d * sizeof(float);
+  const Range ins[] = {{q, qkv_bytes},
+                       {k, qkv_bytes},
+                       {v, qkv_bytes},
+                       {b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)},
+                       {W, static_cast<size_t>(H) * m * d * sizeof(float)},
+                       {dz, g_bytes}};
+  const Range outs[] = {{dq, g_bytes}, {dk, g_bytes}, {dv, g_bytes}, {ws, ws_bytes}};
+  for (int o = 0; o < 4; ++o) {
+    for (const Range& r : ins)
+      if (overlaps(outs[o], r)) return fail(KRPE_ERR_ALIAS, "an output or the workspace overlaps an input");
+    for (int o2 = o + 1; o2 < 4; ++o2)
+      if (overlaps(outs[o], outs[o2])) return fail(KRPE_ERR_ALIAS, "outputs overlap each other or the workspace");
+  }
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const int BHi = static_cast<int>(bh);
+  const bool bf16 = qkv_dtype == KRPE_BF16, nprf = (flags & KRPE_NPRF) != 0;
+  const int N = 1 << L.f.l2, splits = conv_splits(L.f.l2);
+  float* zf = reinterpret_cast<float*>(w + L.zf);
+  float* den = reinterpret_cast<float*>(w + L.den);
+  float* brev = reinterpret_cast<float*>(w + L.brev);
+  float2* hsr = reinterpret_cast<float2*>(w + L.hsr);
+  float* gh = reinterpret_cast<float*>(w + L.gh);
+  float* vh = reinterpret_cast<float*>(w + L.vh);
+  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
+  float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* vmax = reinterpret_cast<float*>(w + L.vmax);
+  float* part = reinterpret_cast<float*>(w + L.part);
+  const float2* tw = reinterpret_cast<const float2*>(w + L.f.tw);
+  const float2* Hs = reinterpret_cast<const float2*>(w + L.f.hs);
+  const float* phiq = reinterpret_cast<const float*>(w + L.f.phiq);
+  const float* phik = reinterpret_cast<const float*>(w + L.f.phik);
+  const long long fstride = static_cast<long long>(m) * N, gstride = static_cast<long long>(d + 1) * N;
+
+  // forward: phi(q), phi(k), z and the denominators
+  if (krpe_status_t s = run_forward(L.f, w, q, k, v, bf16, b, W, zf, den, BHi, H, n, d, m, m, kFeatPrf, nprf, st,
+                                    nullptr))
+    return s;
+  if (krpe_status_t s = hip_check(launch_bwd_prep(bf16, dz, zf, den, v, gh, vh, BHi, n, N, d, st), "prep launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_reverse_bias(b, brev, n, H, st), "bias launch")) return s;
+  if (krpe_status_t s = hip_check(launch_spectrum(L.f.l2, brev, tw, hsr, nullptr, H, n, st), "spectrum launch"))
+    return s;
+  // dv = sum_l phi_l(k) o C^T (phi_l(q) o Gh_c)
+  if (krpe_status_t s = hip_check(launch_vprep(false, gh, 1, N, gstride, d + 1, false, BHi, n, N, vmax, colmax, vsc,
+                                               st),
+                                  "column launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_conv(L.f.l2, phik, phiq, fstride, vsc, colmax, hsr, tw, part, BHi, H, n,
+                                              d + 1, m, st),
+                                  "conv launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_bwd_dv(part, dv, BHi, n, d, d + 1, splits, st), "dv launch")) return s;
+  // dphi_l(q) = sum_c Gh_c o C (V'_c o phi_l(k)), then dq
+  if (krpe_status_t s = hip_check(launch_vprep(false, phik, 1, N, fstride, m, false, BHi, n, N, vmax, colmax, vsc,
+                                               st),
+                                  "column launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_conv(L.f.l2, gh, vh, gstride, vsc, colmax, Hs, tw, part, BHi, H, n, m, d + 1,
+                                              st),
+                                  "conv launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_feature_bwd(bf16, q, W, phiq, part, dq, BHi, H, n, N, d, m, splits, nprf,
+                                                     st),
+                                  "feature launch"))
+    return s;
+  // dphi_l(k) = sum_c V'_c o C^T (Gh_c o phi_l(q)), then dk
+  if (krpe_status_t s = hip_check(launch_vprep(false, phiq, 1, N, fstride, m, false, BHi, n, N, vmax, colmax, vsc,
+                                               st),
+                                  "column launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_conv(L.f.l2, vh, gh, gstride, vsc, colmax, hsr, tw, part, BHi, H, n, m,
+                                              d + 1, st),
+                                  "conv launch"))
+    return s;
+  return hip_check(launch_feature_bwd(bf16, k, W, phik, part, dk, BHi, H, n, N, d, m, splits, nprf, st),
+                   "feature launch");
 }
 
 krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, int H, int n, int d, int m,

@@ -778,7 +778,8 @@ __global__ __launch_bounds__(256) void k_bound_weights(const float* __restrict__
 // m + 1 weights.
 __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part, const float* __restrict__ phiq,
                                                  const float2* __restrict__ Wb, const float2* __restrict__ hnorm,
-                                                 float* __restrict__ z, unsigned* __restrict__ fix,
+                                                 float* __restrict__ z, float* __restrict__ den_out,
+                                                 unsigned* __restrict__ fix,
                                                  unsigned long long* __restrict__ fixmask, int BH, int H, int n, int N,
                                                  int log2N, int d, int m, int nsplit, int tiles_n) {
   extern __shared__ float dyn[];
@@ -829,6 +830,7 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
     const float den = tile[d * 65 + i];
     const float inv = 1.0f / den;
     rden[i] = inv;
+    if (den_out && pos < n) den_out[static_cast<size_t>(bh) * n + pos] = den;
     bool flag = false;
     if (pos < n) {
       const float L = static_cast<float>(2 << log2N);
@@ -927,7 +929,7 @@ __global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int
 template <typename TV>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_fixup(const float* __restrict__ phiq, const float* __restrict__ phik,
                                                const TV* __restrict__ vv,
-                                               const float* __restrict__ b, float* __restrict__ z,
+                                               const float* __restrict__ b, float* __restrict__ z, float* __restrict__ den_out,
                                                const unsigned* __restrict__ fix,
                                                const unsigned long long* __restrict__ fixmask,
                                                double* __restrict__ fixpart, const int2* __restrict__ brange,
@@ -1148,6 +1150,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
     __syncthreads();
     if (kparts == 1) {
+      if (den_out && tid < kFixRows && srows[tid] >= 0)
+        den_out[static_cast<size_t>(bh) * n + srows[tid]] = static_cast<float>(sden[tid]);
       if (pv_wave && my_part == 0) {
         const int col = my_tile * 32 + lr;
 #pragma unroll
@@ -1180,7 +1184,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 __global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restrict__ fix,
                                                        const unsigned long long* __restrict__ fixmask,
                                                        const double* __restrict__ fixpart, float* __restrict__ z,
-                                                       int BH, int n, int d, int slots) {
+                                                       float* __restrict__ den_out, int BH, int n, int d, int slots) {
   __shared__ unsigned long long smask[kFixMaxTiles];
   __shared__ unsigned spre[kFixMaxTiles + 1];
   __shared__ int srows[kFixRows];
@@ -1231,6 +1235,7 @@ __global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restric
         den += part[d];
       }
       z[(static_cast<size_t>(bh) * n + i) * d + c] = static_cast<float>(num / den);
+      if (den_out && c == 0) den_out[static_cast<size_t>(bh) * n + i] = static_cast<float>(den);
     }
   }
 }
@@ -1253,6 +1258,177 @@ __global__ void k_sum_splits(const float* __restrict__ part, float* __restrict__
   float s = 0.f;
   for (int sp = 0; sp < nsplit; ++sp) s += part[(bh * nsplit + sp) * per + r];
   y[e] = s;
+}
+
+// ============================================================= backward ==
+// Gradients of L = <G, z> through Eq. (10) with the feature map of Eq. (5), W
+// fixed.  With A = C o (Phi_q Phi_k^T) (C_ij = c_{j-i}), den = A 1 and
+// z = (A v) / den, the gradient of L with respect to [numerator, denominator]
+// of row i is Gh_i = [G_i / den_i, -(G_i . z_i) / den_i], and with
+// V' = [v, 1] (Eq. (11)'s channels):
+//   dv      = A^T Gh[:, :d]:   dv_j      = sum_l phi_l(k_j) (C^T (phi_l(q) o Gh_c))_j
+//   dPhi_q  = (Gh V'^T o C) Phi_k:  dphi_l(q_i) = sum_c Gh_ic (C (V'_c o phi_l(k)))_i
+//   dPhi_k  = (Gh V'^T o C)^T Phi_q:  dphi_l(k_j) = sum_c V'_jc (C^T (Gh_c o phi_l(q)))_j
+// Each is the product the forward convolution kernel computes,
+// sum_f f_f o C (a_f o col), with the roles of features and columns
+// assigned as written (C^T is the Toeplitz matrix of the reversed b).
+
+// Gh and V' feature-major ([bh][c][pos], c <= d, zero for n <= pos < N), from
+// G, the forward's z and den, and v.  Block: 64 positions of one (batch, head).
+template <typename TV>
+__global__ __launch_bounds__(256) void k_bwd_prep(const float* __restrict__ G, const float* __restrict__ z,
+                                                  const float* __restrict__ den, const TV* __restrict__ v,
+                                                  float* __restrict__ Gh, float* __restrict__ Vh, int n, int N,
+                                                  int d, int tiles) {
+  __shared__ float gs[64][kMaxD + 1];
+  __shared__ float rden[64], dden[64];
+  const int bh = blockIdx.x / tiles, i0 = (blockIdx.x % tiles) * 64;
+  const int tid = threadIdx.x;
+  const float* __restrict__ Gb = G + static_cast<size_t>(bh) * n * d;
+  const float* __restrict__ zb = z + static_cast<size_t>(bh) * n * d;
+  const TV* __restrict__ vb = v + static_cast<size_t>(bh) * n * d;
+  for (int e = tid; e < 64 * d; e += 256) {
+    const int r = e / d, c = e - r * d, pos = i0 + r;
+    gs[r][c] = pos < n ? Gb[static_cast<size_t>(pos) * d + c] : 0.f;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    const int pos = i0 + tid;
+    float dot = 0.f, inv = 0.f;
+    if (pos < n) {
+      inv = 1.0f / den[static_cast<size_t>(bh) * n + pos];
+      for (int c = 0; c < d; ++c) dot = fmaf(gs[tid][c], zb[static_cast<size_t>(pos) * d + c], dot);
+    }
+    rden[tid] = inv;
+    dden[tid] = -dot * inv;
+  }
+  __syncthreads();
+  for (int e = tid; e < (d + 1) * 64; e += 256) {
+    const int c = e >> 6, r = e & 63, pos = i0 + r;
+    if (pos >= N) continue;
+    float gv = 0.f, vv = 0.f;
+    if (pos < n) {
+      gv = c < d ? gs[r][c] * rden[r] : dden[r];
+      vv = c < d ? to_f32(vb[static_cast<size_t>(pos) * d + c]) : 1.f;
+    }
+    const size_t o = (static_cast<size_t>(bh) * (d + 1) + c) * N + pos;
+    Gh[o] = gv;
+    Vh[o] = vv;
+  }
+}
+
+// brev[h][s] = b[h][2n - 2 - s]: the bias of the transposed Toeplitz matrix.
+__global__ void k_reverse_bias(const float* __restrict__ b, float* __restrict__ brev, int n, int H) {
+  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const long long len = 2LL * n - 1;
+  if (e >= len * H) return;
+  const long long h = e / len, s = e - h * len;
+  brev[e] = b[h * len + (len - 1 - s)];
+}
+
+// dv[bh][i][c] = sum_s part[bh][s][c][i] for c < d: the class splits of the
+// convolution kernel's output summed and transposed.  Block: 64 positions.
+__global__ __launch_bounds__(256) void k_bwd_dv(const float* __restrict__ part, float* __restrict__ dv, int n,
+                                                int d, int cols, int nsplit, int tiles) {
+  __shared__ float t[64][kMaxD + 1];
+  const int bh = blockIdx.x / tiles, i0 = (blockIdx.x % tiles) * 64;
+  for (int e = threadIdx.x; e < d * 64; e += 256) {
+    const int c = e >> 6, r = e & 63, pos = i0 + r;
+    float acc = 0.f;
+    if (pos < n)
+      for (int sp = 0; sp < nsplit; ++sp) acc += part[((static_cast<size_t>(bh) * nsplit + sp) * cols + c) * n + pos];
+    t[r][c] = acc;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < d * 64; e += 256) {
+    const int r = e / d, c = e - r * d, pos = i0 + r;
+    if (pos < n) dv[(static_cast<size_t>(bh) * n + pos) * d + c] = t[r][c];
+  }
+}
+
+// Feature-map backward for Eq. (5): d phi_l / dx = phi_l (w_l - x), so
+//   dx = sum_l P_l w_l - x sum_l P_l,   P_l = dphi_l phi_l,
+// and with row normalisation (x = u / |u|, Algorithm 1) du = (dx - x (x . dx)) / |u|
+// (0 for a zero row).  dphi is summed over the nsplit class splits of the
+// convolution kernel's output part[bh][s][l][i]; phi is feature-major [bh][l][N].
+// Block: 64 positions of one (batch, head); wave w accumulates the columns
+// a = w, w + 4, ...; features staged through LDS 32 at a time.
+template <typename TX>
+__global__ __launch_bounds__(256) void k_feature_bwd(const TX* __restrict__ x, const float* __restrict__ W,
+                                                     const float* __restrict__ phi, const float* __restrict__ part,
+                                                     float* __restrict__ dx, int H, int n, int N, int d, int m,
+                                                     int nsplit, int nprf, int tiles) {
+  constexpr int KC = 32, ACC = kMaxD / 4;
+  __shared__ float Ps[KC][64];
+  __shared__ float Ws[KC][kMaxD];
+  __shared__ float red[4][64];
+  const int bh = blockIdx.x / tiles, i0 = (blockIdx.x % tiles) * 64, h = bh % H;
+  const int tid = threadIdx.x, r = tid & 63, w = tid >> 6;
+  const int i = i0 + r;
+  float acc[ACC];
+#pragma unroll
+  for (int j = 0; j < ACC; ++j) acc[j] = 0.f;
+  float rs = 0.f;
+  for (int l0 = 0; l0 < m; l0 += KC) {
+    __syncthreads();
+    for (int e = tid; e < KC * 64; e += 256) {
+      const int lq = e >> 6, rr = e & 63, l = l0 + lq, pos = i0 + rr;
+      float p = 0.f;
+      if (l < m && pos < n) {
+        float dp = 0.f;
+        for (int sp = 0; sp < nsplit; ++sp) dp += part[((static_cast<size_t>(bh) * nsplit + sp) * m + l) * n + pos];
+        p = dp * phi[(static_cast<size_t>(bh) * m + l) * N + pos];
+      }
+      Ps[lq][rr] = p;
+    }
+    for (int e = tid; e < KC * d; e += 256) {
+      const int lq = e / d, a = e - lq * d, l = l0 + lq;
+      Ws[lq][a] = l < m ? W[(static_cast<size_t>(h) * m + l) * d + a] : 0.f;
+    }
+    __syncthreads();
+    for (int lq = 0; lq < KC; ++lq) {
+      const float p = Ps[lq][r];
+      rs += p;
+#pragma unroll
+      for (int j = 0; j < ACC; ++j)
+        if (w + 4 * j < d) acc[j] = fmaf(p, Ws[lq][w + 4 * j], acc[j]);
+    }
+  }
+  // x of the row (normalised when asked) and its norm
+  float xa[ACC];
+  float sq = 0.f;
+#pragma unroll
+  for (int j = 0; j < ACC; ++j) {
+    const int a = w + 4 * j;
+    xa[j] = (a < d && i < n) ? to_f32(x[(static_cast<size_t>(bh) * n + i) * d + a]) : 0.f;
+    sq = fmaf(xa[j], xa[j], sq);
+  }
+  red[w][r] = sq;
+  __syncthreads();
+  sq = red[0][r] + red[1][r] + red[2][r] + red[3][r];
+  const float scale = nprf ? (sq > 0.f ? rsqrtf(sq) : 0.f) : 1.f;
+  float dot = 0.f;
+#pragma unroll
+  for (int j = 0; j < ACC; ++j) {
+    xa[j] *= scale;                   // the x phi was taken of
+    acc[j] = acc[j] - xa[j] * rs;     // dL/dx
+    dot = fmaf(xa[j], acc[j], dot);
+  }
+  if (nprf) {
+    __syncthreads();
+    red[w][r] = dot;
+    __syncthreads();
+    dot = red[0][r] + red[1][r] + red[2][r] + red[3][r];
+#pragma unroll
+    for (int j = 0; j < ACC; ++j) acc[j] = (acc[j] - xa[j] * dot) * scale;
+  }
+  if (i < n) {
+#pragma unroll
+    for (int j = 0; j < ACC; ++j) {
+      const int a = w + 4 * j;
+      if (a < d) dx[(static_cast<size_t>(bh) * n + i) * d + a] = acc[j];
+    }
+  }
 }
 
 // ============================================================ launchers ==
@@ -1444,13 +1620,14 @@ hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb
 }
 
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
-                          unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2, int d, int m,
-                          hipStream_t st) {
+                          float* den_out, unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2,
+                          int d, int m, hipStream_t st) {
   const int tiles_n = (n + 63) / 64;
   const size_t lds = (static_cast<size_t>((d + 1) * 65 + 1) & ~static_cast<size_t>(1)) * sizeof(float) +
                      static_cast<size_t>(m + 1) * sizeof(float2);
   hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), lds, st,
-                     part, phiq, Wb, hnorm, z, fix, fixmask, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2), tiles_n);
+                     part, phiq, Wb, hnorm, z, den_out, fix, fixmask, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2),
+                     tiles_n);
   return hipGetLastError();
 }
 
@@ -1460,7 +1637,7 @@ int fix_slots(int BH) {
 }
 
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b, float* z,
-                        const unsigned* fix, const unsigned long long* fixmask, double* fixpart, int2* brange, int BH,
+                        float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart, int2* brange, int BH,
                         int H, int n, int ld, int d, int m, hipStream_t st) {
   const int slots = fix_slots(BH);
   hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, n);
@@ -1482,13 +1659,56 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
   }
   if (bf16)
     hipLaunchKernelGGL(k_fixup<uint16_t>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
-                       static_cast<const uint16_t*>(v), b, z, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m, slots);
+                       static_cast<const uint16_t*>(v), b, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d,
+                       m, slots);
   else
     hipLaunchKernelGGL(k_fixup<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
-                       static_cast<const float*>(v), b, z, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m, slots);
+                       static_cast<const float*>(v), b, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m,
+                       slots);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, fixmask, fixpart, z,
-                     BH, n, d, slots);
+                     den_out, BH, n, d, slots);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_prep(bool bf16, const float* G, const float* z, const float* den, const void* v, float* Gh,
+                           float* Vh, int BH, int n, int N, int d, hipStream_t st) {
+  const int tiles = (N + 63) / 64;
+  const dim3 grid(static_cast<unsigned>(static_cast<long long>(BH) * tiles)), block(256);
+  if (bf16)
+    hipLaunchKernelGGL(k_bwd_prep<uint16_t>, grid, block, 0, st, G, z, den, static_cast<const uint16_t*>(v), Gh, Vh,
+                       n, N, d, tiles);
+  else
+    hipLaunchKernelGGL(k_bwd_prep<float>, grid, block, 0, st, G, z, den, static_cast<const float*>(v), Gh, Vh, n, N,
+                       d, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_reverse_bias(const float* b, float* brev, int n, int H, hipStream_t st) {
+  const long long total = (2LL * n - 1) * H;
+  hipLaunchKernelGGL(k_reverse_bias, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, st, b, brev, n,
+                     H);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_dv(const float* part, float* dv, int BH, int n, int d, int cols, int nsplit, hipStream_t st) {
+  const int tiles = (n + 63) / 64;
+  hipLaunchKernelGGL(k_bwd_dv, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles)), dim3(256), 0, st,
+                     part, dv, n, d, cols, nsplit, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_feature_bwd(bool bf16, const void* x, const float* W, const float* phi, const float* part,
+                              float* dx, int BH, int H, int n, int N, int d, int m, int nsplit, bool nprf,
+                              hipStream_t st) {
+  const int tiles = (n + 63) / 64;
+  const dim3 grid(static_cast<unsigned>(static_cast<long long>(BH) * tiles)), block(256);
+  if (bf16)
+    hipLaunchKernelGGL(k_feature_bwd<uint16_t>, grid, block, 0, st, static_cast<const uint16_t*>(x), W, phi, part,
+                       dx, H, n, N, d, m, nsplit, nprf ? 1 : 0, tiles);
+  else
+    hipLaunchKernelGGL(k_feature_bwd<float>, grid, block, 0, st, static_cast<const float*>(x), W, phi, part, dx, H,
+                       n, N, d, m, nsplit, nprf ? 1 : 0, tiles);
   return hipGetLastError();
 }
 

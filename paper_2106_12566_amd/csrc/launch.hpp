@@ -31,6 +31,24 @@ struct AttnLayout {
 };
 AttnLayout attn_layout(int B, int H, int n, int d, int m);
 
+// Workspace of krpe_attention_bwd: the forward's workspace first, then the
+// backward's buffers (cmax = max(M, d + 1) columns, M the features).
+struct BwdLayout {
+  AttnLayout f;
+  size_t zf;         // float  [BH][n][d]        z of the forward pass
+  size_t den;        // float  [BH][n]           its denominators
+  size_t brev;       // float  [H][2n-1]         reversed bias (transposed Toeplitz matrix)
+  size_t hsr;        // float2 [H][S][2N/S]      its spectrum
+  size_t gh;         // float  [BH][d+1][N]      [dL/dnumerator, dL/ddenominator], feature-major
+  size_t vh;         // float  [BH][d+1][N]      [v, 1], feature-major
+  size_t vsc;        // float2 [BH][cmax/2][N]   scaled column pairs of each product
+  size_t colmax;     // float  [BH][cmax]
+  size_t vmax;       // float  [BH][chunks][cmax]
+  size_t part;       // float  [BH][splits][cmax][n] class splits of each product
+  size_t total;
+};
+BwdLayout bwd_layout(int B, int H, int n, int d, int M);
+
 // Workspace of krpe_toeplitz_conv.
 struct ConvLayout {
   int l2;
@@ -66,16 +84,26 @@ hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, 
 hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb, int BH, int m, int d, int ksplit,
                                 hipStream_t st);
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
-                          unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2, int d, int m,
-                          hipStream_t st);
+                          float* den_out, unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2,
+                          int d, int m, hipStream_t st);
 // Work-group slots per head of the exact-row kernels, and their partial sums:
 // fixpart holds BH * fix_slots(BH) * 32 * (d + 1) doubles.
 int fix_slots(int BH);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
-                        float* z, const unsigned* fix, const unsigned long long* fixmask, double* fixpart,
+                        float* z, float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart,
                         int2* brange, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
+// Backward (see kernels.hip): Gh, V' feature-major from G, z, den, v; the
+// reversed bias; dv from the class splits of the convolution output; dx from
+// dphi (class splits) and phi.
+hipError_t launch_bwd_prep(bool bf16, const float* G, const float* z, const float* den, const void* v, float* Gh,
+                           float* Vh, int BH, int n, int N, int d, hipStream_t st);
+hipError_t launch_reverse_bias(const float* b, float* brev, int n, int H, hipStream_t st);
+hipError_t launch_bwd_dv(const float* part, float* dv, int BH, int n, int d, int cols, int nsplit, hipStream_t st);
+hipError_t launch_feature_bwd(bool bf16, const void* x, const float* W, const float* phi, const float* part,
+                              float* dx, int BH, int H, int n, int N, int d, int m, int nsplit, bool nprf,
+                              hipStream_t st);
 hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st);
 
 }  // namespace krpe

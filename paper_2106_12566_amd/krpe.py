@@ -17,8 +17,9 @@ import os
 
 import torch
 
-__all__ = ["KrpeError", "load", "lib_path", "feature_map", "toeplitz_conv", "attention_fwd",
-           "attention_fwd_workspace", "toeplitz_conv_workspace", "attention_fwd_fixed_rows", "DTYPES"]
+__all__ = ["KrpeError", "load", "lib_path", "feature_map", "toeplitz_conv", "attention_fwd", "attention_bwd",
+           "attention_fwd_workspace", "attention_bwd_workspace", "toeplitz_conv_workspace",
+           "attention_fwd_fixed_rows", "DTYPES"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libkrpe.so")
@@ -75,6 +76,11 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_attention_fwd_profiled.restype = i
     lib.krpe_attention_fwd_profiled.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, ctypes.c_uint, vp, sz,
                                                 vp, ctypes.POINTER(ctypes.c_void_p)]
+    lib.krpe_attention_bwd_workspace.restype = sz
+    lib.krpe_attention_bwd_workspace.argtypes = [i, i, i, i, i, ctypes.c_uint]
+    lib.krpe_attention_bwd.restype = i
+    lib.krpe_attention_bwd.argtypes = [vp, vp, vp, i, fp, fp, fp, fp, fp, fp, fp, i, i, i, i, i, ctypes.c_uint, vp,
+                                       sz, vp]
     lib.krpe_attention_fwd_stats.restype = i
     lib.krpe_attention_fwd_stats.argtypes = [vp, sz, i, i, i, i, i, ctypes.POINTER(ctypes.c_uint), vp]
     if path is None:
@@ -234,3 +240,43 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
         st = lib.krpe_attention_fwd_profiled(*args, arr)
     _check(st, "krpe_attention_fwd")
     return out
+
+
+def attention_bwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool = False) -> int:
+    return int(load().krpe_attention_bwd_workspace(B, H, n, d, m, NPRF if nprf else 0))
+
+
+def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
+                  dz: torch.Tensor, workspace: torch.Tensor | None = None,
+                  nprf: bool = False) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Gradients (dq, dk, dv) [B,H,n,d] fp32 of sum(dz * z), z = attention_fwd(q, k, v, b, W, nprf=nprf)
+    with PRF features and W fixed (the C header states the formulas)."""
+    lib = load()
+    q, k, v = _gpu(q, "q"), _gpu(k, "k"), _gpu(v, "v")
+    b, W, dz = _gpu(b, "b"), _gpu(W, "W"), _gpu(dz, "dz")
+    if q.dim() != 4:
+        raise KrpeError("q must be [B,H,n,d]")
+    B, H, n, d = q.shape
+    if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
+        raise KrpeError("q, k, v must share shape and dtype")
+    if dz.shape != q.shape or dz.dtype != torch.float32:
+        raise KrpeError("dz must be float32 [B,H,n,d]")
+    if W.dim() != 3 or W.shape[0] != H or W.shape[2] != d or W.dtype != torch.float32:
+        raise KrpeError("W must be float32 [H, m, d]")
+    if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
+        raise KrpeError("b must be float32 [H, 2n-1]")
+    m = W.shape[1]
+    flags = NPRF if nprf else 0
+    wsb = int(lib.krpe_attention_bwd_workspace(B, H, n, d, m, flags))
+    if workspace is None:
+        workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)
+    elif workspace.numel() < wsb:
+        raise KrpeError(f"workspace must hold at least {wsb} bytes")
+    dq = torch.empty((B, H, n, d), dtype=torch.float32, device=q.device)
+    dk = torch.empty_like(dq)
+    dv = torch.empty_like(dq)
+    st = lib.krpe_attention_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q, "q"), _ptr(b), _ptr(W), _ptr(dz), _ptr(dq),
+                                _ptr(dk), _ptr(dv), None, B, H, n, d, m, flags, workspace.data_ptr(),
+                                workspace.numel(), _stream(q.device))
+    _check(st, "krpe_attention_bwd")
+    return dq, dk, dv

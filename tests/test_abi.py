@@ -40,7 +40,7 @@ def test_header_declares_the_boundary():
                      "krpe_toeplitz_conv_workspace", "krpe_attention_fwd_workspace",
                      "krpe_attention_fwd_profiled", "krpe_status_str", "krpe_last_error",
                      "krpe_abi_version", "krpe_feature_map_ex", "krpe_attention_fwd_ex",
-                     "krpe_attention_fwd_workspace_ex"):
+                     "krpe_attention_fwd_workspace_ex", "krpe_attention_bwd", "krpe_attention_bwd_workspace"):
         assert required in names
 
 
@@ -50,7 +50,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.krpe_abi_version() == 4
+    assert lib.krpe_abi_version() == 5
     for s in range(9):
         assert lib.krpe_status_str(s)
     assert lib.krpe_status_str(99) == b"unknown status"
@@ -164,3 +164,23 @@ def test_binding_refuses_cpu_tensors(lib):
         krpe.feature_map(x, W)
     with pytest.raises(krpe.KrpeError):
         krpe.attention_fwd(x, x, x, torch.zeros(1, 15), W)
+
+
+def test_backward_validation(lib):
+    """Argument checks of the backward entry point (all fail before any GPU call)."""
+    wsb = lib.krpe_attention_bwd_workspace(1, 1, 8, 4, 4, 0)
+    assert wsb > lib.krpe_attention_fwd_workspace(1, 1, 8, 4, 4)
+    assert lib.krpe_attention_bwd_workspace(1, 1, 8, 4, 4, 2) == 0      # TRF has no backward here
+    assert lib.krpe_attention_bwd_workspace(1, 1, 8, 4, 4, 1) == wsb
+    D1, D2, D3 = Z + 4096, Z + 8192, Z + 12288
+    call = lambda flags=0, db=None, dq=D1, dz=Q, w=WSP, wb=wsb, n=8: lib.krpe_attention_bwd(
+        Q, K, V, 0, BB, W, dz, dq, D2, D3, db, 1, 1, n, 4, 4, flags, w, wb, None)
+    assert call(flags=2) == UNSUP
+    assert call(flags=8) == UNSUP
+    assert call(db=Z) == UNSUP
+    assert call(dz=None) == NULL
+    assert call(n=0) == SHAPE
+    assert call(wb=8) == WS
+    assert call(dq=Q) == ALIAS
+    assert call(dq=D2) == ALIAS
+    assert call(dq=D1 + 8) == ALIGN
