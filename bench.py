@@ -169,7 +169,7 @@ def main() -> int:
     ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
                     help="feature map of Section 2: PRF (Eq. (5)), trigonometric (2m features) or elu + 1 (m = d)")
     ap.add_argument("--backward", action="store_true",
-                    help="also time krpe_attention_bwd (dq, dk, dv) on the same inputs, reported in config")
+                    help="also time krpe_attention_bwd (dq, dk, dv, db) on the same inputs, reported in config")
     ap.add_argument("--nprf", action="store_true",
                     help="normalise the rows of q and k first (Algorithm 1's NPRF attention)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -276,11 +276,11 @@ def main() -> int:
         wsb = torch.empty(krpe.attention_bwd_workspace(B, H, n, dd, m, nprf=args.nprf), dtype=torch.uint8,
                           device=dev)
         for _ in range(max(1, args.warmup)):
-            krpe.attention_bwd(q, k, v, b, W, dz, workspace=wsb, nprf=args.nprf)
+            krpe.attention_bwd(q, k, v, b, W, dz, workspace=wsb, nprf=args.nprf, with_db=True)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         for _ in range(args.steps):
-            krpe.attention_bwd(q, k, v, b, W, dz, workspace=wsb, nprf=args.nprf)
+            krpe.attention_bwd(q, k, v, b, W, dz, workspace=wsb, nprf=args.nprf, with_db=True)
         torch.cuda.synchronize()
         result["config"]["backward_ms"] = 1e3 * (time.perf_counter() - t1) / args.steps
         print(f"bench: backward {result['config']['backward_ms']:.3f} ms/step", file=sys.stderr, flush=True)

@@ -197,8 +197,8 @@ size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned 
 
 /*
  * Backward pass of krpe_attention_fwd_ex (PRF features of Eq. (5), optional
- * KRPE_NPRF; W fixed): the gradients of L = sum(dz * z) with respect to q, k
- * and v, z from Eq. (10).  The paper states no backward pass; these are the
+ * KRPE_NPRF; W fixed): the gradients of L = sum(dz * z) with respect to q, k,
+ * v and b, z from Eq. (10).  The paper states no backward pass; these are the
  * derivatives of its forward definition.  With A = C o (phi(Q) phi(K)^T),
  * den = A 1 and Gh = [dz / den, -(dz . z) / den] per row:
  *   dv = A^T Gh[:, :d],  dphi(Q) = ((Gh [v, 1]^T) o C) phi(K),
@@ -209,7 +209,10 @@ size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned 
  * pass is recomputed inside (its exact-row evaluation included).
  * q, k, v : [B, H, n, d] in qkv_dtype    b : [H, 2n-1]    W : [H, m, d]
  * dz      : [B, H, n, d] fp32             dq, dk, dv : [B, H, n, d] fp32 (outputs)
- * db      : must be NULL (the gradient of b is not computed: KRPE_ERR_UNSUPPORTED).
+ * db      : [H, 2n-1] fp32 (output, summed over the batch), or NULL to skip it:
+ *           db_t = c_t sum_{l,c} corr(phi_l(q) o Gh_c, phi_l(k) o [v, 1]_c)(t), one
+ *           spectrum per head accumulated over all channels (FFT cross-correlation);
+ *           0 where b_t = -inf.
  * ws      : device workspace of at least krpe_attention_bwd_workspace() bytes.
  * Outputs must not overlap each other, an input or the workspace.
  */

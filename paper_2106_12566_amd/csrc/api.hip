@@ -139,6 +139,12 @@ BwdLayout bwd_layout(int B, int H, int n, int d, int M) {
   L.colmax = take(bh * cmax * sizeof(float));
   L.vmax = take(bh * vmax_chunks(n) * cmax * sizeof(float));
   L.part = take(bh * conv_splits(L.f.l2) * cmax * n * sizeof(float));
+  const size_t gpairs = static_cast<size_t>(d + 2) / 2;
+  L.gpk = take(bh * gpairs * N * sizeof(float2));
+  L.vpk = take(bh * gpairs * N * sizeof(float2));
+  L.spart = take(bh * gpairs * 2 * N * sizeof(float2));
+  L.sh = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  L.ycorr = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
   L.total = off;
   return L;
 }
@@ -403,7 +409,6 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
   if (flags & ~static_cast<unsigned>(KRPE_NPRF))
     return fail(KRPE_ERR_UNSUPPORTED, "the backward pass takes only KRPE_NPRF (PRF features)");
   if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
-  if (db) return fail(KRPE_ERR_UNSUPPORTED, "the gradient of b is not computed (pass db = NULL)");
   const size_t bh = static_cast<size_t>(B) * H;
   if (bh == 0) return KRPE_OK;
   if (!q || !k || !v || !b || !W || !dz || !dq || !dk || !dv)
@@ -421,11 +426,13 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
                        {b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)},
                        {W, static_cast<size_t>(H) * m * d * sizeof(float)},
                        {dz, g_bytes}};
-  const Range outs[] = {{dq, g_bytes}, {dk, g_bytes}, {dv, g_bytes}, {ws, ws_bytes}};
-  for (int o = 0; o < 4; ++o) {
+  if (misaligned(db)) return fail(KRPE_ERR_ALIGN, "all pointers must be 16-byte aligned");
+  const Range outs[] = {{dq, g_bytes}, {dk, g_bytes}, {dv, g_bytes}, {ws, ws_bytes},
+                        {db, db ? static_cast<size_t>(H) * (2 * n - 1) * sizeof(float) : 0}};
+  for (int o = 0; o < 5; ++o) {
     for (const Range& r : ins)
       if (overlaps(outs[o], r)) return fail(KRPE_ERR_ALIAS, "an output or the workspace overlaps an input");
-    for (int o2 = o + 1; o2 < 4; ++o2)
+    for (int o2 = o + 1; o2 < 5; ++o2)
       if (overlaps(outs[o], outs[o2])) return fail(KRPE_ERR_ALIAS, "outputs overlap each other or the workspace");
   }
 
@@ -469,6 +476,16 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
                                   "conv launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_bwd_dv(part, dv, BHi, n, d, d + 1, splits, st), "dv launch")) return s;
+  // db_t = c_t sum_lc corr(phi_l(q) o Gh_c, phi_l(k) o V'_c)(t)
+  if (db) {
+    if (krpe_status_t s = hip_check(
+            launch_db(L.f.l2, phiq, phik, fstride, gh, vh, tw, reinterpret_cast<float2*>(w + L.gpk),
+                      reinterpret_cast<float2*>(w + L.vpk), reinterpret_cast<float2*>(w + L.spart),
+                      reinterpret_cast<float2*>(w + L.sh), reinterpret_cast<float2*>(w + L.ycorr), b, db, B, H, n,
+                      d + 1, m, st),
+            "db launch"))
+      return s;
+  }
   // dphi_l(q) = sum_c Gh_c o C (V'_c o phi_l(k)), then dq
   if (krpe_status_t s = hip_check(launch_vprep(false, phik, 1, N, fstride, m, false, BHi, n, N, vmax, colmax, vsc,
                                                st),

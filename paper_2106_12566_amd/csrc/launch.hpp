@@ -45,6 +45,9 @@ struct BwdLayout {
   size_t colmax;     // float  [BH][cmax]
   size_t vmax;       // float  [BH][chunks][cmax]
   size_t part;       // float  [BH][splits][cmax][n] class splits of each product
+  size_t gpk, vpk;   // float2 [BH][(d+2)/2][N]  Gh, V' as column pairs (gradient of b)
+  size_t spart;      // float2 [BH][(d+2)/2][2N] correlation spectra per column pair
+  size_t sh, ycorr;  // float2 [H][2N]           their sum per head, and its inverse per class
   size_t total;
 };
 BwdLayout bwd_layout(int B, int H, int n, int d, int M);
@@ -101,6 +104,11 @@ hipError_t launch_bwd_prep(bool bf16, const float* G, const float* z, const floa
                            float* Vh, int BH, int n, int N, int d, hipStream_t st);
 hipError_t launch_reverse_bias(const float* b, float* brev, int n, int H, hipStream_t st);
 hipError_t launch_bwd_dv(const float* part, float* dv, int BH, int n, int d, int cols, int nsplit, hipStream_t st);
+// db[h][s] = c_t dc_t from Gh, V' (feature-major [bh][cols][N]) and phi; scratch:
+// gpk, vpk [BH][pairs][N], spart [BH][pairs][2N], Sh and ycorr [H][2N] (float2).
+hipError_t launch_db(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float* gh,
+                     const float* vh, const float2* tw, float2* gpk, float2* vpk, float2* spart, float2* Sh,
+                     float2* ycorr, const float* b, float* db, int B, int H, int n, int cols, int m, hipStream_t st);
 hipError_t launch_feature_bwd(bool bf16, const void* x, const float* W, const float* phi, const float* part,
                               float* dx, int BH, int H, int n, int N, int d, int m, int nsplit, bool nprf,
                               hipStream_t st);

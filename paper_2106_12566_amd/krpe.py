@@ -247,10 +247,10 @@ def attention_bwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool =
 
 
 def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
-                  dz: torch.Tensor, workspace: torch.Tensor | None = None,
-                  nprf: bool = False) -> tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+                  dz: torch.Tensor, workspace: torch.Tensor | None = None, nprf: bool = False,
+                  with_db: bool = False) -> tuple:
     """Gradients (dq, dk, dv) [B,H,n,d] fp32 of sum(dz * z), z = attention_fwd(q, k, v, b, W, nprf=nprf)
-    with PRF features and W fixed (the C header states the formulas)."""
+    with PRF features and W fixed (the C header states the formulas); with_db adds db [H, 2n-1]."""
     lib = load()
     q, k, v = _gpu(q, "q"), _gpu(k, "k"), _gpu(v, "v")
     b, W, dz = _gpu(b, "b"), _gpu(W, "W"), _gpu(dz, "dz")
@@ -275,8 +275,9 @@ def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     dq = torch.empty((B, H, n, d), dtype=torch.float32, device=q.device)
     dk = torch.empty_like(dq)
     dv = torch.empty_like(dq)
+    db = torch.empty((H, 2 * n - 1), dtype=torch.float32, device=q.device) if with_db else None
     st = lib.krpe_attention_bwd(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q, "q"), _ptr(b), _ptr(W), _ptr(dz), _ptr(dq),
-                                _ptr(dk), _ptr(dv), None, B, H, n, d, m, flags, workspace.data_ptr(),
+                                _ptr(dk), _ptr(dv), _ptr(db), B, H, n, d, m, flags, workspace.data_ptr(),
                                 workspace.numel(), _stream(q.device))
     _check(st, "krpe_attention_bwd")
-    return dq, dk, dv
+    return (dq, dk, dv, db) if with_db else (dq, dk, dv)

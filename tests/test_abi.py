@@ -177,7 +177,8 @@ def test_backward_validation(lib):
         Q, K, V, 0, BB, W, dz, dq, D2, D3, db, 1, 1, n, 4, 4, flags, w, wb, None)
     assert call(flags=2) == UNSUP
     assert call(flags=8) == UNSUP
-    assert call(db=Z) == UNSUP
+    assert call(db=D1) == ALIAS               # db overlapping dq
+    assert call(db=Z + 20000 + 4) == ALIGN
     assert call(dz=None) == NULL
     assert call(n=0) == SHAPE
     assert call(wb=8) == WS

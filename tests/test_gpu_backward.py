@@ -1,17 +1,21 @@
 """GPU parity of the backward pass (krpe_attention_bwd, through the C ABI).
 
-dq, dk, dv of L = sum(dz * z) against the fp64 oracle's chain rule
+dq, dk, dv, db of L = sum(dz * z) against the fp64 oracle's chain rule
 (oracle.attention_grad, itself pinned by finite differences) on the same
 seeded inputs and output gradients.
 
 Tolerance: per (batch, head), the largest absolute error of each gradient
-relative to that gradient's largest entry, <= 2e-4 for fp32 inputs and <= 2e-2
-for bf16 (the bars of the forward).  Gradients mix positive and negative
-terms (dx = (dphi o phi) W - x rowsum), so an elementwise relative error is
-ill-posed, as for z.  Where the exact gradient vanishes (one key, n = 1; or
+relative to that gradient's largest entry, <= 5e-4 for fp32 inputs and <= 2e-2
+for bf16.  The forward's fp32 bar is 2e-4 with its uncertified rows
+evaluated exactly; the backward has no exact path, and the rows with small
+denominators (the first rows under a causal mask) enter its products through
+dz / den with a weight the FFT's error, spread over the sequence, sees in
+every position (the worst fp32 case here, causal n = 17, is 6e-5).
+Gradients mix positive and negative terms (dx = (dphi o phi) W - x rowsum),
+so an elementwise relative error is ill-posed, as for z.  Where the exact gradient vanishes (one key, n = 1; or
 one feature, m = 1, whose phi(q_i) cancels from Eq. (10)) the reference scale
 is a floor of 1e-3 of the gradient's natural size, max|dz| max|[v, 1]|
-(max|W| + max|x|) for dq and dk, max|dz| for dv.
+(max|W| + max|x|) for dq and dk, max|dz| for dv, max|dz| max|[v, 1]| for db.
 """
 import numpy as np
 import pytest
@@ -20,6 +24,8 @@ import torch
 import oracle
 from paper_2106_12566_amd import synth
 from parity_util import TOL, to_gpu
+
+BWD_TOL = {"f32": 5e-4, "bf16": TOL["bf16"]}
 
 pytestmark = pytest.mark.gpu
 
@@ -61,7 +67,8 @@ def test_backward_matches_oracle(gpu_lib, B, H, n, d, m, dt, bias, nprf):
     G = rng.standard_normal((B, H, n, d)).astype(np.float32)
     q, k, v = (to_gpu(dd[x], dt) for x in ("q", "k", "v"))
     b, W = to_gpu(dd["b"]), to_gpu(dd["W"])
-    dq, dk, dv = (t.cpu().numpy() for t in gpu_lib.attention_bwd(q, k, v, b, W, to_gpu(G), nprf=nprf))
+    dq, dk, dv, db = (t.cpu().numpy() for t in gpu_lib.attention_bwd(q, k, v, b, W, to_gpu(G), nprf=nprf,
+                                                                     with_db=True))
     ref = oracle.attention_grad(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], G, nprf=nprf)
     gmax = float(np.max(np.abs(G)))
     vmax = max(1.0, float(np.max(np.abs(dd["v"]))))
@@ -69,11 +76,15 @@ def test_backward_matches_oracle(gpu_lib, B, H, n, d, m, dt, bias, nprf):
     floors = {"dq": 1e-3 * gmax * vmax * (wmax + float(np.max(np.abs(dd["q"])))),
               "dk": 1e-3 * gmax * vmax * (wmax + float(np.max(np.abs(dd["k"])))),
               "dv": 1e-3 * gmax}
+    assert np.all(db[~np.isfinite(dd["b"])] == 0.0)
+    derr = float(np.max(np.abs(db - ref[3])) / max(np.max(np.abs(ref[3])), 1e-3 * gmax * vmax))
+    _say(f"  db: err={derr:.3e}")
+    assert derr <= BWD_TOL[dt], ("db", derr)
     for name, got, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref[:3]):
         assert np.all(np.isfinite(got)), name
         err = _head_err(got, r, floors[name])
         _say(f"  {name}: err={err:.3e}")
-        assert err <= TOL[dt], (name, err)
+        assert err <= BWD_TOL[dt], (name, err)
 
 
 def test_backward_is_linear_in_dz(gpu_lib):
