@@ -30,6 +30,17 @@ PEAK_FP32_VECTOR_TFLOPS = 157.3   # MI355X published fp32 vector peak
 PEAK_HBM_GBS = 8000.0
 
 
+def direct_flops(B: int, H: int, n: int, d: int, m: int, b: np.ndarray) -> float:
+    """Algorithmic flops of the direct route: for every (query, key) pair with a finite
+    b_{j-i}, the feature dot product (2m), the weight c phi(q) phi(k) (1) and its product with
+    [v, 1] (2 (d + 1))."""
+    pairs = 0
+    for h in range(b.shape[0]):
+        t = np.arange(-(n - 1), n)
+        pairs += int(np.sum((n - np.abs(t))[np.isfinite(b[h])]))
+    return B * pairs * (2.0 * m + 1.0 + 2.0 * (d + 1))
+
+
 def conv_stage_flops(B: int, H: int, n: int, d: int, m: int) -> float:
     """Algorithmic flops of the FFT convolution + contraction stage.
 
@@ -168,6 +179,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
                     help="feature map of Section 2: PRF (Eq. (5)), trigonometric (2m features) or elu + 1 (m = d)")
+    ap.add_argument("--route", choices=["auto", "fft", "direct"], default="auto",
+                    help="forward route: FFT (Sec. 3.2), direct quadratic evaluation, or by length")
     ap.add_argument("--backward", action="store_true",
                     help="also time krpe_attention_bwd (dq, dk, dv, db) on the same inputs, reported in config")
     ap.add_argument("--nprf", action="store_true",
@@ -210,8 +223,9 @@ def main() -> int:
     if fm == "elu":
         m = dd                       # elu + 1 has one feature per coordinate
     M = 2 * m if fm == "trf" else m  # features per position
-    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, nprf=args.nprf, features=fm), dtype=torch.uint8,
-                     device=dev)
+    rt = args.route
+    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt),
+                     dtype=torch.uint8, device=dev)
     print(f"bench: workload {wl.name} B={B} H={H} n={n} d={dd} m={m} {wl.qkv_dtype}", file=sys.stderr,
           flush=True)
 
@@ -219,12 +233,13 @@ def main() -> int:
     events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(args.steps)]
 
     for _ in range(args.warmup):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf, features=fm)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf, features=fm, route=rt)
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
     for s in range(args.steps):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], nprf=args.nprf, features=fm)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], nprf=args.nprf, features=fm,
+                           route=rt)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
@@ -238,11 +253,19 @@ def main() -> int:
     tokens = B * n
     value = tokens / (ms_per_step * 1e-3)
 
-    flops = conv_stage_flops(B, H, n, dd, M)
-    conv_ms = stages["conv_contract"]
-    achieved_tflops = flops / (conv_ms * 1e-3) / 1e12
+    route_used = krpe.attention_fwd_route(n, dd, m, nprf=args.nprf, features=fm, route=rt)
     s_in = 2 if wl.qkv_dtype == "bf16" else 4
-    conv_gbs = conv_stage_bytes(B, H, n, dd, M, s_in) / (conv_ms * 1e-3) / 1e9
+    if route_used == "fft":
+        flops = conv_stage_flops(B, H, n, dd, M)
+        conv_ms = stages["conv_contract"]
+        conv_gbs = conv_stage_bytes(B, H, n, dd, M, s_in) / (conv_ms * 1e-3) / 1e9
+        roof = {"bound": "alu", "kernel": "k_conv_contract"}
+    else:
+        flops = direct_flops(B, H, n, dd, M, d["b"])
+        conv_ms = stages["combine"]       # the exact-row kernel evaluates every row
+        conv_gbs = None
+        roof = {"bound": "mfma", "kernel": "k_fixup"}
+    achieved_tflops = flops / (conv_ms * 1e-3) / 1e12
     print(f"bench: {ms_per_step:.3f} ms/step, stages {stages}", file=sys.stderr, flush=True)
 
     result = {
@@ -261,13 +284,15 @@ def main() -> int:
         "config": {"workload": wl.name, "B": B, "H": H, "n": n, "d": dd, "m": m,
                    "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
                    "causal": wl.causal, "nprf": args.nprf, "feature_map": fm, "features_per_position": M,
+                   "route": route_used,
                    "ms_per_layer": ms_per_step, "stages_ms": stages,
                    "conv_stage_hbm_gbs": conv_gbs,
                    "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)},
-        "roofline": {"bound": "alu", "kernel": "k_conv_contract", "achieved": achieved_tflops,
+        "roofline": {**roof, "achieved": achieved_tflops,
                      "peak": PEAK_FP32_VECTOR_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_FP32_VECTOR_TFLOPS,
-                     "traffic": measured_traffic("k_conv_contract", wl.name) if fm == "prf" else None},
+                     "traffic": (measured_traffic("k_conv_contract", wl.name)
+                                 if fm == "prf" and route_used == "fft" else None)},
     }
     if args.backward:
         if fm != "prf":

@@ -97,6 +97,17 @@ typedef enum {
  */
 #define KRPE_FEAT_TRF 2u
 #define KRPE_FEAT_ELU 4u
+/*
+ * Route of the forward pass (at most one; neither: chosen by sequence length
+ * from the measured crossover).  KRPE_ROUTE_FFT: the O(n log n) FFT
+ * convolution of Section 3.2 (rows it cannot certify evaluated directly).
+ * KRPE_ROUTE_DIRECT: every row evaluated directly from Eq. (10) as
+ * (phi(Q) phi(K)^T o C) [v, 1] on fp32 MFMA tiles with fp64 totals, O(n^2);
+ * faster than the FFT route for short sequences.  Same results to the
+ * tolerance of the FFT route (the direct route is the more accurate).
+ */
+#define KRPE_ROUTE_DIRECT 8u
+#define KRPE_ROUTE_FFT 16u
 
 /* Version of this ABI (incremented on any incompatible change). */
 int krpe_abi_version(void);
@@ -149,6 +160,14 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
 size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m);
 /* The same for krpe_attention_fwd_ex with option bits (TRF needs more). */
 size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsigned flags);
+
+/*
+ * The route krpe_attention_fwd_ex takes for these sizes and option bits:
+ * KRPE_ROUTE_DIRECT or KRPE_ROUTE_FFT (0 if the sizes or bits are invalid).
+ * Without a route bit it follows a cost model of both routes measured on
+ * MI355X; it counts all n^2 query/key pairs (b is not read on the host).
+ */
+int krpe_attention_fwd_route(int n, int d, int m, unsigned flags);
 
 /*
  * Kernelized attention with RPE, Section 3.2, Eq. (10), with phi from Eq. (5)

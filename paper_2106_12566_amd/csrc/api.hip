@@ -62,7 +62,33 @@ krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm) {
   return KRPE_OK;
 }
 
-constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU;
+constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT;
+
+// Whether the direct route is the faster one for one head of length n with M
+// features and d value columns.  Cost model fitted to MI355X timings of both
+// routes (B H = 96, d = 64, M = 64 and 128, n = 128 .. 4096): the direct
+// route costs about 4.2e-14 s per (query, key) pair and unit of M + d + 1,
+// the FFT route about 2.0e-13 s per channel pair and point of a length-2N
+// transform times log2(2N), plus a fixed 2e-5 s per head-batch of launches.
+// All n^2 pairs are counted: the host does not read b, so a causal mask
+// (half the pairs) is not seen; KRPE_ROUTE_DIRECT forces the direct route.
+bool direct_is_faster(int n, int M, int d) {
+  int l2 = 0;
+  while ((1 << l2) < n) ++l2;
+  const double L = 2.0 * static_cast<double>(1 << l2);
+  const double direct = 4.2e-14 * static_cast<double>(n) * n * (M + d + 1);
+  const double fft = 2.0e-13 * M * ((d + 2) / 2) * L * (l2 + 1);
+  return direct < fft;
+}
+
+// Route of the forward pass: the FFT convolution (Sec. 3.2) or the direct
+// quadratic evaluation of Eq. (10) on MFMA, forced by an option bit or chosen
+// by the measured crossover (the direct route is faster for short sequences).
+bool use_direct(unsigned flags, int n, int M, int d) {
+  if (flags & KRPE_ROUTE_DIRECT) return true;
+  if (flags & KRPE_ROUTE_FFT) return false;
+  return direct_is_faster(n, M, d);
+}
 
 // Feature map selected by the option bits, and its number of features M
 // (the row count of phi): m for PRF, 2m for TRF, d for elu + 1 (which needs
@@ -71,6 +97,8 @@ krpe_status_t feature_kind(unsigned flags, int d, int m, int* kind, int* M) {
   if (flags & ~kKnownFlags) return fail(KRPE_ERR_UNSUPPORTED, "unknown flag bits");
   if ((flags & KRPE_FEAT_TRF) && (flags & KRPE_FEAT_ELU))
     return fail(KRPE_ERR_UNSUPPORTED, "KRPE_FEAT_TRF and KRPE_FEAT_ELU are exclusive");
+  if ((flags & KRPE_ROUTE_DIRECT) && (flags & KRPE_ROUTE_FFT))
+    return fail(KRPE_ERR_UNSUPPORTED, "KRPE_ROUTE_DIRECT and KRPE_ROUTE_FFT are exclusive");
   *kind = (flags & KRPE_FEAT_TRF) ? kFeatTrf : (flags & KRPE_FEAT_ELU) ? kFeatElu : kFeatPrf;
   *M = *kind == kFeatTrf ? 2 * m : (*kind == kFeatElu ? d : m);
   if (*kind == kFeatElu && m != d) return fail(KRPE_ERR_SHAPE, "KRPE_FEAT_ELU needs m == d");
@@ -176,7 +204,7 @@ ConvLayout conv_layout(int B, int H, int C, int n) {
 // row denominators into den_out when not NULL (the backward pass needs them).
 krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const void* k, const void* v, bool bf16,
                           const float* b, const float* W, float* z, float* den_out, int BHi, int H, int n, int d,
-                          int m, int M, int kind, bool nprf, hipStream_t st, void* const* events) {
+                          int m, int M, int kind, bool nprf, bool direct, hipStream_t st, void* const* events) {
   float2* tw = reinterpret_cast<float2*>(w + L.tw);
   float2* Hs = reinterpret_cast<float2*>(w + L.hs);
   float2* hnorm = reinterpret_cast<float2*>(w + L.hnorm);
@@ -195,6 +223,33 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
   const int N = 1 << L.l2;
   const int pairs = (d + 2) / 2;
 
+  if (direct) {
+    // phi(q), phi(k), then every row through the exact-row kernel
+    for (int e = 0; e < 2; ++e)
+      if (krpe_status_t s = record(events, e, st)) return s;
+    if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m,
+                                                       nullptr, nprf, kind, st),
+                                    "feature map launch"))
+      return s;
+    for (int e = 2; e < 4; ++e)
+      if (krpe_status_t s = record(events, e, st)) return s;
+    if (krpe_status_t s = hip_check(launch_mark_all(fix, fixmask, BHi, n, st), "queue launch")) return s;
+    // bf16 values widened once into the (here unused) column-pair buffer,
+    // which holds at least BH n d floats
+    const void* vv = v;
+    if (bf16) {
+      float* vw = reinterpret_cast<float*>(vsc);
+      if (krpe_status_t s = hip_check(launch_widen_bf16(v, vw, static_cast<long long>(BHi) * n * d, st),
+                                      "widen launch"))
+        return s;
+      vv = vw;
+    }
+    if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixpart, brange,
+                                                 BHi, H, n, N, d, M, st),
+                                    "direct launch"))
+      return s;
+    return record(events, 4, st);
+  }
   if (krpe_status_t s = record(events, 0, st)) return s;
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
   if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, hnorm, H, n, st), "spectrum launch")) return s;
@@ -377,7 +432,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
     if (overlaps(rz, r) || overlaps(rws, r)) return fail(KRPE_ERR_ALIAS, "z or the workspace overlaps an input");
 
   return run_forward(L, static_cast<char*>(ws), q, k, v, qkv_dtype == KRPE_BF16, b, W, z, nullptr,
-                     static_cast<int>(bh), H, n, d, m, M, kind, (flags & KRPE_NPRF) != 0,
+                     static_cast<int>(bh), H, n, d, m, M, kind, (flags & KRPE_NPRF) != 0, use_direct(flags, n, M, d),
                      static_cast<hipStream_t>(stream), events);
 }
 
@@ -394,9 +449,16 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
   return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, 0u, ws, ws_bytes, stream, nullptr);
 }
 
+int krpe_attention_fwd_route(int n, int d, int m, unsigned flags) {
+  if (n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
+  int kind = kFeatPrf, M = m;
+  if (feature_kind(flags, d, m, &kind, &M) != KRPE_OK) return 0;
+  return use_direct(flags, n, M, d) ? static_cast<int>(KRPE_ROUTE_DIRECT) : static_cast<int>(KRPE_ROUTE_FFT);
+}
+
 size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned flags) {
   if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
-  if (flags & ~static_cast<unsigned>(KRPE_NPRF)) return 0;
+  if (flags & ~static_cast<unsigned>(KRPE_NPRF | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT)) return 0;
   return bwd_layout(B, H, n, d, m).total;
 }
 
@@ -406,8 +468,10 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
                                  void* stream) {
   g_last_error.clear();
   if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
-  if (flags & ~static_cast<unsigned>(KRPE_NPRF))
-    return fail(KRPE_ERR_UNSUPPORTED, "the backward pass takes only KRPE_NPRF (PRF features)");
+  if (flags & ~static_cast<unsigned>(KRPE_NPRF | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT))
+    return fail(KRPE_ERR_UNSUPPORTED, "the backward pass takes KRPE_NPRF and the route bits (PRF features)");
+  if ((flags & KRPE_ROUTE_DIRECT) && (flags & KRPE_ROUTE_FFT))
+    return fail(KRPE_ERR_UNSUPPORTED, "KRPE_ROUTE_DIRECT and KRPE_ROUTE_FFT are exclusive");
   if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
   const size_t bh = static_cast<size_t>(B) * H;
   if (bh == 0) return KRPE_OK;
@@ -458,9 +522,18 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
   const long long fstride = static_cast<long long>(m) * N, gstride = static_cast<long long>(d + 1) * N;
 
   // forward: phi(q), phi(k), z and the denominators
-  if (krpe_status_t s = run_forward(L.f, w, q, k, v, bf16, b, W, zf, den, BHi, H, n, d, m, m, kFeatPrf, nprf, st,
-                                    nullptr))
+  const bool direct = use_direct(flags, n, m, d);
+  if (krpe_status_t s = run_forward(L.f, w, q, k, v, bf16, b, W, zf, den, BHi, H, n, d, m, m, kFeatPrf, nprf, direct,
+                                    st, nullptr))
     return s;
+  if (direct) {
+    // the direct forward needs no transforms; the backward's products do
+    float2* twm = reinterpret_cast<float2*>(w + L.f.tw);
+    float2* Hsm = reinterpret_cast<float2*>(w + L.f.hs);
+    if (krpe_status_t s = hip_check(launch_twiddles(twm, L.f.l2, st), "twiddle launch")) return s;
+    if (krpe_status_t s = hip_check(launch_spectrum(L.f.l2, b, twm, Hsm, nullptr, H, n, st), "spectrum launch"))
+      return s;
+  }
   if (krpe_status_t s = hip_check(launch_bwd_prep(bf16, dz, zf, den, v, gh, vh, BHi, n, N, d, st), "prep launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_reverse_bias(b, brev, n, H, st), "bias launch")) return s;

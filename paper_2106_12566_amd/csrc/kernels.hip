@@ -1240,6 +1240,30 @@ __global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restric
   }
 }
 
+// Direct (quadratic) route: every row of every head queued for k_fixup, which
+// then evaluates Eq. (10) as S = phi(Q) phi(K)^T o C and S [v, 1] on MFMA.
+// fixmask[bh][t] holds the bits of the rows < n of tile t; fix[bh] = n,
+// fix[BH] = BH n.
+__global__ void k_mark_all(unsigned* __restrict__ fix, unsigned long long* __restrict__ fixmask, int BH, int n,
+                           int tiles_n) {
+  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const long long words = static_cast<long long>(BH) * tiles_n;
+  if (e < words) {
+    const int t = static_cast<int>(e % tiles_n);
+    const int rows = min(64, n - 64 * t);
+    fixmask[e] = rows >= 64 ? ~0ull : ((1ull << rows) - 1ull);
+  }
+  if (e < BH) fix[e] = static_cast<unsigned>(n);
+  if (e == BH) fix[BH] = static_cast<unsigned>(BH) * static_cast<unsigned>(n);
+}
+
+// dst[e] = bf16 src[e] widened to fp32 (exact), so that the direct route's
+// value loads are 4-byte and coalesced like the fp32 ones.
+__global__ void k_widen_bf16(const uint16_t* __restrict__ src, float* __restrict__ dst, long long count) {
+  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (e < count) dst[e] = to_f32(src[e]);
+}
+
 // ------------------------------------------------------ Toeplitz helpers --
 // ones[pos] = 1 for pos < n, 0 below N: the broadcast "feature" with which the
 // convolution kernel computes plain Toeplitz products (m = 1, phi = 1).
@@ -1709,6 +1733,20 @@ hipError_t launch_feature_bwd(bool bf16, const void* x, const float* W, const fl
   else
     hipLaunchKernelGGL(k_feature_bwd<float>, grid, block, 0, st, static_cast<const float*>(x), W, phi, part, dx, H,
                        n, N, d, m, nsplit, nprf ? 1 : 0, tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_widen_bf16(const void* src, float* dst, long long count, hipStream_t st) {
+  hipLaunchKernelGGL(k_widen_bf16, dim3(static_cast<unsigned>((count + 255) / 256)), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(src), dst, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_mark_all(unsigned* fix, unsigned long long* fixmask, int BH, int n, hipStream_t st) {
+  const int tiles_n = (n + 63) / 64;
+  const long long total = static_cast<long long>(BH) * tiles_n > BH + 1 ? static_cast<long long>(BH) * tiles_n : BH + 1;
+  hipLaunchKernelGGL(k_mark_all, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, st, fix, fixmask, BH,
+                     n, tiles_n);
   return hipGetLastError();
 }
 

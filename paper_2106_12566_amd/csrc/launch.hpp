@@ -97,6 +97,10 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
                         int2* brange, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
+// dst = src (bf16) widened to fp32, count elements.
+hipError_t launch_widen_bf16(const void* src, float* dst, long long count, hipStream_t st);
+// Queue every row for the exact-row kernel (the direct route).
+hipError_t launch_mark_all(unsigned* fix, unsigned long long* fixmask, int BH, int n, hipStream_t st);
 // Backward (see kernels.hip): Gh, V' feature-major from G, z, den, v; the
 // reversed bias; dv from the class splits of the convolution output; dx from
 // dphi (class splits) and phi.

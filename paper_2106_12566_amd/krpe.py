@@ -18,6 +18,7 @@ import os
 import torch
 
 __all__ = ["KrpeError", "load", "lib_path", "feature_map", "toeplitz_conv", "attention_fwd", "attention_bwd",
+           "attention_fwd_route",
            "attention_fwd_workspace", "attention_bwd_workspace", "toeplitz_conv_workspace",
            "attention_fwd_fixed_rows", "DTYPES"]
 
@@ -31,6 +32,9 @@ NPRF = 1  # option bit: l2-normalise the rows of q and k (x) before the feature 
 FEAT_TRF = 2  # option bit: trigonometric random features (2m signed features)
 FEAT_ELU = 4  # option bit: elu(x) + 1 (d features, W not read)
 FEATURES = {"prf": 0, "trf": FEAT_TRF, "elu": FEAT_ELU}
+ROUTE_DIRECT = 8  # option bit: evaluate Eq. (10) directly (quadratic, MFMA)
+ROUTE_FFT = 16  # option bit: the FFT route of Section 3.2
+ROUTES = {"auto": 0, "direct": ROUTE_DIRECT, "fft": ROUTE_FFT}
 
 
 class KrpeError(RuntimeError):
@@ -76,6 +80,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_attention_fwd_profiled.restype = i
     lib.krpe_attention_fwd_profiled.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, ctypes.c_uint, vp, sz,
                                                 vp, ctypes.POINTER(ctypes.c_void_p)]
+    lib.krpe_attention_fwd_route.restype = i
+    lib.krpe_attention_fwd_route.argtypes = [i, i, i, ctypes.c_uint]
     lib.krpe_attention_bwd_workspace.restype = sz
     lib.krpe_attention_bwd_workspace.argtypes = [i, i, i, i, i, ctypes.c_uint]
     lib.krpe_attention_bwd.restype = i
@@ -118,10 +124,12 @@ def _dtype_code(t: torch.Tensor, name: str) -> int:
     return DTYPES[t.dtype]
 
 
-def _flags(nprf: bool, features: str) -> int:
+def _flags(nprf: bool, features: str, route: str = "auto") -> int:
     if features not in FEATURES:
         raise KrpeError(f"features must be one of {sorted(FEATURES)}, got {features!r}")
-    return (NPRF if nprf else 0) | FEATURES[features]
+    if route not in ROUTES:
+        raise KrpeError(f"route must be one of {sorted(ROUTES)}, got {route!r}")
+    return (NPRF if nprf else 0) | FEATURES[features] | ROUTES[route]
 
 
 def _proj(W: torch.Tensor | None, H: int, d: int, features: str) -> tuple[torch.Tensor | None, int]:
@@ -180,8 +188,8 @@ def toeplitz_conv(b: torch.Tensor, a: torch.Tensor) -> torch.Tensor:
 
 
 def attention_fwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool = False,
-                            features: str = "prf") -> int:
-    return int(load().krpe_attention_fwd_workspace_ex(B, H, n, d, m, _flags(nprf, features)))
+                            features: str = "prf", route: str = "auto") -> int:
+    return int(load().krpe_attention_fwd_workspace_ex(B, H, n, d, m, _flags(nprf, features, route)))
 
 
 def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d: int, m: int) -> int:
@@ -196,12 +204,14 @@ def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d:
 
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor | None,
                   out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                  events=None, nprf: bool = False, features: str = "prf") -> torch.Tensor:
+                  events=None, nprf: bool = False, features: str = "prf", route: str = "auto") -> torch.Tensor:
     """Eq. (10): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
 
     ``nprf``: normalise the rows of q and k first (Algorithm 1's NPRF attention).
     ``features``: "prf" (Eq. (5)), "trf" (trigonometric, 2m features) or "elu"
     (elu + 1, W unused and may be None).
+    ``route``: "fft" (Section 3.2), "direct" (Eq. (10) evaluated directly on
+    MFMA, faster for short sequences) or "auto" (by sequence length).
 
     ``out`` and ``workspace`` may be passed to reuse allocations (a uint8 tensor
     of at least attention_fwd_workspace() bytes).  ``events``: optional list of
@@ -215,7 +225,7 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     B, H, n, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
         raise KrpeError("q, k, v must share shape and dtype")
-    flags = _flags(nprf, features)
+    flags = _flags(nprf, features, route)
     W, m = _proj(W, H, d, features)
     if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
         raise KrpeError("b must be float32 [H, 2n-1]")
@@ -242,13 +252,23 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     return out
 
 
+def attention_fwd_route(n: int, d: int, m: int, nprf: bool = False, features: str = "prf",
+                        route: str = "auto") -> str:
+    """The route ("direct" or "fft") attention_fwd takes for these sizes and options."""
+    r = int(load().krpe_attention_fwd_route(n, d, m, _flags(nprf, features, route)))
+    if r == 0:
+        raise KrpeError("invalid sizes or options")
+    return "direct" if r == ROUTE_DIRECT else "fft"
+
+
 def attention_bwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool = False) -> int:
     return int(load().krpe_attention_bwd_workspace(B, H, n, d, m, NPRF if nprf else 0))
 
 
+
 def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
                   dz: torch.Tensor, workspace: torch.Tensor | None = None, nprf: bool = False,
-                  with_db: bool = False) -> tuple:
+                  with_db: bool = False, route: str = "auto") -> tuple:
     """Gradients (dq, dk, dv) [B,H,n,d] fp32 of sum(dz * z), z = attention_fwd(q, k, v, b, W, nprf=nprf)
     with PRF features and W fixed (the C header states the formulas); with_db adds db [H, 2n-1]."""
     lib = load()
@@ -266,7 +286,7 @@ def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
         raise KrpeError("b must be float32 [H, 2n-1]")
     m = W.shape[1]
-    flags = NPRF if nprf else 0
+    flags = _flags(nprf, "prf", route)
     wsb = int(lib.krpe_attention_bwd_workspace(B, H, n, d, m, flags))
     if workspace is None:
         workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)

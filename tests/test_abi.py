@@ -40,7 +40,8 @@ def test_header_declares_the_boundary():
                      "krpe_toeplitz_conv_workspace", "krpe_attention_fwd_workspace",
                      "krpe_attention_fwd_profiled", "krpe_status_str", "krpe_last_error",
                      "krpe_abi_version", "krpe_feature_map_ex", "krpe_attention_fwd_ex",
-                     "krpe_attention_fwd_workspace_ex", "krpe_attention_bwd", "krpe_attention_bwd_workspace"):
+                     "krpe_attention_fwd_workspace_ex", "krpe_attention_bwd", "krpe_attention_bwd_workspace",
+                     "krpe_attention_fwd_route"):
         assert required in names
 
 
@@ -106,8 +107,9 @@ def test_attention_validation(lib):
 def test_option_bits_validation(lib):
     wsb = lib.krpe_attention_fwd_workspace(1, 1, 8, 4, 4)
     ex = lambda flags: lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, flags, WSP, wsb, None)
-    assert ex(8) == UNSUP                    # unknown option bit
-    assert ex(1 | 8) == UNSUP
+    assert ex(32) == UNSUP                   # unknown option bit
+    assert ex(1 | 32) == UNSUP
+    assert ex(8 | 16) == UNSUP               # both routes
     assert ex(2 | 4) == UNSUP                # TRF and elu + 1 together
     # elu + 1 needs m == d (here d = 4, m = 3); TRF doubles the features (2m <= 1024)
     assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 3, 4, WSP, wsb, None) == SHAPE
@@ -119,12 +121,13 @@ def test_option_bits_validation(lib):
     assert wse(1) == wse(0)                  # normalisation needs no space
     assert wse(2) > wse(0)                   # 2m trigonometric features
     assert wse(4) == wse(0)                  # elu + 1: M = d = m
-    assert wse(4, m=3) == 0 and wse(6) == 0 and wse(8) == 0
+    assert wse(4, m=3) == 0 and wse(6) == 0 and wse(32) == 0 and wse(24) == 0
+    assert wse(8) == wse(0) and wse(16) == wse(0)   # one workspace serves both routes
     assert wse(2, m=513) == 0
     assert lib.krpe_attention_fwd_ex(None, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, WSP, wsb, None) == NULL
     assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, None, wsb, None) == WS
     fm = lambda flags: lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 4, flags, None)
-    assert fm(8) == UNSUP
+    assert fm(32) == UNSUP
     assert fm(6) == UNSUP
     assert lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 3, 4, None) == SHAPE
     assert lib.krpe_feature_map_ex(Q, 0, None, Z, 1, 1, 8, 4, 4, 2, None) == NULL
@@ -176,7 +179,8 @@ def test_backward_validation(lib):
     call = lambda flags=0, db=None, dq=D1, dz=Q, w=WSP, wb=wsb, n=8: lib.krpe_attention_bwd(
         Q, K, V, 0, BB, W, dz, dq, D2, D3, db, 1, 1, n, 4, 4, flags, w, wb, None)
     assert call(flags=2) == UNSUP
-    assert call(flags=8) == UNSUP
+    assert call(flags=32) == UNSUP
+    assert call(flags=8 | 16) == UNSUP
     assert call(db=D1) == ALIAS               # db overlapping dq
     assert call(db=Z + 20000 + 4) == ALIGN
     assert call(dz=None) == NULL
@@ -185,3 +189,14 @@ def test_backward_validation(lib):
     assert call(dq=Q) == ALIAS
     assert call(dq=D2) == ALIAS
     assert call(dq=D1 + 8) == ALIGN
+
+
+def test_route_query(lib):
+    """Route choice: forced by the option bits, else the cost model (direct for short sequences)."""
+    route = lib.krpe_attention_fwd_route
+    assert route(4096, 64, 128, 8) == 8 and route(128, 64, 64, 16) == 16
+    assert route(128, 64, 64, 0) == 8                 # short: direct
+    assert route(512, 64, 64, 0) == 8
+    assert route(4096, 64, 128, 0) == 16              # the long-n4096 head: FFT
+    assert route(16384, 64, 256, 0) == 16
+    assert route(8, 4, 4, 8 | 16) == 0 and route(0, 4, 4, 0) == 0 and route(8, 4, 3, 4) == 0

@@ -92,16 +92,17 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("route", ["fft", "direct"])
 @pytest.mark.parametrize("B,H,n,d,m,dt,bias,features,nprf,draw", CASES)
-def test_attention_feature_maps(gpu_lib, B, H, n, d, m, dt, bias, features, nprf, draw):
-    _say(f"attention {features} nprf={nprf} W={draw} B={B} H={H} n={n} d={d} m={m} {dt} {bias}")
+def test_attention_feature_maps(gpu_lib, B, H, n, d, m, dt, bias, features, nprf, draw, route):
+    _say(f"attention {features} nprf={nprf} W={draw} B={B} H={H} n={n} d={d} m={m} {dt} {bias} route={route}")
     small_qk = features == "trf" and not nprf
     dd = synth.custom(B, H, n, d, m, seed=43 + n, qkv_dtype=dt, bias=bias, features=draw,
                       qk_scale=0.2 if small_qk else None)
     W = None if features == "elu" else dd["W"]
     q, k, v, b = (to_gpu(dd["q"], dt), to_gpu(dd["k"], dt), to_gpu(dd["v"], dt), to_gpu(dd["b"]))
     z = gpu_lib.attention_fwd(q, k, v, b, None if W is None else to_gpu(W), nprf=nprf,
-                              features=features).cpu().numpy()
+                              features=features, route=route).cpu().numpy()
     assert np.all(np.isfinite(z))
     if B * H * n * n <= 2 ** 22:
         ref, den = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], W, nprf=nprf, kind=features)
@@ -121,9 +122,10 @@ def test_trf_exact_rows_and_option_effect(gpu_lib):
     B, H, n, d, m = 1, 1, 2048, 64, 64
     dd = synth.custom(B, H, n, d, m, seed=44, bias="causal")
     q, k, v, b, W = (to_gpu(dd[x]) for x in ("q", "k", "v", "b", "W"))
-    ws = gpu_lib.attention_fwd_workspace(B, H, n, d, m, nprf=True, features="trf")
+    ws = gpu_lib.attention_fwd_workspace(B, H, n, d, m, nprf=True, features="trf", route="fft")
     work = __import__("torch").empty(ws, dtype=__import__("torch").uint8, device=q.device)
-    zt = gpu_lib.attention_fwd(q, k, v, b, W, workspace=work, nprf=True, features="trf").cpu().numpy()
+    zt = gpu_lib.attention_fwd(q, k, v, b, W, workspace=work, nprf=True, features="trf",
+                               route="fft").cpu().numpy()
     fixed = gpu_lib.attention_fwd_fixed_rows(work, B, H, n, d, m)
     _say(f"trf causal exact rows: {fixed}")
     assert fixed > 0

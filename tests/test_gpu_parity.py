@@ -203,11 +203,12 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("route", ["fft", "direct"])
 @pytest.mark.parametrize("B,H,n,d,m,dt,bias", SMALL)
-def test_attention_small_full_compare(gpu_lib, B, H, n, d, m, dt, bias):
-    _say(f"attention B={B} H={H} n={n} d={d} m={m} {dt} {bias}")
+def test_attention_small_full_compare(gpu_lib, B, H, n, d, m, dt, bias, route):
+    _say(f"attention B={B} H={H} n={n} d={d} m={m} {dt} {bias} route={route}")
     dd = synth.custom(B, H, n, d, m, seed=n + 7 * m, qkv_dtype=dt, bias=bias)
-    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd)).cpu().numpy()
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd), route=route).cpu().numpy()
     if n * n * B * H <= 2 ** 24:
         ref, den = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"])
     else:
@@ -233,12 +234,13 @@ NPRF_CASES = [
 ]
 
 
+@pytest.mark.parametrize("route", ["fft", "direct"])
 @pytest.mark.parametrize("B,H,n,d,m,dt,bias", NPRF_CASES)
-def test_attention_normalised(gpu_lib, B, H, n, d, m, dt, bias):
+def test_attention_normalised(gpu_lib, B, H, n, d, m, dt, bias, route):
     """NPRF attention (Algorithm 1): q, k rows normalised, then Eq. (10)."""
     dd = synth.custom(B, H, n, d, m, seed=31 + n, qkv_dtype=dt, bias=bias)
     q, k, v, b, W = inputs_to_gpu(dd)
-    z = gpu_lib.attention_fwd(q, k, v, b, W, nprf=True).cpu().numpy()
+    z = gpu_lib.attention_fwd(q, k, v, b, W, nprf=True, route=route).cpu().numpy()
     rows = sample_rows(B, H, n, 48, seed=n, extra=[(0, 0, i) for i in range(4)])
     zr, den = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], rows, nprf=True)
     got = np.stack([z[bb, h, i] for bb, h, i in rows])
@@ -251,20 +253,22 @@ def test_attention_normalised(gpu_lib, B, H, n, d, m, dt, bias):
     assert rownorm_err(z0, z) > 1e-4
 
 
-def test_workload1_full(gpu_lib):
+@pytest.mark.parametrize("route", ["auto", "fft"])
+def test_workload1_full(gpu_lib, route):
     """The tiny workload (1 head, n = 128, d = 64, m = 64), every element."""
     dd = synth.make(1)
-    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd)).cpu().numpy()
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd), route=route).cpu().numpy()
     ref, _ = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"])
     err = rownorm_err(z, ref)
     _say(f"workload 1 err={err:.3e}")
     assert err <= TOL["f32"], err
 
 
-def test_workload2_two_heads_full(gpu_lib):
+@pytest.mark.parametrize("route", ["auto", "fft"])
+def test_workload2_two_heads_full(gpu_lib, route):
     """The BERT-base-shaped layer with 2 of its 12 heads, every element."""
     dd = synth.make(2, heads=2)
-    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd)).cpu().numpy()
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd), route=route).cpu().numpy()
     ref, _ = oracle.attention(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"])
     err = rownorm_err(z, ref)
     _say(f"workload 2 (2 heads) err={err:.3e}")
@@ -272,16 +276,17 @@ def test_workload2_two_heads_full(gpu_lib):
 
 
 # ------------------------------------------------ attention, full workloads --
-@pytest.mark.parametrize("wid", [2, 3, 4, 5])
-def test_full_workload_sampled_rows(gpu_lib, wid):
-    """Full-size workloads, as benchmarked; rows sampled over every head."""
+@pytest.mark.parametrize("wid,route", [(2, "auto"), (2, "fft"), (3, "auto"), (3, "fft"), (4, "auto"), (5, "auto")])
+def test_full_workload_sampled_rows(gpu_lib, wid, route):
+    """Full-size workloads, as benchmarked (route "auto"), and by the FFT route where "auto"
+    takes the direct one; rows sampled over every head."""
     wl = synth.WORKLOADS[wid]
-    _say(f"workload {wid}: {wl}")
+    _say(f"workload {wid} route {route}: {wl}")
     dd = synth.make(wid)
     import torch
-    ws = torch.empty(gpu_lib.attention_fwd_workspace(wl.B, wl.H, wl.n, wl.d, wl.m), dtype=torch.uint8,
-                     device="cuda")
-    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd), workspace=ws).cpu().numpy()
+    ws = torch.empty(gpu_lib.attention_fwd_workspace(wl.B, wl.H, wl.n, wl.d, wl.m, route=route),
+                     dtype=torch.uint8, device="cuda")
+    z = gpu_lib.attention_fwd(*inputs_to_gpu(dd), workspace=ws, route=route).cpu().numpy()
     fixed = gpu_lib.attention_fwd_fixed_rows(ws, wl.B, wl.H, wl.n, wl.d, wl.m)
     _say(f"  rows evaluated exactly: {fixed} of {wl.B * wl.H * wl.n}")
     assert np.all(np.isfinite(z))
