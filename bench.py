@@ -41,6 +41,9 @@ def direct_flops(B: int, H: int, n: int, d: int, m: int, b: np.ndarray) -> float
     return B * pairs * (2.0 * m + 1.0 + 2.0 * (d + 1))
 
 
+BLOCK = 16384   # longest sequence one transform covers; longer ones run in blocks
+
+
 def conv_stage_flops(B: int, H: int, n: int, d: int, m: int) -> float:
     """Algorithmic flops of the FFT convolution + contraction stage.
 
@@ -48,7 +51,12 @@ def conv_stage_flops(B: int, H: int, n: int, d: int, m: int) -> float:
     2.5 L log2 L flops each, the pointwise complex product with the spectrum
     over n + 1 bins (6 flops each), forming the channel (1 multiply per
     position) and the contraction with phi(q) (1 multiply-add per position).
+    For n > BLOCK, nb^2 block pairs (nb = ceil(n / BLOCK)) of that count at
+    n = BLOCK, the work the blocked Toeplitz product performs.
     """
+    if n > BLOCK:
+        nb = -(-n // BLOCK)
+        return nb * nb * conv_stage_flops(B, H, BLOCK, d, m)
     L = 2 * n
     per_channel = 5.0 * L * math.log2(L) + 6.0 * (n + 1) + 4.0 * n
     return B * H * m * (d + 1) * per_channel
@@ -137,6 +145,8 @@ def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool 
     import oracle
     wl = d["workload"]
     B, H, n = wl.B, d["H"], wl.n
+    if n > BLOCK:
+        return cpu_baseline_rows(d, budget_s, z_gpu, nprf=nprf, kind=kind)
     units = [(beta, h) for h in range(H) for beta in range(B)]
     rng = np.random.default_rng([2106, 12566, 99])
     rng.shuffle(units)
@@ -169,12 +179,79 @@ def cpu_baseline(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool 
     }, worst, done
 
 
+def cpu_baseline_rows(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: bool = False,
+                      kind: str = "prf"):
+    """As cpu_baseline, on sampled output rows (the oracle's row-at-a-time form of Eq. (10), O(n)
+    per row after one feature map per (batch, head)), for sequences whose n x n weight matrix is
+    too large to form on the host."""
+    import oracle
+    wl = d["workload"]
+    B, H, n = wl.B, d["H"], wl.n
+    rng = np.random.default_rng([2106, 12566, 98])
+    t0 = time.perf_counter()
+    done, worst = 0, 0.0
+    W = None if kind == "elu" else d["W"]
+    while True:
+        beta, h = int(rng.integers(B)), int(rng.integers(H))
+        rows = [(beta, h, int(i)) for i in rng.integers(0, n, 64)]
+        z, _ = oracle.attention_rows(d["q"], d["k"], d["v"], d["b"], W, rows, nprf=nprf, kind=kind)
+        done += len(rows)
+        if z_gpu is not None:
+            got = np.stack([z_gpu[bb, hh, i] for bb, hh, i in rows])
+            num = np.max(np.abs(got - z), axis=-1)
+            worst = max(worst, float(np.max(num / np.max(np.abs(z), axis=-1))))
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    elapsed = time.perf_counter() - t0
+    layer_s = elapsed / done * B * H * n
+    return {
+        "value": B * n / layer_s,
+        "unit": "tokens/s",
+        "cores": blas_threads(),
+        "kind": "oracle",
+        "sample": f"{done} sampled rows of {wl.name} in blocks of 64 rows of one (batch, head), Eq. (10) "
+                  f"row by row in fp64 (oracle.attention_rows, {elapsed:.1f} s, one feature map per "
+                  f"block), extrapolated to the layer's {B * H * n} rows",
+        "layer_s": layer_s,
+    }, worst, done
+
+
+def sweep(lengths, ms, steps: int) -> int:
+    """Forward time against sequence length for one head with d = 64 (the paper's speed test
+    setting), each m, both routes; one JSON line per (n, m, route) on stdout."""
+    import torch
+    from paper_2106_12566_amd import krpe, synth
+    dev = torch.device("cuda", 0)
+    for n in lengths:
+        for m in ms:
+            dd = synth.custom(1, 1, n, 64, m, seed=n)
+            q, k, v, b, W = (torch.from_numpy(dd[x]).to(dev) for x in ("q", "k", "v", "b", "W"))
+            for rt in ("fft", "direct"):
+                ws = torch.empty(krpe.attention_fwd_workspace(1, 1, n, 64, m, route=rt), dtype=torch.uint8,
+                                 device=dev)
+                out = torch.empty_like(q)
+                krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=rt)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(steps):
+                    krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=rt)
+                torch.cuda.synchronize()
+                ms_call = 1e3 * (time.perf_counter() - t0) / steps
+                print(json.dumps({"n": n, "m": m, "route": rt, "ms": ms_call,
+                                  "auto": krpe.attention_fwd_route(n, 64, m)}), flush=True)
+                del ws
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-5)")
+    ap.add_argument("--workload", type=int, default=4, help="synthetic workload id (1-7)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead: forward time against n (1k .. 40k), one head, d = 64, m = 32/64/128, "
+                         "both routes, one JSON line each")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
@@ -207,6 +284,8 @@ def main() -> int:
         print("bench.py: no GPU visible", file=sys.stderr)
         return 1
     torch.cuda.set_device(0)
+    if args.sweep:
+        return sweep([1000, 2000, 4000, 8000, 16000, 24000, 32000, 40000], [32, 64, 128], args.steps)
 
     d = synth.make(args.workload)
     wl = d["workload"]
@@ -284,7 +363,7 @@ def main() -> int:
         "config": {"workload": wl.name, "B": B, "H": H, "n": n, "d": dd, "m": m,
                    "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
                    "causal": wl.causal, "nprf": args.nprf, "feature_map": fm, "features_per_position": M,
-                   "route": route_used,
+                   "route": route_used, "blocks": -(-n // BLOCK) if route_used == "fft" else None,
                    "ms_per_layer": ms_per_step, "stages_ms": stages,
                    "conv_stage_hbm_gbs": conv_gbs,
                    "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)},

@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libkrpe.so")
 SOURCES = [os.path.join(HERE, "csrc", "kernels.hip"), os.path.join(HERE, "csrc", "grad_bias.hip"),
-           os.path.join(HERE, "csrc", "api.hip")]
+           os.path.join(HERE, "csrc", "long_seq.hip"), os.path.join(HERE, "csrc", "api.hip")]
 ARCH = "gfx950"
 
 

@@ -47,10 +47,11 @@ krpe_status_t hip_check(hipError_t e, const char* what) {
   return fail(KRPE_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm) {
+krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm, int max_log2n = kMaxLog2N) {
   if (B < 0 || H < 0 || n < 0 || (need_dm && (d < 0 || m < 0))) return fail(KRPE_ERR_SHAPE, "negative size");
   if (n < 1) return fail(KRPE_ERR_SHAPE, "n must be >= 1 (b has 2n-1 entries)");
-  if (n > (1 << kMaxLog2N)) return fail(KRPE_ERR_UNSUPPORTED, "n > 16384 is not supported");
+  if (n > (1 << max_log2n))
+    return fail(KRPE_ERR_UNSUPPORTED, "n > " + std::to_string(1 << max_log2n) + " is not supported here");
   if (need_dm) {
     if (d < 1 || m < 1) return fail(KRPE_ERR_SHAPE, "d and m must be >= 1");
     if (d > kMaxD) return fail(KRPE_ERR_UNSUPPORTED, "d > 128 is not supported");
@@ -75,9 +76,12 @@ constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRP
 bool direct_is_faster(int n, int M, int d) {
   int l2 = 0;
   while ((1 << l2) < n) ++l2;
+  // beyond one transform block the FFT route runs nb^2 block pairs
+  const int nb = l2 > kMaxLog2N ? (n + (1 << kMaxLog2N) - 1) >> kMaxLog2N : 1;
+  if (l2 > kMaxLog2N) l2 = kMaxLog2N;
   const double L = 2.0 * static_cast<double>(1 << l2);
   const double direct = 4.2e-14 * static_cast<double>(n) * n * (M + d + 1);
-  const double fft = 2.0e-13 * M * ((d + 2) / 2) * L * (l2 + 1);
+  const double fft = 2.0e-13 * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb;
   return direct < fft;
 }
 
@@ -175,6 +179,54 @@ BwdLayout bwd_layout(int B, int H, int n, int d, int M) {
   L.ycorr = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
   L.total = off;
   return L;
+}
+
+LongLayout long_layout(int B, int H, int n, int d, int M) {
+  LongLayout L{};
+  L.nbk = 1 << kMaxLog2N;
+  L.nb = (n + L.nbk - 1) / L.nbk;
+  L.Ntot = L.nb * L.nbk;
+  const size_t bh = static_cast<size_t>(B) * H, nbk = static_cast<size_t>(L.nbk), nb = static_cast<size_t>(L.nb);
+  const size_t cols = static_cast<size_t>(d) + 1, pairs = (cols + 1) / 2;
+  L.ksplit = gram_splits(static_cast<int>(bh), M, L.nbk);
+  size_t off = 0;
+  auto take = [&off](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  L.fix = take((bh + 1) * sizeof(unsigned));
+  L.tw = take(2 * nbk * sizeof(float2));
+  L.hs = take(static_cast<size_t>(H) * 2 * nbk * sizeof(float2));
+  L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
+  L.hunit = take(static_cast<size_t>(H) * sizeof(float2));
+  L.bwin = take(static_cast<size_t>(H) * (2 * nbk - 1) * sizeof(float));
+  L.phiq = take(bh * M * static_cast<size_t>(L.Ntot) * sizeof(float));
+  L.phik = take(bh * M * static_cast<size_t>(L.Ntot) * sizeof(float));
+  L.phiqb = take(nb * bh * M * nbk * sizeof(float));
+  L.phikb = take(nb * bh * M * nbk * sizeof(float));
+  L.vsc = take(nb * bh * pairs * nbk * sizeof(float2));
+  L.colmax = take(nb * bh * cols * sizeof(float));
+  L.vmax = take(bh * vmax_chunks(L.nbk) * static_cast<size_t>(d) * sizeof(float));
+  L.x2 = take(bh * L.ksplit * M * pairs * sizeof(float));
+  L.wbj = take(nb * bh * (static_cast<size_t>(M) + 1) * sizeof(float2));
+  L.wbi = take(bh * (static_cast<size_t>(M) + 1) * sizeof(float2));
+  L.part = take(bh * conv_splits(kMaxLog2N) * cols * nbk * sizeof(float));
+  L.acc = take(bh * conv_splits(kMaxLog2N) * cols * nbk * sizeof(float));
+  L.zb = take(bh * nbk * d * sizeof(float));
+  L.maskb = take(bh * (nbk / 64) * sizeof(unsigned long long));
+  L.maskf = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
+  L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
+  L.brange = take(static_cast<size_t>(H) * sizeof(int2));
+  L.total = off;
+  return L;
+}
+
+// Workspace of the forward pass for these sizes (the blocked layout for long
+// sequences on the FFT route, else the one-transform layout).
+size_t fwd_workspace(int B, int H, int n, int d, int M, bool direct) {
+  if (n > (1 << kMaxLog2N) && !direct) return long_layout(B, H, n, d, M).total;
+  return attn_layout(B, H, n, d, M).total;
 }
 
 ConvLayout conv_layout(int B, int H, int C, int n) {
@@ -281,6 +333,102 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
   return record(events, 4, st);
 }
 
+// Forward pass of Eq. (10) for n > 2^kMaxLog2N on the FFT route: query block
+// I's numerators and denominator summed over the key blocks J, each block
+// pair one convolution run with the Toeplitz block's bias window; the rows
+// certified per block with weights summed over J; the rest evaluated
+// directly over the whole sequence.
+krpe_status_t run_forward_long(const LongLayout& L, char* w, const void* q, const void* k, const void* v, bool bf16,
+                               const float* b, const float* W, float* z, int BHi, int H, int n, int d, int m, int M,
+                               int kind, bool nprf, hipStream_t st, void* const* events) {
+  auto F = [&](size_t o) { return reinterpret_cast<float*>(w + o); };
+  auto F2 = [&](size_t o) { return reinterpret_cast<float2*>(w + o); };
+  unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
+  const int nbk = L.nbk, nb = L.nb, cols = d + 1, pairs = (d + 2) / 2, splits = conv_splits(kMaxLog2N);
+  const size_t bhM = static_cast<size_t>(BHi) * M, esz = bf16 ? 2 : 4;
+  const int tiles_full = (n + 63) / 64;
+  auto len_of = [&](int K) { return n - K * nbk < nbk ? n - K * nbk : nbk; };
+
+  if (krpe_status_t s = record(events, 0, st)) return s;
+  if (krpe_status_t s = hip_check(launch_twiddles(F2(L.tw), kMaxLog2N, st), "twiddle launch")) return s;
+  if (krpe_status_t s = hip_check(launch_unit_hnorm(F2(L.hunit), H, st), "norm launch")) return s;
+  if (krpe_status_t s = record(events, 1, st)) return s;
+  if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, F(L.phiq), F(L.phik), 2, true, L.Ntot, BHi, H, n,
+                                                     d, m, fix, nprf, kind, st),
+                                  "feature map launch"))
+    return s;
+  for (int K = 0; K < nb; ++K) {
+    float* pqb = F(L.phiqb) + static_cast<size_t>(K) * bhM * nbk;
+    float* pkb = F(L.phikb) + static_cast<size_t>(K) * bhM * nbk;
+    if (krpe_status_t s = hip_check(launch_block_rows(F(L.phiq), pqb, BHi, M, nbk, L.Ntot, K, st), "block launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_block_rows(F(L.phik), pkb, BHi, M, nbk, L.Ntot, K, st), "block launch"))
+      return s;
+    // key block K: value column pairs, channel norms and bound weights
+    const char* vk = static_cast<const char*>(v) + static_cast<size_t>(K) * nbk * d * esz;
+    float2* vscK = F2(L.vsc) + static_cast<size_t>(K) * BHi * pairs * nbk;
+    float* colK = F(L.colmax) + static_cast<size_t>(K) * BHi * cols;
+    if (krpe_status_t s = hip_check(launch_vprep(bf16, vk, d, 1, static_cast<long long>(n) * d, d, true, BHi,
+                                                 len_of(K), nbk, F(L.vmax), colK, vscK, st),
+                                    "column launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_gram(pkb, vscK, F(L.x2), BHi, M, nbk, pairs, L.ksplit, st), "norm launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_bound_weights(F(L.x2), colK, F2(L.wbj) + static_cast<size_t>(K) * BHi * (M + 1),
+                                                         BHi, M, d, L.ksplit, st),
+                                    "bound launch"))
+      return s;
+  }
+  if (krpe_status_t s = record(events, 2, st)) return s;
+  for (int I = 0; I < nb; ++I) {
+    const int lenI = len_of(I);
+    const float* pqb = F(L.phiqb) + static_cast<size_t>(I) * bhM * nbk;
+    for (int J = 0; J < nb; ++J) {
+      const float* pkb = F(L.phikb) + static_cast<size_t>(J) * bhM * nbk;
+      if (krpe_status_t s = hip_check(launch_bias_window(b, F(L.bwin), H, n, nbk, (J - I) * nbk, st), "bias launch"))
+        return s;
+      if (krpe_status_t s = hip_check(launch_spectrum(kMaxLog2N, F(L.bwin), F2(L.tw), F2(L.hs), F2(L.hnorm), H, nbk,
+                                                      st),
+                                      "spectrum launch"))
+        return s;
+      if (krpe_status_t s = hip_check(
+              launch_conv(kMaxLog2N, pqb, pkb, static_cast<long long>(M) * nbk,
+                          F2(L.vsc) + static_cast<size_t>(J) * BHi * pairs * nbk,
+                          F(L.colmax) + static_cast<size_t>(J) * BHi * cols, F2(L.hs), F2(L.tw), F(L.part), BHi, H,
+                          lenI, cols, M, st),
+              "conv launch"))
+        return s;
+      if (krpe_status_t s = hip_check(launch_accum(F(L.acc), F(L.part),
+                                                   static_cast<long long>(BHi) * splits * cols * lenI, J == 0, st),
+                                      "sum launch"))
+        return s;
+      if (krpe_status_t s = hip_check(launch_wb_accum(F2(L.wbi), F2(L.wbj) + static_cast<size_t>(J) * BHi * (M + 1),
+                                                      F2(L.hnorm), BHi, H, M, J == 0, st),
+                                      "weight launch"))
+        return s;
+    }
+    unsigned long long* maskb = reinterpret_cast<unsigned long long*>(w + L.maskb);
+    if (krpe_status_t s = hip_check(launch_combine(F(L.acc), pqb, F2(L.wbi), F2(L.hunit), F(L.zb), nullptr, fix, maskb,
+                                                   BHi, H, lenI, kMaxLog2N, d, M, st),
+                                    "combine launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_merge_mask(maskb, reinterpret_cast<unsigned long long*>(w + L.maskf), BHi,
+                                                      (lenI + 63) / 64, tiles_full, I, nbk, st),
+                                    "mask launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_scatter_rows(F(L.zb), z, BHi, n, nbk, d, I, lenI, st), "rows launch"))
+      return s;
+  }
+  if (krpe_status_t s = record(events, 3, st)) return s;
+  if (krpe_status_t s = hip_check(launch_fixup(F(L.phiq), F(L.phik), v, bf16, b, z, nullptr, fix,
+                                               reinterpret_cast<unsigned long long*>(w + L.maskf),
+                                               reinterpret_cast<double*>(w + L.fixpart),
+                                               reinterpret_cast<int2*>(w + L.brange), BHi, H, n, L.Ntot, d, M, st),
+                                  "fixup launch"))
+    return s;
+  return record(events, 4, st);
+}
+
 }  // namespace krpe
 
 using namespace krpe;
@@ -309,7 +457,7 @@ const char* krpe_last_error(void) { return g_last_error.c_str(); }
 krpe_status_t krpe_feature_map_ex(const void* x, int x_dtype, const float* W, float* phi, int B, int H, int n,
                                   int d, int m, unsigned flags, void* stream) {
   g_last_error.clear();
-  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true, kMaxLongLog2N)) return s;
   int kind = kFeatPrf, M = m;
   if (krpe_status_t s = feature_kind(flags, d, m, &kind, &M)) return s;
   if (x_dtype != KRPE_F32 && x_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "x_dtype must be F32 or BF16");
@@ -390,10 +538,10 @@ krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B
 }
 
 size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsigned flags) {
-  if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
+  if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLongLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
   int kind = kFeatPrf, M = m;
   if (feature_kind(flags, d, m, &kind, &M) != KRPE_OK) return 0;
-  return attn_layout(B, H, n, d, M).total;
+  return fwd_workspace(B, H, n, d, M, use_direct(flags, n, M, d));
 }
 
 size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
@@ -404,7 +552,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
                                           const float* W, float* z, int B, int H, int n, int d, int m, unsigned flags,
                                           void* ws, size_t ws_bytes, void* stream, void* const* events) {
   g_last_error.clear();
-  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true, kMaxLongLog2N)) return s;
   int kind = kFeatPrf, M = m;
   if (krpe_status_t s = feature_kind(flags, d, m, &kind, &M)) return s;
   if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");
@@ -416,9 +564,9 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(b) || (needW && misaligned(W)) ||
       misaligned(z) || misaligned(ws))
     return fail(KRPE_ERR_ALIGN, "all pointers must be 16-byte aligned");
-  const AttnLayout L = attn_layout(B, H, n, d, M);
-  if (!ws || ws_bytes < L.total)
-    return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
+  const bool direct = use_direct(flags, n, M, d);
+  const size_t need = fwd_workspace(B, H, n, d, M, direct);
+  if (!ws || ws_bytes < need) return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
   const size_t qkv_bytes = bh * n * d * dtype_size(qkv_dtype);
   const Range ins[] = {{q, qkv_bytes},
                        {k, qkv_bytes},
@@ -431,8 +579,12 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   for (const Range& r : ins)
     if (overlaps(rz, r) || overlaps(rws, r)) return fail(KRPE_ERR_ALIAS, "z or the workspace overlaps an input");
 
-  return run_forward(L, static_cast<char*>(ws), q, k, v, qkv_dtype == KRPE_BF16, b, W, z, nullptr,
-                     static_cast<int>(bh), H, n, d, m, M, kind, (flags & KRPE_NPRF) != 0, use_direct(flags, n, M, d),
+  if (n > (1 << kMaxLog2N) && !direct)
+    return run_forward_long(long_layout(B, H, n, d, M), static_cast<char*>(ws), q, k, v, qkv_dtype == KRPE_BF16, b,
+                            W, z, static_cast<int>(bh), H, n, d, m, M, kind, (flags & KRPE_NPRF) != 0,
+                            static_cast<hipStream_t>(stream), events);
+  return run_forward(attn_layout(B, H, n, d, M), static_cast<char*>(ws), q, k, v, qkv_dtype == KRPE_BF16, b, W, z,
+                     nullptr, static_cast<int>(bh), H, n, d, m, M, kind, (flags & KRPE_NPRF) != 0, direct,
                      static_cast<hipStream_t>(stream), events);
 }
 
@@ -450,7 +602,7 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
 }
 
 int krpe_attention_fwd_route(int n, int d, int m, unsigned flags) {
-  if (n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
+  if (n < 1 || n > (1 << kMaxLongLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
   int kind = kFeatPrf, M = m;
   if (feature_kind(flags, d, m, &kind, &M) != KRPE_OK) return 0;
   return use_direct(flags, n, M, d) ? static_cast<int>(KRPE_ROUTE_DIRECT) : static_cast<int>(KRPE_ROUTE_FFT);
@@ -588,7 +740,7 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
 krpe_status_t krpe_attention_fwd_stats(const void* ws, size_t ws_bytes, int B, int H, int n, int d, int m,
                                        unsigned* fixed_rows, void* stream) {
   g_last_error.clear();
-  if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
+  if (krpe_status_t s = check_dims(B, H, n, d, m, true, kMaxLongLog2N)) return s;
   if (!fixed_rows) return fail(KRPE_ERR_NULL, "fixed_rows must be non-NULL");
   *fixed_rows = 0;
   if (static_cast<size_t>(B) * H == 0) return KRPE_OK;

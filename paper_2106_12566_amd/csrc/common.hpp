@@ -10,6 +10,9 @@
 namespace krpe {
 
 constexpr int kMaxLog2N = 14;  // n <= 16384 (FFT length 2N <= 32768)
+// Longer sequences (attention only) run as blocks of 2^kMaxLog2N positions:
+// n <= 2^kMaxLongLog2N, the Toeplitz matrix taken block by block.
+constexpr int kMaxLongLog2N = 16;
 constexpr int kMaxD = 128;
 constexpr int kMaxM = 1024;
 constexpr int kLog2R = 4;      // 16 complex values per thread

@@ -891,7 +891,7 @@ constexpr int kFixRows = 32;
 constexpr int kFixKeys = 128;
 constexpr int kFixL = 32;                 // features staged per step
 constexpr int kFixStride = kFixKeys + 1;  // LDS row stride (odd: column reads hit distinct banks)
-constexpr int kFixMaxTiles = (1 << kMaxLog2N) / 64;
+constexpr int kFixMaxTiles = (1 << kMaxLongLog2N) / 64;
 constexpr int kFixMaxParts = 16;
 
 // Work items of a head: every group of 32 rows, each split into kparts shares

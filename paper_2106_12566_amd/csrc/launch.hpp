@@ -52,6 +52,31 @@ struct BwdLayout {
 };
 BwdLayout bwd_layout(int B, int H, int n, int d, int M);
 
+// Workspace of krpe_attention_fwd for n > 2^kMaxLog2N on the FFT route
+// (blocks of nbk positions, nb blocks, Ntot = nb nbk).
+struct LongLayout {
+  int nb, nbk, Ntot, ksplit;
+  size_t fix;          // uint   [BH + 1]          (first, as in AttnLayout)
+  size_t tw;           // float2 [2 nbk]
+  size_t hs;           // float2 [H][2 nbk]       spectrum of one block pair
+  size_t hnorm, hunit; // float2 [H]              its norms; ones
+  size_t bwin;         // float  [H][2 nbk - 1]   its bias window
+  size_t phiq, phik;   // float  [BH][M][Ntot]    whole sequence (exact rows)
+  size_t phiqb, phikb; // float  [nb][BH][M][nbk] per block
+  size_t vsc;          // float2 [nb][BH][pairs][nbk]
+  size_t colmax;       // float  [nb][BH][d+1]
+  size_t vmax;         // float  [BH][chunks][d]
+  size_t x2;           // float  [BH][ks][M][pairs]
+  size_t wbj, wbi;     // float2 [nb][BH][M+1], [BH][M+1]
+  size_t part, acc;    // float  [BH][splits][d+1][nbk]
+  size_t zb;           // float  [BH][nbk][d]
+  size_t maskb, maskf; // uint64 [BH][nbk/64], [BH][ceil(n/64)]
+  size_t fixpart;      // double [BH][slots][32][d+1]
+  size_t brange;       // int2   [H]
+  size_t total;
+};
+LongLayout long_layout(int B, int H, int n, int d, int M);
+
 // Workspace of krpe_toeplitz_conv.
 struct ConvLayout {
   int l2;
@@ -97,6 +122,18 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
                         int2* brange, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
+// Long sequences (long_seq.hip): block copies of phi rows, bias windows of a
+// block pair, sums over key blocks, certification weights, row masks, rows.
+hipError_t launch_block_rows(const float* src, float* dst, int BH, int R, int nbk, int Ntot, int K, hipStream_t st);
+hipError_t launch_bias_window(const float* b, float* out, int H, int n, int nbk, int off, hipStream_t st);
+hipError_t launch_accum(float* acc, const float* part, long long count, bool first, hipStream_t st);
+hipError_t launch_wb_accum(float2* wbI, const float2* wbJ, const float2* hnorm, int BH, int H, int M, bool first,
+                           hipStream_t st);
+hipError_t launch_merge_mask(const unsigned long long* blk, unsigned long long* full, int BH, int tiles_b,
+                             int tiles_full, int K, int nbk, hipStream_t st);
+hipError_t launch_scatter_rows(const float* zb, float* z, int BH, int n, int nbk, int d, int K, int lenK,
+                               hipStream_t st);
+hipError_t launch_unit_hnorm(float2* hn, int H, hipStream_t st);
 // dst = src (bf16) widened to fp32, count elements.
 hipError_t launch_widen_bf16(const void* src, float* dst, long long count, hipStream_t st);
 // Queue every row for the exact-row kernel (the direct route).

@@ -53,6 +53,11 @@ WORKLOADS = {
     3: Workload(3, "long-classifier-n2048", 32, 8, 2048, 64, 128, "bf16", "orthogonal", "decay", 0.3, False),
     4: Workload(4, "long-n4096", 8, 12, 4096, 64, 128, "f32", "gaussian", "normal", 1.0, False),
     5: Workload(5, "causal-n16384", 1, 16, 16384, 64, 256, "bf16", "orthogonal", "causal", 0.5, True),
+    # Beyond one transform block: the paper's speed test (one head, d = 64,
+    # synthetic sequences up to 40k tokens; Sec. 3.2) and the causal shape of
+    # workload 5 at four times its length.
+    6: Workload(6, "speed-h1-n40000", 1, 1, 40000, 64, 128, "f32", "gaussian", "normal", 0.5, False),
+    7: Workload(7, "causal-n65536", 1, 16, 65536, 64, 256, "bf16", "orthogonal", "causal", 0.5, True),
 }
 
 

@@ -74,7 +74,16 @@ def test_workspace_queries(lib):
     big = lib.krpe_attention_fwd_workspace(2, 3, 100, 64, 64)
     assert 0 < small < big
     assert lib.krpe_attention_fwd_workspace(1, 1, 0, 4, 4) == 0
-    assert lib.krpe_attention_fwd_workspace(1, 1, 16385, 4, 4) == 0
+    assert lib.krpe_attention_fwd_workspace(1, 1, 65537, 4, 4) == 0
+    # beyond one transform block (n > 16384) the FFT route's blocked layout
+    # holds phi over the whole sequence and per 16384-position block
+    fft_long = lib.krpe_attention_fwd_workspace_ex(1, 2, 40000, 64, 64, 16)
+    assert fft_long >= 2 * 2 * 64 * 49152 * 4 * 2
+    assert lib.krpe_attention_fwd_workspace_ex(1, 2, 40000, 64, 64, 8) > 0
+    assert lib.krpe_attention_fwd_workspace_ex(1, 1, 65536, 64, 64, 0) > 0
+    # the backward and the plain Toeplitz product stay within one block
+    assert lib.krpe_attention_bwd_workspace(1, 1, 16385, 4, 4, 0) == 0
+    assert lib.krpe_toeplitz_conv_workspace(1, 1, 1, 16385) == 0
     assert lib.krpe_attention_fwd_workspace(1, 1, 8, 129, 4) == 0
     assert lib.krpe_toeplitz_conv_workspace(1, 2, 3, 100) > 0
     assert lib.krpe_toeplitz_conv_workspace(1, 2, 3, 0) == 0
@@ -88,7 +97,7 @@ def test_attention_validation(lib):
     assert attn(lib, z=None) == NULL
     assert attn(lib, n=0) == SHAPE
     assert attn(lib, B=-1) == SHAPE
-    assert attn(lib, n=16385) == UNSUP
+    assert attn(lib, n=65537) == UNSUP
     assert attn(lib, d=129) == UNSUP
     assert attn(lib, m=1025) == UNSUP
     assert attn(lib, m=0) == SHAPE
@@ -199,4 +208,6 @@ def test_route_query(lib):
     assert route(512, 64, 64, 0) == 8
     assert route(4096, 64, 128, 0) == 16              # the long-n4096 head: FFT
     assert route(16384, 64, 256, 0) == 16
+    assert route(40000, 64, 64, 0) in (8, 16) and route(65536, 64, 128, 16) == 16
+    assert route(65537, 64, 64, 0) == 0
     assert route(8, 4, 4, 8 | 16) == 0 and route(0, 4, 4, 0) == 0 and route(8, 4, 3, 4) == 0

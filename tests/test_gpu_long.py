@@ -1,0 +1,93 @@
+"""GPU parity of the forward pass for sequences longer than one transform block.
+
+For n > 16384 the FFT route takes the Toeplitz matrix of Eqs. (12)-(13) in
+blocks of 16384 positions (each block pair itself Toeplitz, one run of the
+convolution kernel with its window of b), certifies each query block with
+bounds summed over the key blocks, and evaluates the uncertified rows
+directly over the whole sequence.  Checked against the fp64 oracle on sampled
+rows (including both sides of every block boundary), at the largest supported
+length, with a single-row last block, under every bias family, and against
+the direct route on the whole output.  Tolerances: parity_util.TOL.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2106_12566_amd import synth
+from parity_util import TOL, rownorm_err, sample_rows, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+NBK = 16384
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _boundary_rows(B, H, n):
+    rows = []
+    for edge in range(NBK, n, NBK):
+        for i in (edge - 2, edge - 1, edge, edge + 1):
+            if 0 <= i < n:
+                rows += [(0, 0, i), (B - 1, H - 1, i)]
+    return rows
+
+
+CASES = [
+    # B, H, n, d, m, dtype, bias, nprf
+    (1, 2, 20000, 64, 64, "f32", "normal", False),
+    (2, 1, 16385, 64, 32, "f32", "normal", False),   # last block of one row
+    (1, 1, 32768, 64, 128, "f32", "causal", False),  # two full blocks
+    (1, 1, 40000, 32, 32, "bf16", "decay", True),    # three blocks, ragged
+    (1, 1, 65536, 64, 64, "f32", "causal", True),    # the largest length
+]
+
+
+@pytest.mark.parametrize("B,H,n,d,m,dt,bias,nprf", CASES)
+def test_long_sequence_sampled_rows(gpu_lib, B, H, n, d, m, dt, bias, nprf):
+    _say(f"long fft B={B} H={H} n={n} d={d} m={m} {dt} {bias} nprf={nprf}")
+    dd = synth.custom(B, H, n, d, m, seed=71 + n, qkv_dtype=dt, bias=bias)
+    q, k, v = (to_gpu(dd[x], dt) for x in ("q", "k", "v"))
+    b, W = to_gpu(dd["b"]), to_gpu(dd["W"])
+    ws = gpu_lib.attention_fwd_workspace(B, H, n, d, m, nprf=nprf, route="fft")
+    work = torch.empty(ws, dtype=torch.uint8, device=q.device)
+    z = gpu_lib.attention_fwd(q, k, v, b, W, workspace=work, nprf=nprf, route="fft").cpu().numpy()
+    fixed = gpu_lib.attention_fwd_fixed_rows(work, B, H, n, d, m)
+    assert np.all(np.isfinite(z))
+    rows = sample_rows(B, H, n, 40, seed=n, extra=_boundary_rows(B, H, n) + [(0, 0, i) for i in range(4)])
+    ref, den = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], rows, nprf=nprf)
+    got = np.stack([z[bb, h, i] for bb, h, i in rows])
+    err = rownorm_err(got, ref)
+    _say(f"  err={err:.3e}  exact rows={fixed}  min den={np.min(np.abs(den)):.3e}")
+    assert err <= TOL[dt], err
+
+
+def test_long_sequence_routes_agree(gpu_lib):
+    """Blocked FFT route and direct route on the whole output (each within the
+    oracle's bar, so within twice it of each other), and the automatic route
+    equal to one of them bit for bit."""
+    B, H, n, d, m = 1, 2, 24000, 64, 64
+    dd = synth.custom(B, H, n, d, m, seed=72, bias="normal")
+    q, k, v, b, W = (to_gpu(dd[x]) for x in ("q", "k", "v", "b", "W"))
+    zf = gpu_lib.attention_fwd(q, k, v, b, W, route="fft")
+    zd = gpu_lib.attention_fwd(q, k, v, b, W, route="direct")
+    za = gpu_lib.attention_fwd(q, k, v, b, W)
+    err = rownorm_err(zf.cpu().numpy(), zd.cpu().numpy())
+    _say(f"long routes: fft vs direct {err:.3e}, auto = {gpu_lib.attention_fwd_route(n, d, m)}")
+    assert err <= 2 * TOL["f32"], err
+    assert torch.equal(za, zf) or torch.equal(za, zd)
+
+
+def test_long_sequence_value_shift(gpu_lib):
+    """Adding a constant to every value shifts every output row by it (the rows
+    of Eq. (10) are convex combinations of the values), across block edges."""
+    B, H, n, d, m = 1, 1, 33000, 32, 64
+    dd = synth.custom(B, H, n, d, m, seed=73, bias="decay")
+    q, k, v, b, W = (to_gpu(dd[x]) for x in ("q", "k", "v", "b", "W"))
+    z0 = gpu_lib.attention_fwd(q, k, v, b, W, route="fft")
+    z1 = gpu_lib.attention_fwd(q, k, v + 3.0, b, W, route="fft")
+    err = rownorm_err((z1 - 3.0).cpu().numpy(), z0.cpu().numpy())
+    _say(f"long value shift: {err:.3e}")
+    assert err <= 2 * TOL["f32"], err
