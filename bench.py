@@ -216,30 +216,31 @@ def cpu_baseline_rows(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: 
     }, worst, done
 
 
-def sweep(lengths, ms, steps: int) -> int:
-    """Forward time against sequence length for one head with d = 64 (the paper's speed test
-    setting), each m, both routes; one JSON line per (n, m, route) on stdout."""
+def sweep(lengths, ms, heads, steps: int) -> int:
+    """Forward time against sequence length with d = 64 (the paper's speed test setting is one
+    head), each m and head count, both routes; one JSON line per (H, n, m, route) on stdout."""
     import torch
     from paper_2106_12566_amd import krpe, synth
     dev = torch.device("cuda", 0)
-    for n in lengths:
-        for m in ms:
-            dd = synth.custom(1, 1, n, 64, m, seed=n)
-            q, k, v, b, W = (torch.from_numpy(dd[x]).to(dev) for x in ("q", "k", "v", "b", "W"))
-            for rt in ("fft", "direct"):
-                ws = torch.empty(krpe.attention_fwd_workspace(1, 1, n, 64, m, route=rt), dtype=torch.uint8,
-                                 device=dev)
-                out = torch.empty_like(q)
+    for H, n, m in ((H, n, m) for H in heads for n in lengths for m in ms):
+        if H * n > 16 * 40000:       # keeps the direct route's share of the sweep to seconds
+            continue
+        dd = synth.custom(1, H, n, 64, m, seed=n)
+        q, k, v, b, W = (torch.from_numpy(dd[x]).to(dev) for x in ("q", "k", "v", "b", "W"))
+        for rt in ("fft", "direct"):
+            ws = torch.empty(krpe.attention_fwd_workspace(1, H, n, 64, m, route=rt), dtype=torch.uint8,
+                             device=dev)
+            out = torch.empty_like(q)
+            krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=rt)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
                 krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=rt)
-                torch.cuda.synchronize()
-                t0 = time.perf_counter()
-                for _ in range(steps):
-                    krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=rt)
-                torch.cuda.synchronize()
-                ms_call = 1e3 * (time.perf_counter() - t0) / steps
-                print(json.dumps({"n": n, "m": m, "route": rt, "ms": ms_call,
-                                  "auto": krpe.attention_fwd_route(n, 64, m)}), flush=True)
-                del ws
+            torch.cuda.synchronize()
+            ms_call = 1e3 * (time.perf_counter() - t0) / steps
+            print(json.dumps({"H": H, "n": n, "m": m, "route": rt, "ms": ms_call,
+                              "auto": krpe.attention_fwd_route(1, H, n, 64, m)}), flush=True)
+            del ws
     return 0
 
 
@@ -252,6 +253,7 @@ def main() -> int:
     ap.add_argument("--sweep", action="store_true",
                     help="instead: forward time against n (1k .. 40k), one head, d = 64, m = 32/64/128, "
                          "both routes, one JSON line each")
+    ap.add_argument("--sweep-heads", default="1", help="comma-separated head counts of the sweep")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
@@ -285,7 +287,8 @@ def main() -> int:
         return 1
     torch.cuda.set_device(0)
     if args.sweep:
-        return sweep([1000, 2000, 4000, 8000, 16000, 24000, 32000, 40000], [32, 64, 128], args.steps)
+        return sweep([1000, 2000, 4000, 8000, 16000, 24000, 32000, 40000], [32, 64, 128],
+                     [int(h) for h in args.sweep_heads.split(",")], args.steps)
 
     d = synth.make(args.workload)
     wl = d["workload"]
@@ -332,7 +335,7 @@ def main() -> int:
     tokens = B * n
     value = tokens / (ms_per_step * 1e-3)
 
-    route_used = krpe.attention_fwd_route(n, dd, m, nprf=args.nprf, features=fm, route=rt)
+    route_used = krpe.attention_fwd_route(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt)
     s_in = 2 if wl.qkv_dtype == "bf16" else 4
     if route_used == "fft":
         flops = conv_stage_flops(B, H, n, dd, M)

@@ -36,7 +36,10 @@
  *   any input or the workspace (KRPE_ERR_ALIAS).  Workspace contents are
  *   undefined on return.
  * - Supported sizes: 1 <= n <= 16384 (any n; the FFT length is 2N with N the
- *   next power of two >= n), 1 <= d <= 128, 1 <= m <= 1024, B, H >= 0, C >= 0.
+ *   next power of two >= n), except the attention forward pass
+ *   (krpe_attention_fwd*, krpe_feature_map*): 1 <= n <= 65536, longer
+ *   sequences taking the Toeplitz matrix in blocks of 16384 positions;
+ *   1 <= d <= 128, 1 <= m <= 1024, B, H >= 0, C >= 0.
  *   B*H == 0 (or C == 0) is a valid empty call that enqueues nothing.
  * - Precondition (not checked: it would need to read device memory): every
  *   query row's window of b holds a finite entry (b_0 finite suffices), so
@@ -165,9 +168,10 @@ size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsign
  * The route krpe_attention_fwd_ex takes for these sizes and option bits:
  * KRPE_ROUTE_DIRECT or KRPE_ROUTE_FFT (0 if the sizes or bits are invalid).
  * Without a route bit it follows a cost model of both routes measured on
- * MI355X; it counts all n^2 query/key pairs (b is not read on the host).
+ * MI355X (work over the B*H heads plus each route's fixed cost); it counts
+ * all n^2 query/key pairs (b is not read on the host).
  */
-int krpe_attention_fwd_route(int n, int d, int m, unsigned flags);
+int krpe_attention_fwd_route(int B, int H, int n, int d, int m, unsigned flags);
 
 /*
  * Kernelized attention with RPE, Section 3.2, Eq. (10), with phi from Eq. (5)

@@ -65,33 +65,39 @@ krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm, int ma
 
 constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT;
 
-// Whether the direct route is the faster one for one head of length n with M
+// Whether the direct route is the faster one for BH heads of length n with M
 // features and d value columns.  Cost model fitted to MI355X timings of both
-// routes (B H = 96, d = 64, M = 64 and 128, n = 128 .. 4096): the direct
-// route costs about 4.2e-14 s per (query, key) pair and unit of M + d + 1,
-// the FFT route about 2.0e-13 s per channel pair and point of a length-2N
-// transform times log2(2N), plus a fixed 2e-5 s per head-batch of launches.
-// All n^2 pairs are counted: the host does not read b, so a causal mask
-// (half the pairs) is not seen; KRPE_ROUTE_DIRECT forces the direct route.
-bool direct_is_faster(int n, int M, int d) {
+// routes (B H = 1, 4, 16, 96; d = 64; M = 32 .. 256; n = 128 .. 40000): each
+// route's time is its work over all heads at a measured rate plus a fixed
+// cost (the launch chain and its latency-bound small kernels).  Direct:
+// 3.8e-14 s per (query, key) pair and unit of M + d + 1, plus 6.5e-5 s.  FFT:
+// per channel pair, feature and point of the length-2N transform times
+// log2(2N), 2.2e-13 s up to N = 4096, 7.5e-13 s at N = 8192 (one work-group
+// per CU, twiddles re-read) and 3.5e-13 s at N = 16384, over the nb^2 block
+// pairs of a blocked sequence, plus 3.3e-4 s.  All n^2 pairs are counted: the
+// host does not read b, so a causal mask (half the pairs) is not seen; the
+// route bits force either route.
+bool direct_is_faster(long long BH, int n, int M, int d) {
   int l2 = 0;
   while ((1 << l2) < n) ++l2;
   // beyond one transform block the FFT route runs nb^2 block pairs
   const int nb = l2 > kMaxLog2N ? (n + (1 << kMaxLog2N) - 1) >> kMaxLog2N : 1;
   if (l2 > kMaxLog2N) l2 = kMaxLog2N;
   const double L = 2.0 * static_cast<double>(1 << l2);
-  const double direct = 4.2e-14 * static_cast<double>(n) * n * (M + d + 1);
-  const double fft = 2.0e-13 * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb;
+  const double heads = static_cast<double>(BH);
+  const double direct = 3.8e-14 * heads * static_cast<double>(n) * n * (M + d + 1) + 6.5e-5;
+  const double rate = l2 <= 12 ? 2.2e-13 : (l2 == 13 ? 7.5e-13 : 3.5e-13);
+  const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb + 3.3e-4;
   return direct < fft;
 }
 
 // Route of the forward pass: the FFT convolution (Sec. 3.2) or the direct
 // quadratic evaluation of Eq. (10) on MFMA, forced by an option bit or chosen
-// by the measured crossover (the direct route is faster for short sequences).
-bool use_direct(unsigned flags, int n, int M, int d) {
+// by the measured cost model (the direct route is faster for short sequences).
+bool use_direct(unsigned flags, long long BH, int n, int M, int d) {
   if (flags & KRPE_ROUTE_DIRECT) return true;
   if (flags & KRPE_ROUTE_FFT) return false;
-  return direct_is_faster(n, M, d);
+  return direct_is_faster(BH, n, M, d);
 }
 
 // Feature map selected by the option bits, and its number of features M
@@ -117,9 +123,22 @@ krpe_status_t record(void* const* events, int i, hipStream_t st) {
 
 }  // namespace
 
+// Feature splits of the forward convolution: the m features of a unit are
+// split into contiguous ranges (each its own partial result) until the launch
+// has about four units per CU, keeping at least 8 features per range.  Only
+// launches with few (batch, head) rows split.
+int conv_fsplit(int l2, int BH, int cols, int M, int nkb) {
+  if (l2 > kMaxLog2N) return 1;
+  const long long units = static_cast<long long>(conv_units(l2, BH, cols)) * nkb;
+  int fs = 1;
+  while (units * fs < 1024 && M / (2 * fs) >= 8) fs *= 2;
+  return fs;
+}
+
 AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   AttnLayout L{};
   L.l2 = log2_ceil(n);
+  L.fsplit = conv_fsplit(L.l2, B * H, d + 1, m, 1);
   const size_t N = static_cast<size_t>(1) << L.l2;
   const size_t bh = static_cast<size_t>(B) * H;
   const size_t cols = static_cast<size_t>(d) + 1, pairs = (cols + 1) / 2;
@@ -141,7 +160,8 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.vmax = take(bh * vmax_chunks(n) * static_cast<size_t>(d) * sizeof(float));
   L.x2 = take(bh * L.ksplit * m * pairs * sizeof(float));
   L.wb = take(bh * (static_cast<size_t>(m) + 1) * sizeof(float2));
-  L.part = take(bh * conv_splits(L.l2) * cols * n * sizeof(float));
+  L.part = take(bh * L.fsplit * conv_splits(L.l2) * cols * n * sizeof(float));
+  L.psum = take(L.fsplit > 1 ? bh * cols * n * sizeof(float) : 0);
   L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
@@ -189,6 +209,7 @@ LongLayout long_layout(int B, int H, int n, int d, int M) {
   const size_t bh = static_cast<size_t>(B) * H, nbk = static_cast<size_t>(L.nbk), nb = static_cast<size_t>(L.nb);
   const size_t cols = static_cast<size_t>(d) + 1, pairs = (cols + 1) / 2;
   L.ksplit = gram_splits(static_cast<int>(bh), M, L.nbk);
+  L.fsplit = conv_fsplit(kMaxLog2N, B * H, d + 1, M, L.nb);
   size_t off = 0;
   auto take = [&off](size_t bytes) {
     const size_t at = off;
@@ -197,10 +218,10 @@ LongLayout long_layout(int B, int H, int n, int d, int M) {
   };
   L.fix = take((bh + 1) * sizeof(unsigned));
   L.tw = take(2 * nbk * sizeof(float2));
-  L.hs = take(static_cast<size_t>(H) * 2 * nbk * sizeof(float2));
-  L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
+  L.hs = take(nb * H * 2 * nbk * sizeof(float2));
+  L.hnorm = take(nb * H * sizeof(float2));
   L.hunit = take(static_cast<size_t>(H) * sizeof(float2));
-  L.bwin = take(static_cast<size_t>(H) * (2 * nbk - 1) * sizeof(float));
+  L.bwin = take(nb * H * (2 * nbk - 1) * sizeof(float));
   L.phiq = take(bh * M * static_cast<size_t>(L.Ntot) * sizeof(float));
   L.phik = take(bh * M * static_cast<size_t>(L.Ntot) * sizeof(float));
   L.phiqb = take(nb * bh * M * nbk * sizeof(float));
@@ -211,8 +232,8 @@ LongLayout long_layout(int B, int H, int n, int d, int M) {
   L.x2 = take(bh * L.ksplit * M * pairs * sizeof(float));
   L.wbj = take(nb * bh * (static_cast<size_t>(M) + 1) * sizeof(float2));
   L.wbi = take(bh * (static_cast<size_t>(M) + 1) * sizeof(float2));
-  L.part = take(bh * conv_splits(kMaxLog2N) * cols * nbk * sizeof(float));
-  L.acc = take(bh * conv_splits(kMaxLog2N) * cols * nbk * sizeof(float));
+  L.part = take(bh * nb * L.fsplit * conv_splits(kMaxLog2N) * cols * nbk * sizeof(float));
+  L.psum = take(bh * cols * nbk * sizeof(float));
   L.zb = take(bh * nbk * d * sizeof(float));
   L.maskb = take(bh * (nbk / 64) * sizeof(unsigned long long));
   L.maskf = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
@@ -315,8 +336,8 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
                                   "column launch"))
     return s;
   if (krpe_status_t s = record(events, 2, st)) return s;
-  if (krpe_status_t s = hip_check(launch_conv(L.l2, phiq, phik, static_cast<long long>(M) * N, vsc, colmax, Hs, tw,
-                                              part, BHi, H, n, d + 1, M, st),
+  if (krpe_status_t s = hip_check(launch_conv_split(L.l2, phiq, phik, static_cast<long long>(M) * N, vsc, colmax, Hs,
+                                                    nullptr, tw, part, BHi, H, n, d + 1, M, 1, L.fsplit, st),
                                   "conv launch"))
     return s;
   if (krpe_status_t s = record(events, 3, st)) return s;
@@ -324,7 +345,18 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
     return s;
   if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, M, d, L.ksplit, st), "bound launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_combine(part, phiq, wb, hnorm, z, den_out, fix, fixmask, BHi, H, n, L.l2, d, M, st),
+  // feature splits: their partial results summed first, at full parallelism
+  const float* sums = part;
+  int nsum = conv_splits(L.l2);
+  if (L.fsplit > 1) {
+    float* psum = reinterpret_cast<float*>(w + L.psum);
+    if (krpe_status_t s = hip_check(launch_sum_splits(part, psum, BHi, d + 1, n, L.fsplit * nsum, st), "sum launch"))
+      return s;
+    sums = psum;
+    nsum = 1;
+  }
+  if (krpe_status_t s = hip_check(launch_combine(sums, phiq, wb, hnorm, z, den_out, fix, fixmask, BHi, H, n, L.l2, d, M,
+                                                 nsum, st),
                                   "combine launch"))
     return s;
   if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, den_out, fix, fixmask, fixpart, brange, BHi, H, n, N, d, M, st),
@@ -383,33 +415,27 @@ krpe_status_t run_forward_long(const LongLayout& L, char* w, const void* q, cons
   for (int I = 0; I < nb; ++I) {
     const int lenI = len_of(I);
     const float* pqb = F(L.phiqb) + static_cast<size_t>(I) * bhM * nbk;
-    for (int J = 0; J < nb; ++J) {
-      const float* pkb = F(L.phikb) + static_cast<size_t>(J) * bhM * nbk;
-      if (krpe_status_t s = hip_check(launch_bias_window(b, F(L.bwin), H, n, nbk, (J - I) * nbk, st), "bias launch"))
-        return s;
-      if (krpe_status_t s = hip_check(launch_spectrum(kMaxLog2N, F(L.bwin), F2(L.tw), F2(L.hs), F2(L.hnorm), H, nbk,
-                                                      st),
-                                      "spectrum launch"))
-        return s;
-      if (krpe_status_t s = hip_check(
-              launch_conv(kMaxLog2N, pqb, pkb, static_cast<long long>(M) * nbk,
-                          F2(L.vsc) + static_cast<size_t>(J) * BHi * pairs * nbk,
-                          F(L.colmax) + static_cast<size_t>(J) * BHi * cols, F2(L.hs), F2(L.tw), F(L.part), BHi, H,
-                          lenI, cols, M, st),
-              "conv launch"))
-        return s;
-      if (krpe_status_t s = hip_check(launch_accum(F(L.acc), F(L.part),
-                                                   static_cast<long long>(BHi) * splits * cols * lenI, J == 0, st),
-                                      "sum launch"))
-        return s;
-      if (krpe_status_t s = hip_check(launch_wb_accum(F2(L.wbi), F2(L.wbj) + static_cast<size_t>(J) * BHi * (M + 1),
-                                                      F2(L.hnorm), BHi, H, M, J == 0, st),
-                                      "weight launch"))
-        return s;
-    }
+    // the nb blocks of C in block row I: windows, spectra, then every key
+    // block in one convolution launch (blocks of C that are all zero skip)
+    if (krpe_status_t s = hip_check(launch_bias_window(b, F(L.bwin), H, n, nbk, nb, I, st), "bias launch")) return s;
+    if (krpe_status_t s = hip_check(launch_spectrum(kMaxLog2N, F(L.bwin), F2(L.tw), F2(L.hs), F2(L.hnorm), nb * H,
+                                                    nbk, st),
+                                    "spectrum launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_conv_split(kMaxLog2N, pqb, F(L.phikb), static_cast<long long>(M) * nbk,
+                                                      F2(L.vsc), F(L.colmax), F2(L.hs), F2(L.hnorm), F2(L.tw),
+                                                      F(L.part), BHi, H, lenI, cols, M, nb, L.fsplit, st),
+                                    "conv launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_wb_accum(F2(L.wbi), F2(L.wbj), F2(L.hnorm), BHi, H, M, nb, st),
+                                    "weight launch"))
+      return s;
     unsigned long long* maskb = reinterpret_cast<unsigned long long*>(w + L.maskb);
-    if (krpe_status_t s = hip_check(launch_combine(F(L.acc), pqb, F2(L.wbi), F2(L.hunit), F(L.zb), nullptr, fix, maskb,
-                                                   BHi, H, lenI, kMaxLog2N, d, M, st),
+    if (krpe_status_t s = hip_check(launch_sum_splits(F(L.part), F(L.psum), BHi, cols, lenI, nb * L.fsplit * splits, st),
+                                    "sum launch"))
+      return s;
+    if (krpe_status_t s = hip_check(launch_combine(F(L.psum), pqb, F2(L.wbi), F2(L.hunit), F(L.zb), nullptr, fix, maskb,
+                                                   BHi, H, lenI, kMaxLog2N, d, M, 1, st),
                                     "combine launch"))
       return s;
     if (krpe_status_t s = hip_check(launch_merge_mask(maskb, reinterpret_cast<unsigned long long*>(w + L.maskf), BHi,
@@ -435,7 +461,7 @@ using namespace krpe;
 
 extern "C" {
 
-int krpe_abi_version(void) { return 5; }
+int krpe_abi_version(void) { return 6; }
 
 const char* krpe_status_str(int s) {
   switch (s) {
@@ -541,7 +567,7 @@ size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsign
   if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLongLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
   int kind = kFeatPrf, M = m;
   if (feature_kind(flags, d, m, &kind, &M) != KRPE_OK) return 0;
-  return fwd_workspace(B, H, n, d, M, use_direct(flags, n, M, d));
+  return fwd_workspace(B, H, n, d, M, use_direct(flags, static_cast<long long>(B) * H, n, M, d));
 }
 
 size_t krpe_attention_fwd_workspace(int B, int H, int n, int d, int m) {
@@ -564,7 +590,7 @@ krpe_status_t krpe_attention_fwd_profiled(const void* q, const void* k, const vo
   if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(b) || (needW && misaligned(W)) ||
       misaligned(z) || misaligned(ws))
     return fail(KRPE_ERR_ALIGN, "all pointers must be 16-byte aligned");
-  const bool direct = use_direct(flags, n, M, d);
+  const bool direct = use_direct(flags, static_cast<long long>(B) * H, n, M, d);
   const size_t need = fwd_workspace(B, H, n, d, M, direct);
   if (!ws || ws_bytes < need) return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(need) + " bytes");
   const size_t qkv_bytes = bh * n * d * dtype_size(qkv_dtype);
@@ -601,11 +627,12 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
   return krpe_attention_fwd_profiled(q, k, v, qkv_dtype, b, W, z, B, H, n, d, m, 0u, ws, ws_bytes, stream, nullptr);
 }
 
-int krpe_attention_fwd_route(int n, int d, int m, unsigned flags) {
-  if (n < 1 || n > (1 << kMaxLongLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
+int krpe_attention_fwd_route(int B, int H, int n, int d, int m, unsigned flags) {
+  if (B < 1 || H < 1 || n < 1 || n > (1 << kMaxLongLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
   int kind = kFeatPrf, M = m;
   if (feature_kind(flags, d, m, &kind, &M) != KRPE_OK) return 0;
-  return use_direct(flags, n, M, d) ? static_cast<int>(KRPE_ROUTE_DIRECT) : static_cast<int>(KRPE_ROUTE_FFT);
+  return use_direct(flags, static_cast<long long>(B) * H, n, M, d) ? static_cast<int>(KRPE_ROUTE_DIRECT)
+                                                                   : static_cast<int>(KRPE_ROUTE_FFT);
 }
 
 size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned flags) {
@@ -674,7 +701,7 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
   const long long fstride = static_cast<long long>(m) * N, gstride = static_cast<long long>(d + 1) * N;
 
   // forward: phi(q), phi(k), z and the denominators
-  const bool direct = use_direct(flags, n, m, d);
+  const bool direct = use_direct(flags, static_cast<long long>(B) * H, n, m, d);
   if (krpe_status_t s = run_forward(L.f, w, q, k, v, bf16, b, W, zf, den, BHi, H, n, d, m, m, kFeatPrf, nprf, direct,
                                     st, nullptr))
     return s;

@@ -600,12 +600,23 @@ __device__ __forceinline__ void conv_split(int hs, const float* __restrict__ pk,
   }
 }
 
+// Work units: (bh, key block J < nkb, feature split fs < fsplit, class split
+// hs, column pair cp), unit-major in that order.  Key block J of a launch
+// reads phi(k), the column pairs and their scales at batch index J BH + bh
+// and the spectrum at J H + h; phi(q) at bh; the feature split takes features
+// [fs mf, fs mf + mf) of the m, mf = ceil(m / fsplit).  Unit (bh, J, fs, hs)
+// writes its own partial result, split index (J fsplit + fs) HSPLIT + hs of
+// row bh, so the nkb fsplit HSPLIT partials of a row sum to the product.
+// With nkb = fsplit = 1 this is one (bh, hs) per unit.  When hnorm is given,
+// a unit whose spectrum has ||h||_1 = 0 (an all-zero block of C) skips the
+// transforms and writes zeros.
 template <int L2>
 __global__ __launch_bounds__(Conf<L2>::THREADS) __attribute__((amdgpu_waves_per_eu(Conf<L2>::WPE))) void
 k_conv_contract(
     const float* __restrict__ phiq, const float* __restrict__ phik, long long phi_bh_stride,
     const float2* __restrict__ vsc, const float* __restrict__ colmax, const float2* __restrict__ Hs,
-    const float2* __restrict__ tw, float* __restrict__ part, int H, int n, int cols, int m, int units) {
+    const float2* __restrict__ hnorm, const float2* __restrict__ tw, float* __restrict__ part, int BH, int H, int n,
+    int cols, int m, int nkb, int fsplit, int units) {
   using C = Conf<L2>;
   using F = typename C::F;
   constexpr int KH = C::KH, FOLD = C::FOLD;
@@ -615,33 +626,40 @@ k_conv_contract(
   const int g = C::G == 1 ? 0 : threadIdx.x / F::T, tau = C::G == 1 ? threadIdx.x : threadIdx.x % F::T;
   const int pairs = (cols + 1) / 2;
   // Column pairs are padded to a multiple of G, so that the units of one
-  // work-group share (bh, hs): they run the same class split (same barriers).
+  // work-group share (bh, J, fs, hs): they run the same class split (same
+  // barriers) and the same number of features.
   const int pairs_p = (pairs + C::G - 1) / C::G * C::G;
   const int unit = xcd_block(blockIdx.x, gridDim.x) * C::G + g;
   int cp = unit % pairs_p;
   const int rest = unit / pairs_p;
   const bool active = unit < units && cp < pairs;
   if (cp >= pairs) cp = pairs - 1;  // padding unit: keeps the barriers uniform, results discarded
-  const int hs = rest % C::HSPLIT, bh = rest / C::HSPLIT, h = bh % H;
+  const int hs = rest % C::HSPLIT, vb = rest / C::HSPLIT;
+  const int fs = vb % fsplit, jb = vb / fsplit;
+  const int J = jb % nkb, bh = jb / nkb, h = bh % H;
+  const int kb = J * BH + bh, hw = J * H + h;
+  const int mf = (m + fsplit - 1) / fsplit, l0 = fs * mf;
+  const int mcount = m - l0 < mf ? m - l0 : mf;
   const int c0 = 2 * cp, c1 = 2 * cp + 1;
   float2* lds = lds_all + g * (F::P > 1 ? KH * F::LDS : 0);
-  const float2* __restrict__ vrow = vsc + (static_cast<size_t>(bh) * pairs + cp) * C::N;
+  const float2* __restrict__ vrow = vsc + (static_cast<size_t>(kb) * pairs + cp) * C::N;
 
-  const float2* __restrict__ Hh = Hs + (static_cast<size_t>(h) * C::S + hs * KH) * F::N;
+  const float2* __restrict__ Hh = Hs + (static_cast<size_t>(hw) * C::S + hs * KH) * F::N;
   float acc0[FOLD][F::R], acc1[FOLD][F::R];
 #pragma unroll
   for (int q = 0; q < FOLD; ++q)
 #pragma unroll
     for (int i = 0; i < F::R; ++i) acc0[q][i] = acc1[q][i] = 0.f;
 
-  const float* __restrict__ pk = phik + bh * phi_bh_stride;
-  const float* __restrict__ pq = phiq + bh * phi_bh_stride;
-  conv_split<C>(hs, pk, pq, vrow, tw, Hh, lds, tau, m, acc0, acc1);
+  const float* __restrict__ pk = phik + kb * phi_bh_stride + static_cast<size_t>(l0) * C::N;
+  const float* __restrict__ pq = phiq + bh * phi_bh_stride + static_cast<size_t>(l0) * C::N;
+  const bool live = mcount > 0 && (hnorm == nullptr || hnorm[hw].x != 0.f);
+  if (live) conv_split<C>(hs, pk, pq, vrow, tw, Hh, lds, tau, mcount, acc0, acc1);
 
   if (active) {
-    const float s0 = colmax[static_cast<size_t>(bh) * cols + c0];
-    const float s1 = c1 < cols ? colmax[static_cast<size_t>(bh) * cols + c1] : 0.f;
-    float* __restrict__ out = part + ((static_cast<size_t>(bh) * C::HSPLIT + hs) * cols + c0) * n;
+    const float s0 = colmax[static_cast<size_t>(kb) * cols + c0];
+    const float s1 = c1 < cols ? colmax[static_cast<size_t>(kb) * cols + c1] : 0.f;
+    float* __restrict__ out = part + ((static_cast<size_t>(vb) * C::HSPLIT + hs) * cols + c0) * n;
 #pragma unroll
     for (int q = 0; q < FOLD; ++q)
 #pragma unroll
@@ -1279,8 +1297,15 @@ __global__ void k_sum_splits(const float* __restrict__ part, float* __restrict__
   if (e >= total) return;
   const long long per = static_cast<long long>(C) * n;
   const long long bh = e / per, r = e % per;
+  // independent loads in flight (sums in split order, as a plain loop)
+  const float* __restrict__ p = part + bh * nsplit * per + r;
   float s = 0.f;
-  for (int sp = 0; sp < nsplit; ++sp) s += part[(bh * nsplit + sp) * per + r];
+  int sp = 0;
+  for (; sp + 4 <= nsplit; sp += 4) {
+    const float a0 = p[sp * per], a1 = p[(sp + 1) * per], a2 = p[(sp + 2) * per], a3 = p[(sp + 3) * per];
+    s = (((s + a0) + a1) + a2) + a3;
+  }
+  for (; sp < nsplit; ++sp) s += p[sp * per];
   y[e] = s;
 }
 
@@ -1468,14 +1493,15 @@ hipError_t spectrum_l2(const float* b, const float2* tw, float2* Hs, float2* hno
 
 template <int L2>
 hipError_t conv_l2(const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
-                   const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
-                   int cols, int m, hipStream_t st) {
+                   const float* colmax, const float2* Hs, const float2* hnorm, const float2* tw, float* part, int BH,
+                   int H, int n, int cols, int m, int nkb, int fsplit, hipStream_t st) {
   using C = Conf<L2>;
   const int pairs_p = ((cols + 1) / 2 + C::G - 1) / C::G * C::G;
-  const long long units = static_cast<long long>(BH) * C::HSPLIT * pairs_p;
+  const long long units = static_cast<long long>(BH) * nkb * fsplit * C::HSPLIT * pairs_p;
   const long long blocks = units / C::G;
   hipLaunchKernelGGL(k_conv_contract<L2>, dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0, st, phiq, phik,
-                     phi_bh_stride, vsc, colmax, Hs, tw, part, H, n, cols, m, static_cast<int>(units));
+                     phi_bh_stride, vsc, colmax, Hs, hnorm, tw, part, BH, H, n, cols, m, nkb, fsplit,
+                     static_cast<int>(units));
   return hipGetLastError();
 }
 
@@ -1623,7 +1649,22 @@ int vmax_chunks(int n) { return (n + kVmaxChunk - 1) / kVmaxChunk; }
 hipError_t launch_conv(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
                        const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
                        int cols, int m, hipStream_t st) {
-  return dispatch<ConvFn>(l2, phiq, phik, phi_bh_stride, vsc, colmax, Hs, tw, part, BH, H, n, cols, m, st);
+  return dispatch<ConvFn>(l2, phiq, phik, phi_bh_stride, vsc, colmax, Hs, static_cast<const float2*>(nullptr), tw,
+                          part, BH, H, n, cols, m, 1, 1, st);
+}
+
+hipError_t launch_conv_split(int l2, const float* phiq, const float* phik, long long phi_bh_stride,
+                             const float2* vsc, const float* colmax, const float2* Hs, const float2* hnorm,
+                             const float2* tw, float* part, int BH, int H, int n, int cols, int m, int nkb,
+                             int fsplit, hipStream_t st) {
+  return dispatch<ConvFn>(l2, phiq, phik, phi_bh_stride, vsc, colmax, Hs, hnorm, tw, part, BH, H, n, cols, m, nkb,
+                          fsplit, st);
+}
+
+int conv_units(int l2, int BH, int cols) {
+  int hsplit = 2;
+  (void)dispatch<SplitFn>(l2, &hsplit);
+  return BH * hsplit * ((cols + 1) / 2);
 }
 
 hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, int m, int N, int pairs,
@@ -1645,13 +1686,12 @@ hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb
 
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
                           float* den_out, unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2,
-                          int d, int m, hipStream_t st) {
+                          int d, int m, int nsplit, hipStream_t st) {
   const int tiles_n = (n + 63) / 64;
   const size_t lds = (static_cast<size_t>((d + 1) * 65 + 1) & ~static_cast<size_t>(1)) * sizeof(float) +
                      static_cast<size_t>(m + 1) * sizeof(float2);
   hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), lds, st,
-                     part, phiq, Wb, hnorm, z, den_out, fix, fixmask, BH, H, n, 1 << l2, l2, d, m, conv_splits(l2),
-                     tiles_n);
+                     part, phiq, Wb, hnorm, z, den_out, fix, fixmask, BH, H, n, 1 << l2, l2, d, m, nsplit, tiles_n);
   return hipGetLastError();
 }
 

@@ -12,6 +12,7 @@ namespace krpe {
 struct AttnLayout {
   int l2;            // log2 N, N = next power of two >= n
   int ksplit;        // position slices of the channel-norm products
+  int fsplit;        // feature splits of the convolution (conv_fsplit)
   size_t tw;         // float2 [2N]              W_{2N}^k
   size_t hs;         // float2 [H][S][2N/S]      spectrum of c by residue class, / 2N
   size_t hnorm;      // float2 [H]               (||h||_1, ||h||_2)
@@ -22,7 +23,8 @@ struct AttnLayout {
   size_t vmax;       // float  [BH][chunks][d]   column maxima per chunk of positions
   size_t x2;         // float  [BH][ks][m][pairs] squared norms of the packed channels
   size_t wb;         // float2 [BH][m+1]         bound weights of the certification
-  size_t part;       // float  [BH][splits][d+1][n] numerators / denominator per class split
+  size_t part;       // float  [BH][fsplit][splits][d+1][n] numerators / denominator per feature and class split
+  size_t psum;       // float  [BH][d+1][n]      their sums (fsplit > 1 only)
   size_t fix;        // uint   [BH + 1]          rows queued per head, then their total
   size_t fixmask;    // uint64 [BH][ceil(n/64)]  queued rows: bit i % 64 of word i / 64
   size_t fixpart;    // double [BH][slots][32][d+1] key-share partial sums of the exact rows
@@ -55,12 +57,13 @@ BwdLayout bwd_layout(int B, int H, int n, int d, int M);
 // Workspace of krpe_attention_fwd for n > 2^kMaxLog2N on the FFT route
 // (blocks of nbk positions, nb blocks, Ntot = nb nbk).
 struct LongLayout {
-  int nb, nbk, Ntot, ksplit;
+  int nb, nbk, Ntot, ksplit, fsplit;
   size_t fix;          // uint   [BH + 1]          (first, as in AttnLayout)
   size_t tw;           // float2 [2 nbk]
-  size_t hs;           // float2 [H][2 nbk]       spectrum of one block pair
-  size_t hnorm, hunit; // float2 [H]              its norms; ones
-  size_t bwin;         // float  [H][2 nbk - 1]   its bias window
+  size_t hs;           // float2 [nb][H][2 nbk]   spectra of query block I against each key block
+  size_t hnorm;        // float2 [nb][H]          their norms
+  size_t hunit;        // float2 [H]              ones
+  size_t bwin;         // float  [nb][H][2 nbk - 1] their bias windows
   size_t phiq, phik;   // float  [BH][M][Ntot]    whole sequence (exact rows)
   size_t phiqb, phikb; // float  [nb][BH][M][nbk] per block
   size_t vsc;          // float2 [nb][BH][pairs][nbk]
@@ -68,7 +71,8 @@ struct LongLayout {
   size_t vmax;         // float  [BH][chunks][d]
   size_t x2;           // float  [BH][ks][M][pairs]
   size_t wbj, wbi;     // float2 [nb][BH][M+1], [BH][M+1]
-  size_t part, acc;    // float  [BH][splits][d+1][nbk]
+  size_t part;         // float  [BH][nb][fsplit][splits][d+1][nbk]
+  size_t psum;         // float  [BH][d+1][nbk]   their sums
   size_t zb;           // float  [BH][nbk][d]
   size_t maskb, maskf; // uint64 [BH][nbk/64], [BH][ceil(n/64)]
   size_t fixpart;      // double [BH][slots][32][d+1]
@@ -76,6 +80,8 @@ struct LongLayout {
   size_t total;
 };
 LongLayout long_layout(int B, int H, int n, int d, int M);
+// Feature splits of a forward convolution launch over nkb key blocks.
+int conv_fsplit(int l2, int BH, int cols, int M, int nkb);
 
 // Workspace of krpe_toeplitz_conv.
 struct ConvLayout {
@@ -85,6 +91,8 @@ struct ConvLayout {
 ConvLayout conv_layout(int B, int H, int C, int n);
 
 int conv_splits(int l2);
+// Work units of one launch_conv at these sizes (no key blocks, no feature split).
+int conv_units(int l2, int BH, int cols);
 int gram_splits(int BH, int m, int N);
 
 hipError_t launch_twiddles(float2* tw, int l2, hipStream_t st);
@@ -106,14 +114,22 @@ hipError_t launch_vprep(bool bf16, const void* v, long long sp, long long sc, lo
 hipError_t launch_conv(int l2, const float* phiq, const float* phik, long long phi_bh_stride, const float2* vsc,
                        const float* colmax, const float2* Hs, const float2* tw, float* part, int BH, int H, int n,
                        int cols, int m, hipStream_t st);
+// launch_conv over nkb key blocks and fsplit feature splits (the unit layout
+// of k_conv_contract); hnorm (or nullptr) lets all-zero blocks of C skip.
+hipError_t launch_conv_split(int l2, const float* phiq, const float* phik, long long phi_bh_stride,
+                             const float2* vsc, const float* colmax, const float2* Hs, const float2* hnorm,
+                             const float2* tw, float* part, int BH, int H, int n, int cols, int m, int nkb,
+                             int fsplit, hipStream_t st);
 hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, int m, int N, int pairs,
                        int ksplit, hipStream_t st);
 // Wb[bh][l] = (A_l, D_l) for l < m, Wb[bh][m] = (max column scale, 0) from the channel norms.
 hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb, int BH, int m, int d, int ksplit,
                                 hipStream_t st);
+// nsplit: partial results per (bh) row of part (conv_splits(l2) times the
+// key blocks and feature splits of the convolution launch).
 hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb, const float2* hnorm, float* z,
                           float* den_out, unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2,
-                          int d, int m, hipStream_t st);
+                          int d, int m, int nsplit, hipStream_t st);
 // Work-group slots per head of the exact-row kernels, and their partial sums:
 // fixpart holds BH * fix_slots(BH) * 32 * (d + 1) doubles.
 int fix_slots(int BH);
@@ -125,9 +141,8 @@ hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
 // Long sequences (long_seq.hip): block copies of phi rows, bias windows of a
 // block pair, sums over key blocks, certification weights, row masks, rows.
 hipError_t launch_block_rows(const float* src, float* dst, int BH, int R, int nbk, int Ntot, int K, hipStream_t st);
-hipError_t launch_bias_window(const float* b, float* out, int H, int n, int nbk, int off, hipStream_t st);
-hipError_t launch_accum(float* acc, const float* part, long long count, bool first, hipStream_t st);
-hipError_t launch_wb_accum(float2* wbI, const float2* wbJ, const float2* hnorm, int BH, int H, int M, bool first,
+hipError_t launch_bias_window(const float* b, float* out, int H, int n, int nbk, int nb, int I, hipStream_t st);
+hipError_t launch_wb_accum(float2* wbI, const float2* wbJ, const float2* hnorm, int BH, int H, int M, int nb,
                            hipStream_t st);
 hipError_t launch_merge_mask(const unsigned long long* blk, unsigned long long* full, int BH, int tiles_b,
                              int tiles_full, int K, int nbk, hipStream_t st);

@@ -4,10 +4,10 @@
 // queries of block I and is itself Toeplitz, with entries c_{j - i + (J - I) nbk},
 // i.e. the bias window b[(J - I) nbk - (nbk - 1) .. (J - I) nbk + (nbk - 1)].  The
 // numerators and denominator of Eq. (10) of query block I are the sums over J
-// of the blockwise products, each one run of the convolution kernel.  These
-// are the helpers around those runs: block copies of phi, the bias windows,
-// the sums over J, the certification weights summed over J, and the
-// scattering of the block results.  In a translation unit of their own so
+// of the blockwise products, all J in one run of the convolution kernel (one
+// partial result per J, summed by the combine kernel).  These are the helpers
+// around those runs: block copies of phi, the bias windows, the certification
+// weights summed over J, and the scattering of the block results.  In a translation unit of their own so
 // that the convolution kernel's code generation does not change with them.
 #include <hip/hip_runtime.h>
 
@@ -28,41 +28,42 @@ __global__ void k_block_rows(const float* __restrict__ src, float* __restrict__ 
   dst[e] = src[row * Ntot + static_cast<long long>(K) * nbk + i];
 }
 
-// out[h][s] = b_t with t = s - (nbk - 1) + off for s < 2 nbk - 1, -inf where t
-// is outside (-n, n) (such offsets pair no real query with a real key).
-__global__ void k_bias_window(const float* __restrict__ b, float* __restrict__ out, int n, int nbk, int off,
+// Bias windows of query block I against every key block J < nb:
+// out[J][h][s] = b_t with t = s - (nbk - 1) + (J - I) nbk for s < 2 nbk - 1,
+// -inf where t is outside (-n, n) (such offsets pair no real query with a
+// real key).
+__global__ void k_bias_window(const float* __restrict__ b, float* __restrict__ out, int H, int n, int nbk, int I,
                               long long total) {
   const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (e >= total) return;
-  const long long len = 2LL * nbk - 1, h = e / len, s = e - h * len;
-  const long long t = s - (nbk - 1) + off;
+  const long long len = 2LL * nbk - 1, w = e / len, s = e - w * len;
+  const long long J = w / H, h = w % H;
+  const long long t = s - (nbk - 1) + (J - I) * nbk;
   out[e] = (t > -n && t < n) ? b[h * (2LL * n - 1) + t + n - 1] : -INFINITY;
 }
 
-// acc = part (first) or acc + part.
-__global__ void k_accum(float* __restrict__ acc, const float* __restrict__ part, long long count, int first) {
-  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (e >= count) return;
-  acc[e] = first ? part[e] : acc[e] + part[e];
-}
-
-// Certification weights of query block I summed over key blocks J: the FFT
-// error of block (I, J) scales with ||h_IJ||_2 (hnorm[h].y) times the channel
-// norms of key block J (wbJ), so wbI[bh][l] = sum_J ||h_IJ|| wbJ[bh][l] for
-// l < M, and wbI[bh][M] (the largest column scale) is the maximum over J.
+// Certification weights of query block I summed over the key blocks J: the
+// FFT error of block (I, J) scales with ||h_IJ||_2 (hnorm[J H + h].y) times
+// the channel norms of key block J (wbJ[J]), so
+// wbI[bh][l] = sum_J ||h_IJ|| wbJ[J][bh][l] for l < M, and wbI[bh][M] (the
+// largest column scale) is the maximum over J.
 __global__ void k_wb_accum(float2* __restrict__ wbI, const float2* __restrict__ wbJ, const float2* __restrict__ hnorm,
-                           int BH, int H, int M, int first) {
+                           int BH, int H, int M, int nb) {
   const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (e >= static_cast<long long>(BH) * (M + 1)) return;
+  const long long per = static_cast<long long>(BH) * (M + 1);
+  if (e >= per) return;
   const int bh = static_cast<int>(e / (M + 1)), l = static_cast<int>(e % (M + 1));
-  const float2 w = wbJ[e];
-  if (l < M) {
-    const float hn = hnorm[bh % H].y;
-    const float2 v = make_float2(w.x * hn, w.y * hn);
-    wbI[e] = first ? v : make_float2(wbI[e].x + v.x, wbI[e].y + v.y);
-  } else {
-    wbI[e] = first ? w : make_float2(fmaxf(wbI[e].x, w.x), 0.f);
+  float2 acc = make_float2(0.f, 0.f);
+  for (int J = 0; J < nb; ++J) {
+    const float2 w = wbJ[J * per + e];
+    if (l < M) {
+      const float hn = hnorm[J * H + bh % H].y;
+      acc = make_float2(fmaf(w.x, hn, acc.x), fmaf(w.y, hn, acc.y));
+    } else {
+      acc.x = fmaxf(acc.x, w.x);
+    }
   }
+  wbI[e] = acc;
 }
 
 // full[bh][K nbk / 64 + t] = blk[bh][t], t < tiles_b: the queued rows of block K
@@ -101,21 +102,16 @@ hipError_t launch_block_rows(const float* src, float* dst, int BH, int R, int nb
   return hipGetLastError();
 }
 
-hipError_t launch_bias_window(const float* b, float* out, int H, int n, int nbk, int off, hipStream_t st) {
-  const long long total = static_cast<long long>(H) * (2LL * nbk - 1);
-  hipLaunchKernelGGL(k_bias_window, dim3(grid_of(total)), dim3(256), 0, st, b, out, n, nbk, off, total);
+hipError_t launch_bias_window(const float* b, float* out, int H, int n, int nbk, int nb, int I, hipStream_t st) {
+  const long long total = static_cast<long long>(nb) * H * (2LL * nbk - 1);
+  hipLaunchKernelGGL(k_bias_window, dim3(grid_of(total)), dim3(256), 0, st, b, out, H, n, nbk, I, total);
   return hipGetLastError();
 }
 
-hipError_t launch_accum(float* acc, const float* part, long long count, bool first, hipStream_t st) {
-  hipLaunchKernelGGL(k_accum, dim3(grid_of(count)), dim3(256), 0, st, acc, part, count, first ? 1 : 0);
-  return hipGetLastError();
-}
-
-hipError_t launch_wb_accum(float2* wbI, const float2* wbJ, const float2* hnorm, int BH, int H, int M, bool first,
+hipError_t launch_wb_accum(float2* wbI, const float2* wbJ, const float2* hnorm, int BH, int H, int M, int nb,
                            hipStream_t st) {
   const long long total = static_cast<long long>(BH) * (M + 1);
-  hipLaunchKernelGGL(k_wb_accum, dim3(grid_of(total)), dim3(256), 0, st, wbI, wbJ, hnorm, BH, H, M, first ? 1 : 0);
+  hipLaunchKernelGGL(k_wb_accum, dim3(grid_of(total)), dim3(256), 0, st, wbI, wbJ, hnorm, BH, H, M, nb);
   return hipGetLastError();
 }
 

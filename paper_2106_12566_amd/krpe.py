@@ -81,7 +81,7 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_attention_fwd_profiled.argtypes = [vp, vp, vp, i, fp, fp, fp, i, i, i, i, i, ctypes.c_uint, vp, sz,
                                                 vp, ctypes.POINTER(ctypes.c_void_p)]
     lib.krpe_attention_fwd_route.restype = i
-    lib.krpe_attention_fwd_route.argtypes = [i, i, i, ctypes.c_uint]
+    lib.krpe_attention_fwd_route.argtypes = [i, i, i, i, i, ctypes.c_uint]
     lib.krpe_attention_bwd_workspace.restype = sz
     lib.krpe_attention_bwd_workspace.argtypes = [i, i, i, i, i, ctypes.c_uint]
     lib.krpe_attention_bwd.restype = i
@@ -252,10 +252,10 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     return out
 
 
-def attention_fwd_route(n: int, d: int, m: int, nprf: bool = False, features: str = "prf",
+def attention_fwd_route(B: int, H: int, n: int, d: int, m: int, nprf: bool = False, features: str = "prf",
                         route: str = "auto") -> str:
     """The route ("direct" or "fft") attention_fwd takes for these sizes and options."""
-    r = int(load().krpe_attention_fwd_route(n, d, m, _flags(nprf, features, route)))
+    r = int(load().krpe_attention_fwd_route(B, H, n, d, m, _flags(nprf, features, route)))
     if r == 0:
         raise KrpeError("invalid sizes or options")
     return "direct" if r == ROUTE_DIRECT else "fft"

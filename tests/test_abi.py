@@ -51,7 +51,7 @@ def test_library_exports_every_declared_symbol(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert lib.krpe_abi_version() == 5
+    assert lib.krpe_abi_version() == 6
     for s in range(9):
         assert lib.krpe_status_str(s)
     assert lib.krpe_status_str(99) == b"unknown status"
@@ -203,11 +203,13 @@ def test_backward_validation(lib):
 def test_route_query(lib):
     """Route choice: forced by the option bits, else the cost model (direct for short sequences)."""
     route = lib.krpe_attention_fwd_route
-    assert route(4096, 64, 128, 8) == 8 and route(128, 64, 64, 16) == 16
-    assert route(128, 64, 64, 0) == 8                 # short: direct
-    assert route(512, 64, 64, 0) == 8
-    assert route(4096, 64, 128, 0) == 16              # the long-n4096 head: FFT
-    assert route(16384, 64, 256, 0) == 16
-    assert route(40000, 64, 64, 0) in (8, 16) and route(65536, 64, 128, 16) == 16
-    assert route(65537, 64, 64, 0) == 0
-    assert route(8, 4, 4, 8 | 16) == 0 and route(0, 4, 4, 0) == 0 and route(8, 4, 3, 4) == 0
+    assert route(8, 12, 4096, 64, 128, 8) == 8 and route(8, 12, 128, 64, 64, 16) == 16
+    assert route(8, 12, 128, 64, 64, 0) == 8            # short: direct
+    assert route(8, 12, 512, 64, 64, 0) == 8
+    assert route(8, 12, 4096, 64, 128, 0) == 16         # the long-n4096 layer: FFT
+    assert route(1, 16, 16384, 64, 256, 0) == 16
+    assert route(1, 1, 1000, 64, 64, 0) == 8            # one head: the FFT route's fixed cost dominates
+    assert route(1, 1, 40000, 64, 128, 0) == 16 and route(1, 16, 65536, 64, 256, 0) == 16
+    assert route(1, 1, 65536, 64, 128, 8) == 8          # forced, past one transform block
+    assert route(1, 1, 65537, 64, 64, 0) == 0 and route(0, 1, 8, 4, 4, 0) == 0
+    assert route(1, 1, 8, 4, 4, 8 | 16) == 0 and route(1, 1, 0, 4, 4, 0) == 0 and route(1, 1, 8, 4, 3, 4) == 0

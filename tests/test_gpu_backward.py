@@ -53,6 +53,7 @@ CASES = [
     (1, 1, 1000, 32, 16, "f32", "causal", False),
     (1, 1, 2048, 64, 32, "f32", "normal", False),
     (1, 1, 4096, 64, 128, "f32", "normal", False),  # the long-n4096 head shape
+    (1, 1, 5000, 64, 16, "f32", "causal", False),   # N = 8192: two-fold residue classes
     (2, 2, 256, 64, 32, "f32", "normal", True),
     (1, 1, 1000, 64, 64, "bf16", "causal", True),
     (1, 1, 1025, 128, 40, "f32", "decay", True),   # d = 128, just past a power of two

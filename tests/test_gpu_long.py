@@ -75,7 +75,7 @@ def test_long_sequence_routes_agree(gpu_lib):
     zd = gpu_lib.attention_fwd(q, k, v, b, W, route="direct")
     za = gpu_lib.attention_fwd(q, k, v, b, W)
     err = rownorm_err(zf.cpu().numpy(), zd.cpu().numpy())
-    _say(f"long routes: fft vs direct {err:.3e}, auto = {gpu_lib.attention_fwd_route(n, d, m)}")
+    _say(f"long routes: fft vs direct {err:.3e}, auto = {gpu_lib.attention_fwd_route(B, H, n, d, m)}")
     assert err <= 2 * TOL["f32"], err
     assert torch.equal(za, zf) or torch.equal(za, zd)
 

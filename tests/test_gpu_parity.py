@@ -79,7 +79,7 @@ def test_toeplitz_conv_matches_direct_product(gpu_lib, B, H, C, n, sigma):
     assert err <= 2e-4, err
 
 
-@pytest.mark.parametrize("n", [5, 64, 1000, 4096])
+@pytest.mark.parametrize("n", [5, 64, 1000, 4096, 8000])
 def test_toeplitz_special_cases(gpu_lib, n):
     """Identity, shift, full sum and cumulative sum (textbook routines)."""
     _say(f"toeplitz special n={n}")
