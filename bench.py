@@ -44,19 +44,29 @@ def direct_flops(B: int, H: int, n: int, d: int, m: int, b: np.ndarray) -> float
 BLOCK = 16384   # longest sequence one transform covers; longer ones run in blocks
 
 
-def conv_stage_flops(B: int, H: int, n: int, d: int, m: int) -> float:
+def conv_stage_flops(B: int, H: int, n: int, d: int, m: int, b: np.ndarray | None = None) -> float:
     """Algorithmic flops of the FFT convolution + contraction stage.
 
     Per channel (m (d+1) channels per head): two real FFTs of length L = 2n at
     2.5 L log2 L flops each, the pointwise complex product with the spectrum
     over n + 1 bins (6 flops each), forming the channel (1 multiply per
     position) and the contraction with phi(q) (1 multiply-add per position).
-    For n > BLOCK, nb^2 block pairs (nb = ceil(n / BLOCK)) of that count at
-    n = BLOCK, the work the blocked Toeplitz product performs.
+    For n > BLOCK, that count at n = BLOCK for every block pair (I, J) of the
+    blocked Toeplitz product (nb = ceil(n / BLOCK) blocks each way) whose
+    window of b holds a finite entry (the kernel skips the others), per head.
     """
     if n > BLOCK:
         nb = -(-n // BLOCK)
-        return nb * nb * conv_stage_flops(B, H, BLOCK, d, m)
+        pair = conv_stage_flops(B, 1, BLOCK, d, m)
+        live = 0
+        for h in range(H):
+            fin = np.isfinite(b[h]) if b is not None else np.ones(2 * n - 1, bool)
+            for D in range(-(nb - 1), nb):
+                lo = max(D * BLOCK - (BLOCK - 1), -(n - 1))
+                hi = min(D * BLOCK + (BLOCK - 1), n - 1)
+                if lo <= hi and fin[lo + n - 1:hi + n].any():
+                    live += nb - abs(D)
+        return live * pair
     L = 2 * n
     per_channel = 5.0 * L * math.log2(L) + 6.0 * (n + 1) + 4.0 * n
     return B * H * m * (d + 1) * per_channel
@@ -338,7 +348,7 @@ def main() -> int:
     route_used = krpe.attention_fwd_route(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt)
     s_in = 2 if wl.qkv_dtype == "bf16" else 4
     if route_used == "fft":
-        flops = conv_stage_flops(B, H, n, dd, M)
+        flops = conv_stage_flops(B, H, n, dd, M, d["b"])
         conv_ms = stages["conv_contract"]
         conv_gbs = conv_stage_bytes(B, H, n, dd, M, s_in) / (conv_ms * 1e-3) / 1e9
         roof = {"bound": "alu", "kernel": "k_conv_contract"}
