@@ -72,8 +72,8 @@ constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRP
 // cost (the launch chain and its latency-bound small kernels).  Direct:
 // 3.8e-14 s per (query, key) pair and unit of M + d + 1, plus 6.5e-5 s.  FFT:
 // per channel pair, feature and point of the length-2N transform times
-// log2(2N), 2.2e-13 s up to N = 4096, 7.5e-13 s at N = 8192 (one work-group
-// per CU, twiddles re-read) and 3.5e-13 s at N = 16384, over the nb^2 block
+// log2(2N), 2.2e-13 s up to N = 4096, 5.0e-13 s at N = 8192 (its units keep
+// nothing in registers across features) and 3.5e-13 s at N = 16384, over the nb^2 block
 // pairs of a blocked sequence, plus 3.3e-4 s.  All n^2 pairs are counted: the
 // host does not read b, so a causal mask (half the pairs) is not seen; the
 // route bits force either route.
@@ -86,7 +86,7 @@ bool direct_is_faster(long long BH, int n, int M, int d) {
   const double L = 2.0 * static_cast<double>(1 << l2);
   const double heads = static_cast<double>(BH);
   const double direct = 3.8e-14 * heads * static_cast<double>(n) * n * (M + d + 1) + 6.5e-5;
-  const double rate = l2 <= 12 ? 2.2e-13 : (l2 == 13 ? 7.5e-13 : 3.5e-13);
+  const double rate = l2 <= 12 ? 2.2e-13 : (l2 == 13 ? 5.0e-13 : 3.5e-13);
   const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb + 3.3e-4;
   return direct < fft;
 }
@@ -150,7 +150,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
     return at;
   };
   L.fix = take((bh + 1) * sizeof(unsigned));  // first: its offset does not depend on the sizes
-  L.tw = take(2 * N * sizeof(float2));
+  L.tw = take(static_cast<size_t>(twiddle_slots(L.l2)) * sizeof(float2));
   L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
   L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
   L.phiq = take(bh * m * N * sizeof(float));
@@ -217,7 +217,7 @@ LongLayout long_layout(int B, int H, int n, int d, int M) {
     return at;
   };
   L.fix = take((bh + 1) * sizeof(unsigned));
-  L.tw = take(2 * nbk * sizeof(float2));
+  L.tw = take(static_cast<size_t>(twiddle_slots(kMaxLog2N)) * sizeof(float2));
   L.hs = take(nb * H * 2 * nbk * sizeof(float2));
   L.hnorm = take(nb * H * sizeof(float2));
   L.hunit = take(static_cast<size_t>(H) * sizeof(float2));
@@ -262,7 +262,7 @@ ConvLayout conv_layout(int B, int H, int C, int n) {
     off = align_up(off + bytes);
     return at;
   };
-  L.tw = take(2 * N * sizeof(float2));
+  L.tw = take(static_cast<size_t>(twiddle_slots(L.l2)) * sizeof(float2));
   L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
   L.ones = take(N * sizeof(float));
   L.vsc = take(bh * pairs * N * sizeof(float2));

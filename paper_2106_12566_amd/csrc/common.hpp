@@ -28,9 +28,9 @@ constexpr int kFeatElu = 2;
 // The 2N frequency bins are split into S = 2 FOLD residue classes
 // k = S k' + r; class r is a length L' = 2N / S transform (L' = N / FOLD) of
 // the input folded FOLD times (Section 3.2 leaves the FFT open; see the
-// convolution kernel for the algebra).  FOLD = 1 up to N = 4096 (the classes
-// are the even and odd bins), 2 at N = 8192 and 4 at N = 16384: transforms
-// never exceed 4096 points, which keeps their state in the register file.
+// convolution kernel for the algebra).  FOLD = 1 up to N = 8192 (the classes
+// are the even and odd bins) and 4 at N = 16384: transforms never exceed
+// 8192 points (64 KiB of LDS).
 //
 // A transform is owned by T = L' / R threads (R complex values each); a
 // work-group holds G units of T threads (G > 1 only for transforms of fewer
@@ -39,22 +39,30 @@ constexpr int kFeatElu = 2;
 // accumulators.
 template <int L2>
 struct Conf {
-  static constexpr int FOLD = L2 <= 12 ? 1 : (L2 == 13 ? 2 : 4);
+  // Classes of the length-2N spectrum: two (one 2N/2-point transform each)
+  // up to N = 8192, eight (4096 points each, four folds) at N = 16384.
+  static constexpr int FOLD = L2 <= 13 ? 1 : 4;
   static constexpr int S = 2 * FOLD;                  // residue classes
-  static constexpr int L2T = L2 <= 12 ? L2 : 12;       // log2 of the transform length
+  static constexpr int L2T = L2 <= 13 ? L2 : 12;       // log2 of the transform length
   // 8 values per thread at N = 16384: 512 threads share the 64 positions x
   // 2 columns of accumulators a 256-thread group could not hold
   static constexpr int LOG2R = L2 == 14 ? 3 : kLog2R;
-  using F = Fft<L2T, LOG2R, 1 + L2 - L2T>;  // twiddles come from the W_{2N} table
+  // Compact per-pass twiddle tables (and the per-thread first-pass table of
+  // the convolution) for the lengths whose units cannot keep their twiddles
+  // in registers.
+  static constexpr bool TWC = L2 == 13;
+  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC>;  // twiddles come from the W_{2N} table
   static constexpr int N = 1 << L2;
   static constexpr int LT = F::N;  // transform length 2N / S
   static constexpr int G = F::T >= 128 ? 1 : 256 / F::T;  // units per work-group
   static constexpr int THREADS = G * F::T;
   static constexpr int WAVES = (THREADS + 63) / 64;
   static constexpr int LDS_SLOTS = F::P > 1 ? G * F::LDS : 1;
-  // Two work-groups per CU (register budget 256 per thread) for the
-  // mid-size transforms: one runs while the other waits at a barrier.
-  static constexpr int WPE = (L2 >= 9 && L2 <= 12) ? 2 : 1;
+  // Two work-groups per CU for the mid-size transforms: one runs while the
+  // other waits at a barrier (register budget 256 per thread; 128 for the
+  // 512-thread groups of N = 8192, which then re-read their per-position
+  // values, spectrum and twiddles from the L1-friendly tables).
+  static constexpr int WPE = (L2 >= 9 && L2 <= 12) ? 2 : (L2 == 13 ? 4 : 1);
   static constexpr int KH =
       (WPE == 1 && FOLD <= 2 && F::T <= 256 && F::R <= 16 && 2 * G * F::LDS * 8 <= 144 * 1024) ? 2 : 1;
   static constexpr int HSPLIT = S / KH;  // work units per column pair and head

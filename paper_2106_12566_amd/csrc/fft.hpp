@@ -195,7 +195,12 @@ struct Dft {
 // TWS = log2(table length / N): the twiddle table always holds W_M^k, k < M,
 // for some M = N << TWS (M = 2N for a transform of the full half-length, 4N
 // when the transform is a quarter of the circular length).
-template <int LOG2N_, int LOG2R_, int TWS = 1>
+// TWC: the passes p >= 1 read their twiddles W_{L_p}^k (L_p = N >> (LR p),
+// the pass's sub-problem length) from compact tables stored after 2 M
+// entries of the table (see twc_offset), instead of every 2^(LR p + TWS)-th
+// entry of W_M: a few KiB that stay in the L1 cache when the twiddles are
+// re-read per transform rather than kept in registers.
+template <int LOG2N_, int LOG2R_, int TWS = 1, bool TWC = false>
 struct Fft {
   static constexpr int LOG2N = LOG2N_;
   static constexpr int N = 1 << LOG2N;
@@ -238,6 +243,23 @@ struct Fft {
     }
   }
   __host__ __device__ static constexpr int pad(int a) { return a + (a >> (LR > 0 ? LR : 1)); }
+  // Table entries: W_M (M), the per-thread first-pass table of the users
+  // that keep one (M), then W_{L_p} for p = 1 .. P - 1.
+  static constexpr int M_TAB = N << TWS;
+  __host__ __device__ static constexpr int twc_offset(int p) {
+    int off = 2 * M_TAB;
+    for (int q = 1; q < p; ++q) off += N >> (LR * q);
+    return off;
+  }
+  static constexpr int TABLE = TWC ? twc_offset(P) : M_TAB;
+  template <int p>
+  __device__ __forceinline__ static float2 twiddle(const float2* __restrict__ tw, int ts) {
+    if constexpr (TWC && p > 0) {
+      return tw[twc_offset(p) + ts];
+    } else {
+      return tw[ts << (LR * p + TWS)];
+    }
+  }
   static constexpr int LDS = N + (N >> (LR > 0 ? LR : 1)) + 1;  // float2 slots per transform
 
   // Position (before padding) held by register i of thread tau after the
@@ -297,7 +319,7 @@ struct Fft {
         const int t = (tau + T * u) % SP;
 #pragma unroll
         for (int s = 1; s < RP; ++s) {
-          const float2 w = tw[(t * s) << (LR * p + TWS)];
+          const float2 w = twiddle<p>(tw, t * s);
 #pragma unroll
           for (int k = 0; k < K; ++k) x[k][u * RP + s] = cmul(x[k][u * RP + s], w);
         }
@@ -346,7 +368,7 @@ struct Fft {
         const int t = (tau + T * u) % SP;
 #pragma unroll
         for (int s = 1; s < RP; ++s) {
-          const float2 w = tw[(t * s) << (LR * p + TWS)];
+          const float2 w = twiddle<p>(tw, t * s);
 #pragma unroll
           for (int k = 0; k < K; ++k) x[k][u * RP + s] = cmulc(x[k][u * RP + s], w);
         }

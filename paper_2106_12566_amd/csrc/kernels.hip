@@ -53,6 +53,35 @@ __global__ void k_twiddles(float2* __restrict__ tw, int log2n) {
   }
 }
 
+// Entries past W_{2N} of the extended twiddle table of Conf<L2> (C::TWC):
+//   [M, 2M):        per-thread first-pass twiddles of the convolution units,
+//                   entry M + (r R + i) T + tau = W_{2N}^{tau (r + S i)}
+//   [2M, TABLE):    W_{L_p}^k, k < L_p, for the passes p >= 1 (Fft::twc_offset)
+// with M = 2N, computed in double and rounded.
+template <int L2>
+__global__ void k_twiddles_ext(float2* __restrict__ tw) {
+  using C = Conf<L2>;
+  using F = typename C::F;
+  constexpr int M = F::M_TAB;
+  const int e = M + blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= F::TABLE) return;
+  long long num;
+  long long den;
+  if (e < 2 * M) {
+    const int q = e - M, tau = q % F::T, i = (q / F::T) % F::R, r = q / (F::T * F::R);
+    num = (static_cast<long long>(tau) * (r + C::S * i)) % M;
+    den = M;
+  } else {
+    int p = 1;
+    while (p + 1 < F::P && e >= F::twc_offset(p + 1)) ++p;
+    num = e - F::twc_offset(p);
+    den = F::N >> (F::LR * p);
+  }
+  double sn, cs;
+  sincospi(-2.0 * static_cast<double>(num) / static_cast<double>(den), &sn, &cs);
+  tw[e] = make_float2(static_cast<float>(cs), static_cast<float>(sn));
+}
+
 // ------------------------------------------------------------ spectrum --
 // c_{-s} embedded circularly in length 2N (see the header comment).
 __device__ __forceinline__ float circ_kernel(const float* __restrict__ bh, int s, int n, int N) {
@@ -446,12 +475,15 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
   // Merged first-pass twiddles (MERGE), or the plain twists W_{2N}^{r j}
   // (single-pass transforms), of every class of the unit.
   float2 w0[KH][F::R];
+  // With the extended table (C::TWC) the merged twiddles of thread ta are
+  // read from the per-thread table, lanes at consecutive entries.
   auto load_w0 = [&](const float2* __restrict__ t, int ta) {
 #pragma unroll
     for (int k = 0; k < KH; ++k)
 #pragma unroll
       for (int i = 0; i < F::R; ++i)
-        w0[k][i] = MERGE ? t[ta * (R0 + k + S * i)] : t[(R0 + k) * (ta + F::T * i)];
+        w0[k][i] = MERGE ? (C::TWC ? t[F::M_TAB + ((R0 + k) * F::R + i) * F::T + ta] : t[ta * (R0 + k + S * i)])
+                         : t[(R0 + k) * (ta + F::T * i)];
   };
   if constexpr (HOIST) load_w0(tw, tau);
   // With registers to spare, phi(k) of the next feature is loaded at the top
@@ -1526,6 +1558,20 @@ struct ConvFn {
   static hipError_t run(A... a) { return conv_l2<L2>(a...); }
 };
 template <int L2>
+struct TwExtFn {
+  static hipError_t run(float2* tw, int extra, hipStream_t st) {
+    hipLaunchKernelGGL(k_twiddles_ext<L2>, dim3((extra + 255) / 256), dim3(256), 0, st, tw);
+    return hipGetLastError();
+  }
+};
+template <int L2>
+struct TableFn {
+  static hipError_t run(int* out) {
+    *out = Conf<L2>::TWC ? Conf<L2>::F::TABLE : 2 * Conf<L2>::N;
+    return hipSuccess;
+  }
+};
+template <int L2>
 struct SplitFn {
   static hipError_t run(int* out) {
     *out = Conf<L2>::HSPLIT;
@@ -1534,6 +1580,12 @@ struct SplitFn {
 };
 
 }  // namespace
+
+int twiddle_slots(int l2) {
+  int t = 2 << l2;
+  (void)dispatch<TableFn>(l2, &t);
+  return t;
+}
 
 int conv_splits(int l2) {
   int s = 2;
@@ -1552,6 +1604,11 @@ int gram_splits(int BH, int m, int N) {
 hipError_t launch_twiddles(float2* tw, int l2, hipStream_t st) {
   const int count = 2 << l2;
   hipLaunchKernelGGL(k_twiddles, dim3((count + 255) / 256), dim3(256), 0, st, tw, l2);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  const int extra = twiddle_slots(l2) - count;
+  if (extra > 0) {
+    if (hipError_t e = dispatch<TwExtFn>(l2, tw, extra, st); e != hipSuccess) return e;
+  }
   return hipGetLastError();
 }
 

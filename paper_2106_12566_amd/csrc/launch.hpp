@@ -95,6 +95,9 @@ int conv_splits(int l2);
 int conv_units(int l2, int BH, int cols);
 int gram_splits(int BH, int m, int N);
 
+// Entries (float2) of the twiddle table of length 2^l2: W_{2N}^k, k < 2N, and
+// for N >= 8192 the per-thread and per-pass tables after it.
+int twiddle_slots(int l2);
 hipError_t launch_twiddles(float2* tw, int l2, hipStream_t st);
 hipError_t launch_spectrum(int l2, const float* b, const float2* tw, float2* Hs, float2* hnorm, int H, int n,
                            hipStream_t st);
