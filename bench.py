@@ -78,6 +78,22 @@ def conv_stage_bytes(B, H, n, d, m, s_in) -> float:
     return B * H * (2 * n * m * 4 + n * d * s_in + (d + 1) * n * 4) + H * 2 * n * 8
 
 
+def feature_stage_roofline(B, H, n, d, m, s_in, ms) -> dict:
+    """The feature-map stage of the FFT route (phi(q), phi(k) by MFMA with the exp epilogue, then
+    the value columns' maxima and scaled pairs): algorithmic HBM bytes (q, k, W read once, v read
+    twice, phi(q), phi(k) and the N-padded value pairs written once) and MFMA flops (2 n m d per
+    (batch, head) and input) over the stage's event time, as fractions of the HBM and fp32 MFMA
+    peaks."""
+    N = 1 << max(0, (n - 1).bit_length())
+    pairs = (d + 2) // 2
+    hbm = B * H * (2 * n * d * s_in + 2 * n * d * s_in + 2 * m * N * 4 + pairs * N * 8) + H * m * d * 4
+    flops = 2.0 * 2 * B * H * n * m * d
+    gbs = hbm / (ms * 1e-3) / 1e9
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"ms": ms, "hbm_bytes": hbm, "achieved_gbs": gbs, "hbm_frac": gbs / PEAK_HBM_GBS,
+            "mfma_tflops": tf, "mfma_frac": tf / PEAK_FP32_VECTOR_TFLOPS}
+
+
 def measured_traffic(kernel: str, workload: str):
     """HBM bytes per launch of `kernel` from the committed profiler record, or None when the
     record is for another workload or the device sources changed since the counters were taken."""
@@ -379,6 +395,8 @@ def main() -> int:
                    "route": route_used, "blocks": -(-n // BLOCK) if route_used == "fft" else None,
                    "ms_per_layer": ms_per_step, "stages_ms": stages,
                    "conv_stage_hbm_gbs": conv_gbs,
+                   "feature_stage_roofline": (feature_stage_roofline(B, H, n, dd, M, s_in, stages["feature_map"])
+                                              if route_used == "fft" and n <= BLOCK and fm == "prf" else None),
                    "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)},
         "roofline": {**roof, "achieved": achieved_tflops,
                      "peak": PEAK_FP32_VECTOR_TFLOPS, "unit": "TFLOP/s",

@@ -340,18 +340,24 @@ __global__ __launch_bounds__(256) void k_vmax(const TV* __restrict__ v, long lon
   const int pos0 = ch * kVmaxChunk, np = min(kVmaxChunk, n - pos0);
   if (tid < 64) cm[tid] = 0u;
   __syncthreads();
-  const int total = np * nc;
-  for (int e = tid; e < total; e += 256) {
-    int r, c;
-    if (sc == 1) {
-      r = e / nc;
-      c = e - r * nc;
-    } else {
-      c = e / np;
-      r = e - c * np;
+  if (sc == 1) {
+    // rows contiguous in the columns: thread (tid & 63) keeps its column's
+    // maximum over rows tid >> 6, + 4, ... in a register (loads coalesced
+    // along the row), then one LDS maximum per thread
+    const int c = tid & 63;
+    float mx = 0.f;
+    if (c < nc) {
+#pragma unroll 8
+      for (int r = tid >> 6; r < np; r += 4) mx = fmaxf(mx, fabsf(to_f32(vb[(pos0 + r) * sp + c0 + c])));
     }
-    const float x = fabsf(to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]));
-    atomicMax(&cm[c], __float_as_uint(x));  // x >= 0: bit patterns order like the values
+    if (c < nc) atomicMax(&cm[c], __float_as_uint(mx));  // mx >= 0: bit patterns order like the values
+  } else {
+    const int total = np * nc;
+    for (int e = tid; e < total; e += 256) {
+      const int c = e / np, r = e - c * np;
+      const float x = fabsf(to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]));
+      atomicMax(&cm[c], __float_as_uint(x));
+    }
   }
   __syncthreads();
   if (tid < nc) pmax[(static_cast<size_t>(bh) * nchunk + ch) * ncols + c0 + tid] = __uint_as_float(cm[tid]);
@@ -386,17 +392,20 @@ __global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long l
   }
   const int np = max(0, min(64, n - pos0));
   const int nv = max(0, min(nc, ncols - c0));  // value columns of this group
-  const int total = np * nv;
-  for (int e = tid; e < total; e += 256) {
-    int r, c;
-    if (sc == 1) {
-      r = e / nv;
-      c = e - r * nv;
-    } else {
-      c = e / np;
-      r = e - c * np;
+  if (sc == 1) {
+    // thread (tid & 63) reads its column along rows tid >> 6, + 4, ...
+    const int c = tid & 63;
+    if (c < nv) {
+#pragma unroll
+      for (int r = tid >> 6; r < 64; r += 4)
+        if (r < np) tile[c][r] = to_f32(vb[(pos0 + r) * sp + c0 + c]);
     }
-    tile[c][r] = to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]);
+  } else {
+    const int total = np * nv;
+    for (int e = tid; e < total; e += 256) {
+      const int c = e / np, r = e - c * np;
+      tile[c][r] = to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]);
+    }
   }
   __syncthreads();
   const int npairs = (nc + 1) / 2;
@@ -734,28 +743,41 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
   for (int k = 0; k < kGramPK; ++k)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[k][j] = 0.f;
-  for (int p0 = pos_begin; p0 < pos_end; p0 += 64) {
-    __syncthreads();
-    for (int e = tid; e < 64 * 16; e += 256) {
-      const int x = e & 63, q = e >> 6;
-      float a[4];
+  // The next chunk's values are loaded into registers while the current
+  // chunk is multiplied out of LDS (thread tid holds positions tid & 63 of
+  // feature quads tid >> 6 + 4 e and of pairs tid >> 6 + 4 e).
+  constexpr int kGramPB = (kMaxPairs + 3) / 4;
+  float na[4][4];
+  float2 nb[kGramPB];
+  const int xl = tid & 63, ql = tid >> 6;
+  auto fetch = [&](int p0) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int l = l0 + 4 * q + j;
-        a[j] = (l < m && p0 + x < pos_end) ? pk[static_cast<size_t>(l) * N + p0 + x] : 0.f;
+        const int l = l0 + 4 * (ql + 4 * e) + j;
+        na[e][j] = (l < m && p0 + xl < pos_end) ? pk[static_cast<size_t>(l) * N + p0 + xl] : 0.f;
       }
-      A4[x][q] = make_float4(a[0] * a[0], a[1] * a[1], a[2] * a[2], a[3] * a[3]);
+#pragma unroll
+    for (int e = 0; e < kGramPB; ++e) {
+      const int p = ql + 4 * e;
+      nb[e] = (p < pairs && p0 + xl < pos_end) ? vb[static_cast<size_t>(p) * N + p0 + xl] : make_float2(0.f, 0.f);
     }
-    for (int e = tid; e < 64 * pairs; e += 256) {
-      const int p = e >> 6, x = e & 63;
-      float q2 = 0.f;
-      if (p0 + x < pos_end) {
-        const float2 w = vb[static_cast<size_t>(p) * N + p0 + x];
-        q2 = w.x * w.x + w.y * w.y;
-      }
-      Bq[x][p] = q2;
+  };
+  if (pos_begin < pos_end) fetch(pos_begin);
+  for (int p0 = pos_begin; p0 < pos_end; p0 += 64) {
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      A4[xl][ql + 4 * e] = make_float4(na[e][0] * na[e][0], na[e][1] * na[e][1], na[e][2] * na[e][2],
+                                       na[e][3] * na[e][3]);
+#pragma unroll
+    for (int e = 0; e < kGramPB; ++e) {
+      const int p = ql + 4 * e;
+      if (p < pairs) Bq[xl][p] = nb[e].x * nb[e].x + nb[e].y * nb[e].y;
     }
     __syncthreads();
+    if (p0 + 64 < pos_end) fetch(p0 + 64);
 #pragma unroll 4
     for (int x = 0; x < 64; ++x) {
       const float4 a = A4[x][lg];
