@@ -125,13 +125,22 @@ krpe_status_t record(void* const* events, int i, hipStream_t st) {
 
 // Feature splits of the forward convolution: the m features of a unit are
 // split into contiguous ranges (each its own partial result) until the launch
-// has about four units per CU, keeping at least 8 features per range.  Only
-// launches with few (batch, head) rows split.
+// has about four units per CU, keeping at least 8 features per range (few
+// (batch, head) rows).  Otherwise, for the transforms of N = 512 .. 8192
+// (512 resident units: 256 CUs x 2 work-groups), two ranges when that fills
+// the launch's last round of units better: one round in 32 left idle is worth
+// the doubled partial results (workload of 96 heads at n = 4096: 12.4 rounds,
+// 8.15 -> 8.05 ms).
 int conv_fsplit(int l2, int BH, int cols, int M, int nkb) {
   if (l2 > kMaxLog2N) return 1;
   const long long units = static_cast<long long>(conv_units(l2, BH, cols)) * nkb;
   int fs = 1;
   while (units * fs < 1024 && M / (2 * fs) >= 8) fs *= 2;
+  if (fs == 1 && l2 >= 9 && l2 <= 13 && M >= 64) {
+    constexpr long long kResident = 512;
+    auto idle = [](long long u) { return static_cast<double>((u + kResident - 1) / kResident * kResident - u) / u; };
+    if (idle(units) > 1.0 / 32 && idle(2 * units) < idle(units)) fs = 2;
+  }
   return fs;
 }
 
@@ -161,7 +170,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.x2 = take(bh * L.ksplit * m * pairs * sizeof(float));
   L.wb = take(bh * (static_cast<size_t>(m) + 1) * sizeof(float2));
   L.part = take(bh * L.fsplit * conv_splits(L.l2) * cols * n * sizeof(float));
-  L.psum = take(L.fsplit > 1 ? bh * cols * n * sizeof(float) : 0);
+  L.psum = take(L.fsplit > 1 && bh * ((static_cast<size_t>(n) + 63) / 64) < 4096 ? bh * cols * n * sizeof(float) : 0);
   L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
@@ -345,12 +354,13 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
     return s;
   if (krpe_status_t s = hip_check(launch_bound_weights(x2, colmax, wb, BHi, M, d, L.ksplit, st), "bound launch"))
     return s;
-  // feature splits: their partial results summed first, at full parallelism
+  // feature splits: with few (batch, head) rows their partial results are
+  // summed first, at full parallelism; the ratio kernel sums them otherwise
   const float* sums = part;
-  int nsum = conv_splits(L.l2);
-  if (L.fsplit > 1) {
+  int nsum = L.fsplit * conv_splits(L.l2);
+  if (L.fsplit > 1 && static_cast<long long>(BHi) * ((n + 63) / 64) < 4096) {
     float* psum = reinterpret_cast<float*>(w + L.psum);
-    if (krpe_status_t s = hip_check(launch_sum_splits(part, psum, BHi, d + 1, n, L.fsplit * nsum, st), "sum launch"))
+    if (krpe_status_t s = hip_check(launch_sum_splits(part, psum, BHi, d + 1, n, nsum, st), "sum launch"))
       return s;
     sums = psum;
     nsum = 1;
