@@ -128,8 +128,10 @@ __device__ __forceinline__ void corr_split(int hs, const float* __restrict__ pk,
 
 // phiq/phik: [bh][m][N] (phi_bh_stride apart); V' and Gh packed as column
 // pairs vpk/gpk [bh][pairs][N] (float2, unscaled).
+// Two waves per SIMD (at most 256 registers, a few spilled) beat one wave
+// with everything in registers: 13.2 -> 8.4 ms at n = 4096, 96 heads.
 template <int L2>
-__global__ __launch_bounds__(Conf<L2>::THREADS) void
+__global__ __launch_bounds__(Conf<L2>::THREADS) __attribute__((amdgpu_waves_per_eu(Conf<L2>::WPE > 2 ? 2 : Conf<L2>::WPE))) void
 k_corr_spectrum(const float* __restrict__ phiq, const float* __restrict__ phik, long long phi_bh_stride,
                 const float2* __restrict__ vpk, const float2* __restrict__ gpk, const float2* __restrict__ tw,
                 float2* __restrict__ spart, int pairs, int m, int units) {
