@@ -352,11 +352,16 @@ __global__ __launch_bounds__(256) void k_vmax(const TV* __restrict__ v, long lon
     }
     if (c < nc) atomicMax(&cm[c], __float_as_uint(mx));  // mx >= 0: bit patterns order like the values
   } else {
-    const int total = np * nc;
-    for (int e = tid; e < total; e += 256) {
-      const int c = e / np, r = e - c * np;
-      const float x = fabsf(to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]));
-      atomicMax(&cm[c], __float_as_uint(x));
+    // columns strided: wave w takes columns w, w + 4, ..., its lanes the
+    // positions lane, lane + 64, ... (loads coalesced along the column), and
+    // reduces across the wave
+    const int wave = tid >> 6, lane = tid & 63;
+    for (int c = wave; c < nc; c += 4) {
+      float mx = 0.f;
+      for (int r = lane; r < np; r += 64) mx = fmaxf(mx, fabsf(to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc])));
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+      if (lane == 0) cm[c] = __float_as_uint(mx);
     }
   }
   __syncthreads();
@@ -401,11 +406,11 @@ __global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long l
         if (r < np) tile[c][r] = to_f32(vb[(pos0 + r) * sp + c0 + c]);
     }
   } else {
-    const int total = np * nv;
-    for (int e = tid; e < total; e += 256) {
-      const int c = e / np, r = e - c * np;
-      tile[c][r] = to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]);
-    }
+    // columns strided: thread (tid & 63) reads position tid & 63 of columns
+    // tid >> 6, + 4, ... (coalesced along the column)
+    const int r = tid & 63;
+    if (r < np)
+      for (int c = tid >> 6; c < nv; c += 4) tile[c][r] = to_f32(vb[(pos0 + r) * sp + (c0 + c) * sc]);
   }
   __syncthreads();
   const int npairs = (nc + 1) / 2;
