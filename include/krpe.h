@@ -150,7 +150,7 @@ size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n);
  *   y[beta, h, ch, i] = sum_{j<n} exp(b[h, j - i + n - 1]) * a[beta, h, ch, j]
  * b : [H, 2n-1] fp32     a, y : [B, H, C, n] fp32 (sequence-contiguous channels)
  * Computed as a zero-padded length-2N FFT convolution (split into residue
- * classes of its frequency bins, each a transform of at most 4096 points).
+ * classes of its frequency bins, each a transform of at most 8192 points).
  */
 krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
                                  int B, int H, int C, int n,
