@@ -875,8 +875,16 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
     const int pos = i0 + i;
     float t = 1.f;
     if (pos < n) {
-      t = p0[static_cast<size_t>(c) * n + pos];
-      for (int sp = 1; sp < nsplit; ++sp) t += p0[(static_cast<size_t>(sp) * cols + c) * n + pos];
+      // the partials' loads issued together, summed in split order
+      const float* __restrict__ pc = p0 + static_cast<size_t>(c) * n + pos;
+      const size_t step = static_cast<size_t>(cols) * n;
+      t = pc[0];
+      int sp = 1;
+      for (; sp + 3 <= nsplit; sp += 3) {
+        const float a1 = pc[sp * step], a2 = pc[(sp + 1) * step], a3 = pc[(sp + 2) * step];
+        t = ((t + a1) + a2) + a3;
+      }
+      for (; sp < nsplit; ++sp) t += pc[sp * step];
     }
     tile[c * 65 + i] = t;
   }
