@@ -390,7 +390,12 @@ __global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long l
     float sv = 1.f;  // the ones column
     if (c < ncols) {
       sv = 0.f;
-      for (int ch = 0; ch < nchunk; ++ch) sv = fmaxf(sv, pmax[(static_cast<size_t>(bh) * nchunk + ch) * ncols + c]);
+      const float* __restrict__ pm = pmax + static_cast<size_t>(bh) * nchunk * ncols + c;
+      int ch = 0;
+      for (; ch + 4 <= nchunk; ch += 4)
+        sv = fmaxf(fmaxf(sv, fmaxf(pm[ch * ncols], pm[(ch + 1) * ncols])),
+                   fmaxf(pm[(ch + 2) * ncols], pm[(ch + 3) * ncols]));
+      for (; ch < nchunk; ++ch) sv = fmaxf(sv, pm[ch * ncols]);
     }
     if (pt == 0) colmax[static_cast<size_t>(bh) * cols + c] = sv;
     scale[tid] = sv > 0.f ? sv : 1.f;
@@ -723,11 +728,11 @@ k_conv_contract(
 // X2[bh][ks][l][p] = sum over positions of slice ks of phi_l(k_j)^2 |vsc_p(j)|^2
 // = ||x_{l,p}||^2 restricted to the slice, x_{l,p} the packed signal the
 // convolution kernel transforms for feature l and column pair p.  Block
-// (bh, l-tile of 64, slice ks), positions staged through LDS 64 at a time;
-// thread t accumulates a 4 x kGramPK register tile: features 4 (t % 16) + j
-// and pairs t / 16 + 16 k.
+// (bh, l-tile of 64, slice ks), positions staged through LDS 64 at a time, the
+// product phi^2 |vsc|^2 over positions on the matrix cores: wave w takes the
+// 32 features 32 (w & 1) .. and the 32-pair tiles w >> 1, (w >> 1) + 2.
 constexpr int kMaxPairs = (kMaxD + 2) / 2;
-constexpr int kGramPK = (kMaxPairs + 15) / 16;
+constexpr int kGramPT = (kMaxPairs + 31) / 32;  // 32-pair tiles
 
 __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, const float2* __restrict__ vsc,
                                               float* __restrict__ X2, int m, int N, int pairs, int ltiles,
@@ -738,16 +743,18 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
   const int ks = bid % ksplit;
   bid /= ksplit;
   const int lt = bid % ltiles, bh = bid / ltiles;
-  const int tid = threadIdx.x, lg = tid & 15, pg = tid >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ft = wave & 1, pt0 = wave >> 1, lr = lane & 31, lk = lane >> 5;
   const int l0 = lt * 64;
   const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * N;
   const float2* __restrict__ vb = vsc + static_cast<size_t>(bh) * pairs * N;
   const int slice = N / ksplit, pos_begin = ks * slice, pos_end = pos_begin + slice;
-  float acc[kGramPK][4];
+  const float* __restrict__ Af = reinterpret_cast<const float*>(&A4[0][0]);  // [position][68]: feature f at f
+  floatx16 acc[2];
 #pragma unroll
-  for (int k = 0; k < kGramPK; ++k)
+  for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[k][j] = 0.f;
+    for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
   // The next chunk's values are loaded into registers while the current
   // chunk is multiplied out of LDS (thread tid holds positions tid & 63 of
   // feature quads tid >> 6 + 4 e and of pairs tid >> 6 + 4 e).
@@ -783,31 +790,31 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
     }
     __syncthreads();
     if (p0 + 64 < pos_end) fetch(p0 + 64);
-#pragma unroll 4
-    for (int x = 0; x < 64; ++x) {
-      const float4 a = A4[x][lg];
+    // A[feature][position] = phi^2, B[position][pair] = |vsc|^2, 2 positions per step
 #pragma unroll
-      for (int k = 0; k < kGramPK; ++k) {
-        const int p = pg + 16 * k;
-        if (p < pairs) {
-          const float bq = Bq[x][p];
-          acc[k][0] = fmaf(a.x, bq, acc[k][0]);
-          acc[k][1] = fmaf(a.y, bq, acc[k][1]);
-          acc[k][2] = fmaf(a.z, bq, acc[k][2]);
-          acc[k][3] = fmaf(a.w, bq, acc[k][3]);
+    for (int t = 0; t < 2; ++t) {
+      const int p = 32 * (pt0 + 2 * t) + lr;
+      if (pt0 + 2 * t < kGramPT && 32 * (pt0 + 2 * t) < pairs) {
+#pragma unroll 8
+        for (int s2 = 0; s2 < 32; ++s2) {
+          const int x = 2 * s2 + lk;
+          const float a = Af[x * 68 + 32 * ft + lr];
+          const float bq = p < pairs ? Bq[x][p] : 0.f;
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bq, acc[t], 0, 0, 0);
         }
       }
     }
   }
+  // result tile t: lane holds pair 32 (pt0 + 2 t) + lr, features 32 ft + row(e)
   float* __restrict__ out = X2 + (static_cast<size_t>(bh) * ksplit + ks) * m * pairs;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int l = l0 + 4 * lg + j;
-    if (l < m) {
+  for (int t = 0; t < 2; ++t) {
+    const int p = 32 * (pt0 + 2 * t) + lr;
+    if (pt0 + 2 * t < kGramPT && p < pairs) {
 #pragma unroll
-      for (int k = 0; k < kGramPK; ++k) {
-        const int p = pg + 16 * k;
-        if (p < pairs) out[static_cast<size_t>(l) * pairs + p] = acc[k][j];
+      for (int e = 0; e < 16; ++e) {
+        const int l = l0 + 32 * ft + 8 * (e >> 2) + 4 * lk + (e & 3);
+        if (l < m) out[static_cast<size_t>(l) * pairs + p] = acc[t][e];
       }
     }
   }
