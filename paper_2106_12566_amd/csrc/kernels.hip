@@ -827,27 +827,33 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
 __global__ __launch_bounds__(256) void k_bound_weights(const float* __restrict__ X2, const float* __restrict__ colmax,
                                                        float2* __restrict__ Wb, int BH, int m, int d, int pairs,
                                                        int ksplit) {
-  const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (e >= static_cast<long long>(BH) * (m + 1)) return;
+  // one wave per (bh, l): lane p (p < pairs, two rounds of 64) sums its
+  // slices, the wave reduces the maxima
+  const long long e = static_cast<long long>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (e >= static_cast<long long>(BH) * (m + 1)) return;  // uniform per wave
+  const int lane = threadIdx.x & 63;
   const int bh = static_cast<int>(e / (m + 1)), l = static_cast<int>(e % (m + 1));
   const float* __restrict__ s = colmax + static_cast<size_t>(bh) * (d + 1);
-  if (l == m) {
-    float smax = 0.f;
-    for (int c = 0; c < d; ++c) smax = fmaxf(smax, s[c]);
-    Wb[e] = make_float2(smax, 0.f);
-    return;
-  }
   float A = 0.f, D = 0.f;
-  for (int p = 0; p < pairs; ++p) {
-    float x2 = 0.f;
-    for (int ks = 0; ks < ksplit; ++ks) x2 += X2[((static_cast<size_t>(bh) * ksplit + ks) * m + l) * pairs + p];
-    const float nrm = sqrtf(x2);
-    const int c0 = 2 * p, c1 = 2 * p + 1;
-    if (c0 < d) A = fmaxf(A, nrm * s[c0]);
-    if (c1 < d) A = fmaxf(A, nrm * s[c1]);
-    if (c0 == d || c1 == d) D = nrm;
+  if (l == m) {
+    for (int c = lane; c < d; c += 64) A = fmaxf(A, s[c]);
+  } else {
+    for (int p = lane; p < pairs; p += 64) {
+      float x2 = 0.f;
+      for (int ks = 0; ks < ksplit; ++ks) x2 += X2[((static_cast<size_t>(bh) * ksplit + ks) * m + l) * pairs + p];
+      const float nrm = sqrtf(x2);
+      const int c0 = 2 * p, c1 = 2 * p + 1;
+      if (c0 < d) A = fmaxf(A, nrm * s[c0]);
+      if (c1 < d) A = fmaxf(A, nrm * s[c1]);
+      if (c0 == d || c1 == d) D = nrm;
+    }
   }
-  Wb[e] = make_float2(A, D);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    A = fmaxf(A, __shfl_xor(A, off));
+    D = fmaxf(D, __shfl_xor(D, off));  // one lane holds D, the others 0
+  }
+  if (lane == 0) Wb[e] = make_float2(A, D);
 }
 
 // -------------------------------------------------------------- combine --
@@ -1777,8 +1783,8 @@ hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, 
 
 hipError_t launch_bound_weights(const float* X2, const float* colmax, float2* Wb, int BH, int m, int d,
                                 int ksplit, hipStream_t st) {
-  const long long total = static_cast<long long>(BH) * (m + 1);
-  hipLaunchKernelGGL(k_bound_weights, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, st, X2, colmax,
+  const long long total = static_cast<long long>(BH) * (m + 1);  // one wave each
+  hipLaunchKernelGGL(k_bound_weights, dim3(static_cast<unsigned>((total + 3) / 4)), dim3(256), 0, st, X2, colmax,
                      Wb, BH, m, d, (d + 2) / 2, ksplit);
   return hipGetLastError();
 }
