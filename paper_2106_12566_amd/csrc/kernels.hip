@@ -1013,6 +1013,7 @@ __global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int
   }
   __syncthreads();
   int lo = 2 * n, hi = -1;
+#pragma unroll 8
   for (int sidx = threadIdx.x; sidx < 2 * n - 1; sidx += 256)
     if (bh[sidx] != -INFINITY) {
       lo = min(lo, sidx);

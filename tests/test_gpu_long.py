@@ -64,6 +64,25 @@ def test_long_sequence_sampled_rows(gpu_lib, B, H, n, d, m, dt, bias, nprf):
     assert err <= TOL[dt], err
 
 
+@pytest.mark.parametrize("features,nprf,bias", [("trf", True, "causal"), ("elu", False, "normal")])
+def test_long_sequence_other_feature_maps(gpu_lib, features, nprf, bias):
+    """The trigonometric and elu + 1 maps through the blocked route (signed
+    features certified with |phi|), sampled rows against the oracle."""
+    B, H, n, d, m = 1, 1, 20000, 32, 32
+    _say(f"long fft {features} nprf={nprf} {bias} n={n}")
+    dd = synth.custom(B, H, n, d, m, seed=74, bias=bias)
+    W = None if features == "elu" else dd["W"]
+    q, k, v, b = (to_gpu(dd[x]) for x in ("q", "k", "v", "b"))
+    z = gpu_lib.attention_fwd(q, k, v, b, None if W is None else to_gpu(W), nprf=nprf, features=features,
+                              route="fft").cpu().numpy()
+    assert np.all(np.isfinite(z))
+    rows = sample_rows(B, H, n, 32, seed=n + 1, extra=_boundary_rows(B, H, n) + [(0, 0, i) for i in range(4)])
+    ref, _ = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], W, rows, nprf=nprf, kind=features)
+    err = rownorm_err(np.stack([z[bb, h, i] for bb, h, i in rows]), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL["f32"], err
+
+
 def test_long_sequence_routes_agree(gpu_lib):
     """Blocked FFT route and direct route on the whole output (each within the
     oracle's bar, so within twice it of each other), and the automatic route
