@@ -1495,6 +1495,9 @@ __global__ __launch_bounds__(256) void k_feature_bwd(const TX* __restrict__ x, c
   const int bh = blockIdx.x / tiles, i0 = (blockIdx.x % tiles) * 64, h = bh % H;
   const int tid = threadIdx.x, r = tid & 63, w = tid >> 6;
   const int i = i0 + r;
+  // wave w owns the cpw contiguous columns w cpw .. (cpw a multiple of 4, so
+  // the weights are read as float4, one LDS read per four products)
+  const int cpw = ((d + 3) / 4 + 3) / 4 * 4, cbase = w * cpw;
   float acc[ACC];
 #pragma unroll
   for (int j = 0; j < ACC; ++j) acc[j] = 0.f;
@@ -1511,17 +1514,26 @@ __global__ __launch_bounds__(256) void k_feature_bwd(const TX* __restrict__ x, c
       }
       Ps[lq][rr] = p;
     }
-    for (int e = tid; e < KC * d; e += 256) {
-      const int lq = e / d, a = e - lq * d, l = l0 + lq;
-      Ws[lq][a] = l < m ? W[(static_cast<size_t>(h) * m + l) * d + a] : 0.f;
+    // columns past d (up to the waves' 4 cpw) zero: they meet the
+    // discarded accumulators only, which must stay finite
+    for (int e = tid; e < KC * 4 * cpw; e += 256) {
+      const int lq = e / (4 * cpw), a = e - lq * (4 * cpw), l = l0 + lq;
+      Ws[lq][a] = (l < m && a < d) ? W[(static_cast<size_t>(h) * m + l) * d + a] : 0.f;
     }
     __syncthreads();
     for (int lq = 0; lq < KC; ++lq) {
       const float p = Ps[lq][r];
       rs += p;
 #pragma unroll
-      for (int j = 0; j < ACC; ++j)
-        if (w + 4 * j < d) acc[j] = fmaf(p, Ws[lq][w + 4 * j], acc[j]);
+      for (int q = 0; q < ACC / 4; ++q) {
+        if (4 * q < cpw) {
+          const float4 wv = *reinterpret_cast<const float4*>(&Ws[lq][cbase + 4 * q]);
+          acc[4 * q] = fmaf(p, wv.x, acc[4 * q]);
+          acc[4 * q + 1] = fmaf(p, wv.y, acc[4 * q + 1]);
+          acc[4 * q + 2] = fmaf(p, wv.z, acc[4 * q + 2]);
+          acc[4 * q + 3] = fmaf(p, wv.w, acc[4 * q + 3]);
+        }
+      }
     }
   }
   // x of the row (normalised when asked) and its norm
@@ -1529,8 +1541,8 @@ __global__ __launch_bounds__(256) void k_feature_bwd(const TX* __restrict__ x, c
   float sq = 0.f;
 #pragma unroll
   for (int j = 0; j < ACC; ++j) {
-    const int a = w + 4 * j;
-    xa[j] = (a < d && i < n) ? to_f32(x[(static_cast<size_t>(bh) * n + i) * d + a]) : 0.f;
+    const int a = cbase + j;
+    xa[j] = (j < cpw && a < d && i < n) ? to_f32(x[(static_cast<size_t>(bh) * n + i) * d + a]) : 0.f;
     sq = fmaf(xa[j], xa[j], sq);
   }
   red[w][r] = sq;
@@ -1555,8 +1567,8 @@ __global__ __launch_bounds__(256) void k_feature_bwd(const TX* __restrict__ x, c
   if (i < n) {
 #pragma unroll
     for (int j = 0; j < ACC; ++j) {
-      const int a = w + 4 * j;
-      if (a < d) dx[(static_cast<size_t>(bh) * n + i) * d + a] = acc[j];
+      const int a = cbase + j;
+      if (j < cpw && a < d) dx[(static_cast<size_t>(bh) * n + i) * d + a] = acc[j];
     }
   }
 }
