@@ -191,6 +191,80 @@ struct Dft {
   }
 };
 
+// tan(2*pi*e/64) for e = 0..8 (exact 0 and 1 at the ends).
+__host__ __device__ constexpr float tan64(int e) {
+  constexpr float t[9] = {0.0f, 0.09849140335716425f, 0.198912367379658f, 0.3033466836073424f,
+                          0.41421356237309503f, 0.5345111359507916f, 0.6681786379192989f,
+                          0.8206787908286602f, 1.0f};
+  return e >= 0 ? t[e] : -t[-e];
+}
+
+// Butterfly with a constant twiddle: p = a + w b, q = a - w b, w = exp(-+2 pi i
+// K / NN) (sign as in rot).  w is split as i^qt * c (1 + i t) with the angle of
+// c (1 + i t) within 45 degrees of the real axis: b (1 + i t) takes two FMAs,
+// the quarter turn i^qt only renames and negates, and the scale c is folded
+// into the four FMAs of the sum and difference, 6 instructions in place of
+// the 8 of a complex product followed by an add and a subtract (4 adds when w
+// is a power of i).
+template <int NN, int K, bool INV>
+__device__ __forceinline__ void twiddle_butterfly(float2 a, float2 b, float2& p, float2& q) {
+  static_assert(64 % NN == 0, "twiddle_butterfly: NN must divide 64");
+  constexpr int k = (((K % NN) + NN) % NN) * (64 / NN);
+  constexpr int e = INV ? k : (64 - k) % 64;  // w = exp(+i 2 pi e / 64)
+  constexpr int qt = ((e + 8) / 16) % 4;      // nearest quarter turn
+  constexpr int er = e - 16 * (((e + 8) / 16));  // residual angle in [-8, 8)
+  constexpr float t = tan64(er), c = cos64(er < 0 ? -er : er);
+  float2 r = b;
+  if constexpr (er != 0) r = make_float2(fmaf(-t, b.y, b.x), fmaf(t, b.x, b.y));
+  if constexpr (qt == 1) r = make_float2(-r.y, r.x);
+  if constexpr (qt == 2) r = make_float2(-r.x, -r.y);
+  if constexpr (qt == 3) r = make_float2(r.y, -r.x);
+  if constexpr (er == 0) {
+    p = cadd(a, r);
+    q = csub(a, r);
+  } else {
+    p = make_float2(fmaf(c, r.x, a.x), fmaf(c, r.y, a.y));
+    q = make_float2(fmaf(-c, r.x, a.x), fmaf(-c, r.y, a.y));
+  }
+}
+
+// Length 16 = 4 x 4 with the twiddles of the outer radix-4 stage fused into
+// its butterflies: column s1 takes the DFT over r0 of W_16^{r0 s1} y[r0][s1],
+// i.e. with w = W_16^{s1}:  t0, t1 = y0 +- w^2 y2;  u+, u- = y1 +- w^2 y3;
+// X0, X2 = t0 +- w u+;  X1, X3 = t1 +- W_4 w u-.
+template <bool INV>
+struct Dft<16, INV> {
+  template <int S1, int OFF, int ST, int NR>
+  __device__ __forceinline__ static void column(float2 (&x)[NR], const float2 (&y)[16]) {
+    float2 t0, t1, up, um, X0, X1, X2, X3;
+    twiddle_butterfly<16, 2 * S1, INV>(y[0 * 4 + S1], y[2 * 4 + S1], t0, t1);
+    twiddle_butterfly<16, 2 * S1, INV>(y[1 * 4 + S1], y[3 * 4 + S1], up, um);
+    twiddle_butterfly<16, S1, INV>(t0, up, X0, X2);
+    twiddle_butterfly<16, S1 + 4, INV>(t1, um, X1, X3);
+    x[OFF + ST * (S1 + 0)] = X0;
+    x[OFF + ST * (S1 + 4)] = X1;
+    x[OFF + ST * (S1 + 8)] = X2;
+    x[OFF + ST * (S1 + 12)] = X3;
+  }
+  template <int OFF, int ST, int NR>
+  __device__ __forceinline__ static void run(float2 (&x)[NR]) {
+    // y[r0*4 + s1] = DFT4 over r1 of x[OFF + ST*(r0 + 4 r1)]
+    float2 y[16];
+#pragma unroll
+    for (int r0 = 0; r0 < 4; ++r0)
+#pragma unroll
+      for (int r1 = 0; r1 < 4; ++r1) y[r0 * 4 + r1] = x[OFF + ST * (r0 + 4 * r1)];
+    Dft<4, INV>::template run<0, 1>(y);
+    Dft<4, INV>::template run<4, 1>(y);
+    Dft<4, INV>::template run<8, 1>(y);
+    Dft<4, INV>::template run<12, 1>(y);
+    column<0, OFF, ST>(x, y);
+    column<1, OFF, ST>(x, y);
+    column<2, OFF, ST>(x, y);
+    column<3, OFF, ST>(x, y);
+  }
+};
+
 // ------------------------------------------------------------- FFT plan --
 // TWS = log2(table length / N): the twiddle table always holds W_M^k, k < M,
 // for some M = N << TWS (M = 2N for a transform of the full half-length, 4N
@@ -261,6 +335,15 @@ struct Fft {
     }
   }
   static constexpr int LDS = N + (N >> (LR > 0 ? LR : 1)) + 1;  // float2 slots per transform
+  // Order in which a pass reads its RP inputs from LDS: grouped by the
+  // radix-4 sub-DFT of Dft<RP> that consumes them first (inputs r0 + A r1,
+  // A = RP / 4), so that sub-DFT can start while the later reads are still in
+  // flight.
+  template <int RP>
+  __host__ __device__ static constexpr int read_order(int j) {
+    constexpr int A = RP >= 4 ? RP / 4 : 1;
+    return RP >= 4 ? (j / 4) + A * (j % 4) : j;
+  }
 
   // Position (before padding) held by register i of thread tau after the
   // forward transform (digit-reversed order).
@@ -303,7 +386,10 @@ struct Fft {
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
-          for (int r = 0; r < RP; ++r) x[k][u * RP + r] = lds[k * LDS + pad(base + SP * r)];
+          for (int j = 0; j < RP; ++j) {
+            const int r = read_order<RP>(j);
+            x[k][u * RP + r] = lds[k * LDS + pad(base + SP * r)];
+          }
       }
     }
 #pragma unroll
@@ -354,7 +440,10 @@ struct Fft {
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
-          for (int s = 0; s < RP; ++s) x[k][u * RP + s] = lds[k * LDS + pad(base + SP * s)];
+          for (int j = 0; j < RP; ++j) {
+            const int s = read_order<RP>(j);
+            x[k][u * RP + s] = lds[k * LDS + pad(base + SP * s)];
+          }
       }
     }
     if constexpr (W0 && p == 0) {
