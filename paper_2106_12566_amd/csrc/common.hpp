@@ -51,7 +51,9 @@ struct Conf {
   // the convolution) for the lengths whose units cannot keep their twiddles
   // in registers.
   static constexpr bool TWC = L2 == 13;
-  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC>;  // twiddles come from the W_{2N} table
+  // twiddles come from the W_{2N} table; affine LDS addressing at N = 16384,
+  // where it removes most of the register spills
+  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC, L2 == 14>;
   static constexpr int N = 1 << L2;
   static constexpr int LT = F::N;  // transform length 2N / S
   static constexpr int G = F::T >= 128 ? 1 : 256 / F::T;  // units per work-group

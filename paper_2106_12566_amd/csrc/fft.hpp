@@ -274,7 +274,11 @@ struct Dft<16, INV> {
 // entries of the table (see twc_offset), instead of every 2^(LR p + TWS)-th
 // entry of W_M: a few KiB that stay in the L1 cache when the twiddles are
 // re-read per transform rather than kept in registers.
-template <int LOG2N_, int LOG2R_, int TWS = 1, bool TWC = false>
+// AFF: address LDS as pad(base) + constant per butterfly (see pad_step):
+// one address register instead of one per value, which frees registers but
+// lets the compiler pair accesses into 16-byte ds_read2 / ds_write2 forms,
+// slower than 8-byte ones where the LDS is the busier pipe.
+template <int LOG2N_, int LOG2R_, int TWS = 1, bool TWC = false, bool AFF = false>
 struct Fft {
   static constexpr int LOG2N = LOG2N_;
   static constexpr int N = 1 << LOG2N;
@@ -317,6 +321,11 @@ struct Fft {
     }
   }
   __host__ __device__ static constexpr int pad(int a) { return a + (a >> (LR > 0 ? LR : 1)); }
+  // pad(base + c) for the positions base + SP r of one butterfly (c = SP r):
+  // they never straddle a padding group unevenly, so the padded address is
+  // pad(base) plus a constant, pad(base + c) = pad(base) + c + (c >> LR)
+  // (checked exhaustively for every pass of every length and radix used).
+  __host__ __device__ static constexpr int pad_step(int c) { return c + (c >> (LR > 0 ? LR : 1)); }
   // Table entries: W_M (M), the per-thread first-pass table of the users
   // that keep one (M), then W_{L_p} for p = 1 .. P - 1.
   static constexpr int M_TAB = N << TWS;
@@ -382,13 +391,13 @@ struct Fft {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
-        const int base = (b / SP) * L + (b % SP);
+        const int base = (b / SP) * L + (b % SP), pb = pad(base);
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
           for (int j = 0; j < RP; ++j) {
             const int r = read_order<RP>(j);
-            x[k][u * RP + r] = lds[k * LDS + pad(base + SP * r)];
+            x[k][u * RP + r] = lds[k * LDS + (AFF ? pb + pad_step(SP * r) : pad(base + SP * r))];
           }
       }
     }
@@ -415,11 +424,11 @@ struct Fft {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
-        const int base = (b / SP) * L + (b % SP);
+        const int base = (b / SP) * L + (b % SP), pb = pad(base);
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
-          for (int s = 0; s < RP; ++s) lds[k * LDS + pad(base + SP * s)] = x[k][u * RP + s];
+          for (int s = 0; s < RP; ++s) lds[k * LDS + (AFF ? pb + pad_step(SP * s) : pad(base + SP * s))] = x[k][u * RP + s];
       }
       fwd_pass<p + 1, K, W0>(x, lds, tw, tau, w0);
     }
@@ -436,13 +445,13 @@ struct Fft {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
-        const int base = (b / SP) * L + (b % SP);
+        const int base = (b / SP) * L + (b % SP), pb = pad(base);
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
           for (int j = 0; j < RP; ++j) {
             const int s = read_order<RP>(j);
-            x[k][u * RP + s] = lds[k * LDS + pad(base + SP * s)];
+            x[k][u * RP + s] = lds[k * LDS + (AFF ? pb + pad_step(SP * s) : pad(base + SP * s))];
           }
       }
     }
@@ -469,11 +478,11 @@ struct Fft {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int b = tau + T * u;
-        const int base = (b / SP) * L + (b % SP);
+        const int base = (b / SP) * L + (b % SP), pb = pad(base);
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
-          for (int r = 0; r < RP; ++r) lds[k * LDS + pad(base + SP * r)] = x[k][u * RP + r];
+          for (int r = 0; r < RP; ++r) lds[k * LDS + (AFF ? pb + pad_step(SP * r) : pad(base + SP * r))] = x[k][u * RP + r];
       }
       inv_pass<p - 1, K, W0>(x, lds, tw, tau, w0);
     }
