@@ -36,6 +36,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -254,6 +255,123 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
         }
       } else {
         const float val = i < n ? expf(fmaf(acc[v], row_scale[ii], -half_sq[ii])) * inv_sqrt_m : 0.f;
+        if constexpr (FEATURE_MAJOR)
+          phi[(static_cast<size_t>(bh) * M + l) * ld + i] = val;
+        else
+          phi[(static_cast<size_t>(bh) * n + i) * M + l] = val;
+      }
+    }
+  }
+}
+
+// k_feature_map for d = 64 with the operands loaded straight into registers.
+// The MFMA sums over k in any order both operands agree on, so half-wave h
+// supplies k = 32 h + s at step s: each lane needs 32 contiguous values of
+// its x row and of its W row (8 float4 loads each, all in flight at once),
+// no LDS staging and no barriers.  The row norm is the lane's half plus the
+// other half-wave's.  Same tiles, outputs and epilogue as k_feature_map.
+template <typename TX>
+__device__ __forceinline__ void load_half_row64(const TX* __restrict__ row, bool ok, float (&r)[32]) {
+  if constexpr (std::is_same<TX, float>::value) {
+    const float4* p = reinterpret_cast<const float4*>(row);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float4 v = ok ? p[j] : make_float4(0.f, 0.f, 0.f, 0.f);
+      r[4 * j] = v.x;
+      r[4 * j + 1] = v.y;
+      r[4 * j + 2] = v.z;
+      r[4 * j + 3] = v.w;
+    }
+  } else {
+    const uint4* p = reinterpret_cast<const uint4*>(row);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint4 v = ok ? p[j] : make_uint4(0u, 0u, 0u, 0u);
+      const unsigned w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        r[8 * j + 2 * e] = __uint_as_float(w[e] << 16);
+        r[8 * j + 2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
+      }
+    }
+  }
+}
+
+template <typename TX, bool FEATURE_MAJOR>
+__global__ __launch_bounds__(256) void k_feature_map64(const TX* __restrict__ x0, const TX* __restrict__ x1,
+                                                       const float* __restrict__ W, float* __restrict__ phi0,
+                                                       float* __restrict__ phi1, int H, int n, int ld, int m,
+                                                       float inv_sqrt_m, int tiles_n, int tiles_m, int BH,
+                                                       unsigned* __restrict__ fix_counts, int nprf, int trf) {
+  constexpr int D = 64;
+  // Clear the exact-evaluation queue counters (fix_counts[0..BH]) for k_combine.
+  if (fix_counts && threadIdx.x == 0 && blockIdx.x <= static_cast<unsigned>(BH)) fix_counts[blockIdx.x] = 0u;
+  int bid = blockIdx.x;
+  const int tn = bid % tiles_n;
+  bid /= tiles_n;
+  const int tm = bid % tiles_m;
+  bid /= tiles_m;
+  const int bh = bid % BH;
+  const int src = bid / BH;
+  const TX* __restrict__ x = src == 0 ? x0 : x1;
+  float* __restrict__ phi = src == 0 ? phi0 : phi1;
+  const int h = bh % H;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, c = lane & 31;
+  const int i0 = tn * 64 + (wave & 1) * 32, l0 = tm * 64 + (wave >> 1) * 32;  // this wave's 32 x 32 tile
+  const int xi = i0 + c, wl = l0 + c;  // x row and W row this lane supplies
+  float xr[32], wr[32];
+  load_half_row64(x + (static_cast<size_t>(bh) * n + (xi < n ? xi : 0)) * D + 32 * half, xi < n, xr);
+  load_half_row64(W + (static_cast<size_t>(h) * m + (wl < m ? wl : 0)) * D + 32 * half, wl < m, wr);
+  float sq = 0.f;
+#pragma unroll
+  for (int s = 0; s < 32; ++s) sq = fmaf(xr[s], xr[s], sq);
+  sq += __shfl_xor(sq, 32);  // ||x||^2 of position xi
+  floatx16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+#pragma unroll
+  for (int s = 0; s < 32; ++s) {
+    if constexpr (FEATURE_MAJOR)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(wr[s], xr[s], acc, 0, 0, 0);
+    else
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(xr[s], wr[s], acc, 0, 0, 0);
+  }
+  const int n_store = FEATURE_MAJOR ? ld : n;
+  const int M = trf ? 2 * m : m;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    // 32x32 MFMA result layout: lane holds column lane%32, rows 8(v/4) + 4(lane/32) + v%4
+    const int row = 8 * (v >> 2) + 4 * half + (v & 3);
+    const int li = FEATURE_MAJOR ? row : c;  // feature within the wave tile
+    const int ii = FEATURE_MAJOR ? c : row;  // position within the wave tile
+    // ||x||^2 of position i0 + ii lives in lanes ii and ii + 32
+    const float sqi = FEATURE_MAJOR ? sq : __shfl(sq, ii);
+    const bool nz = sqi > 0.f;
+    // phi of x / ||x|| when normalising (Algorithm 1, first step): the
+    // projections scale by 1 / ||x|| and ||x||^2 / 2 becomes 1/2 (a zero row
+    // stays zero)
+    const float half_sq = nprf ? (nz ? 0.5f : 0.f) : 0.5f * sqi;
+    const float row_scale = nprf ? (nz ? rsqrtf(sqi) : 0.f) : 1.f;
+    const int l = l0 + li, i = i0 + ii;
+    if (i < n_store && l < m) {
+      if (trf) {
+        float sv = 0.f, cv = 0.f;
+        if (i < n) {
+          const float amp = expf(half_sq) * inv_sqrt_m;
+          sincosf(acc[v] * row_scale, &sv, &cv);
+          sv *= amp;
+          cv *= amp;
+        }
+        if constexpr (FEATURE_MAJOR) {
+          phi[(static_cast<size_t>(bh) * M + l) * ld + i] = sv;
+          phi[(static_cast<size_t>(bh) * M + m + l) * ld + i] = cv;
+        } else {
+          phi[(static_cast<size_t>(bh) * n + i) * M + l] = sv;
+          phi[(static_cast<size_t>(bh) * n + i) * M + m + l] = cv;
+        }
+      } else {
+        const float val = i < n ? expf(fmaf(acc[v], row_scale, -half_sq)) * inv_sqrt_m : 0.f;
         if constexpr (FEATURE_MAJOR)
           phi[(static_cast<size_t>(bh) * M + l) * ld + i] = val;
         else
@@ -1713,6 +1831,28 @@ hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const f
   const float inv_sqrt_m = static_cast<float>(1.0 / std::sqrt(static_cast<double>(m)));
   const dim3 grid(static_cast<unsigned>(blocks));
   const int np = nprf ? 1 : 0, trf = kind == kFeatTrf ? 1 : 0;
+  if (d == 64) {
+    if (bf16) {
+      const uint16_t* a = static_cast<const uint16_t*>(x0);
+      const uint16_t* c = static_cast<const uint16_t*>(x1);
+      if (feature_major)
+        hipLaunchKernelGGL((k_feature_map64<uint16_t, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
+                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+      else
+        hipLaunchKernelGGL((k_feature_map64<uint16_t, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
+                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+    } else {
+      const float* a = static_cast<const float*>(x0);
+      const float* c = static_cast<const float*>(x1);
+      if (feature_major)
+        hipLaunchKernelGGL((k_feature_map64<float, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
+                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+      else
+        hipLaunchKernelGGL((k_feature_map64<float, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
+                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+    }
+    return hipGetLastError();
+  }
   if (bf16) {
     const uint16_t* a = static_cast<const uint16_t*>(x0);
     const uint16_t* c = static_cast<const uint16_t*>(x1);
