@@ -38,6 +38,7 @@ def _say(*a):
     (2, 2, 257, 128, 200, "bf16", True),
     (1, 1, 70, 33, 130, "f32", False),
     (1, 1, 64, 16, 512, "f32", True),       # 1024 features, the most supported
+    (2, 1, 90, 64, 48, "bf16", True),       # d = 64 register-operand kernel, bf16
 ])
 def test_feature_map_trf(gpu_lib, B, H, n, d, m, dt, nprf):
     _say(f"feature_map trf B={B} H={H} n={n} d={d} m={m} {dt} nprf={nprf}")

@@ -27,6 +27,7 @@ def _say(*a):
     (1, 2, 1, 5, 3, "f32"),         # degenerate sizes
     (2, 2, 257, 128, 200, "bf16"),  # d = 128 (four K-chunks), bf16 inputs
     (1, 1, 70, 33, 130, "f32"),     # ragged d
+    (2, 2, 150, 64, 80, "bf16"),    # d = 64 register-operand kernel, bf16, ragged n and m
 ])
 def test_feature_map(gpu_lib, B, H, n, d, m, dt):
     _say(f"feature_map B={B} H={H} n={n} d={d} m={m} {dt}")
