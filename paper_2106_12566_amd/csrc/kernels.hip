@@ -1236,6 +1236,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       const int i = srows[r];
       sq[e] = i >= 0 ? pq[static_cast<size_t>(l) * ld + i] : 0.f;
     }
+    __syncthreads();  // sq staged
     double zt[16];
 #pragma unroll
     for (int v = 0; v < 16; ++v) zt[v] = 0.0;
@@ -1250,44 +1251,40 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       floatx16 sacc;
 #pragma unroll
       for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
-      // phi(k) of the chunk, kFixL features at a time; the next step's values
-      // are loaded into registers while the matrix cores work on this one
-      float kn[kFixL * kFixKeys / 256];
+      // phi(k) of the chunk, kFixL features at a time, loaded by every wave
+      // straight into its B operands (keys jc + 32 wave + lr, features l0 +
+      // 2 q + lk: 32 consecutive keys per half-wave, coalesced); the next
+      // step's values are in flight while the matrix cores work on this one
+      float kb[kFixL / 2], kn[kFixL / 2];
+      const int jkey = jc + wave * 32 + lr;
+      // uniform row base per step plus one per-lane offset (half-wave row, key)
+      const unsigned koff = static_cast<unsigned>(lk * ld + jkey);
       auto load_step = [&](int l0) {
 #pragma unroll
-        for (int q = 0; q < kFixL * kFixKeys / 256; ++q) {
-          const int e = tid + 256 * q;
-          const int l = l0 + e / kFixKeys, j = jc + e % kFixKeys;
-          kn[q] = (l < m && j < n) ? pk[static_cast<size_t>(l) * ld + j] : 0.f;
+        for (int q = 0; q < kFixL / 2; ++q) {
+          const float* __restrict__ prow = pk + static_cast<size_t>(l0 + 2 * q) * ld;
+          kn[q] = (l0 + 2 * q + lk < m && jkey < n) ? prow[koff] : 0.f;
         }
       };
       load_step(0);
       for (int l0 = 0; l0 < m; l0 += kFixL) {
-        __syncthreads();  // sq staged / sk free
 #pragma unroll
-        for (int q = 0; q < kFixL * kFixKeys / 256; ++q) {
-          const int e = tid + 256 * q;
-          sk[(e / kFixKeys) * kFixStride + e % kFixKeys] = kn[q];
-        }
-        __syncthreads();
+        for (int q = 0; q < kFixL / 2; ++q) kb[q] = kn[q];
         if (l0 + kFixL < m) load_step(l0 + kFixL);
         const int lend = min(kFixL, m - l0);
         if (lend == kFixL) {
-          // full step: all operands read first, then the matrix ops back to back
-          float qa[kFixL / 2], kb[kFixL / 2];
+          float qa[kFixL / 2];
 #pragma unroll
-          for (int q = 0; q < kFixL / 2; ++q) {
-            qa[q] = sq[(l0 + 2 * q + lk) * kFixRows + lr];
-            kb[q] = sk[(2 * q + lk) * kFixStride + wave * 32 + lr];
-          }
+          for (int q = 0; q < kFixL / 2; ++q) qa[q] = sq[(l0 + 2 * q + lk) * kFixRows + lr];
 #pragma unroll
           for (int q = 0; q < kFixL / 2; ++q) sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[q], kb[q], sacc, 0, 0, 0);
         } else {
-          for (int kk = 0; kk < lend; kk += 2) {
-            const int l = kk + lk;
+          // features past m load as zeros on the B side; the A side is zeroed too
+#pragma unroll
+          for (int q = 0; q < kFixL / 2; ++q) {
+            const int l = 2 * q + lk;
             const float qa = l < lend ? sq[(l0 + l) * kFixRows + lr] : 0.f;
-            const float kb = sk[l * kFixStride + wave * 32 + lr];
-            sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa, kb, sacc, 0, 0, 0);
+            sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa, kb[q], sacc, 0, 0, 0);
           }
         }
       }
