@@ -130,12 +130,16 @@ krpe_status_t record(void* const* events, int i, hipStream_t st) {
 // (512 resident units: 256 CUs x 2 work-groups), two ranges when that fills
 // the launch's last round of units better: one round in 32 left idle is worth
 // the doubled partial results (workload of 96 heads at n = 4096: 12.4 rounds,
-// 8.15 -> 8.05 ms).
+// 8.15 -> 8.05 ms).  At N = 16384 (one 512-thread work-group per CU) two
+// ranges measured faster at every shape with M >= 64 tried, by more than the
+// last round explains (16 heads, m = 256: 21.5 -> 18.5 ms; n = 65536 in
+// 4 x 4 blocks: 214 -> 190 ms); four were no faster than two.
 int conv_fsplit(int l2, int BH, int cols, int M, int nkb) {
   if (l2 > kMaxLog2N) return 1;
   const long long units = static_cast<long long>(conv_units(l2, BH, cols)) * nkb;
   int fs = 1;
   while (units * fs < 1024 && M / (2 * fs) >= 8) fs *= 2;
+  if (fs == 1 && l2 == kMaxLog2N && M >= 64) return 2;
   if (fs == 1 && l2 >= 9 && l2 <= 13 && M >= 64) {
     constexpr long long kResident = 512;
     auto idle = [](long long u) { return static_cast<double>((u + kResident - 1) / kResident * kResident - u) / u; };
