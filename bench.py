@@ -242,6 +242,63 @@ def cpu_baseline_rows(d: dict, budget_s: float, z_gpu: np.ndarray | None, nprf: 
     }, worst, done
 
 
+def time_config(wid: int, steps: int, warmup: int, route: str, rows: int = 16) -> dict:
+    """One synthetic workload at its stated size: forward time (wall clock over `steps` calls
+    after `warmup`, inputs resident on the GPU), stage times from the library's HIP events, the
+    route taken, the rows evaluated exactly, the convolution's fraction of the fp32 vector peak
+    (FFT route) or the exact-row kernel's fp32 MFMA rate (direct route), and the per-row
+    normwise error of `rows` sampled rows (plus the first and last) against the fp64 oracle."""
+    import torch
+    import oracle
+    from paper_2106_12566_amd import krpe, synth
+    d = synth.make(wid)
+    wl = d["workload"]
+    B, H, n, dd, m = wl.B, d["H"], wl.n, wl.d, wl.m
+    dev = torch.device("cuda", 0)
+    tdt = torch.bfloat16 if wl.qkv_dtype == "bf16" else torch.float32
+    q, k, v = (torch.from_numpy(d[x]).to(dev).to(tdt) for x in ("q", "k", "v"))
+    b, W = torch.from_numpy(d["b"]).to(dev), torch.from_numpy(d["W"]).to(dev)
+    out = torch.empty((B, H, n, dd), dtype=torch.float32, device=dev)
+    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, route=route), dtype=torch.uint8, device=dev)
+    hip = HipEvents()
+    events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(steps)]
+    for _ in range(warmup):
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=route)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], route=route)
+    torch.cuda.synchronize()
+    ms = 1e3 * (time.perf_counter() - t0) / steps
+    stage = [float(np.mean([hip.elapsed_ms(ev[i], ev[i + 1]) for ev in events])) for i in range(4)]
+    for ev in events:
+        for e in ev:
+            hip.destroy(e)
+    used = krpe.attention_fwd_route(B, H, n, dd, m, route=route)
+    res = {"workload": wl.name, "B": B, "H": H, "n": n, "m": m, "qkv_dtype": wl.qkv_dtype, "route": used,
+           "ms_per_layer": ms, "tokens_per_s": B * n / (ms * 1e-3),
+           "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)}
+    if used == "fft":
+        tf = conv_stage_flops(B, H, n, dd, m, d["b"]) / (stage[2] * 1e-3) / 1e12
+        res.update({"conv_ms": stage[2], "conv_tflops": tf, "conv_frac": tf / PEAK_FP32_VECTOR_TFLOPS,
+                    "rest_ms": stage[0] + stage[1] + stage[3]})
+    else:
+        tf = direct_flops(B, H, n, dd, m, d["b"]) / (stage[3] * 1e-3) / 1e12
+        res.update({"exact_kernel_ms": stage[3], "exact_kernel_tflops": tf,
+                    "exact_kernel_frac": tf / PEAK_FP32_VECTOR_TFLOPS})
+    rng = np.random.default_rng([2106, 12566, 97, wid])
+    sel = [(0, 0, 0), (B - 1, H - 1, n - 1)] + [(int(rng.integers(B)), int(rng.integers(H)), int(rng.integers(n)))
+                                                for _ in range(rows)]
+    zr, _ = oracle.attention_rows(d["q"], d["k"], d["v"], d["b"], d["W"], sel)
+    zg = out.cpu().numpy()
+    got = np.stack([zg[bb, hh, i] for bb, hh, i in sel])
+    res["parity_rownorm_err_sampled"] = float(np.max(np.max(np.abs(got - zr), axis=-1)
+                                                     / np.max(np.abs(zr), axis=-1)))
+    res["parity_rows"] = len(sel)
+    del ws, out
+    return res
+
+
 def sweep(lengths, ms, heads, steps: int) -> int:
     """Forward time against sequence length with d = 64 (the paper's speed test setting is one
     head), each m and head count, both routes; one JSON line per (H, n, m, route) on stdout."""
@@ -282,6 +339,9 @@ def main() -> int:
     ap.add_argument("--sweep-heads", default="1", help="comma-separated head counts of the sweep")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle time on the host")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload results (workloads 1-5 at their stated sizes, by the route "
+                         "the library picks and, where that is the direct one, by the FFT route too)")
     ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
                     help="feature map of Section 2: PRF (Eq. (5)), trigonometric (2m features) or elu + 1 (m = d)")
     ap.add_argument("--route", choices=["auto", "fft", "direct"], default="auto",
@@ -427,6 +487,18 @@ def main() -> int:
             dst.copy_(src)
         torch.cuda.synchronize()
         result["config"]["copy_calibration_bytes"] = src.numel() * 4
+    if not args.no_configs and fm == "prf" and not args.nprf and rt == "auto":
+        per = {}
+        for wid in range(1, 6):
+            res = time_config(wid, max(3, min(args.steps, 10)), max(1, min(args.warmup, 3)), "auto")
+            if res["route"] == "direct":
+                fft = time_config(wid, max(3, min(args.steps, 10)), max(1, min(args.warmup, 3)), "fft")
+                res["fft_route"] = {k2: fft[k2] for k2 in ("ms_per_layer", "conv_ms", "conv_frac", "exact_rows",
+                                                            "parity_rownorm_err_sampled")}
+            per[str(wid)] = res
+            print(f"bench: workload {wid} {res['workload']}: {res['ms_per_layer']:.3f} ms/layer ({res['route']})",
+                  file=sys.stderr, flush=True)
+        result["config"]["per_workload"] = per
     if not args.no_cpu_baseline:
         z_gpu = out.cpu().numpy()
         cb, err, units = cpu_baseline(d, args.cpu_budget, z_gpu, nprf=args.nprf, kind=fm)

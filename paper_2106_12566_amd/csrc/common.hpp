@@ -51,9 +51,14 @@ struct Conf {
   // the convolution) for the lengths whose units cannot keep their twiddles
   // in registers.
   static constexpr bool TWC = L2 == 13;
-  // twiddles come from the W_{2N} table; affine LDS addressing at N = 16384,
-  // where it removes most of the register spills
-  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC, L2 == 14>;
+  // phi rows and value pairs read through buffer resources, with phi(k) (and
+  // at N = 4096 phi(q)) loaded a feature ahead: measured faster at N = 2048
+  // and 4096 only (slower at 512, 1024 and 16384).
+  static constexpr bool BUF = L2 == 11 || L2 == 12;
+  // Twiddles come from the W_{2N} table.  Affine LDS addressing where it
+  // frees the registers that the loads one feature ahead need, and at
+  // N = 16384.
+  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC, L2 == 14 || BUF>;
   static constexpr int N = 1 << L2;
   static constexpr int LT = F::N;  // transform length 2N / S
   static constexpr int G = F::T >= 128 ? 1 : 256 / F::T;  // units per work-group
@@ -76,6 +81,9 @@ struct Conf {
   static constexpr bool PREF = VREG && WPE == 1;
   static constexpr bool HREG = THREADS <= 256 || L2 == 14;
   static constexpr bool HOIST = (THREADS <= 256 && FOLD != 2) || L2 == 14;
+  // phi(q) too loaded a feature ahead (where the registers allow it without
+  // spills)
+  static constexpr bool NEXTQ = L2 == 12;
 };
 
 // Work-groups are dispatched round-robin over the 8 XCDs (each with its own
@@ -87,6 +95,24 @@ __device__ __forceinline__ int xcd_block(int b, int nblocks) {
   const int xcd = b % kXcd, slot = b / kXcd;
   return (xcd < rem) ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
 }
+
+// Reads through a raw buffer resource (gfx9 descriptor: base, byte range,
+// word 3 = 0x00020000): a per-lane byte offset (VGPR) plus a wave-uniform
+// byte offset (SGPR), with no 64-bit address arithmetic per load.  Reads at
+// or past `bytes` return zero.
+struct BufRd {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ __forceinline__ BufRd(const void* base, uint32_t bytes)
+      : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000)) {}
+  __device__ __forceinline__ float f32(uint32_t voff, uint32_t soff) const {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+  }
+  // (The 8-byte result is bit-cast whole: taking its two halves apart by index
+  // lowers to a single 4-byte load.)
+  __device__ __forceinline__ float2 f64(uint32_t voff, uint32_t soff) const {
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+  }
+};
 
 __device__ __forceinline__ float to_f32(float v) { return v; }
 __device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float(static_cast<uint32_t>(v) << 16); }

@@ -17,7 +17,9 @@
 //                    with phi(q), all in registers/LDS of one work-group.
 //  k_combine         the ratio of Eq. (10), plus a per-row rounding-error bound.
 //  k_fixup           exact evaluation of Eq. (10) for rows the bound rejects.
-//  k_toeplitz        the Toeplitz product alone (the krpe_toeplitz_conv op).
+//
+// The Toeplitz product alone (krpe_toeplitz_conv) runs k_conv_contract with
+// phi(q) = phi(k) = a row of ones and the channels as the value columns.
 //
 // The Toeplitz product of a length-n signal a is the first n outputs of the
 // circular convolution of length L = 2N (N = next power of two >= n) of the
@@ -590,6 +592,29 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
   // loop, phi_l(q) being real and the rotation linear.
   constexpr bool PRETWIST = MERGE && KH == 1 && FOLD == 1 && VREG && R0 != 0;
   constexpr int NP = FOLD * F::N;  // row length of phi and v
+  // With C::BUF, phi rows and value pairs are read through buffer resources:
+  // the lane's byte offset in a VGPR, the feature's and register's offset in
+  // an SGPR (no 64-bit address arithmetic per load); reads past the unit's
+  // rows return zero.  Otherwise through plain pointers.
+  constexpr bool BUF = C::BUF;
+  const BufRd bk(pk, static_cast<uint32_t>(m) * NP * 4u), bq(pq, static_cast<uint32_t>(m) * NP * 4u);
+  const BufRd bv(vrow, static_cast<uint32_t>(NP) * 8u);
+  auto phi_at = [&](bool kside, int ta, int l, int p, int i) {
+    if constexpr (BUF) {
+      return (kside ? bk : bq).f32(static_cast<uint32_t>(ta) * 4u,
+                                   static_cast<uint32_t>(l * NP + F::T * i + p * F::N) * 4u);
+    } else {
+      return (kside ? pk : pq)[static_cast<size_t>(l) * NP + ta + F::T * i + p * F::N];
+    }
+  };
+  auto v_at = [&](int ta, int p, int i) {
+    if constexpr (BUF) {
+      return bv.f64(static_cast<uint32_t>(ta) * 8u, static_cast<uint32_t>(F::T * i + p * F::N) * 8u);
+    } else {
+      return vrow[ta + F::T * i + p * F::N];
+    }
+  };
+  constexpr bool KS = true, QS = false;
   // Spectrum classes, register order (see k_spectrum): kept in registers when
   // the work-group is small enough, else re-read just before the product.
   float2 Hr[HREG ? KH : 1][F::R];
@@ -605,7 +630,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
     for (int p = 0; p < FOLD; ++p)
 #pragma unroll
       for (int i = 0; i < F::R; ++i) {
-        const float2 vv = vrow[tau + F::T * i + p * F::N];
+        const float2 vv = v_at(tau, p, i);
         vx[p][i] = PRETWIST ? rot_dyn<F::R * S, false>(vv, R0 * i) : vv;
       }
   }
@@ -623,19 +648,29 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
                          : t[(R0 + k) * (ta + F::T * i)];
   };
   if constexpr (HOIST) load_w0(tw, tau);
-  // With registers to spare, phi(k) of the next feature is loaded at the top
-  // of the iteration and stays in flight across the transform (the barriers
-  // only wait for LDS traffic).
-  float a_next[PREF ? FOLD : 1][PREF ? F::R : 1];
-  if constexpr (PREF) {
+  // phi(k) of the next feature is loaded a whole feature ahead so that its
+  // latency is hidden behind the transforms: with registers to spare (PREF) at
+  // the top of the iteration, else (NEXTK) with this feature's phi(q) after
+  // the inverse transform; with C::NEXTQ phi(q) too is loaded a feature
+  // ahead.
+  constexpr bool NEXTK = VREG && !PREF && BUF;
+  constexpr bool NEXTQ = NEXTK && C::NEXTQ;
+  constexpr bool AHEAD = PREF || NEXTK;
+  float a_next[AHEAD ? FOLD : 1][AHEAD ? F::R : 1];
+  float f_next[NEXTQ ? FOLD : 1][NEXTQ ? F::R : 1];
+  if constexpr (AHEAD) {
 #pragma unroll
     for (int p = 0; p < FOLD; ++p)
 #pragma unroll
-      for (int i = 0; i < F::R; ++i) a_next[p][i] = pk[tau + F::T * i + p * F::N];
+      for (int i = 0; i < F::R; ++i) a_next[p][i] = phi_at(KS, tau, 0, p, i);
+  }
+  if constexpr (NEXTQ) {
+#pragma unroll
+    for (int p = 0; p < FOLD; ++p)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i) f_next[p][i] = phi_at(QS, tau, 0, p, i);
   }
   for (int l = 0; l < m; ++l) {
-    const float* __restrict__ pkl = pk + static_cast<size_t>(l) * NP;
-    const float* __restrict__ pql = pq + static_cast<size_t>(l) * NP;
     // Large work-groups have too few registers to keep the loop-invariant
     // twiddles: hide the table pointer from loop-invariant code motion so they
     // are re-read (from L1) inside the transforms instead.
@@ -653,17 +688,17 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
     for (int p = 0; p < FOLD; ++p)
 #pragma unroll
       for (int i = 0; i < F::R; ++i)
-        a[p][i] = PREF ? a_next[PREF ? p : 0][PREF ? i : 0] : pkl[taul + F::T * i + p * F::N];
+        a[p][i] = AHEAD ? a_next[AHEAD ? p : 0][AHEAD ? i : 0] : phi_at(KS, taul, l, p, i);
     if constexpr (PREF) {
 #pragma unroll
       for (int p = 0; p < FOLD; ++p)
 #pragma unroll
-        for (int i = 0; i < F::R; ++i) f[p][i] = pql[tau + F::T * i + p * F::N];
-      if (l + 1 < m) {
+        for (int i = 0; i < F::R; ++i) f[p][i] = phi_at(QS, tau, l, p, i);
+      if (BUF || l + 1 < m) {  // (buffer reads past the last feature give zero)
 #pragma unroll
         for (int p = 0; p < FOLD; ++p)
 #pragma unroll
-          for (int i = 0; i < F::R; ++i) a_next[p][i] = pkl[NP + tau + F::T * i + p * F::N];
+          for (int i = 0; i < F::R; ++i) a_next[p][i] = phi_at(KS, tau, l + 1, p, i);
       }
     }
     float2 x[KH][F::R];
@@ -672,7 +707,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       float2 xb[FOLD];
 #pragma unroll
       for (int p = 0; p < FOLD; ++p) {
-        const float2 vv = VREG ? vx[VREG ? p : 0][VREG ? i : 0] : vrow[taul + F::T * i + p * F::N];
+        const float2 vv = VREG ? vx[VREG ? p : 0][VREG ? i : 0] : v_at(taul, p, i);
         xb[p] = make_float2(a[p][i] * vv.x, a[p][i] * vv.y);
       }
       constexpr_for<KH>([&](auto kc) {
@@ -716,7 +751,16 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
 #pragma unroll
       for (int p = 0; p < FOLD; ++p)
 #pragma unroll
-        for (int i = 0; i < F::R; ++i) f[p][i] = pql[taul + F::T * i + p * F::N];
+        for (int i = 0; i < F::R; ++i) {
+          // (NEXTK and NEXTQ come with buffer reads: zero past the last feature)
+          if constexpr (NEXTQ) {
+            f[p][i] = f_next[NEXTQ ? p : 0][NEXTQ ? i : 0];
+            f_next[NEXTQ ? p : 0][NEXTQ ? i : 0] = phi_at(QS, taul, l + 1, p, i);
+          } else {
+            f[p][i] = phi_at(QS, taul, l, p, i);
+          }
+          if constexpr (NEXTK) a_next[NEXTK ? p : 0][NEXTK ? i : 0] = phi_at(KS, taul, l + 1, p, i);
+        }
     }
 #pragma unroll
     for (int i = 0; i < F::R; ++i) {

@@ -5,12 +5,14 @@ dq, dk, dv, db of L = sum(dz * z) against the fp64 oracle's chain rule
 seeded inputs and output gradients.
 
 Tolerance: per (batch, head), the largest absolute error of each gradient
-relative to that gradient's largest entry, <= 5e-4 for fp32 inputs and <= 2e-2
-for bf16.  The forward's fp32 bar is 2e-4 with its uncertified rows
-evaluated exactly; the backward has no exact path, and the rows with small
-denominators (the first rows under a causal mask) enter its products through
-dz / den with a weight the FFT's error, spread over the sequence, sees in
-every position (the worst fp32 case here, causal n = 17, is 6e-5).
+relative to that gradient's largest entry, <= 2e-4 for fp32 inputs and <= 2e-2
+for bf16 (the forward's bars), except the fp32 cases under a causal mask,
+which are allowed 5e-4 (CAUSAL_F32 below): the backward has no exact path, and
+the rows with small denominators (the first rows under a causal mask, whose
+window holds a single key) enter its products through dz / den with a weight
+the FFT's error, spread over the sequence, sees in every position.  Measured:
+dk 2.3e-4 of its largest entry at causal n = 17 with three heads, dq 3.0e-4
+at causal n = 5000; every other case stays within 2e-4.
 Gradients mix positive and negative terms (dx = (dphi o phi) W - x rowsum),
 so an elementwise relative error is ill-posed, as for z.  Where the exact gradient vanishes (one key, n = 1; or
 one feature, m = 1, whose phi(q_i) cancels from Eq. (10)) the reference scale
@@ -25,9 +27,12 @@ import oracle
 from paper_2106_12566_amd import synth
 from parity_util import TOL, to_gpu
 
-BWD_TOL = {"f32": 5e-4, "bf16": TOL["bf16"]}
+BWD_TOL = {"f32": TOL["f32"], "bf16": TOL["bf16"]}
 
 pytestmark = pytest.mark.gpu
+
+# bar of the fp32 cases under a causal mask (see the module docstring)
+CAUSAL_F32 = 5e-4
 
 
 def _say(*a):
@@ -71,6 +76,7 @@ def test_backward_matches_oracle(gpu_lib, B, H, n, d, m, dt, bias, nprf):
     dq, dk, dv, db = (t.cpu().numpy() for t in gpu_lib.attention_bwd(q, k, v, b, W, to_gpu(G), nprf=nprf,
                                                                      with_db=True))
     ref = oracle.attention_grad(dd["q"], dd["k"], dd["v"], dd["b"], dd["W"], G, nprf=nprf)
+    tol = CAUSAL_F32 if (dt == "f32" and bias == "causal") else BWD_TOL[dt]
     gmax = float(np.max(np.abs(G)))
     vmax = max(1.0, float(np.max(np.abs(dd["v"]))))
     wmax = float(np.max(np.abs(dd["W"])))
@@ -80,12 +86,12 @@ def test_backward_matches_oracle(gpu_lib, B, H, n, d, m, dt, bias, nprf):
     assert np.all(db[~np.isfinite(dd["b"])] == 0.0)
     derr = float(np.max(np.abs(db - ref[3])) / max(np.max(np.abs(ref[3])), 1e-3 * gmax * vmax))
     _say(f"  db: err={derr:.3e}")
-    assert derr <= BWD_TOL[dt], ("db", derr)
+    assert derr <= tol, ("db", derr)
     for name, got, r in zip(("dq", "dk", "dv"), (dq, dk, dv), ref[:3]):
         assert np.all(np.isfinite(got)), name
         err = _head_err(got, r, floors[name])
         _say(f"  {name}: err={err:.3e}")
-        assert err <= BWD_TOL[dt], (name, err)
+        assert err <= tol, (name, err)
 
 
 def test_backward_is_linear_in_dz(gpu_lib):

@@ -7,7 +7,7 @@ broken copies of it and show that every planted mistake is caught.
 Sources of truth used here (none of them re-types the oracle's formula):
 * brute force with scalar Python loops straight from Eq. (5) and Eq. (10);
 * the paper's own factorisation route: vec-stacked A_1, A_2, the Toeplitz
-  matrix of Eqs. (12)-(13) and the final ratio of Algorithm 1;
+  matrix of Eqs. (12)-(13) and the ratio of Eq. (10);
 * the closed form Eq. (3) (linear attention) that Eq. (10) reduces to when b
   is constant, and its prefix-sum form under the causal mask;
 * the PRF variance lemma of Section 3.3 (unbiasedness and exact variance of the PRF kernel estimate);
@@ -98,26 +98,33 @@ def check_brute_force(impl):
         assert _rownorm_err(z, _brute_attention(q, k, v, b, W)) < 1e-12, (n, d, m)
 
 
-def check_algorithm1_route(impl):
-    """Vec-stacked A_1, A_2 (Eq. (11)), D = C A (Eqs. (12)-(13)), then the ratio."""
+def check_toeplitz_factorisation(impl):
+    """Eqs. (11)-(13): with A the n x (m d + m) matrix whose row j is
+    [vec(phi(k_j)^T v_j), phi(k_j)] and C = {c_{j-i}}, every entry of
+    D-tilde = C A equals its summation form sum_j c_{j-i} A[j, :] (scalar
+    loops), and phi(q_i) applied to the two blocks of row i gives the
+    numerator and denominator of Eq. (10) (the oracle's z and den)."""
     rng = np.random.default_rng(12)
     n, d, m = 13, 5, 6
     q, k, v, b, W = _rand_case(rng, 1, 1, n, d, m)
     Wh, bh = W[0], b[0]
     phi = lambda x: np.exp(x @ Wh.T - 0.5 * (x * x).sum(-1, keepdims=True)) / np.sqrt(m)
-    fq, fk = phi(q[0, 0]), phi(k[0, 0])
-    A1 = np.stack([np.outer(fk[j], v[0, 0, j]).reshape(-1) for j in range(n)])   # n x (m d)
-    A2 = fk                                                                       # n x m
-    C = np.empty((n, n))
-    for i in range(n):                      # row i: c_{-i}, ..., c_{n-1-i}
-        for j in range(n):
-            C[i, j] = math.exp(bh[(j - i) + n - 1])
-    D1 = (C @ A1).reshape(n, m, d)
-    D2 = C @ A2
-    X = np.stack([(fq[i] @ D1[i]) / (fq[i] @ D2[i]) for i in range(n)])
+    fq, fk, vv = phi(q[0, 0]), phi(k[0, 0]), v[0, 0]
+    A = np.concatenate([np.einsum("jl,jc->jlc", fk, vv).reshape(n, m * d), fk], axis=1)
+    C = np.array([[math.exp(bh[(j - i) + n - 1]) for j in range(n)] for i in range(n)])
+    Dt = C @ A
+    for i in (0, 4, n - 1):
+        for l in (0, m - 1):
+            for c in (0, d - 1):
+                s1 = sum(math.exp(bh[j - i + n - 1]) * fk[j, l] * vv[j, c] for j in range(n))
+                assert abs(Dt[i, l * d + c] - s1) <= 1e-13 * abs(s1)
+            s2 = sum(math.exp(bh[j - i + n - 1]) * fk[j, l] for j in range(n))
+            assert abs(Dt[i, m * d + l] - s2) <= 1e-13 * abs(s2)
+    num = np.einsum("il,ilc->ic", fq, Dt[:, : m * d].reshape(n, m, d))
+    den_ref = np.einsum("il,il->i", fq, Dt[:, m * d:])
     z, den = impl.attention(q, k, v, b, W)
-    assert _rownorm_err(z[0, 0], X) < 1e-12
-    assert np.allclose(den[0, 0], np.einsum("il,il->i", fq, D2), rtol=1e-12)
+    assert _rownorm_err(z[0, 0], num / den_ref[:, None]) < 1e-12
+    assert np.allclose(den[0, 0], den_ref, rtol=1e-12)
 
 
 def check_single_position(impl):
@@ -516,7 +523,7 @@ def check_grad_invariants(impl):
     assert np.max(np.abs(np.sum(dk * k, axis=-1))) < 1e-10 * np.max(np.abs(dk)) * np.max(np.abs(k))
 
 
-ALL_CHECKS = [check_brute_force, check_algorithm1_route, check_single_position,
+ALL_CHECKS = [check_brute_force, check_toeplitz_factorisation, check_single_position,
               check_const_bias_is_linear_attention, check_causal_prefix_sums,
               check_only_diagonal, check_shift_kernel, check_invariants,
               check_causality, check_prf_variance_lemma, check_toeplitz_special_cases,
