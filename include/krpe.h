@@ -44,7 +44,8 @@
  * - Precondition (not checked: it would need to read device memory): every
  *   query row's window of b holds a finite entry (b_0 finite suffices), so
  *   every denominator of Eq. (10) is > 0.  Otherwise that row of z is NaN.
- * - Functions are stateless and thread-safe.
+ * - Functions are stateless and thread-safe, except krpe_toeplitz_conv_noalloc,
+ *   whose calls on one GPU share a static workspace (see its note).
  */
 #ifndef KRPE_H_
 #define KRPE_H_
@@ -155,6 +156,25 @@ size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n);
 krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
                                  int B, int H, int C, int n,
                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * krpe_toeplitz_conv for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid hipMalloc):
+ * the same product with no workspace argument.  Its workspace is a static
+ * device array of KRPE_NOALLOC_SCRATCH_BYTES bytes inside the library, one
+ * copy per GPU, held from the library's load until the process ends; the call
+ * allocates and frees nothing.  Sizes whose workspace (the value of
+ * krpe_toeplitz_conv_workspace) exceeds it return KRPE_ERR_UNSUPPORTED before
+ * any HIP call.  Every call on a GPU shares that GPU's array: calls that
+ * overlap on one GPU (two streams, or two threads) race and must be
+ * serialised by the caller.  The array keeps the last call's contents; every
+ * call writes all of the workspace it reads.  The first call on a device
+ * looks the array's address up (hipGetSymbolAddress), briefly making the
+ * stream's device current if it is not.
+ */
+#define KRPE_NOALLOC_SCRATCH_BYTES (64u << 20)
+krpe_status_t krpe_toeplitz_conv_noalloc(const float* b, const float* a, float* y,
+                                         int B, int H, int C, int n, void* stream);
 
 /*
  * Bytes of workspace krpe_attention_fwd needs (0 if the sizes are invalid or

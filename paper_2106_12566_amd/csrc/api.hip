@@ -4,6 +4,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 #include <string>
 
 #include "common.hpp"
@@ -469,6 +470,99 @@ krpe_status_t run_forward_long(const LongLayout& L, char* w, const void* q, cons
   return record(events, 4, st);
 }
 
+// ------------------------------------------------ no-allocation scratch --
+// Workspace of krpe_toeplitz_conv_noalloc: a file-scope device array, one copy
+// per GPU the library runs on, held from the library's load until the process
+// ends.  Host code uses it only through the device address that
+// hipGetSymbolAddress returns (looked up once per device, with that device
+// current): the array's name on the host is a stand-in, not that address.
+constexpr size_t kScratchBytes = static_cast<size_t>(KRPE_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device, once looked up
+
+// Device address of the scratch array on the device `stream` belongs to (the
+// current device for the null stream).  The first call on a device makes that
+// device current for the lookup and restores the caller's.
+krpe_status_t scratch_address(hipStream_t stream, void** out) {
+  int cur = 0;
+  if (krpe_status_t s = hip_check(hipGetDevice(&cur), "hipGetDevice")) return s;
+  int dev = cur;
+  if (stream) {
+    hipDevice_t sd = 0;
+    if (krpe_status_t s = hip_check(hipStreamGetDevice(stream, &sd), "hipStreamGetDevice")) return s;
+    dev = static_cast<int>(sd);
+  }
+  if (dev < 0 || dev >= kMaxDevices) return fail(KRPE_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur)
+      if (krpe_status_t s = hip_check(hipSetDevice(dev), "hipSetDevice")) return s;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
+    if (krpe_status_t s = hip_check(e, "hipGetSymbolAddress(scratch)")) return s;
+    if (!p) return fail(KRPE_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return KRPE_OK;
+}
+}  // namespace
+
+// The Toeplitz product of krpe_toeplitz_conv on a given workspace.
+krpe_status_t toeplitz_conv(const float* b, const float* a, float* y, int B, int H, int C, int n, void* ws,
+                            size_t ws_bytes, void* stream) {
+  if (C < 0) return fail(KRPE_ERR_SHAPE, "negative size");
+  if (krpe_status_t s = check_dims(B, H, n, 0, 0, false)) return s;
+  if (static_cast<long long>(B) * H * C * n >= (1LL << 31))
+    return fail(KRPE_ERR_UNSUPPORTED, "B * H * C * n >= 2^31 is not supported");
+  const size_t bh = static_cast<size_t>(B) * H;
+  if (bh == 0 || C == 0) return KRPE_OK;
+  if (!b || !a || !y) return fail(KRPE_ERR_NULL, "b, a and y must be non-NULL");
+  if (misaligned(b) || misaligned(a) || misaligned(y) || misaligned(ws))
+    return fail(KRPE_ERR_ALIGN, "b, a, y, ws must be 16-byte aligned");
+  const ConvLayout L = conv_layout(B, H, C, n);
+  if (!ws || ws_bytes < L.total)
+    return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
+  const Range ry{y, bh * C * n * sizeof(float)};
+  const Range rws{ws, ws_bytes};
+  const Range ra{a, bh * C * n * sizeof(float)};
+  const Range rb{b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)};
+  if (overlaps(ry, ra) || overlaps(ry, rb) || overlaps(ry, rws) || overlaps(rws, ra) || overlaps(rws, rb))
+    return fail(KRPE_ERR_ALIAS, "y or the workspace overlaps an input");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  float2* tw = reinterpret_cast<float2*>(w + L.tw);
+  float2* Hs = reinterpret_cast<float2*>(w + L.hs);
+  float* ones = reinterpret_cast<float*>(w + L.ones);
+  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
+  float* colmax = reinterpret_cast<float*>(w + L.colmax);
+  float* vmax = reinterpret_cast<float*>(w + L.vmax);
+  float* part = reinterpret_cast<float*>(w + L.part);
+  const int BHi = static_cast<int>(bh);
+  const int N = 1 << L.l2;
+  const int splits = conv_splits(L.l2);
+  // The product runs through the attention's convolution kernel with one
+  // feature equal to 1 everywhere: a_c plays the role of the value column c.
+  if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
+  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch")) return s;
+  if (krpe_status_t s = hip_check(launch_ones(ones, n, N, st), "ones launch")) return s;
+  if (krpe_status_t s = hip_check(launch_vprep(false, a, 1, n, static_cast<long long>(C) * n, C, false, BHi, n, N,
+                                               vmax, colmax, vsc, st),
+                                  "column launch"))
+    return s;
+  if (krpe_status_t s = hip_check(launch_conv(L.l2, ones, ones, 0, vsc, colmax, Hs, tw, splits > 1 ? part : y, BHi,
+                                              H, n, C, 1, st),
+                                  "conv launch"))
+    return s;
+  if (splits > 1) return hip_check(launch_sum_splits(part, y, BHi, C, n, splits, st), "sum launch");
+  return KRPE_OK;
+}
+
 }  // namespace krpe
 
 using namespace krpe;
@@ -530,51 +624,26 @@ size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n) {
 krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y, int B, int H, int C, int n, void* ws,
                                  size_t ws_bytes, void* stream) {
   g_last_error.clear();
+  return toeplitz_conv(b, a, y, B, H, C, n, ws, ws_bytes, stream);
+}
+
+krpe_status_t krpe_toeplitz_conv_noalloc(const float* b, const float* a, float* y, int B, int H, int C, int n,
+                                         void* stream) {
+  g_last_error.clear();
+  // sizes first (no HIP call for a rejected request), then the workspace
   if (C < 0) return fail(KRPE_ERR_SHAPE, "negative size");
   if (krpe_status_t s = check_dims(B, H, n, 0, 0, false)) return s;
   if (static_cast<long long>(B) * H * C * n >= (1LL << 31))
     return fail(KRPE_ERR_UNSUPPORTED, "B * H * C * n >= 2^31 is not supported");
-  const size_t bh = static_cast<size_t>(B) * H;
-  if (bh == 0 || C == 0) return KRPE_OK;
-  if (!b || !a || !y) return fail(KRPE_ERR_NULL, "b, a and y must be non-NULL");
-  if (misaligned(b) || misaligned(a) || misaligned(y) || misaligned(ws))
-    return fail(KRPE_ERR_ALIGN, "b, a, y, ws must be 16-byte aligned");
-  const ConvLayout L = conv_layout(B, H, C, n);
-  if (!ws || ws_bytes < L.total)
-    return fail(KRPE_ERR_WORKSPACE, "workspace needs " + std::to_string(L.total) + " bytes");
-  const Range ry{y, bh * C * n * sizeof(float)};
-  const Range rws{ws, ws_bytes};
-  const Range ra{a, bh * C * n * sizeof(float)};
-  const Range rb{b, static_cast<size_t>(H) * (2 * n - 1) * sizeof(float)};
-  if (overlaps(ry, ra) || overlaps(ry, rb) || overlaps(ry, rws) || overlaps(rws, ra) || overlaps(rws, rb))
-    return fail(KRPE_ERR_ALIAS, "y or the workspace overlaps an input");
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  char* w = static_cast<char*>(ws);
-  float2* tw = reinterpret_cast<float2*>(w + L.tw);
-  float2* Hs = reinterpret_cast<float2*>(w + L.hs);
-  float* ones = reinterpret_cast<float*>(w + L.ones);
-  float2* vsc = reinterpret_cast<float2*>(w + L.vsc);
-  float* colmax = reinterpret_cast<float*>(w + L.colmax);
-  float* vmax = reinterpret_cast<float*>(w + L.vmax);
-  float* part = reinterpret_cast<float*>(w + L.part);
-  const int BHi = static_cast<int>(bh);
-  const int N = 1 << L.l2;
-  const int splits = conv_splits(L.l2);
-  // The product runs through the attention's convolution kernel with one
-  // feature equal to 1 everywhere: a_c plays the role of the value column c.
-  if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
-  if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch")) return s;
-  if (krpe_status_t s = hip_check(launch_ones(ones, n, N, st), "ones launch")) return s;
-  if (krpe_status_t s = hip_check(launch_vprep(false, a, 1, n, static_cast<long long>(C) * n, C, false, BHi, n, N,
-                                               vmax, colmax, vsc, st),
-                                  "column launch"))
-    return s;
-  if (krpe_status_t s = hip_check(launch_conv(L.l2, ones, ones, 0, vsc, colmax, Hs, tw, splits > 1 ? part : y, BHi,
-                                              H, n, C, 1, st),
-                                  "conv launch"))
-    return s;
-  if (splits > 1) return hip_check(launch_sum_splits(part, y, BHi, C, n, splits, st), "sum launch");
-  return KRPE_OK;
+  if (static_cast<size_t>(B) * H == 0 || C == 0) return KRPE_OK;
+  const size_t need = conv_layout(B, H, C, n).total;
+  if (need > kScratchBytes)
+    return fail(KRPE_ERR_UNSUPPORTED, "these sizes need " + std::to_string(need) +
+                                          " bytes of workspace, more than the " + std::to_string(kScratchBytes) +
+                                          " of the static scratch: use krpe_toeplitz_conv with a workspace");
+  void* ws = nullptr;
+  if (krpe_status_t s = scratch_address(static_cast<hipStream_t>(stream), &ws)) return s;
+  return toeplitz_conv(b, a, y, B, H, C, n, ws, kScratchBytes, stream);
 }
 
 size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsigned flags) {

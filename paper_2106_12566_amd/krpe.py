@@ -17,7 +17,8 @@ import os
 
 import torch
 
-__all__ = ["KrpeError", "load", "lib_path", "feature_map", "toeplitz_conv", "attention_fwd", "attention_bwd",
+__all__ = ["KrpeError", "load", "lib_path", "feature_map", "toeplitz_conv", "toeplitz_conv_noalloc",
+           "attention_fwd", "attention_bwd",
            "attention_fwd_route",
            "attention_fwd_workspace", "attention_bwd_workspace", "toeplitz_conv_workspace",
            "attention_fwd_fixed_rows", "DTYPES"]
@@ -69,6 +70,8 @@ def load(path: str | None = None) -> ctypes.CDLL:
     lib.krpe_toeplitz_conv_workspace.argtypes = [i, i, i, i]
     lib.krpe_toeplitz_conv.restype = i
     lib.krpe_toeplitz_conv.argtypes = [fp, fp, fp, i, i, i, i, vp, sz, vp]
+    lib.krpe_toeplitz_conv_noalloc.restype = i
+    lib.krpe_toeplitz_conv_noalloc.argtypes = [fp, fp, fp, i, i, i, i, vp]
     lib.krpe_attention_fwd_workspace.restype = sz
     lib.krpe_attention_fwd_workspace.argtypes = [i, i, i, i, i]
     lib.krpe_attention_fwd_workspace_ex.restype = sz
@@ -185,6 +188,29 @@ def toeplitz_conv(b: torch.Tensor, a: torch.Tensor) -> torch.Tensor:
                                 _stream(a.device))
     _check(st, "krpe_toeplitz_conv")
     return y
+
+
+def toeplitz_conv_noalloc(b: torch.Tensor, a: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """toeplitz_conv through krpe_toeplitz_conv_noalloc: no workspace, the library's static scratch instead.
+
+    Only the output is allocated here (or passed as ``out``); the call itself allocates nothing.  Calls
+    that overlap on one GPU share that scratch and race.
+    """
+    lib = load()
+    b = _gpu(b, "b")
+    a = _gpu(a, "a")
+    if a.dim() != 4 or b.dim() != 2:
+        raise KrpeError("a must be [B,H,C,n] and b [H,2n-1]")
+    B, H, C, n = a.shape
+    if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32 or a.dtype != torch.float32:
+        raise KrpeError("b must be float32 [H, 2n-1] and a float32 [B,H,C,n]")
+    if out is None:
+        out = torch.empty_like(a)
+    elif out.shape != a.shape or out.dtype != torch.float32 or not out.is_contiguous():
+        raise KrpeError("out must be a contiguous float32 tensor shaped like a")
+    st = lib.krpe_toeplitz_conv_noalloc(_ptr(b), _ptr(a), _ptr(out), B, H, C, n, _stream(a.device))
+    _check(st, "krpe_toeplitz_conv_noalloc")
+    return out
 
 
 def attention_fwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool = False,

@@ -157,6 +157,18 @@ def test_toeplitz_validation(lib):
     assert call(C=0, a=None, y=None) == OK
 
 
+def test_toeplitz_noalloc_refuses_sizes_beyond_the_scratch(lib):
+    """The no-allocation entry point refuses, on the host and before any HIP call, sizes whose
+    workspace exceeds its static scratch (64 MiB), and validates sizes like krpe_toeplitz_conv."""
+    big = (64, 4, 64, 16384)
+    assert lib.krpe_toeplitz_conv_workspace(*big) > (64 << 20)
+    assert lib.krpe_toeplitz_conv_noalloc(None, None, None, *big, None) == UNSUP
+    assert b"static scratch" in lib.krpe_last_error()
+    assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, -1, 10, None) == SHAPE
+    assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, 2, 20000, None) == UNSUP
+    assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, 0, 10, None) == OK
+
+
 def test_feature_map_validation(lib):
     call = lambda x=Q, dt=0, w=W, phi=Z, B=1, H=1, n=8, d=4, m=4: lib.krpe_feature_map(
         x, dt, w, phi, B, H, n, d, m, None)
