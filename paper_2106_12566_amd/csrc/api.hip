@@ -179,6 +179,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
+  L.cexp = take(static_cast<size_t>(H) * (2 * static_cast<size_t>(n) - 1) * sizeof(float));
   L.total = off;
   return L;
 }
@@ -253,6 +254,7 @@ LongLayout long_layout(int B, int H, int n, int d, int M) {
   L.maskf = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
+  L.cexp = take(static_cast<size_t>(H) * (2 * static_cast<size_t>(n) - 1) * sizeof(float));
   L.total = off;
   return L;
 }
@@ -307,6 +309,7 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
   unsigned long long* fixmask = reinterpret_cast<unsigned long long*>(w + L.fixmask);
   double* fixpart = reinterpret_cast<double*>(w + L.fixpart);
   int2* brange = reinterpret_cast<int2*>(w + L.brange);
+  float* cexp = reinterpret_cast<float*>(w + L.cexp);
   const int N = 1 << L.l2;
   const int pairs = (d + 2) / 2;
 
@@ -331,7 +334,7 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
         return s;
       vv = vw;
     }
-    if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixpart, brange,
+    if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixpart, brange, cexp,
                                                  BHi, H, n, N, d, M, st),
                                     "direct launch"))
       return s;
@@ -374,7 +377,8 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
                                                  nsum, st),
                                   "combine launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, den_out, fix, fixmask, fixpart, brange, BHi, H, n, N, d, M, st),
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, den_out, fix, fixmask, fixpart, brange, cexp, BHi,
+                                               H, n, N, d, M, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);
@@ -464,7 +468,8 @@ krpe_status_t run_forward_long(const LongLayout& L, char* w, const void* q, cons
   if (krpe_status_t s = hip_check(launch_fixup(F(L.phiq), F(L.phik), v, bf16, b, z, nullptr, fix,
                                                reinterpret_cast<unsigned long long*>(w + L.maskf),
                                                reinterpret_cast<double*>(w + L.fixpart),
-                                               reinterpret_cast<int2*>(w + L.brange), BHi, H, n, L.Ntot, d, M, st),
+                                               reinterpret_cast<int2*>(w + L.brange), F(L.cexp), BHi, H, n, L.Ntot, d,
+                                               M, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);

@@ -107,6 +107,9 @@ struct BufRd {
   __device__ __forceinline__ float f32(uint32_t voff, uint32_t soff) const {
     return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
   }
+  __device__ __forceinline__ uint16_t u16(uint32_t voff, uint32_t soff) const {
+    return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+  }
   // (The 8-byte result is bit-cast whole: taking its two halves apart by index
   // lowers to a single 4-byte load.)
   __device__ __forceinline__ float2 f64(uint32_t voff, uint32_t soff) const {

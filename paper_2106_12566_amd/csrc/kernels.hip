@@ -1132,21 +1132,22 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
   }
 }
 
-// ---------------------------------------------------------------- fixup --
-// Exact evaluation of Eq. (10) for the rows k_combine could not certify, on
-// the matrix cores.  The queued rows of head bh form groups of 32 in row
-// order; a group's keys (with a finite b_{j-i}) are walked in chunks of 128
-// aligned to multiples of 128, and when the head has fewer groups than
-// work-group slots each group's chunks are split into contiguous shares
-// (fix_key_parts).  Work-group (bh, k) takes items k, k + slots, ...:
-//   S = phi(q_rows) phi(k_chunk)^T      32 x 128, fp32 MFMA over the m features
-//   P = S * c_{j-i}                     0 where b_{j-i} = -inf or j >= n
-//   Z += P [v, 1]                       fp32 MFMA per chunk, totals in fp64
-// An unsplit group writes its rows; shares go to fixpart and k_fixup_combine
-// adds them in share order.  Chunks outside a row's range add exact zeros, so
-// a row's result depends only on its values and the share boundaries.  Waves:
-// S takes one 32-key tile each; P V takes the ceil(d / 32) column tiles, the
-// spare waves splitting the chunk's keys.
+// Exact rows: Eq. (10) evaluated directly for the rows queued per head (the
+// rows the FFT route cannot certify, or every row on the direct route), in
+// groups of 32 rows taken in row order from the 64-bit row masks.  A group's
+// keys run in chunks of 128, each an item's share when a head has few groups
+// and more work-group slots (fix_key_parts).  Wave w of the work-group takes
+// the 32 keys jc + 32 w of every chunk of the item:
+//   S^T = phi(k_keys) phi(q_rows)^T   32 keys x 32 rows, fp32 MFMA over the m features
+//   P   = S^T * c_{j-i}               c = exp(b) from a table per head; 0 for keys >= n
+//   Z  += P^T [v, ...]                fp32 MFMA, whose A operand is exactly the
+//                                     layout S^T leaves in the registers (no LDS)
+// and the denominator as the sum of P over the keys.  Per 32 keys the fp32
+// sums are added into fp64 totals; the four waves' totals are added in wave
+// order at the end, so results are bitwise deterministic.  Keys outside a
+// row's finite-b range contribute exact zeros, and chunks outside the
+// group's range are skipped.  An unsplit group writes its rows; shares go to
+// fixpart and k_fixup_combine adds them in share order.
 constexpr int kFixRows = 32;
 constexpr int kFixKeys = 128;
 constexpr int kFixL = 32;                 // features staged per step
@@ -1165,10 +1166,13 @@ __host__ __device__ inline int fix_key_parts(int ngroups, int slots, int n) {
   return k < 1 ? 1 : (k > kFixMaxParts ? kFixMaxParts : k);
 }
 
-// Range [lo, hi] of s = t + n - 1 where b_t is finite, per head (lo > hi if none).
-__global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int2* __restrict__ brange, int n) {
+// Range [lo, hi] of s = t + n - 1 where b_t is finite, per head (lo > hi if
+// none), and the table cexp[h][s] = exp(b[h][s]) (c_t of Eq. (6)).
+__global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int2* __restrict__ brange,
+                                                float* __restrict__ cexp, int n) {
   __shared__ int smin, smax;
   const float* __restrict__ bh = b + static_cast<size_t>(blockIdx.x) * (2 * n - 1);
+  float* __restrict__ ch = cexp + static_cast<size_t>(blockIdx.x) * (2 * n - 1);
   if (threadIdx.x == 0) {
     smin = 2 * n;
     smax = -1;
@@ -1176,11 +1180,14 @@ __global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int
   __syncthreads();
   int lo = 2 * n, hi = -1;
 #pragma unroll 8
-  for (int sidx = threadIdx.x; sidx < 2 * n - 1; sidx += 256)
-    if (bh[sidx] != -INFINITY) {
+  for (int sidx = threadIdx.x; sidx < 2 * n - 1; sidx += 256) {
+    const float bv = bh[sidx];
+    ch[sidx] = expf(bv);
+    if (bv != -INFINITY) {
       lo = min(lo, sidx);
       hi = max(hi, sidx);
     }
+  }
   atomicMin(&smin, lo);
   atomicMax(&smax, hi);
   __syncthreads();
@@ -1188,25 +1195,20 @@ __global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int
 }
 
 template <typename TV>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_fixup(const float* __restrict__ phiq, const float* __restrict__ phik,
-                                               const TV* __restrict__ vv,
-                                               const float* __restrict__ b, float* __restrict__ z, float* __restrict__ den_out,
-                                               const unsigned* __restrict__ fix,
-                                               const unsigned long long* __restrict__ fixmask,
-                                               double* __restrict__ fixpart, const int2* __restrict__ brange,
-                                               int BH, int H, int n, int ld, int d, int m, int slots) {
-  extern __shared__ __align__(16) float sq[];   // phi(q) of the group's rows, [l][32]
-  __shared__ __align__(16) float sk[kFixL * kFixStride];  // phi(k) chunk [l][key]; then P [row][key]
-  __shared__ double dsum[8][kFixRows];
-  __shared__ double sden[kFixRows];
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_fixup(
+    const float* __restrict__ phiq, const float* __restrict__ phik, const TV* __restrict__ vv,
+    const float* __restrict__ cexp, float* __restrict__ z, float* __restrict__ den_out,
+    const unsigned* __restrict__ fix, const unsigned long long* __restrict__ fixmask, double* __restrict__ fixpart,
+    const int2* __restrict__ brange, int BH, int H, int n, int ld, int d, int m, int slots) {
+  extern __shared__ __align__(16) float sq[];  // phi(q) of the group's rows, [l][32], l < m rounded up to 32
+  __shared__ double red[2][16][64];            // another wave's totals (two column tiles)
+  __shared__ double rden[4][kFixRows];
   __shared__ int srows[kFixRows];
   __shared__ int smin, smax;
   __shared__ unsigned long long smask[kFixMaxTiles];
   __shared__ unsigned spre[kFixMaxTiles + 1];
-  double* red = reinterpret_cast<double*>(sk);  // after the key loop: partial numerators
-  static_assert(sizeof(float) * kFixL * kFixStride >= 2 * 1024 * sizeof(double), "red fits in sk");
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int lr = lane & 31, lk = lane >> 5;
+  const int lr = lane & 31, lh = lane >> 5;
   // slot-major order: the first item of every head is dispatched first
   const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
   const unsigned count = fix[bh];
@@ -1215,23 +1217,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const int items = ngroups * kparts;
   if (kslot >= items) return;  // uniform per work-group
   const int h = bh % H;
-  const float* __restrict__ bhv = b + static_cast<size_t>(h) * (2 * n - 1);
+  const float* __restrict__ ch = cexp + static_cast<size_t>(h) * (2 * n - 1);
   const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * ld;
   const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * ld;
-  const size_t vbase = static_cast<size_t>(bh) * n * d;
-  // column tiles of P V and the waves that share one (key split)
+  const TV* __restrict__ vh = vv + static_cast<size_t>(bh) * n * d;
+  const BufRd bk(pk, static_cast<uint32_t>(m) * ld * 4u), bv(vh, static_cast<uint32_t>(n) * d * sizeof(TV));
+  const BufRd bc(ch, static_cast<uint32_t>(2 * n - 1) * 4u);
+  const int mr = (m + 31) & ~31;
   const int tiles = (d + 31) / 32;
-  const int wpt = tiles == 3 ? 1 : 4 / tiles;
-  const int my_tile = wave / wpt, my_part = wave % wpt;
-  const bool pv_wave = wave < tiles * wpt;
-  const int pv_keys = kFixKeys / wpt;
-  auto vload = [&](int j, int c) -> float { return to_f32(vv[vbase + static_cast<size_t>(j) * d + c]); };
 
   // Queued rows in row order: group g takes the ranks 32 g .. 32 g + 31 of
   // the set bits of the head's mask words (prefix counts in spre).
   const int tiles_n = (n + 63) / 64;
   for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
-  // Range of s = t + n - 1 where b_t is finite.
   if (tid == 0) {
     const int2 br = brange[h];
     smin = br.x;
@@ -1248,7 +1246,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
   for (int item = kslot; item < items; item += slots) {
     const int grp = item / kparts, kpart = item % kparts;
-    __syncthreads();  // previous group's srows / sq / red consumed
+    __syncthreads();  // previous item's srows / sq / red consumed
     if (tid < kFixRows) {
       const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
       int row = -1;
@@ -1275,163 +1273,152 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
     const int jlo = max(0, first + smin - (n - 1));
     const int jhi = min(n - 1, last + smax - (n - 1));
-    for (int e = tid; e < m * kFixRows; e += 256) {
+    for (int e = tid; e < mr * kFixRows; e += 256) {
       const int l = e / kFixRows, r = e % kFixRows;
       const int i = srows[r];
-      sq[e] = i >= 0 ? pq[static_cast<size_t>(l) * ld + i] : 0.f;
+      sq[e] = (i >= 0 && l < m) ? pq[static_cast<size_t>(l) * ld + i] : 0.f;
     }
-    __syncthreads();  // sq staged
-    double zt[16];
-#pragma unroll
-    for (int v = 0; v < 16; ++v) zt[v] = 0.0;
-    double dacc = 0.0;
+    const int myrow = srows[lr];  // the query row of this lane in S^T and P
+    __syncthreads();              // sq staged
 
     // this item's share of the group's key chunks (contiguous, chunk-aligned)
     const int c0 = jlo / kFixKeys, nch = jhi >= jlo ? jhi / kFixKeys - c0 + 1 : 0;
     const int cb = c0 + static_cast<int>(static_cast<long long>(nch) * kpart / kparts);
     const int ce = c0 + static_cast<int>(static_cast<long long>(nch) * (kpart + 1) / kparts);
-    for (int jc = cb * kFixKeys; jc < ce * kFixKeys; jc += kFixKeys) {
-      // ---- S = phi(q_rows) phi(k_chunk)^T: wave w holds keys jc + 32 w ...
-      floatx16 sacc;
+    // column tiles of [v]: two per pass (the S^T products are recomputed for
+    // a second pass when d > 64)
+    for (int t0 = 0; t0 < tiles; t0 += 2) {
+      double zt[2][16];
+      double dsum = 0.0;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) sacc[v] = 0.f;
-      // phi(k) of the chunk, kFixL features at a time, loaded by every wave
-      // straight into its B operands (keys jc + 32 wave + lr, features l0 +
-      // 2 q + lk: 32 consecutive keys per half-wave, coalesced); the next
-      // step's values are in flight while the matrix cores work on this one
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) zt[t][e] = 0.0;
+      // phi(k) operands of one 32-feature step: A[key jc + lr][feature l0 + 2 q + lh]
       float kb[kFixL / 2], kn[kFixL / 2];
-      const int jkey = jc + wave * 32 + lr;
-      // uniform row base per step plus one per-lane offset (half-wave row, key)
-      const unsigned koff = static_cast<unsigned>(lk * ld + jkey);
-      auto load_step = [&](int l0) {
+      // (reads past the m feature rows give zero; keys >= n are masked in P)
+      auto load_k = [&](int jc, int l0) {
+        const uint32_t voff = static_cast<uint32_t>(lh * ld + jc + lr) * 4u;
 #pragma unroll
-        for (int q = 0; q < kFixL / 2; ++q) {
-          const float* __restrict__ prow = pk + static_cast<size_t>(l0 + 2 * q) * ld;
-          kn[q] = (l0 + 2 * q + lk < m && jkey < n) ? prow[koff] : 0.f;
-        }
+        for (int q = 0; q < kFixL / 2; ++q)
+          kn[q] = bk.f32(voff, static_cast<uint32_t>((l0 + 2 * q) * ld) * 4u);
       };
-      load_step(0);
-      for (int l0 = 0; l0 < m; l0 += kFixL) {
+      int jc = cb * kFixKeys + 32 * wave;
+      if (jc < ce * kFixKeys) load_k(jc, 0);
+      for (; jc < ce * kFixKeys; jc += kFixKeys) {
+        // value rows of these 32 keys, in the key order of the P V steps:
+        // step e uses key jc + 8 (e / 4) + 4 lh + e % 4 on lane half lh
+        // (reads past the n value rows give zero; columns >= d are masked)
+        float vb[2][16];
 #pragma unroll
-        for (int q = 0; q < kFixL / 2; ++q) kb[q] = kn[q];
-        if (l0 + kFixL < m) load_step(l0 + kFixL);
-        const int lend = min(kFixL, m - l0);
-        if (lend == kFixL) {
-          float qa[kFixL / 2];
+        for (int t = 0; t < 2; ++t) {
+          const int col = (t0 + t) * 32 + lr;
+          const uint32_t voff = static_cast<uint32_t>((jc + 4 * lh) * d + min(col, d - 1)) * sizeof(TV);
 #pragma unroll
-          for (int q = 0; q < kFixL / 2; ++q) qa[q] = sq[(l0 + 2 * q + lk) * kFixRows + lr];
+          for (int e = 0; e < 16; ++e) {
+            const uint32_t soff = static_cast<uint32_t>((8 * (e >> 2) + (e & 3)) * d) * sizeof(TV);
+            float x;
+            if constexpr (sizeof(TV) == 2) {
+              x = to_f32(bv.u16(voff, soff));
+            } else {
+              x = bv.f32(voff, soff);
+            }
+            vb[t][e] = col < d ? x : 0.f;
+          }
+        }
+        // ---- S^T[key][row] over the m features
+        floatx16 sacc;
 #pragma unroll
-          for (int q = 0; q < kFixL / 2; ++q) sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[q], kb[q], sacc, 0, 0, 0);
-        } else {
-          // features past m load as zeros on the B side; the A side is zeroed too
+        for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
+        for (int l0 = 0; l0 < mr; l0 += kFixL) {
+#pragma unroll
+          for (int q = 0; q < kFixL / 2; ++q) kb[q] = kn[q];
+          if (l0 + kFixL < mr) {
+            load_k(jc, l0 + kFixL);
+          } else if (jc + kFixKeys < ce * kFixKeys) {
+            load_k(jc + kFixKeys, 0);  // the next key block's first step
+          }
 #pragma unroll
           for (int q = 0; q < kFixL / 2; ++q) {
-            const int l = 2 * q + lk;
-            const float qa = l < lend ? sq[(l0 + l) * kFixRows + lr] : 0.f;
-            sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa, kb[q], sacc, 0, 0, 0);
+            const float qb = sq[(l0 + 2 * q + lh) * kFixRows + lr];
+            sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(kb[q], qb, sacc, 0, 0, 0);
           }
         }
-      }
-      __syncthreads();  // sk reads done: it now holds P
-      // ---- P = S * c_{j-i}; lane holds key wave*32 + lr, rows 8(v/4) + 4 lk + v%4
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
-        const int key = wave * 32 + lr, j = jc + key, i = srows[row];
-        float pv = 0.f;
-        if (i >= 0 && j < n) {
-          const float bj = bhv[j - i + n - 1];
-          if (bj != -INFINITY) pv = sacc[v] * expf(bj);
-        }
-        sk[row * kFixStride + key] = pv;
-      }
-      __syncthreads();
-      // ---- denominators: thread (row tid % 32, keys 16 (tid / 32) ...)
-      {
-        const int row = tid & 31, seg = tid >> 5;
+        // ---- P = S^T c_{j-i}: lane holds keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow
+        // (c indices are >= 0 for a queued row; past 2n - 2 they read zero)
+        float pv[16];
         float ds = 0.f;
+        const uint32_t coff = static_cast<uint32_t>(jc + 4 * lh - myrow + n - 1) * 4u;
 #pragma unroll
-        for (int k2 = 0; k2 < 16; ++k2) ds += sk[row * kFixStride + seg * 16 + k2];
-        dacc += static_cast<double>(ds);
-      }
-      // ---- numerators: Z[row][c] += sum_key P[row][key] v[key][c]
-      if (pv_wave) {
-        floatx16 zc;
+        for (int e = 0; e < 16; ++e) {
+          const int key = jc + 8 * (e >> 2) + 4 * lh + (e & 3);
+          const float c = bc.f32(coff, static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u);
+          pv[e] = (myrow >= 0 && key < n) ? sacc[e] * c : 0.f;
+          ds += pv[e];
+        }
+        dsum += static_cast<double>(ds);
+        // ---- Z[row][col] += sum_key P[row][key] v[key][col]
 #pragma unroll
-        for (int v = 0; v < 16; ++v) zc[v] = 0.f;
-        const int col = my_tile * 32 + lr;
-        const int kb0 = my_part * pv_keys;
-        // v rows in blocks of 32 keys, the next block in flight during the
-        // matrix ops of this one
-        float vb[16], vn[16];
-        auto load_v = [&](int k0) {
+        for (int t = 0; t < 2; ++t) {
+          if (t0 + t < tiles) {
+            floatx16 zc;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const int j = jc + k0 + 2 * q + lk;
-            vn[q] = (col < d && j < n) ? vload(j, col) : 0.f;
-          }
-        };
-        load_v(kb0);
-        for (int k0 = kb0; k0 < kb0 + pv_keys; k0 += 32) {
+            for (int e = 0; e < 16; ++e) zc[e] = 0.f;
 #pragma unroll
-          for (int q = 0; q < 16; ++q) vb[q] = vn[q];
-          if (k0 + 32 < kb0 + pv_keys) load_v(k0 + 32);
+            for (int e = 0; e < 16; ++e) zc = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[e], vb[t][e], zc, 0, 0, 0);
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            const float pa = sk[lr * kFixStride + k0 + 2 * q + lk];
-            zc = __builtin_amdgcn_mfma_f32_32x32x2f32(pa, vb[q], zc, 0, 0, 0);
+            for (int e = 0; e < 16; ++e) zt[t][e] += static_cast<double>(zc[e]);
           }
         }
-#pragma unroll
-        for (int v = 0; v < 16; ++v) zt[v] += static_cast<double>(zc[v]);
       }
-    }
-    // ---- reduce the key splits, the denominators, and write the rows
-    dsum[tid >> 5][tid & 31] = dacc;
-    for (int part = 1; part < wpt; ++part) {
+      // ---- the four waves' totals, added in wave order
+      dsum += __shfl_xor(dsum, 32);  // the other half-wave's keys of row lr
+      if (t0 == 0 && lh == 0) rden[wave][lr] = dsum;
+      for (int w = 1; w < 4; ++w) {
+        __syncthreads();
+        if (wave == w) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) red[t][e][lane] = zt[t][e];
+        }
+        __syncthreads();
+        if (wave == 0) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) zt[t][e] += red[t][e][lane];
+        }
+      }
       __syncthreads();
-      if (pv_wave && my_part == part) {
+      // wave 0 holds the totals: row 8 (e / 4) + 4 lh + e % 4, column (t0 + t) 32 + lr
+      if (wave == 0) {
+        double* __restrict__ out =
+            kparts == 1 ? nullptr : fixpart + (static_cast<size_t>(bh) * slots + item) * kFixRows * (d + 1);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) red[my_tile * 1024 + v * 64 + lane] = zt[v];
-      }
-      __syncthreads();
-      if (pv_wave && my_part == 0) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) zt[v] += red[my_tile * 1024 + v * 64 + lane];
-      }
-    }
-    __syncthreads();
-    if (tid < kFixRows) {
-      double den = 0.0;
-      for (int sg = 0; sg < 8; ++sg) den += dsum[sg][tid];
-      sden[tid] = den;
-    }
-    __syncthreads();
-    if (kparts == 1) {
-      if (den_out && tid < kFixRows && srows[tid] >= 0)
-        den_out[static_cast<size_t>(bh) * n + srows[tid]] = static_cast<float>(sden[tid]);
-      if (pv_wave && my_part == 0) {
-        const int col = my_tile * 32 + lr;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
+        for (int e = 0; e < 16; ++e) {
+          const int row = 8 * (e >> 2) + 4 * lh + (e & 3);
           const int i = srows[row];
-          if (i >= 0 && col < d)
-            z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[v] / sden[row]);
-        }
-      }
-    } else {
-      // partial sums of this key share: fixpart[bh][item][row][c], c = d the denominator
-      double* __restrict__ out = fixpart + (static_cast<size_t>(bh) * slots + item) * kFixRows * (d + 1);
-      if (pv_wave && my_part == 0) {
-        const int col = my_tile * 32 + lr;
+          const double den = ((rden[0][row] + rden[1][row]) + rden[2][row]) + rden[3][row];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int row = 8 * (v >> 2) + 4 * lk + (v & 3);
-          if (col < d) out[row * (d + 1) + col] = zt[v];
+          for (int t = 0; t < 2; ++t) {
+            const int col = (t0 + t) * 32 + lr;
+            if (i < 0 || t0 + t >= tiles || col >= d) continue;
+            if (kparts == 1) {
+              z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[t][e] / den);
+            } else {
+              out[row * (d + 1) + col] = zt[t][e];
+            }
+          }
+          if (t0 == 0 && lr == 0) {
+            if (kparts == 1) {
+              if (den_out && i >= 0) den_out[static_cast<size_t>(bh) * n + i] = static_cast<float>(den);
+            } else {
+              out[row * (d + 1) + d] = den;
+            }
+          }
         }
       }
-      if (tid < kFixRows) out[tid * (d + 1) + d] = sden[tid];
     }
   }
 }
@@ -2000,13 +1987,13 @@ int fix_slots(int BH) {
 }
 
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b, float* z,
-                        float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart, int2* brange, int BH,
-                        int H, int n, int ld, int d, int m, hipStream_t st) {
+                        float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart, int2* brange,
+                        float* cexp, int BH, int H, int n, int ld, int d, int m, hipStream_t st) {
   const int slots = fix_slots(BH);
-  hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, n);
+  hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, cexp, n);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   const long long blocks = static_cast<long long>(BH) * slots;
-  const size_t lds = static_cast<size_t>(m) * kFixRows * sizeof(float);
+  const size_t lds = static_cast<size_t>((m + 31) & ~31) * kFixRows * sizeof(float);
   if (lds > 64 * 1024) {
     // phi(q) of a group exceeds the default dynamic LDS limit for m > 512
     static const hipError_t once = [] {
@@ -2022,12 +2009,12 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
   }
   if (bf16)
     hipLaunchKernelGGL(k_fixup<uint16_t>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
-                       static_cast<const uint16_t*>(v), b, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d,
-                       m, slots);
+                       static_cast<const uint16_t*>(v), cexp, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld,
+                       d, m, slots);
   else
     hipLaunchKernelGGL(k_fixup<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
-                       static_cast<const float*>(v), b, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m,
-                       slots);
+                       static_cast<const float*>(v), cexp, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d,
+                       m, slots);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, fixmask, fixpart, z,
                      den_out, BH, n, d, slots);

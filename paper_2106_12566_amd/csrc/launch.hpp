@@ -29,6 +29,7 @@ struct AttnLayout {
   size_t fixmask;    // uint64 [BH][ceil(n/64)]  queued rows: bit i % 64 of word i / 64
   size_t fixpart;    // double [BH][slots][32][d+1] key-share partial sums of the exact rows
   size_t brange;     // int2   [H]               range of finite b per head
+  size_t cexp;       // float  [H][2n-1]         c = exp(b) (exact rows)
   size_t total;
 };
 AttnLayout attn_layout(int B, int H, int n, int d, int m);
@@ -77,6 +78,7 @@ struct LongLayout {
   size_t maskb, maskf; // uint64 [BH][nbk/64], [BH][ceil(n/64)]
   size_t fixpart;      // double [BH][slots][32][d+1]
   size_t brange;       // int2   [H]
+  size_t cexp;         // float  [H][2n-1]       c = exp(b) (exact rows)
   size_t total;
 };
 LongLayout long_layout(int B, int H, int n, int d, int M);
@@ -138,7 +140,7 @@ hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb
 int fix_slots(int BH);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
                         float* z, float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart,
-                        int2* brange, int BH, int H, int n, int ld, int d, int m,
+                        int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
 // Long sequences (long_seq.hip): block copies of phi rows, bias windows of a
