@@ -68,15 +68,15 @@ constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRP
 
 // Whether the direct route is the faster one for BH heads of length n with M
 // features and d value columns.  Cost model fitted to MI355X timings of both
-// routes (B H = 1, 4, 16, 96; d = 64; M = 32 .. 256; n = 128 .. 40000): each
-// route's time is its work over all heads at a measured rate plus a fixed
-// cost (the launch chain and its latency-bound small kernels).  Direct:
-// 3.8e-14 s per (query, key) pair and unit of M + d + 1, plus 6.5e-5 s.  FFT:
-// per channel pair, feature and point of the length-2N transform times
-// log2(2N), 2.2e-13 s up to N = 4096, 5.0e-13 s at N = 8192 (its units keep
-// nothing in registers across features) and 3.5e-13 s at N = 16384, over the nb^2 block
-// pairs of a blocked sequence, plus 3.3e-4 s.  All n^2 pairs are counted: the
-// host does not read b, so a causal mask (half the pairs) is not seen; the
+// routes (B H = 1, 16, 96; d = 64; M = 64, 128; n = 512 .. 16384, not
+// causal): each route's time is its work over all heads at a measured rate
+// plus a fixed cost (the launch chain and its latency-bound small kernels).
+// Direct: 2.45e-14 s per (query, key) pair and unit of M + d + 1, plus
+// 5e-5 s.  FFT: per column pair, feature and point of the length-2N
+// transform times log2(2N), 1.65e-13 s up to N = 4096, 3.8e-13 s at N = 8192
+// and 3.0e-13 s at N = 16384, over the nb^2 block pairs of a blocked
+// sequence, plus 1.5e-4 s.  All n^2 pairs are counted: the host does not read
+// b, so a causal mask (half the pairs on the direct route) is not seen; the
 // route bits force either route.
 bool direct_is_faster(long long BH, int n, int M, int d) {
   int l2 = 0;
@@ -86,9 +86,9 @@ bool direct_is_faster(long long BH, int n, int M, int d) {
   if (l2 > kMaxLog2N) l2 = kMaxLog2N;
   const double L = 2.0 * static_cast<double>(1 << l2);
   const double heads = static_cast<double>(BH);
-  const double direct = 3.8e-14 * heads * static_cast<double>(n) * n * (M + d + 1) + 6.5e-5;
-  const double rate = l2 <= 12 ? 2.2e-13 : (l2 == 13 ? 5.0e-13 : 3.5e-13);
-  const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb + 3.3e-4;
+  const double direct = 2.45e-14 * heads * static_cast<double>(n) * n * (M + d + 1) + 5.0e-5;
+  const double rate = l2 <= 12 ? 1.65e-13 : (l2 == 13 ? 3.8e-13 : 3.0e-13);
+  const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb + 1.5e-4;
   return direct < fft;
 }
 
