@@ -267,35 +267,53 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
 }
 
 // k_feature_map for d = 64 with the operands loaded straight into registers.
-// The MFMA sums over k in any order both operands agree on, so half-wave h
-// supplies k = 32 h + s at step s: each lane needs 32 contiguous values of
-// its x row and of its W row (8 float4 loads each, all in flight at once),
-// no LDS staging and no barriers.  The row norm is the lane's half plus the
-// other half-wave's.  Same tiles, outputs and epilogue as k_feature_map.
+// d = 64.  Work-group: 128 positions of one (source, batch-head) and every
+// feature, four waves of 32 positions each.  The x rows are read once with
+// coalesced 16-byte loads (consecutive threads, consecutive addresses),
+// staged through LDS (rows padded to 68 floats: the 16-byte reads of 16
+// lanes then fall in distinct banks) and kept in registers; W then streams
+// through the same LDS buffer 128 features at a time (35 KiB of LDS: four
+// work-groups per CU).  The MFMA sums over k in any order both
+// operands agree on: half-wave h supplies k = 32 h + s at step s.  Same
+// outputs and epilogue as k_feature_map.
+constexpr int kFm64Pos = 128;
+constexpr int kFm64Stride = 68;
+
 template <typename TX>
-__device__ __forceinline__ void load_half_row64(const TX* __restrict__ row, bool ok, float (&r)[32]) {
+__device__ __forceinline__ void stage_rows64(const TX* __restrict__ src, int rows_ok, float* __restrict__ dst,
+                                             int nrows) {
+  // nrows x 64 values -> dst[row][kFm64Stride], zero past rows_ok
   if constexpr (std::is_same<TX, float>::value) {
-    const float4* p = reinterpret_cast<const float4*>(row);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float4 v = ok ? p[j] : make_float4(0.f, 0.f, 0.f, 0.f);
-      r[4 * j] = v.x;
-      r[4 * j + 1] = v.y;
-      r[4 * j + 2] = v.z;
-      r[4 * j + 3] = v.w;
+    for (int e = threadIdx.x; e < nrows * 16; e += 256) {
+      const int row = e >> 4, c4 = e & 15;
+      const float4 v = row < rows_ok ? reinterpret_cast<const float4*>(src)[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+      *reinterpret_cast<float4*>(dst + row * kFm64Stride + 4 * c4) = v;
     }
   } else {
-    const uint4* p = reinterpret_cast<const uint4*>(row);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint4 v = ok ? p[j] : make_uint4(0u, 0u, 0u, 0u);
+    for (int e = threadIdx.x; e < nrows * 8; e += 256) {
+      const int row = e >> 3, c8 = e & 7;
+      const uint4 v = row < rows_ok ? reinterpret_cast<const uint4*>(src)[e] : make_uint4(0u, 0u, 0u, 0u);
       const unsigned w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        r[8 * j + 2 * e] = __uint_as_float(w[e] << 16);
-        r[8 * j + 2 * e + 1] = __uint_as_float(w[e] & 0xffff0000u);
-      }
+      float* o = dst + row * kFm64Stride + 8 * c8;
+      *reinterpret_cast<float4*>(o) = make_float4(__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+                                                  __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u));
+      *reinterpret_cast<float4*>(o + 4) =
+          make_float4(__uint_as_float(w[2] << 16), __uint_as_float(w[2] & 0xffff0000u), __uint_as_float(w[3] << 16),
+                      __uint_as_float(w[3] & 0xffff0000u));
     }
+  }
+}
+
+// 32 values k = 32 h .. 32 h + 31 of LDS row `row` (8 x 16-byte reads)
+__device__ __forceinline__ void lds_half_row64(const float* __restrict__ rows, int row, int h, float (&r)[32]) {
+  const float4* p = reinterpret_cast<const float4*>(rows + row * kFm64Stride + 32 * h);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float4 v = p[j];
+    r[4 * j] = v.x;
+    r[4 * j + 1] = v.y;
+    r[4 * j + 2] = v.z;
+    r[4 * j + 3] = v.w;
   }
 }
 
@@ -303,16 +321,17 @@ template <typename TX, bool FEATURE_MAJOR>
 __global__ __launch_bounds__(256) void k_feature_map64(const TX* __restrict__ x0, const TX* __restrict__ x1,
                                                        const float* __restrict__ W, float* __restrict__ phi0,
                                                        float* __restrict__ phi1, int H, int n, int ld, int m,
-                                                       float inv_sqrt_m, int tiles_n, int tiles_m, int BH,
+                                                       float inv_sqrt_m, int tiles_n, int BH,
                                                        unsigned* __restrict__ fix_counts, int nprf, int trf) {
   constexpr int D = 64;
+  __shared__ __align__(16) float xs[kFm64Pos * kFm64Stride];  // x tile, then W 128 features at a time
+  float* const ws = xs;
   // Clear the exact-evaluation queue counters (fix_counts[0..BH]) for k_combine.
-  if (fix_counts && threadIdx.x == 0 && blockIdx.x <= static_cast<unsigned>(BH)) fix_counts[blockIdx.x] = 0u;
+  if (fix_counts && threadIdx.x == 0)
+    for (int b = blockIdx.x; b <= BH; b += gridDim.x) fix_counts[b] = 0u;
   int bid = blockIdx.x;
   const int tn = bid % tiles_n;
   bid /= tiles_n;
-  const int tm = bid % tiles_m;
-  bid /= tiles_m;
   const int bh = bid % BH;
   const int src = bid / BH;
   const TX* __restrict__ x = src == 0 ? x0 : x1;
@@ -320,66 +339,82 @@ __global__ __launch_bounds__(256) void k_feature_map64(const TX* __restrict__ x0
   const int h = bh % H;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, c = lane & 31;
-  const int i0 = tn * 64 + (wave & 1) * 32, l0 = tm * 64 + (wave >> 1) * 32;  // this wave's 32 x 32 tile
-  const int xi = i0 + c, wl = l0 + c;  // x row and W row this lane supplies
-  float xr[32], wr[32];
-  load_half_row64(x + (static_cast<size_t>(bh) * n + (xi < n ? xi : 0)) * D + 32 * half, xi < n, xr);
-  load_half_row64(W + (static_cast<size_t>(h) * m + (wl < m ? wl : 0)) * D + 32 * half, wl < m, wr);
+  const int p0 = tn * kFm64Pos;
+  const int i0 = p0 + 32 * wave;  // this wave's 32 positions
+  const int rows_ok = min(kFm64Pos, n - p0);
+  stage_rows64(x + (static_cast<size_t>(bh) * n + p0) * D, rows_ok, xs, kFm64Pos);
+  __syncthreads();
+  float xr[32];
+  lds_half_row64(xs, 32 * wave + c, half, xr);
   float sq = 0.f;
 #pragma unroll
-  for (int s = 0; s < 32; ++s) sq = fmaf(xr[s], xr[s], sq);
-  sq += __shfl_xor(sq, 32);  // ||x||^2 of position xi
-  floatx16 acc;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-#pragma unroll
-  for (int s = 0; s < 32; ++s) {
-    if constexpr (FEATURE_MAJOR)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(wr[s], xr[s], acc, 0, 0, 0);
-    else
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(xr[s], wr[s], acc, 0, 0, 0);
-  }
+  for (int s2 = 0; s2 < 32; ++s2) sq = fmaf(xr[s2], xr[s2], sq);
+  sq += __shfl_xor(sq, 32);  // ||x||^2 of position i0 + c
   const int n_store = FEATURE_MAJOR ? ld : n;
   const int M = trf ? 2 * m : m;
+  for (int l0 = 0; l0 < m; l0 += 64) {
+    if (l0 % 128 == 0) {
+      __syncthreads();  // x rows / the previous W features consumed
+      stage_rows64(W + (static_cast<size_t>(h) * m + l0) * D, min(128, m - l0), ws, 128);
+      __syncthreads();
+    }
+    floatx16 acc[2];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    // 32x32 MFMA result layout: lane holds column lane%32, rows 8(v/4) + 4(lane/32) + v%4
-    const int row = 8 * (v >> 2) + 4 * half + (v & 3);
-    const int li = FEATURE_MAJOR ? row : c;  // feature within the wave tile
-    const int ii = FEATURE_MAJOR ? c : row;  // position within the wave tile
-    // ||x||^2 of position i0 + ii lives in lanes ii and ii + 32
-    const float sqi = FEATURE_MAJOR ? sq : __shfl(sq, ii);
-    const bool nz = sqi > 0.f;
-    // phi of x / ||x|| when normalising (Algorithm 1, first step): the
-    // projections scale by 1 / ||x|| and ||x||^2 / 2 becomes 1/2 (a zero row
-    // stays zero)
-    const float half_sq = nprf ? (nz ? 0.5f : 0.f) : 0.5f * sqi;
-    const float row_scale = nprf ? (nz ? rsqrtf(sqi) : 0.f) : 1.f;
-    const int l = l0 + li, i = i0 + ii;
-    if (i < n_store && l < m) {
-      if (trf) {
-        float sv = 0.f, cv = 0.f;
-        if (i < n) {
-          const float amp = expf(half_sq) * inv_sqrt_m;
-          sincosf(acc[v] * row_scale, &sv, &cv);
-          sv *= amp;
-          cv *= amp;
-        }
-        if constexpr (FEATURE_MAJOR) {
-          phi[(static_cast<size_t>(bh) * M + l) * ld + i] = sv;
-          phi[(static_cast<size_t>(bh) * M + m + l) * ld + i] = cv;
-        } else {
-          phi[(static_cast<size_t>(bh) * n + i) * M + l] = sv;
-          phi[(static_cast<size_t>(bh) * n + i) * M + m + l] = cv;
-        }
-      } else {
-        const float val = i < n ? expf(fmaf(acc[v], row_scale, -half_sq)) * inv_sqrt_m : 0.f;
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
+      float wr[32];
+      lds_half_row64(ws, (l0 % 128) + 32 * t + c, half, wr);
+#pragma unroll
+      for (int s2 = 0; s2 < 32; ++s2) {
         if constexpr (FEATURE_MAJOR)
-          phi[(static_cast<size_t>(bh) * M + l) * ld + i] = val;
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(wr[s2], xr[s2], acc[t], 0, 0, 0);
         else
-          phi[(static_cast<size_t>(bh) * n + i) * M + l] = val;
+          acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(xr[s2], wr[s2], acc[t], 0, 0, 0);
       }
     }
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        // 32x32 MFMA result layout: lane holds column lane%32, rows 8(v/4) + 4(lane/32) + v%4
+        const int row = 8 * (v >> 2) + 4 * half + (v & 3);
+        const int li = FEATURE_MAJOR ? row : c;  // feature within the 32-feature tile t
+        const int ii = FEATURE_MAJOR ? c : row;  // position within the wave's 32
+        // ||x||^2 of position i0 + ii lives in lanes ii and ii + 32
+        const float sqi = FEATURE_MAJOR ? sq : __shfl(sq, ii);
+        const bool nz = sqi > 0.f;
+        // phi of x / ||x|| when normalising (Algorithm 1, first step): the
+        // projections scale by 1 / ||x|| and ||x||^2 / 2 becomes 1/2 (a zero
+        // row stays zero)
+        const float half_sq = nprf ? (nz ? 0.5f : 0.f) : 0.5f * sqi;
+        const float row_scale = nprf ? (nz ? rsqrtf(sqi) : 0.f) : 1.f;
+        const int l = l0 + 32 * t + li, i = i0 + ii;
+        if (i < n_store && l < m) {
+          if (trf) {
+            float sv = 0.f, cv = 0.f;
+            if (i < n) {
+              const float amp = expf(half_sq) * inv_sqrt_m;
+              sincosf(acc[t][v] * row_scale, &sv, &cv);
+              sv *= amp;
+              cv *= amp;
+            }
+            if constexpr (FEATURE_MAJOR) {
+              phi[(static_cast<size_t>(bh) * M + l) * ld + i] = sv;
+              phi[(static_cast<size_t>(bh) * M + m + l) * ld + i] = cv;
+            } else {
+              phi[(static_cast<size_t>(bh) * n + i) * M + l] = sv;
+              phi[(static_cast<size_t>(bh) * n + i) * M + m + l] = cv;
+            }
+          } else {
+            const float val = i < n ? expf(fmaf(acc[t][v], row_scale, -half_sq)) * inv_sqrt_m : 0.f;
+            if constexpr (FEATURE_MAJOR)
+              phi[(static_cast<size_t>(bh) * M + l) * ld + i] = val;
+            else
+              phi[(static_cast<size_t>(bh) * n + i) * M + l] = val;
+          }
+        }
+      }
   }
 }
 
@@ -1860,24 +1895,28 @@ hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const f
   const dim3 grid(static_cast<unsigned>(blocks));
   const int np = nprf ? 1 : 0, trf = kind == kFeatTrf ? 1 : 0;
   if (d == 64) {
+    // 128 positions and every feature per work-group
+    const int tiles128 = (rows + kFm64Pos - 1) / kFm64Pos;
+    const dim3 grid(static_cast<unsigned>(static_cast<long long>(tiles128) * BH * nsrc));
+    const int tiles_n = tiles128;
     if (bf16) {
       const uint16_t* a = static_cast<const uint16_t*>(x0);
       const uint16_t* c = static_cast<const uint16_t*>(x1);
       if (feature_major)
         hipLaunchKernelGGL((k_feature_map64<uint16_t, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
-                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+                           inv_sqrt_m, tiles_n, BH, fix_counts, np, trf);
       else
         hipLaunchKernelGGL((k_feature_map64<uint16_t, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
-                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+                           inv_sqrt_m, tiles_n, BH, fix_counts, np, trf);
     } else {
       const float* a = static_cast<const float*>(x0);
       const float* c = static_cast<const float*>(x1);
       if (feature_major)
         hipLaunchKernelGGL((k_feature_map64<float, true>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
-                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+                           inv_sqrt_m, tiles_n, BH, fix_counts, np, trf);
       else
         hipLaunchKernelGGL((k_feature_map64<float, false>), grid, block, 0, st, a, c, W, phi0, phi1, H, n, ld, m,
-                           inv_sqrt_m, tiles_n, tiles_m, BH, fix_counts, np, trf);
+                           inv_sqrt_m, tiles_n, BH, fix_counts, np, trf);
     }
     return hipGetLastError();
   }
