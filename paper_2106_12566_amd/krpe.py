@@ -43,15 +43,17 @@ class KrpeError(RuntimeError):
 
 
 def lib_path() -> str:
-    return _LIB_PATH
+    """The library this binding loads: $KRPE_LIBRARY if set (e.g. a build with host-side
+    sanitizers), else libkrpe.so next to this file."""
+    return os.environ.get("KRPE_LIBRARY") or _LIB_PATH
 
 
 def load(path: str | None = None) -> ctypes.CDLL:
-    """Load libkrpe.so (once).  Raises KrpeError if it has not been built."""
+    """Load the library (once).  Raises KrpeError if it has not been built."""
     global _lib
     if _lib is not None and path is None:
         return _lib
-    p = path or _LIB_PATH
+    p = path or lib_path()
     if not os.path.exists(p):
         raise KrpeError(f"{p} is missing: build it with `python -m paper_2106_12566_amd.build`")
     lib = ctypes.CDLL(p)
