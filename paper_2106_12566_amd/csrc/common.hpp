@@ -77,8 +77,10 @@ struct Conf {
   // Per-position values (v pairs, prefetched phi), the spectrum and the
   // hoisted twiddles stay in registers only for work-groups of <= 256
   // threads (512 registers per thread); larger ones re-read them.
-  static constexpr bool VREG = THREADS <= 256 && FOLD == 1;
-  static constexpr bool PREF = VREG && WPE == 1;
+  // (At N = 16384 the FOLD x R value pairs of a thread stay in registers too:
+  // the loop's twiddles and spectrum are its only other loop-invariant state.)
+  static constexpr bool VREG = (THREADS <= 256 && FOLD == 1) || L2 == 14;
+  static constexpr bool PREF = VREG && WPE == 1 && FOLD == 1;
   static constexpr bool HREG = THREADS <= 256 || L2 == 14;
   static constexpr bool HOIST = (THREADS <= 256 && FOLD != 2) || L2 == 14;
   // phi(q) too loaded a feature ahead (where the registers allow it without

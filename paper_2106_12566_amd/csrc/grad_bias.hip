@@ -32,7 +32,7 @@ __device__ __forceinline__ void corr_loop(const float* __restrict__ pk, const fl
                                           float2 (&acc)[C::KH][C::F::R]) {
   using F = typename C::F;
   constexpr int FOLD = C::FOLD, KH = C::KH, S = C::S;
-  constexpr bool MERGE = F::P > 1, REG = C::VREG;
+  constexpr bool MERGE = F::P > 1, REG = C::VREG && FOLD == 1;
   constexpr int NP = FOLD * F::N;
   float2 vx[REG ? FOLD : 1][REG ? F::R : 1], gx[REG ? FOLD : 1][REG ? F::R : 1];
   if constexpr (REG) {

@@ -621,11 +621,14 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
   constexpr int FOLD = C::FOLD, KH = C::KH, S = C::S;
   constexpr bool VREG = C::VREG, PREF = C::PREF, HREG = C::HREG, HOIST = C::HOIST;
   constexpr bool MERGE = F::P > 1;
-  // One class and no fold (the classes of a length-N transform): the
-  // per-register twist factor W_{RS}^{r i} of the input is applied to v once,
-  // phi_l(k) being real, and that of the output to the accumulators after the
-  // loop, phi_l(q) being real and the rotation linear.
-  constexpr bool PRETWIST = MERGE && KH == 1 && FOLD == 1 && VREG && R0 != 0;
+  // One class per unit with v in registers: the per-register twist factor
+  // W_{RS}^{r i} and the fold factors W_S^{p r} of the input are applied to v
+  // once, phi_l(k) being real, so the fold is a plain sum of phi v.
+  constexpr bool PRETWIST = MERGE && KH == 1 && VREG && R0 != 0;
+  // The output twist W_{2N}^{-r i} W_S^{-q r} of a unit with one class does
+  // not depend on the feature either: the accumulators hold the untwisted
+  // sums of phi_l(q) IDFT(...) and are rotated once after the loop.
+  constexpr bool POSTTWIST = MERGE && KH == 1 && R0 != 0;
   constexpr int NP = FOLD * F::N;  // row length of phi and v
   // With C::BUF, phi rows and value pairs are read through buffer resources:
   // the lane's byte offset in a VGPR, the feature's and register's offset in
@@ -666,7 +669,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
 #pragma unroll
       for (int i = 0; i < F::R; ++i) {
         const float2 vv = v_at(tau, p, i);
-        vx[p][i] = PRETWIST ? rot_dyn<F::R * S, false>(vv, R0 * i) : vv;
+        vx[p][i] = PRETWIST ? rot_dyn<S, false>(rot_dyn<F::R * S, false>(vv, R0 * i), p * R0) : vv;
       }
   }
   // Merged first-pass twiddles (MERGE), or the plain twists W_{2N}^{r j}
@@ -747,10 +750,10 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       }
       constexpr_for<KH>([&](auto kc) {
         constexpr int k = decltype(kc)::value, r = R0 + k;
-        // fold: u = sum_p xb[p] W_S^{p r}
+        // fold: u = sum_p xb[p] W_S^{p r} (the factors already in v with PRETWIST)
         float2 u = xb[0];
 #pragma unroll
-        for (int p = 1; p < FOLD; ++p) u = cadd(u, rot_dyn<S, false>(xb[p], p * r));
+        for (int p = 1; p < FOLD; ++p) u = cadd(u, PRETWIST ? xb[p] : rot_dyn<S, false>(xb[p], p * r));
         if constexpr (r == 0 || PRETWIST) {
           x[k][i] = u;
         } else if constexpr (MERGE) {
@@ -802,7 +805,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       float2 yk[KH];
       constexpr_for<KH>([&](auto kc) {
         constexpr int k = decltype(kc)::value, r = R0 + k;
-        if constexpr (r == 0 || PRETWIST) {
+        if constexpr (r == 0 || POSTTWIST) {
           yk[k] = x[k][i];
         } else if constexpr (MERGE) {
           yk[k] = rot_dyn<F::R * S, true>(x[k][i], r * i);
@@ -815,7 +818,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
         float2 y = make_float2(0.f, 0.f);
 #pragma unroll
         for (int k = 0; k < KH; ++k) {
-          const float2 t = rot_dyn<S, true>(yk[k], q * (R0 + k));  // W_S^{-q r}
+          const float2 t = POSTTWIST ? yk[k] : rot_dyn<S, true>(yk[k], q * (R0 + k));  // W_S^{-q r}
           y = k == 0 ? t : cadd(y, t);
         }
         acc0[q][i] = fmaf(f[q][i], y.x, acc0[q][i]);
@@ -823,13 +826,16 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       }
     }
   }
-  if constexpr (PRETWIST) {
+  if constexpr (POSTTWIST) {
 #pragma unroll
-    for (int i = 0; i < F::R; ++i) {
-      const float2 y = rot_dyn<F::R * S, true>(make_float2(acc0[0][i], acc1[0][i]), R0 * i);
-      acc0[0][i] = y.x;
-      acc1[0][i] = y.y;
-    }
+    for (int q = 0; q < FOLD; ++q)
+#pragma unroll
+      for (int i = 0; i < F::R; ++i) {
+        const float2 y = rot_dyn<S, true>(rot_dyn<F::R * S, true>(make_float2(acc0[q][i], acc1[q][i]), R0 * i),
+                                          q * R0);
+        acc0[q][i] = y.x;
+        acc1[q][i] = y.y;
+      }
   }
 }
 
