@@ -318,7 +318,7 @@ __device__ __forceinline__ void lds_half_row64(const float* __restrict__ rows, i
 }
 
 template <typename TX, bool FEATURE_MAJOR>
-__global__ __launch_bounds__(256) void k_feature_map64(const TX* __restrict__ x0, const TX* __restrict__ x1,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FEATURE_MAJOR ? 4 : 1))) void k_feature_map64(const TX* __restrict__ x0, const TX* __restrict__ x1,
                                                        const float* __restrict__ W, float* __restrict__ phi0,
                                                        float* __restrict__ phi1, int H, int n, int ld, int m,
                                                        float inv_sqrt_m, int tiles_n, int BH,
