@@ -259,22 +259,25 @@ def time_config(wid: int, steps: int, warmup: int, route: str, rows: int = 16) -
     q, k, v = (torch.from_numpy(d[x]).to(dev).to(tdt) for x in ("q", "k", "v"))
     b, W = torch.from_numpy(d["b"]).to(dev), torch.from_numpy(d["W"]).to(dev)
     out = torch.empty((B, H, n, dd), dtype=torch.float32, device=dev)
-    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, route=route), dtype=torch.uint8, device=dev)
+    # a causal workload states its mask (read by the route choice only)
+    cz = bool(wl.causal)
+    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, route=route, causal=cz), dtype=torch.uint8,
+                     device=dev)
     hip = HipEvents()
     events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(steps)]
     for _ in range(warmup):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=route)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, route=route, causal=cz)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(steps):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], route=route)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], route=route, causal=cz)
     torch.cuda.synchronize()
     ms = 1e3 * (time.perf_counter() - t0) / steps
     stage = [float(np.mean([hip.elapsed_ms(ev[i], ev[i + 1]) for ev in events])) for i in range(4)]
     for ev in events:
         for e in ev:
             hip.destroy(e)
-    used = krpe.attention_fwd_route(B, H, n, dd, m, route=route)
+    used = krpe.attention_fwd_route(B, H, n, dd, m, route=route, causal=cz)
     res = {"workload": wl.name, "B": B, "H": H, "n": n, "m": m, "qkv_dtype": wl.qkv_dtype, "route": used,
            "ms_per_layer": ms, "tokens_per_s": B * n / (ms * 1e-3),
            "exact_rows": krpe.attention_fwd_fixed_rows(ws, B, H, n, dd, m)}
@@ -392,7 +395,8 @@ def main() -> int:
         m = dd                       # elu + 1 has one feature per coordinate
     M = 2 * m if fm == "trf" else m  # features per position
     rt = args.route
-    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt),
+    cz = bool(wl.causal)  # a causal workload states its mask (read by the route choice only)
+    ws = torch.empty(krpe.attention_fwd_workspace(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt, causal=cz),
                      dtype=torch.uint8, device=dev)
     print(f"bench: workload {wl.name} B={B} H={H} n={n} d={dd} m={m} {wl.qkv_dtype}", file=sys.stderr,
           flush=True)
@@ -401,13 +405,13 @@ def main() -> int:
     events = [[hip.create() for _ in range(krpe.STAGE_EVENTS)] for _ in range(args.steps)]
 
     for _ in range(args.warmup):
-        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf, features=fm, route=rt)
+        krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, nprf=args.nprf, features=fm, route=rt, causal=cz)
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
     for s in range(args.steps):
         krpe.attention_fwd(q, k, v, b, W, out=out, workspace=ws, events=events[s], nprf=args.nprf, features=fm,
-                           route=rt)
+                           route=rt, causal=cz)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
@@ -421,7 +425,7 @@ def main() -> int:
     tokens = B * n
     value = tokens / (ms_per_step * 1e-3)
 
-    route_used = krpe.attention_fwd_route(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt)
+    route_used = krpe.attention_fwd_route(B, H, n, dd, m, nprf=args.nprf, features=fm, route=rt, causal=cz)
     s_in = 2 if wl.qkv_dtype == "bf16" else 4
     if route_used == "fft":
         flops = conv_stage_flops(B, H, n, dd, M, d["b"])

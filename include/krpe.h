@@ -112,6 +112,16 @@ typedef enum {
  */
 #define KRPE_ROUTE_DIRECT 8u
 #define KRPE_ROUTE_FFT 16u
+/*
+ * KRPE_HINT_CAUSAL: the caller states that b[h][t + n - 1] = -inf for every
+ * t > 0 (query i attends to keys j <= i only, the causal mask of Sec. 3.2's
+ * relative-position view).  Read by the route choice alone: the direct route
+ * visits only the keys inside each row's finite-b range, so with the hint
+ * its cost model counts n (n + 1) / 2 query/key pairs instead of n^2.
+ * Results do not depend on it (both routes evaluate Eq. (10) for the b
+ * given), and a wrong hint only costs time.
+ */
+#define KRPE_HINT_CAUSAL 32u
 
 /* Version of this ABI (incremented on any incompatible change). */
 int krpe_abi_version(void);
@@ -189,7 +199,8 @@ size_t krpe_attention_fwd_workspace_ex(int B, int H, int n, int d, int m, unsign
  * KRPE_ROUTE_DIRECT or KRPE_ROUTE_FFT (0 if the sizes or bits are invalid).
  * Without a route bit it follows a cost model of both routes measured on
  * MI355X (work over the B*H heads plus each route's fixed cost); it counts
- * all n^2 query/key pairs (b is not read on the host).
+ * all n^2 query/key pairs (b is not read on the host), n (n + 1) / 2 with
+ * KRPE_HINT_CAUSAL.
  */
 int krpe_attention_fwd_route(int B, int H, int n, int d, int m, unsigned flags);
 

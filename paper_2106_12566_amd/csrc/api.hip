@@ -64,7 +64,9 @@ krpe_status_t check_dims(int B, int H, int n, int d, int m, bool need_dm, int ma
   return KRPE_OK;
 }
 
-constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT;
+constexpr unsigned kKnownFlags =
+    KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT | KRPE_HINT_CAUSAL;
+constexpr unsigned kBwdFlags = KRPE_NPRF | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT | KRPE_HINT_CAUSAL;
 
 // Whether the direct route is the faster one for BH heads of length n with M
 // features and d value columns.  Cost model fitted to MI355X timings of both
@@ -75,10 +77,13 @@ constexpr unsigned kKnownFlags = KRPE_NPRF | KRPE_FEAT_TRF | KRPE_FEAT_ELU | KRP
 // 5e-5 s.  FFT: per column pair, feature and point of the length-2N
 // transform times log2(2N), 1.65e-13 s up to N = 4096, 3.8e-13 s at N = 8192
 // and 3.0e-13 s at N = 16384, over the nb^2 block pairs of a blocked
-// sequence, plus 1.5e-4 s.  All n^2 pairs are counted: the host does not read
-// b, so a causal mask (half the pairs on the direct route) is not seen; the
-// route bits force either route.
-bool direct_is_faster(long long BH, int n, int M, int d) {
+// sequence, plus 1.5e-4 s.  All n^2 pairs are counted, as the host does not
+// read b, unless the caller states a causal mask (KRPE_HINT_CAUSAL): the
+// exact-row kernel then visits the n (n + 1) / 2 pairs j <= i only (measured
+// at n = 16384, 16 heads, m = 256: 14.8 ms direct, 19.1 ms FFT), and a blocked
+// FFT route runs the nb (nb + 1) / 2 block pairs on or below the diagonal.
+// The route bits force either route.
+bool direct_is_faster(long long BH, int n, int M, int d, bool causal) {
   int l2 = 0;
   while ((1 << l2) < n) ++l2;
   // beyond one transform block the FFT route runs nb^2 block pairs
@@ -86,9 +91,12 @@ bool direct_is_faster(long long BH, int n, int M, int d) {
   if (l2 > kMaxLog2N) l2 = kMaxLog2N;
   const double L = 2.0 * static_cast<double>(1 << l2);
   const double heads = static_cast<double>(BH);
-  const double direct = 2.45e-14 * heads * static_cast<double>(n) * n * (M + d + 1) + 5.0e-5;
+  const double pairs = causal ? 0.5 * static_cast<double>(n) * (n + 1) : static_cast<double>(n) * n;
+  const double direct = 2.45e-14 * heads * pairs * (M + d + 1) + 5.0e-5;
   const double rate = l2 <= 12 ? 1.65e-13 : (l2 == 13 ? 3.8e-13 : 3.0e-13);
-  const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * nb * nb + 1.5e-4;
+  // (a causal mask leaves nb (nb + 1) / 2 of the block pairs live; the others are skipped)
+  const double blocks = causal ? 0.5 * nb * (nb + 1) : static_cast<double>(nb) * nb;
+  const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * blocks + 1.5e-4;
   return direct < fft;
 }
 
@@ -98,7 +106,7 @@ bool direct_is_faster(long long BH, int n, int M, int d) {
 bool use_direct(unsigned flags, long long BH, int n, int M, int d) {
   if (flags & KRPE_ROUTE_DIRECT) return true;
   if (flags & KRPE_ROUTE_FFT) return false;
-  return direct_is_faster(BH, n, M, d);
+  return direct_is_faster(BH, n, M, d, (flags & KRPE_HINT_CAUSAL) != 0);
 }
 
 // Feature map selected by the option bits, and its number of features M
@@ -725,7 +733,7 @@ int krpe_attention_fwd_route(int B, int H, int n, int d, int m, unsigned flags) 
 
 size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned flags) {
   if (B < 0 || H < 0 || n < 1 || n > (1 << kMaxLog2N) || d < 1 || d > kMaxD || m < 1 || m > kMaxM) return 0;
-  if (flags & ~static_cast<unsigned>(KRPE_NPRF | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT)) return 0;
+  if (flags & ~kBwdFlags) return 0;
   return bwd_layout(B, H, n, d, m).total;
 }
 
@@ -735,8 +743,8 @@ krpe_status_t krpe_attention_bwd(const void* q, const void* k, const void* v, in
                                  void* stream) {
   g_last_error.clear();
   if (krpe_status_t s = check_dims(B, H, n, d, m, true)) return s;
-  if (flags & ~static_cast<unsigned>(KRPE_NPRF | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT))
-    return fail(KRPE_ERR_UNSUPPORTED, "the backward pass takes KRPE_NPRF and the route bits (PRF features)");
+  if (flags & ~kBwdFlags)
+    return fail(KRPE_ERR_UNSUPPORTED, "the backward pass takes KRPE_NPRF, the route bits and KRPE_HINT_CAUSAL (PRF features)");
   if ((flags & KRPE_ROUTE_DIRECT) && (flags & KRPE_ROUTE_FFT))
     return fail(KRPE_ERR_UNSUPPORTED, "KRPE_ROUTE_DIRECT and KRPE_ROUTE_FFT are exclusive");
   if (qkv_dtype != KRPE_F32 && qkv_dtype != KRPE_BF16) return fail(KRPE_ERR_DTYPE, "qkv_dtype must be F32 or BF16");

@@ -1241,7 +1241,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const float* __restrict__ cexp, float* __restrict__ z, float* __restrict__ den_out,
     const unsigned* __restrict__ fix, const unsigned long long* __restrict__ fixmask, double* __restrict__ fixpart,
     const int2* __restrict__ brange, int BH, int H, int n, int ld, int d, int m, int slots) {
-  extern __shared__ __align__(16) float sq[];  // phi(q) of the group's rows, [l][32], l < m rounded up to 32
+  extern __shared__ __align__(16) float sq[];  // phi(q) of the group's rows, [l][32], l < m rounded up to 64
   __shared__ double red[2][16][64];            // another wave's totals (two column tiles)
   __shared__ double rden[4][kFixRows];
   __shared__ int srows[kFixRows];
@@ -1264,7 +1264,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const TV* __restrict__ vh = vv + static_cast<size_t>(bh) * n * d;
   const BufRd bk(pk, static_cast<uint32_t>(m) * ld * 4u), bv(vh, static_cast<uint32_t>(n) * d * sizeof(TV));
   const BufRd bc(ch, static_cast<uint32_t>(2 * n - 1) * 4u);
-  const int mr = (m + 31) & ~31;
+  // features in steps of 2 kFixL (phi(k) operands ping-pong between two
+  // register sets); sq and the buffer reads give zeros past m
+  const int mr = (m + 2 * kFixL - 1) & ~(2 * kFixL - 1);
   const int tiles = (d + 31) / 32;
 
   // Queued rows in row order: group g takes the ranks 32 g .. 32 g + 31 of
@@ -1335,17 +1337,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 16; ++e) zt[t][e] = 0.0;
-      // phi(k) operands of one 32-feature step: A[key jc + lr][feature l0 + 2 q + lh]
-      float kb[kFixL / 2], kn[kFixL / 2];
+      // phi(k) operands of one 32-feature step: A[key jc + lr][feature l0 + 2 q + lh],
+      // two sets: a step multiplies one while the other is loaded
+      float ka[kFixL / 2], kc[kFixL / 2];
       // (reads past the m feature rows give zero; keys >= n are masked in P)
-      auto load_k = [&](int jc, int l0) {
+      auto load_k = [&](float (&dst)[kFixL / 2], int jc, int l0) {
         const uint32_t voff = static_cast<uint32_t>(lh * ld + jc + lr) * 4u;
 #pragma unroll
         for (int q = 0; q < kFixL / 2; ++q)
-          kn[q] = bk.f32(voff, static_cast<uint32_t>((l0 + 2 * q) * ld) * 4u);
+          dst[q] = bk.f32(voff, static_cast<uint32_t>((l0 + 2 * q) * ld) * 4u);
+      };
+      auto s_step = [&](const float (&kk)[kFixL / 2], int l0, floatx16& acc) {
+#pragma unroll
+        for (int q = 0; q < kFixL / 2; ++q) {
+          const float qb = sq[(l0 + 2 * q + lh) * kFixRows + lr];
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(kk[q], qb, acc, 0, 0, 0);
+        }
       };
       int jc = cb * kFixKeys + 32 * wave;
-      if (jc < ce * kFixKeys) load_k(jc, 0);
+      if (jc < ce * kFixKeys) load_k(ka, jc, 0);
       for (; jc < ce * kFixKeys; jc += kFixKeys) {
         // value rows of these 32 keys, in the key order of the P V steps:
         // step e uses key jc + 8 (e / 4) + 4 lh + e % 4 on lane half lh
@@ -1371,19 +1381,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         floatx16 sacc;
 #pragma unroll
         for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
-        for (int l0 = 0; l0 < mr; l0 += kFixL) {
-#pragma unroll
-          for (int q = 0; q < kFixL / 2; ++q) kb[q] = kn[q];
-          if (l0 + kFixL < mr) {
-            load_k(jc, l0 + kFixL);
+        for (int l0 = 0; l0 < mr; l0 += 2 * kFixL) {
+          load_k(kc, jc, l0 + kFixL);
+          s_step(ka, l0, sacc);
+          if (l0 + 2 * kFixL < mr) {
+            load_k(ka, jc, l0 + 2 * kFixL);
           } else if (jc + kFixKeys < ce * kFixKeys) {
-            load_k(jc + kFixKeys, 0);  // the next key block's first step
+            load_k(ka, jc + kFixKeys, 0);  // the next key block's first step
           }
-#pragma unroll
-          for (int q = 0; q < kFixL / 2; ++q) {
-            const float qb = sq[(l0 + 2 * q + lh) * kFixRows + lr];
-            sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(kb[q], qb, sacc, 0, 0, 0);
-          }
+          s_step(kc, l0 + kFixL, sacc);
         }
         // ---- P = S^T c_{j-i}: lane holds keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow
         // (c indices are >= 0 for a queued row; past 2n - 2 they read zero)
@@ -2038,7 +2044,7 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
   hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, cexp, n);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   const long long blocks = static_cast<long long>(BH) * slots;
-  const size_t lds = static_cast<size_t>((m + 31) & ~31) * kFixRows * sizeof(float);
+  const size_t lds = static_cast<size_t>((m + 2 * kFixL - 1) & ~(2 * kFixL - 1)) * kFixRows * sizeof(float);
   if (lds > 64 * 1024) {
     // phi(q) of a group exceeds the default dynamic LDS limit for m > 512
     static const hipError_t once = [] {

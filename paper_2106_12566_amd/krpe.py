@@ -36,6 +36,7 @@ FEATURES = {"prf": 0, "trf": FEAT_TRF, "elu": FEAT_ELU}
 ROUTE_DIRECT = 8  # option bit: evaluate Eq. (10) directly (quadratic, MFMA)
 ROUTE_FFT = 16  # option bit: the FFT route of Section 3.2
 ROUTES = {"auto": 0, "direct": ROUTE_DIRECT, "fft": ROUTE_FFT}
+HINT_CAUSAL = 32  # option bit: b is -inf for every t > 0 (read by the route choice only)
 
 
 class KrpeError(RuntimeError):
@@ -129,12 +130,12 @@ def _dtype_code(t: torch.Tensor, name: str) -> int:
     return DTYPES[t.dtype]
 
 
-def _flags(nprf: bool, features: str, route: str = "auto") -> int:
+def _flags(nprf: bool, features: str, route: str = "auto", causal: bool = False) -> int:
     if features not in FEATURES:
         raise KrpeError(f"features must be one of {sorted(FEATURES)}, got {features!r}")
     if route not in ROUTES:
         raise KrpeError(f"route must be one of {sorted(ROUTES)}, got {route!r}")
-    return (NPRF if nprf else 0) | FEATURES[features] | ROUTES[route]
+    return (NPRF if nprf else 0) | FEATURES[features] | ROUTES[route] | (HINT_CAUSAL if causal else 0)
 
 
 def _proj(W: torch.Tensor | None, H: int, d: int, features: str) -> tuple[torch.Tensor | None, int]:
@@ -216,8 +217,8 @@ def toeplitz_conv_noalloc(b: torch.Tensor, a: torch.Tensor, out: torch.Tensor | 
 
 
 def attention_fwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool = False,
-                            features: str = "prf", route: str = "auto") -> int:
-    return int(load().krpe_attention_fwd_workspace_ex(B, H, n, d, m, _flags(nprf, features, route)))
+                            features: str = "prf", route: str = "auto", causal: bool = False) -> int:
+    return int(load().krpe_attention_fwd_workspace_ex(B, H, n, d, m, _flags(nprf, features, route, causal)))
 
 
 def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d: int, m: int) -> int:
@@ -232,7 +233,8 @@ def attention_fwd_fixed_rows(workspace: torch.Tensor, B: int, H: int, n: int, d:
 
 def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor | None,
                   out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
-                  events=None, nprf: bool = False, features: str = "prf", route: str = "auto") -> torch.Tensor:
+                  events=None, nprf: bool = False, features: str = "prf", route: str = "auto",
+                  causal: bool = False) -> torch.Tensor:
     """Eq. (10): z [B,H,n,d] fp32 from q, k, v [B,H,n,d] (fp32 or bf16), b [H,2n-1], W [H,m,d].
 
     ``nprf``: normalise the rows of q and k first (Algorithm 1's NPRF attention).
@@ -240,6 +242,8 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     (elu + 1, W unused and may be None).
     ``route``: "fft" (Section 3.2), "direct" (Eq. (10) evaluated directly on
     MFMA, faster for short sequences) or "auto" (by sequence length).
+    ``causal``: the caller states that b is -inf for every t > 0; only the
+    "auto" route choice reads it (the direct route then costs half the pairs).
 
     ``out`` and ``workspace`` may be passed to reuse allocations (a uint8 tensor
     of at least attention_fwd_workspace() bytes).  ``events``: optional list of
@@ -253,7 +257,7 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     B, H, n, d = q.shape
     if k.shape != q.shape or v.shape != q.shape or k.dtype != q.dtype or v.dtype != q.dtype:
         raise KrpeError("q, k, v must share shape and dtype")
-    flags = _flags(nprf, features, route)
+    flags = _flags(nprf, features, route, causal)
     W, m = _proj(W, H, d, features)
     if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
         raise KrpeError("b must be float32 [H, 2n-1]")
@@ -281,9 +285,9 @@ def attention_fwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
 
 
 def attention_fwd_route(B: int, H: int, n: int, d: int, m: int, nprf: bool = False, features: str = "prf",
-                        route: str = "auto") -> str:
+                        route: str = "auto", causal: bool = False) -> str:
     """The route ("direct" or "fft") attention_fwd takes for these sizes and options."""
-    r = int(load().krpe_attention_fwd_route(B, H, n, d, m, _flags(nprf, features, route)))
+    r = int(load().krpe_attention_fwd_route(B, H, n, d, m, _flags(nprf, features, route, causal)))
     if r == 0:
         raise KrpeError("invalid sizes or options")
     return "direct" if r == ROUTE_DIRECT else "fft"
@@ -296,7 +300,7 @@ def attention_bwd_workspace(B: int, H: int, n: int, d: int, m: int, nprf: bool =
 
 def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Tensor, W: torch.Tensor,
                   dz: torch.Tensor, workspace: torch.Tensor | None = None, nprf: bool = False,
-                  with_db: bool = False, route: str = "auto") -> tuple:
+                  with_db: bool = False, route: str = "auto", causal: bool = False) -> tuple:
     """Gradients (dq, dk, dv) [B,H,n,d] fp32 of sum(dz * z), z = attention_fwd(q, k, v, b, W, nprf=nprf)
     with PRF features and W fixed (the C header states the formulas); with_db adds db [H, 2n-1]."""
     lib = load()
@@ -314,7 +318,7 @@ def attention_bwd(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, b: torch.Te
     if b.shape != (H, 2 * n - 1) or b.dtype != torch.float32:
         raise KrpeError("b must be float32 [H, 2n-1]")
     m = W.shape[1]
-    flags = _flags(nprf, "prf", route)
+    flags = _flags(nprf, "prf", route, causal)
     wsb = int(lib.krpe_attention_bwd_workspace(B, H, n, d, m, flags))
     if workspace is None:
         workspace = torch.empty(max(wsb, 1), dtype=torch.uint8, device=q.device)

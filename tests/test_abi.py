@@ -116,8 +116,8 @@ def test_attention_validation(lib):
 def test_option_bits_validation(lib):
     wsb = lib.krpe_attention_fwd_workspace(1, 1, 8, 4, 4)
     ex = lambda flags: lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, flags, WSP, wsb, None)
-    assert ex(32) == UNSUP                   # unknown option bit
-    assert ex(1 | 32) == UNSUP
+    assert ex(64) == UNSUP                   # unknown option bit
+    assert ex(1 | 64) == UNSUP
     assert ex(8 | 16) == UNSUP               # both routes
     assert ex(2 | 4) == UNSUP                # TRF and elu + 1 together
     # elu + 1 needs m == d (here d = 4, m = 3); TRF doubles the features (2m <= 1024)
@@ -130,13 +130,14 @@ def test_option_bits_validation(lib):
     assert wse(1) == wse(0)                  # normalisation needs no space
     assert wse(2) > wse(0)                   # 2m trigonometric features
     assert wse(4) == wse(0)                  # elu + 1: M = d = m
-    assert wse(4, m=3) == 0 and wse(6) == 0 and wse(32) == 0 and wse(24) == 0
+    assert wse(4, m=3) == 0 and wse(6) == 0 and wse(64) == 0 and wse(24) == 0
+    assert wse(32) == wse(0)                 # the causal hint needs no space
     assert wse(8) == wse(0) and wse(16) == wse(0)   # one workspace serves both routes
     assert wse(2, m=513) == 0
     assert lib.krpe_attention_fwd_ex(None, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, WSP, wsb, None) == NULL
     assert lib.krpe_attention_fwd_ex(Q, K, V, 0, BB, W, Z, 1, 1, 8, 4, 4, 1, None, wsb, None) == WS
     fm = lambda flags: lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 4, flags, None)
-    assert fm(32) == UNSUP
+    assert fm(64) == UNSUP
     assert fm(6) == UNSUP
     assert lib.krpe_feature_map_ex(Q, 0, W, Z, 1, 1, 8, 4, 3, 4, None) == SHAPE
     assert lib.krpe_feature_map_ex(Q, 0, None, Z, 1, 1, 8, 4, 4, 2, None) == NULL
@@ -200,7 +201,7 @@ def test_backward_validation(lib):
     call = lambda flags=0, db=None, dq=D1, dz=Q, w=WSP, wb=wsb, n=8: lib.krpe_attention_bwd(
         Q, K, V, 0, BB, W, dz, dq, D2, D3, db, 1, 1, n, 4, 4, flags, w, wb, None)
     assert call(flags=2) == UNSUP
-    assert call(flags=32) == UNSUP
+    assert call(flags=64) == UNSUP
     assert call(flags=8 | 16) == UNSUP
     assert call(db=D1) == ALIAS               # db overlapping dq
     assert call(db=Z + 20000 + 4) == ALIGN
@@ -225,3 +226,7 @@ def test_route_query(lib):
     assert route(1, 1, 65536, 64, 128, 8) == 8          # forced, past one transform block
     assert route(1, 1, 65537, 64, 64, 0) == 0 and route(0, 1, 8, 4, 4, 0) == 0
     assert route(1, 1, 8, 4, 4, 8 | 16) == 0 and route(1, 1, 0, 4, 4, 0) == 0 and route(1, 1, 8, 4, 3, 4) == 0
+    # a stated causal mask halves the direct route's pairs: the causal-n16384 layer goes direct,
+    # the causal-n65536 one stays on the FFT route; a route bit still wins over the hint
+    assert route(1, 16, 16384, 64, 256, 32) == 8 and route(1, 16, 65536, 64, 256, 32) == 16
+    assert route(1, 16, 16384, 64, 256, 32 | 16) == 16 and route(8, 12, 4096, 64, 128, 32) == 8
