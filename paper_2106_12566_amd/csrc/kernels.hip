@@ -1287,7 +1287,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
     spre[tiles_n] = acc;
   }
-  for (int item = kslot; item < items; item += slots) {
+  // Items in serpentine order: round i takes kslot in [i slots, (i + 1) slots)
+  // counted up for even i and down for odd i, so under a causal mask (group g
+  // sees about 32 (g + 1) keys) every work-group's total is about the same.
+  for (int round = 0; round * slots < items; ++round) {
+    const int item = (round & 1) ? (round + 1) * slots - 1 - kslot : round * slots + kslot;
+    if (item >= items) continue;  // uniform per work-group
     const int grp = item / kparts, kpart = item % kparts;
     __syncthreads();  // previous item's srows / sq / red consumed
     if (tid < kFixRows) {
