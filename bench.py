@@ -419,6 +419,9 @@ def main() -> int:
     stage_names = ["spectrum", "feature_map", "conv_contract", "combine"]
     stages = {name: float(np.mean([hip.elapsed_ms(ev[i], ev[i + 1]) for ev in events]))
               for i, name in enumerate(stage_names)}
+    # per-call device time (first to last event of each step): spread over the timed steps
+    per_call = np.array([hip.elapsed_ms(ev[0], ev[4]) for ev in events])
+    call_pct = {f"p{q}": float(np.percentile(per_call, q)) for q in (10, 50, 90)}
     for ev in events:
         for e in ev:
             hip.destroy(e)
@@ -457,7 +460,7 @@ def main() -> int:
                    "qkv_dtype": wl.qkv_dtype, "features": wl.features, "bias": wl.bias,
                    "causal": wl.causal, "nprf": args.nprf, "feature_map": fm, "features_per_position": M,
                    "route": route_used, "blocks": -(-n // BLOCK) if route_used == "fft" else None,
-                   "ms_per_layer": ms_per_step, "stages_ms": stages,
+                   "ms_per_layer": ms_per_step, "stages_ms": stages, "call_ms_percentiles": call_pct,
                    "conv_stage_hbm_gbs": conv_gbs,
                    "feature_stage_roofline": (feature_stage_roofline(B, H, n, dd, M, s_in, stages["feature_map"])
                                               if route_used == "fft" and n <= BLOCK and fm == "prf" else None),
