@@ -222,7 +222,9 @@ krpe_status_t krpe_attention_fwd(const void* q, const void* k, const void* v, in
  * krpe_attention_fwd with option bits: KRPE_NPRF normalises the rows of q
  * and k first (Algorithm 1's NPRF attention); KRPE_FEAT_TRF / KRPE_FEAT_ELU
  * select the feature map (W [H, m, d] as above; not read for elu + 1, where
- * m == d).  Workspace: krpe_attention_fwd_workspace_ex with the same flags.
+ * m == d); KRPE_ROUTE_DIRECT / KRPE_ROUTE_FFT force a route and
+ * KRPE_HINT_CAUSAL informs the route choice.  Workspace:
+ * krpe_attention_fwd_workspace_ex with the same flags.
  */
 krpe_status_t krpe_attention_fwd_ex(const void* q, const void* k, const void* v, int qkv_dtype,
                                     const float* b, const float* W, float* z,
@@ -251,7 +253,8 @@ size_t krpe_attention_bwd_workspace(int B, int H, int n, int d, int m, unsigned 
 
 /*
  * Backward pass of krpe_attention_fwd_ex (PRF features of Eq. (5), optional
- * KRPE_NPRF; W fixed): the gradients of L = sum(dz * z) with respect to q, k,
+ * KRPE_NPRF, the route bits and KRPE_HINT_CAUSAL for the recomputed forward;
+ * W fixed): the gradients of L = sum(dz * z) with respect to q, k,
  * v and b, z from Eq. (10).  The paper states no backward pass; these are the
  * derivatives of its forward definition.  With A = C o (phi(Q) phi(K)^T),
  * den = A 1 and Gh = [dz / den, -(dz . z) / den] per row:
