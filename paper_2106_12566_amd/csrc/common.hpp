@@ -75,10 +75,11 @@ struct Conf {
   static constexpr int HSPLIT = S / KH;  // work units per column pair and head
   static constexpr int CONV_LDS_SLOTS = F::P > 1 ? G * KH * F::LDS : 1;
   // Per-position values (v pairs, prefetched phi), the spectrum and the
-  // hoisted twiddles stay in registers only for work-groups of <= 256
-  // threads (512 registers per thread); larger ones re-read them.
-  // (At N = 16384 the FOLD x R value pairs of a thread stay in registers too:
-  // the loop's twiddles and spectrum are its only other loop-invariant state.)
+  // hoisted twiddles stay in registers for work-groups of <= 256 threads
+  // (their 256-register budget holds them); the 512-thread groups of
+  // N = 8192 re-read them.  At N = 16384 (512 threads, one group per CU) the
+  // FOLD x R value pairs of a thread stay in registers too, pre-rotated by
+  // the class and fold twists; phi is not loaded ahead there (PREF).
   static constexpr bool VREG = (THREADS <= 256 && FOLD == 1) || L2 == 14;
   static constexpr bool PREF = VREG && WPE == 1 && FOLD == 1;
   static constexpr bool HREG = THREADS <= 256 || L2 == 14;
