@@ -57,8 +57,12 @@ struct Conf {
   static constexpr bool BUF = L2 == 11 || L2 == 12;
   // Twiddles come from the W_{2N} table.  Affine LDS addressing where it
   // frees the registers that the loads one feature ahead need, and at
-  // N = 16384.
-  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC, L2 == 14 || BUF>;
+  // N = 16384.  At N = 4096 and 16384 the LDS layout has two padding slots
+  // per 16 positions (Fft's PAD): timed one hand-over at a time, it removes
+  // the bank conflicts of the cross-wave boundary and is the fastest single
+  // layout at every boundary of both transforms.
+  static constexpr int PAD = (L2 == 14 || L2 == 12) ? 3 : 0;
+  using F = Fft<L2T, LOG2R, 1 + L2 - L2T, TWC, L2 == 14 || BUF, PAD>;
   static constexpr int N = 1 << L2;
   static constexpr int LT = F::N;  // transform length 2N / S
   static constexpr int G = F::T >= 128 ? 1 : 256 / F::T;  // units per work-group

@@ -274,11 +274,13 @@ struct Dft<16, INV> {
 // entries of the table (see twc_offset), instead of every 2^(LR p + TWS)-th
 // entry of W_M: a few KiB that stay in the L1 cache when the twiddles are
 // re-read per transform rather than kept in registers.
-// AFF: address LDS as pad(base) + constant per butterfly (see pad_step):
+// AFF: address LDS as pad(base) + constant per butterfly (see pad):
 // one address register instead of one per value, which frees registers but
 // lets the compiler pair accesses into 16-byte ds_read2 / ds_write2 forms,
 // slower than 8-byte ones where the LDS is the busier pipe.
-template <int LOG2N_, int LOG2R_, int TWS = 1, bool TWC = false, bool AFF = false>
+// PAD: LDS layout of the hand-overs (see pad); 0 keeps one padding slot per R
+// positions.
+template <int LOG2N_, int LOG2R_, int TWS = 1, bool TWC = false, bool AFF = false, int PAD = 0>
 struct Fft {
   static constexpr int LOG2N = LOG2N_;
   static constexpr int N = 1 << LOG2N;
@@ -320,12 +322,20 @@ struct Fft {
       __syncthreads();
     }
   }
-  __host__ __device__ static constexpr int pad(int a) { return a + (a >> (LR > 0 ? LR : 1)); }
+  // LDS layout of the hand-overs: position a at slot a + PM (a >> PSH), PM
+  // padding slots per 2^PSH positions.  PAD selects (PSH, PM): 0 -> (LR, 1),
+  // 1 -> (3, 1), 2 -> (4, 1), 3 -> (4, 2), 4 -> (5, 1).  Every boundary uses
+  // the same layout: the positions a wave writes at a boundary are then the
+  // slots it owns in its pass, so a wave-local hand-over (no work-group
+  // barrier) never writes a slot that another wave still reads from the
+  // previous boundary.
+  static constexpr int PSH = PAD == 0 ? (LR > 0 ? LR : 1) : (PAD == 1 ? 3 : (PAD == 4 ? 5 : 4));
+  static constexpr int PM = PAD == 3 ? 2 : 1;
+  __host__ __device__ static constexpr int pad(int a) { return a + PM * (a >> PSH); }
   // pad(base + c) for the positions base + SP r of one butterfly (c = SP r):
   // they never straddle a padding group unevenly, so the padded address is
-  // pad(base) plus a constant, pad(base + c) = pad(base) + c + (c >> LR)
-  // (checked exhaustively for every pass of every length and radix used).
-  __host__ __device__ static constexpr int pad_step(int c) { return c + (c >> (LR > 0 ? LR : 1)); }
+  // pad(base) plus a constant, pad(base + c) = pad(base) + pad(c) (checked
+  // exhaustively for every pass of every length, radix and layout used).
   // Table entries: W_M (M), the per-thread first-pass table of the users
   // that keep one (M), then W_{L_p} for p = 1 .. P - 1.
   static constexpr int M_TAB = N << TWS;
@@ -343,7 +353,7 @@ struct Fft {
       return tw[ts << (LR * p + TWS)];
     }
   }
-  static constexpr int LDS = N + (N >> (LR > 0 ? LR : 1)) + 1;  // float2 slots per transform
+  static constexpr int LDS = N + PM * (N >> PSH) + 1;  // float2 slots per transform
   // Order in which a pass reads its RP inputs from LDS: grouped by the
   // radix-4 sub-DFT of Dft<RP> that consumes them first (inputs r0 + A r1,
   // A = RP / 4), so that sub-DFT can start while the later reads are still in
@@ -397,7 +407,7 @@ struct Fft {
 #pragma unroll
           for (int j = 0; j < RP; ++j) {
             const int r = read_order<RP>(j);
-            x[k][u * RP + r] = lds[k * LDS + (AFF ? pb + pad_step(SP * r) : pad(base + SP * r))];
+            x[k][u * RP + r] = lds[k * LDS + (AFF ? pb + pad(SP * r) : pad(base + SP * r))];
           }
       }
     }
@@ -428,7 +438,7 @@ struct Fft {
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
-          for (int s = 0; s < RP; ++s) lds[k * LDS + (AFF ? pb + pad_step(SP * s) : pad(base + SP * s))] = x[k][u * RP + s];
+          for (int s = 0; s < RP; ++s) lds[k * LDS + (AFF ? pb + pad(SP * s) : pad(base + SP * s))] = x[k][u * RP + s];
       }
       fwd_pass<p + 1, K, W0>(x, lds, tw, tau, w0);
     }
@@ -451,7 +461,7 @@ struct Fft {
 #pragma unroll
           for (int j = 0; j < RP; ++j) {
             const int s = read_order<RP>(j);
-            x[k][u * RP + s] = lds[k * LDS + (AFF ? pb + pad_step(SP * s) : pad(base + SP * s))];
+            x[k][u * RP + s] = lds[k * LDS + (AFF ? pb + pad(SP * s) : pad(base + SP * s))];
           }
       }
     }
@@ -482,7 +492,7 @@ struct Fft {
 #pragma unroll
         for (int k = 0; k < K; ++k)
 #pragma unroll
-          for (int r = 0; r < RP; ++r) lds[k * LDS + (AFF ? pb + pad_step(SP * r) : pad(base + SP * r))] = x[k][u * RP + r];
+          for (int r = 0; r < RP; ++r) lds[k * LDS + (AFF ? pb + pad(SP * r) : pad(base + SP * r))] = x[k][u * RP + r];
       }
       inv_pass<p - 1, K, W0>(x, lds, tw, tau, w0);
     }

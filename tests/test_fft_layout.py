@@ -83,6 +83,10 @@ def pass_positions(log2n, log2r):
                 yield p, (b // SP) * L + b % SP, SP, RP, lr
 
 
+# LDS layout modes of the header (its PAD parameter): (shift, slots per group)
+PAD_MODES = {1: (3, 1), 2: (4, 1), 3: (4, 2), 4: (5, 1)}
+
+
 @pytest.mark.parametrize("log2r", [3, 4])
 def test_affine_padded_addresses(log2r):
     count = 0
@@ -95,9 +99,27 @@ def test_affine_padded_addresses(log2r):
 
             for r in range(RP):
                 c = SP * r
-                assert pad(base + c) == pad(base) + c + (c >> sh), (log2n, log2r, p, base, r)
+                assert pad(base + c) == pad(base) + pad(c), (log2n, log2r, p, base, r)
                 count += 1
     assert count > 50000
+
+
+@pytest.mark.parametrize("log2n,log2r,mode", [(12, 3, 3), (12, 4, 3), (12, 3, 2), (12, 3, 1), (12, 4, 4)])
+def test_affine_padded_addresses_of_the_other_layouts(log2n, log2r, mode):
+    """Two padding slots per 16 positions (the layout of the 4096-point transforms at 8 and 16
+    values per thread) and the other modes: every butterfly's padded addresses are still
+    pad(base) + pad(c), and the layout is one-to-one."""
+    sh, mult = PAD_MODES[mode]
+
+    def pad(a):
+        return a + mult * (a >> sh)
+
+    for p, base, SP, RP, lr in pass_positions(log2n, log2r):
+        for r in range(RP):
+            c = SP * r
+            assert pad(base + c) == pad(base) + pad(c), (log2n, log2r, mode, p, base, r)
+    n = 1 << log2n
+    assert len({pad(a) for a in range(n)}) == n
 
 
 def read_order(rp, j):
@@ -118,7 +140,8 @@ def test_header_forms_match():
     text = re.sub(r"\s+", " ", header_text())
     assert "return RP >= 4 ? (j / 4) + A * (j % 4) : j;" in text
     assert "constexpr int A = RP >= 4 ? RP / 4 : 1;" in text
-    assert "static constexpr int pad_step(int c) { return c + (c >> (LR > 0 ? LR : 1)); }" in text
-    assert "static constexpr int pad(int a) { return a + (a >> (LR > 0 ? LR : 1)); }" in text
+    assert "static constexpr int pad(int a) { return a + PM * (a >> PSH); }" in text
+    assert "static constexpr int PSH = PAD == 0 ? (LR > 0 ? LR : 1) : (PAD == 1 ? 3 : (PAD == 4 ? 5 : 4));" in text
+    assert "static constexpr int PM = PAD == 3 ? 2 : 1;" in text
     assert "constexpr int qt = ((e + 8) / 16) % 4;" in text
     assert "constexpr int er = e - 16 * (((e + 8) / 16));" in text
