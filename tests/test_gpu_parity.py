@@ -358,3 +358,19 @@ def test_reuses_output_and_workspace(gpu_lib):
     gpu_lib.attention_fwd(q, k, v, b, W, out=out, workspace=ws)
     ref = gpu_lib.attention_fwd(q, k, v, b, W)
     assert torch.equal(out, ref)
+
+
+def test_empty_batch_and_channels(gpu_lib):
+    """Degenerate sizes through the binding: no batch rows (B = 0) and no channels (C = 0) are
+    valid calls that enqueue nothing and return empty results."""
+    import torch
+    q = torch.empty((0, 2, 64, 16), device="cuda")
+    b = torch.zeros((2, 127), device="cuda")
+    W = torch.randn((2, 8, 16), device="cuda")
+    for route in ("auto", "fft", "direct"):
+        z = gpu_lib.attention_fwd(q, q, q, b, W, route=route)
+        assert z.shape == (0, 2, 64, 16)
+    a = torch.empty((1, 2, 0, 64), device="cuda")
+    y = gpu_lib.toeplitz_conv(b, a)
+    assert y.shape == (1, 2, 0, 64)
+    torch.cuda.synchronize()
