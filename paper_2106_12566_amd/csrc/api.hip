@@ -29,6 +29,11 @@ int log2_ceil(int n) {
 
 size_t align_up(size_t v) { return (v + 255) & ~static_cast<size_t>(255); }
 
+// Bytes of an array of `rows` rows of N floats that the convolution reads as
+// phi rows, plus one row of slack: with buffer reads its loop loads one row
+// past a unit's last row (never used), which for the last unit lands here.
+size_t phi_bytes(size_t rows, size_t N) { return (rows + 1) * N * sizeof(float); }
+
 bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
 
 struct Range {
@@ -175,8 +180,8 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.tw = take(static_cast<size_t>(twiddle_slots(L.l2)) * sizeof(float2));
   L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
   L.hnorm = take(static_cast<size_t>(H) * sizeof(float2));
-  L.phiq = take(bh * m * N * sizeof(float));
-  L.phik = take(bh * m * N * sizeof(float));
+  L.phiq = take(phi_bytes(bh * m, N));
+  L.phik = take(phi_bytes(bh * m, N));
   L.vsc = take(bh * pairs * N * sizeof(float2));
   L.colmax = take(bh * cols * sizeof(float));
   L.vmax = take(bh * vmax_chunks(n) * static_cast<size_t>(d) * sizeof(float));
@@ -208,8 +213,8 @@ BwdLayout bwd_layout(int B, int H, int n, int d, int M) {
   L.den = take(bh * n * sizeof(float));
   L.brev = take(static_cast<size_t>(H) * (2 * n - 1) * sizeof(float));
   L.hsr = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
-  L.gh = take(bh * (d + 1) * N * sizeof(float));
-  L.vh = take(bh * (d + 1) * N * sizeof(float));
+  L.gh = take(phi_bytes(bh * (d + 1), N));
+  L.vh = take(phi_bytes(bh * (d + 1), N));
   L.vsc = take(bh * pairs * N * sizeof(float2));
   L.colmax = take(bh * cmax * sizeof(float));
   L.vmax = take(bh * vmax_chunks(n) * cmax * sizeof(float));
@@ -288,7 +293,7 @@ ConvLayout conv_layout(int B, int H, int C, int n) {
   };
   L.tw = take(static_cast<size_t>(twiddle_slots(L.l2)) * sizeof(float2));
   L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
-  L.ones = take(N * sizeof(float));
+  L.ones = take(phi_bytes(1, N));
   L.vsc = take(bh * pairs * N * sizeof(float2));
   L.colmax = take(bh * C * sizeof(float));
   L.vmax = take(bh * vmax_chunks(n) * static_cast<size_t>(C) * sizeof(float));

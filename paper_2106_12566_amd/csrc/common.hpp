@@ -105,8 +105,10 @@ __device__ __forceinline__ int xcd_block(int b, int nblocks) {
 
 // Reads through a raw buffer resource (gfx9 descriptor: base, byte range,
 // word 3 = 0x00020000): a per-lane byte offset (VGPR) plus a wave-uniform
-// byte offset (SGPR), with no 64-bit address arithmetic per load.  Reads at
-// or past `bytes` return zero.
+// byte offset (SGPR), with no 64-bit address arithmetic per load.  The range
+// check covers the VGPR offset only: a read whose VGPR offset is at or past
+// `bytes` returns zero, but the SGPR offset is added unchecked, so callers keep
+// the sum inside the buffer themselves.
 struct BufRd {
   __amdgpu_buffer_rsrc_t r;
   __device__ __forceinline__ BufRd(const void* base, uint32_t bytes)

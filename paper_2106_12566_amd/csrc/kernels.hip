@@ -632,8 +632,12 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
   constexpr int NP = FOLD * F::N;  // row length of phi and v
   // With C::BUF, phi rows and value pairs are read through buffer resources:
   // the lane's byte offset in a VGPR, the feature's and register's offset in
-  // an SGPR (no 64-bit address arithmetic per load); reads past the unit's
-  // rows return zero.  Otherwise through plain pointers.
+  // an SGPR (no 64-bit address arithmetic per load).  Otherwise through plain
+  // pointers.  With buffer reads the loop loads phi a feature ahead without a
+  // branch: on its last iteration feature m, never used, which the range
+  // check (it covers the VGPR offset only) does not stop.  That read stays
+  // within one phi row past the unit's m rows, and the workspace layouts keep
+  // a row of slack after every array the convolution reads as phi rows.
   constexpr bool BUF = C::BUF;
   const BufRd bk(pk, static_cast<uint32_t>(m) * NP * 4u), bq(pq, static_cast<uint32_t>(m) * NP * 4u);
   const BufRd bv(vrow, static_cast<uint32_t>(NP) * 8u);
@@ -732,7 +736,7 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       for (int p = 0; p < FOLD; ++p)
 #pragma unroll
         for (int i = 0; i < F::R; ++i) f[p][i] = phi_at(QS, tau, l, p, i);
-      if (BUF || l + 1 < m) {  // (buffer reads past the last feature give zero)
+      if (BUF || l + 1 < m) {  // (see the buffer reads above)
 #pragma unroll
         for (int p = 0; p < FOLD; ++p)
 #pragma unroll
@@ -790,7 +794,8 @@ __device__ __forceinline__ void conv_loop(const float* __restrict__ pk, const fl
       for (int p = 0; p < FOLD; ++p)
 #pragma unroll
         for (int i = 0; i < F::R; ++i) {
-          // (NEXTK and NEXTQ come with buffer reads: zero past the last feature)
+          // (the last iteration loads a feature m that is never used: see the
+          // buffer reads above)
           if constexpr (NEXTQ) {
             f[p][i] = f_next[NEXTQ ? p : 0][NEXTQ ? i : 0];
             f_next[NEXTQ ? p : 0][NEXTQ ? i : 0] = phi_at(QS, taul, l + 1, p, i);
@@ -1207,6 +1212,40 @@ __host__ __device__ inline int fix_key_parts(int ngroups, int slots, int n) {
   return k < 1 ? 1 : (k > kFixMaxParts ? kFixMaxParts : k);
 }
 
+// Exclusive prefix counts of the set bits of the row-mask words w[0, nw):
+// pre[t] = number of queued rows in words < t, pre[nw] = all of them
+// (nw <= kFixMaxTiles).  All 256 threads of the work-group take part: thread
+// tid counts words 4 tid .. 4 tid + 3, a wave scan and the four wave totals
+// (wtot, LDS) give each thread its offset.  Ends with a barrier.
+__device__ __forceinline__ void fix_mask_prefix(const unsigned long long* w, unsigned* pre, unsigned* wtot, int nw) {
+  constexpr int P = kFixMaxTiles / 256;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  unsigned c[P], sum = 0;
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int t = P * tid + j;
+    c[j] = t < nw ? static_cast<unsigned>(__popcll(w[t])) : 0u;
+    sum += c[j];
+  }
+  unsigned x = sum;  // inclusive scan over the wave
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const unsigned y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) wtot[wave] = x;
+  __syncthreads();
+  unsigned acc = x - sum;
+  for (int v = 0; v < wave; ++v) acc += wtot[v];
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    if (P * tid + j < nw) pre[P * tid + j] = acc;
+    acc += c[j];
+  }
+  if (tid == 255) pre[nw] = acc;  // the last thread's running count is the total
+  __syncthreads();
+}
+
 // Range [lo, hi] of s = t + n - 1 where b_t is finite, per head (lo > hi if
 // none), and the table cexp[h][s] = exp(b[h][s]) (c_t of Eq. (6)).
 __global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int2* __restrict__ brange,
@@ -1235,7 +1274,7 @@ __global__ __launch_bounds__(256) void k_brange(const float* __restrict__ b, int
   if (threadIdx.x == 0) brange[blockIdx.x] = make_int2(smin, smax);
 }
 
-template <typename TV>
+template <typename TV, bool MTAIL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_fixup(
     const float* __restrict__ phiq, const float* __restrict__ phik, const TV* __restrict__ vv,
     const float* __restrict__ cexp, float* __restrict__ z, float* __restrict__ den_out,
@@ -1248,6 +1287,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ int smin, smax;
   __shared__ unsigned long long smask[kFixMaxTiles];
   __shared__ unsigned spre[kFixMaxTiles + 1];
+  __shared__ unsigned swtot[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
   // slot-major order: the first item of every head is dispatched first
@@ -1264,8 +1304,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const TV* __restrict__ vh = vv + static_cast<size_t>(bh) * n * d;
   const BufRd bk(pk, static_cast<uint32_t>(m) * ld * 4u), bv(vh, static_cast<uint32_t>(n) * d * sizeof(TV));
   const BufRd bc(ch, static_cast<uint32_t>(2 * n - 1) * 4u);
+  const BufRd bq(pq, static_cast<uint32_t>(m) * ld * 4u);
   // features in steps of 2 kFixL (phi(k) operands ping-pong between two
-  // register sets); sq and the buffer reads give zeros past m
+  // register sets); the operands of features m .. mr - 1 are zeros
   const int mr = (m + 2 * kFixL - 1) & ~(2 * kFixL - 1);
   const int tiles = (d + 31) / 32;
 
@@ -1279,14 +1320,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     smax = br.y;
   }
   __syncthreads();
-  if (tid == 0) {
-    unsigned acc = 0;
-    for (int t = 0; t < tiles_n; ++t) {
-      spre[t] = acc;
-      acc += static_cast<unsigned>(__popcll(smask[t]));
-    }
-    spre[tiles_n] = acc;
-  }
+  fix_mask_prefix(smask, spre, swtot, tiles_n);
   // Items in serpentine order: round i takes kslot in [i slots, (i + 1) slots)
   // counted up for even i and down for odd i, so under a causal mask (group g
   // sees about 32 (g + 1) keys) every work-group's total is about the same.
@@ -1321,10 +1355,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     }
     const int jlo = max(0, first + smin - (n - 1));
     const int jhi = min(n - 1, last + smax - (n - 1));
-    for (int e = tid; e < mr * kFixRows; e += 256) {
-      const int l = e / kFixRows, r = e % kFixRows;
-      const int i = srows[r];
-      sq[e] = (i >= 0 && l < m) ? pq[static_cast<size_t>(l) * ld + i] : 0.f;
+    {
+      // thread tid stages feature rows tid / 32 + 8 k of row srows[tid % 32];
+      // the rows m .. mr - 1 are zero
+      const int r = tid & (kFixRows - 1), i = srows[r], l1 = tid >> 5;
+      const uint32_t voff = static_cast<uint32_t>(l1 * ld + max(i, 0)) * 4u;
+#pragma unroll 8
+      for (int l = l1; l < m; l += 256 / kFixRows) {
+        const float x = bq.f32(voff, static_cast<uint32_t>((l - l1) * ld) * 4u);
+        sq[l * kFixRows + r] = i >= 0 ? x : 0.f;
+      }
+      for (int l = m + l1; l < mr; l += 256 / kFixRows) sq[l * kFixRows + r] = 0.f;
     }
     const int myrow = srows[lr];  // the query row of this lane in S^T and P
     __syncthreads();              // sq staged
@@ -1343,14 +1384,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
         for (int e = 0; e < 16; ++e) zt[t][e] = 0.0;
       // phi(k) operands of one 32-feature step: A[key jc + lr][feature l0 + 2 q + lh],
-      // two sets: a step multiplies one while the other is loaded
+      // two sets: a step multiplies one while the other is loaded.  Keys past
+      // n read key n - 1 (masked in P).  The buffer range check covers the
+      // lane (VGPR) offset only: when m is not a multiple of 64 (MTAIL) the
+      // feature offset goes into the lane offset too, so the rows past m read
+      // zero.
       float ka[kFixL / 2], kc[kFixL / 2];
-      // (reads past the m feature rows give zero; keys >= n are masked in P)
       auto load_k = [&](float (&dst)[kFixL / 2], int jc, int l0) {
-        const uint32_t voff = static_cast<uint32_t>(lh * ld + jc + lr) * 4u;
+        uint32_t voff = static_cast<uint32_t>(lh * ld + min(jc + lr, n - 1)) * 4u;
+        if constexpr (MTAIL) {
+          // (opaque: the 16 sums are formed per step, not kept live across steps)
+          voff += static_cast<uint32_t>(l0 * ld) * 4u;
+          asm volatile("" : "+v"(voff));
+        }
 #pragma unroll
-        for (int q = 0; q < kFixL / 2; ++q)
-          dst[q] = bk.f32(voff, static_cast<uint32_t>((l0 + 2 * q) * ld) * 4u);
+        for (int q = 0; q < kFixL / 2; ++q) {
+          const uint32_t fo = static_cast<uint32_t>((MTAIL ? 2 * q : l0 + 2 * q) * ld) * 4u;
+          dst[q] = MTAIL ? bk.f32(voff + fo, 0u) : bk.f32(voff, fo);
+        }
       };
       auto s_step = [&](const float (&kk)[kFixL / 2], int l0, floatx16& acc) {
 #pragma unroll
@@ -1364,23 +1415,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       for (; jc < ce * kFixKeys; jc += kFixKeys) {
         // value rows of these 32 keys, in the key order of the P V steps:
         // step e uses key jc + 8 (e / 4) + 4 lh + e % 4 on lane half lh
-        // (reads past the n value rows give zero; columns >= d are masked)
+        // (columns >= d are masked).  In the last block of a sequence whose
+        // length is not a multiple of 32 the row offset goes into the
+        // range-checked lane offset: rows past n read zero.
+        const bool full = jc + 32 <= n;  // uniform
         float vb[2][16];
+        auto load_v = [&](auto tail) {
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const int col = (t0 + t) * 32 + lr;
-          const uint32_t voff = static_cast<uint32_t>((jc + 4 * lh) * d + min(col, d - 1)) * sizeof(TV);
+          for (int t = 0; t < 2; ++t) {
+            const int col = (t0 + t) * 32 + lr;
+            const uint32_t voff = static_cast<uint32_t>((jc + 4 * lh) * d + min(col, d - 1)) * sizeof(TV);
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const uint32_t soff = static_cast<uint32_t>((8 * (e >> 2) + (e & 3)) * d) * sizeof(TV);
-            float x;
-            if constexpr (sizeof(TV) == 2) {
-              x = to_f32(bv.u16(voff, soff));
-            } else {
-              x = bv.f32(voff, soff);
+            for (int e = 0; e < 16; ++e) {
+              const uint32_t eoff = static_cast<uint32_t>((8 * (e >> 2) + (e & 3)) * d) * sizeof(TV);
+              const uint32_t vo = decltype(tail)::value ? voff + eoff : voff;
+              const uint32_t so = decltype(tail)::value ? 0u : eoff;
+              float x;
+              if constexpr (sizeof(TV) == 2) {
+                x = to_f32(bv.u16(vo, so));
+              } else {
+                x = bv.f32(vo, so);
+              }
+              vb[t][e] = col < d ? x : 0.f;
             }
-            vb[t][e] = col < d ? x : 0.f;
           }
+        };
+        if (full) {
+          load_v(std::false_type{});
+        } else {
+          load_v(std::true_type{});
         }
         // ---- S^T[key][row] over the m features
         floatx16 sacc;
@@ -1397,15 +1460,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
           s_step(kc, l0 + kFixL, sacc);
         }
         // ---- P = S^T c_{j-i}: lane holds keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow
-        // (c indices are >= 0 for a queued row; past 2n - 2 they read zero)
+        // (index key - row + n - 1 lies in [0, 2n - 2] for keys < n; a lane
+        // without a row reads row 0's entries, masked below; past n as for v)
         float pv[16];
         float ds = 0.f;
-        const uint32_t coff = static_cast<uint32_t>(jc + 4 * lh - myrow + n - 1) * 4u;
+        const uint32_t coff = static_cast<uint32_t>(jc + 4 * lh - max(myrow, 0) + n - 1) * 4u;
+        float cv[16];
+        if (full) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff, static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff + static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u, 0u);
+        }
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int key = jc + 8 * (e >> 2) + 4 * lh + (e & 3);
-          const float c = bc.f32(coff, static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u);
-          pv[e] = (myrow >= 0 && key < n) ? sacc[e] * c : 0.f;
+          pv[e] = (myrow >= 0 && key < n) ? sacc[e] * cv[e] : 0.f;
           ds += pv[e];
         }
         dsum += static_cast<double>(ds);
@@ -1484,6 +1555,7 @@ __global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restric
                                                        float* __restrict__ den_out, int BH, int n, int d, int slots) {
   __shared__ unsigned long long smask[kFixMaxTiles];
   __shared__ unsigned spre[kFixMaxTiles + 1];
+  __shared__ unsigned swtot[4];
   __shared__ int srows[kFixRows];
   const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
   const unsigned count = fix[bh];
@@ -1494,14 +1566,7 @@ __global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restric
   const int tiles_n = (n + 63) / 64;
   for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
   __syncthreads();
-  if (tid == 0) {
-    unsigned acc = 0;
-    for (int t = 0; t < tiles_n; ++t) {
-      spre[t] = acc;
-      acc += static_cast<unsigned>(__popcll(smask[t]));
-    }
-    spre[tiles_n] = acc;
-  }
+  fix_mask_prefix(smask, spre, swtot, tiles_n);
   for (int grp = kslot; grp < ngroups; grp += slots) {
     __syncthreads();
     if (tid < kFixRows) {
@@ -2054,23 +2119,29 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
     // phi(q) of a group exceeds the default dynamic LDS limit for m > 512
     static const hipError_t once = [] {
       const int bytes = static_cast<int>(kMaxM * kFixRows * sizeof(float));
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fixup<float>),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-      if (e == hipSuccess)
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_fixup<uint16_t>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-      return e;
+      const void* fns[] = {reinterpret_cast<const void*>(&k_fixup<float, false>),
+                           reinterpret_cast<const void*>(&k_fixup<float, true>),
+                           reinterpret_cast<const void*>(&k_fixup<uint16_t, false>),
+                           reinterpret_cast<const void*>(&k_fixup<uint16_t, true>)};
+      for (const void* f : fns)
+        if (hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes); e != hipSuccess)
+          return e;
+      return hipSuccess;
     }();
     if (once != hipSuccess) return once;
   }
-  if (bf16)
-    hipLaunchKernelGGL(k_fixup<uint16_t>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
-                       static_cast<const uint16_t*>(v), cexp, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld,
-                       d, m, slots);
-  else
-    hipLaunchKernelGGL(k_fixup<float>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik,
-                       static_cast<const float*>(v), cexp, z, den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d,
-                       m, slots);
+  const bool mtail = m % (2 * kFixL) != 0;
+  auto go = [&](auto kernel, const auto* vt) {
+    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik, vt, cexp, z,
+                       den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m, slots);
+  };
+  if (bf16) {
+    const auto* vt = static_cast<const uint16_t*>(v);
+    if (mtail) go(k_fixup<uint16_t, true>, vt); else go(k_fixup<uint16_t, false>, vt);
+  } else {
+    const auto* vt = static_cast<const float*>(v);
+    if (mtail) go(k_fixup<float, true>, vt); else go(k_fixup<float, false>, vt);
+  }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, fixmask, fixpart, z,
                      den_out, BH, n, d, slots);

@@ -90,6 +90,9 @@ def test_workspace_queries(lib):
     assert lib.krpe_toeplitz_conv_workspace(2, 2, 3, 100) > lib.krpe_toeplitz_conv_workspace(1, 2, 3, 100)
     # workspace covers phi(q), phi(k) in fp32 at least
     assert lib.krpe_attention_fwd_workspace(8, 12, 4096, 64, 128) >= 2 * 8 * 12 * 4096 * 128 * 4
+    # ... plus one row of slack after each: the convolution's look-ahead load
+    # reads one row past the last head's rows (never used)
+    assert lib.krpe_attention_fwd_workspace(8, 12, 4096, 64, 128) >= 2 * (8 * 12 * 128 + 1) * 4096 * 4
 
 
 def test_attention_validation(lib):
