@@ -191,6 +191,7 @@ AttnLayout attn_layout(int B, int H, int n, int d, int m) {
   L.psum = take(L.fsplit > 1 && bh * ((static_cast<size_t>(n) + 63) / 64) < 4096 ? bh * cols * n * sizeof(float) : 0);
   L.fixmask = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
+  L.fixplan = take(fix_plan_bytes(static_cast<int>(bh), n));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
   L.cexp = take(static_cast<size_t>(H) * (2 * static_cast<size_t>(n) - 1) * sizeof(float));
   L.total = off;
@@ -266,6 +267,7 @@ LongLayout long_layout(int B, int H, int n, int d, int M) {
   L.maskb = take(bh * (nbk / 64) * sizeof(unsigned long long));
   L.maskf = take(bh * ((static_cast<size_t>(n) + 63) / 64) * sizeof(unsigned long long));
   L.fixpart = take(bh * fix_slots(static_cast<int>(bh)) * 32 * cols * sizeof(double));
+  L.fixplan = take(fix_plan_bytes(static_cast<int>(bh), n));
   L.brange = take(static_cast<size_t>(H) * sizeof(int2));
   L.cexp = take(static_cast<size_t>(H) * (2 * static_cast<size_t>(n) - 1) * sizeof(float));
   L.total = off;
@@ -321,6 +323,7 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
   unsigned* fix = reinterpret_cast<unsigned*>(w + L.fix);
   unsigned long long* fixmask = reinterpret_cast<unsigned long long*>(w + L.fixmask);
   double* fixpart = reinterpret_cast<double*>(w + L.fixpart);
+  int* fixplan = reinterpret_cast<int*>(w + L.fixplan);
   int2* brange = reinterpret_cast<int2*>(w + L.brange);
   float* cexp = reinterpret_cast<float*>(w + L.cexp);
   const int N = 1 << L.l2;
@@ -347,8 +350,8 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
         return s;
       vv = vw;
     }
-    if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixpart, brange, cexp,
-                                                 BHi, H, n, N, d, M, st),
+    if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixplan, fixpart,
+                                                 brange, cexp, BHi, H, n, N, d, M, st),
                                     "direct launch"))
       return s;
     return record(events, 4, st);
@@ -390,8 +393,8 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
                                                  nsum, st),
                                   "combine launch"))
     return s;
-  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, den_out, fix, fixmask, fixpart, brange, cexp, BHi,
-                                               H, n, N, d, M, st),
+  if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, v, bf16, b, z, den_out, fix, fixmask, fixplan, fixpart,
+                                               brange, cexp, BHi, H, n, N, d, M, st),
                                   "fixup launch"))
     return s;
   return record(events, 4, st);
@@ -480,6 +483,7 @@ krpe_status_t run_forward_long(const LongLayout& L, char* w, const void* q, cons
   if (krpe_status_t s = record(events, 3, st)) return s;
   if (krpe_status_t s = hip_check(launch_fixup(F(L.phiq), F(L.phik), v, bf16, b, z, nullptr, fix,
                                                reinterpret_cast<unsigned long long*>(w + L.maskf),
+                                               reinterpret_cast<int*>(w + L.fixplan),
                                                reinterpret_cast<double*>(w + L.fixpart),
                                                reinterpret_cast<int2*>(w + L.brange), F(L.cexp), BHi, H, n, L.Ntot, d,
                                                M, st),

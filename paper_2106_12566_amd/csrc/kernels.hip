@@ -1180,10 +1180,11 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
 
 // Exact rows: Eq. (10) evaluated directly for the rows queued per head (the
 // rows the FFT route cannot certify, or every row on the direct route), in
-// groups of 32 rows taken in row order from the 64-bit row masks.  A group's
-// keys run in chunks of 128, each an item's share when a head has few groups
-// and more work-group slots (fix_key_parts).  Wave w of the work-group takes
-// the 32 keys jc + 32 w of every chunk of the item:
+// groups of 32 rows taken in row order.  A group's keys run in chunks of 128;
+// when a head has fewer groups than work-group slots, k_fix_plan cuts each
+// group's chunks into parts of about equal size (work items), else an item is
+// a whole group.  Wave w of the work-group takes the 32 keys jc + 32 w of
+// every chunk of the item:
 //   S^T = phi(k_keys) phi(q_rows)^T   32 keys x 32 rows, fp32 MFMA over the m features
 //   P   = S^T * c_{j-i}               c = exp(b) from a table per head; 0 for keys >= n
 //   Z  += P^T [v, ...]                fp32 MFMA, whose A operand is exactly the
@@ -1192,42 +1193,47 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
 // sums are added into fp64 totals; the four waves' totals are added in wave
 // order at the end, so results are bitwise deterministic.  Keys outside a
 // row's finite-b range contribute exact zeros, and chunks outside the
-// group's range are skipped.  An unsplit group writes its rows; shares go to
-// fixpart and k_fixup_combine adds them in share order.
+// group's range are skipped.  A group in one part writes its rows; parts go
+// to fixpart and k_fixup_combine adds them in part order.
 constexpr int kFixRows = 32;
 constexpr int kFixKeys = 128;
-constexpr int kFixL = 32;                 // features staged per step
-constexpr int kFixStride = kFixKeys + 1;  // LDS row stride (odd: column reads hit distinct banks)
+constexpr int kFixL = 32;  // features staged per step
 constexpr int kFixMaxTiles = (1 << kMaxLongLog2N) / 64;
-constexpr int kFixMaxParts = 16;
+constexpr int kFixMaxGroups = (1 << kMaxLongLog2N) / kFixRows;
+// smallest part (chunks) worth a work item of its own
+constexpr int kFixMinPart = 8;
 
-// Work items of a head: every group of 32 rows, each split into kparts shares
-// of its key chunks when the head has fewer groups than work-group slots.
-// A share keeps at least 4 of the n / 128 chunks.
-__host__ __device__ inline int fix_key_parts(int ngroups, int slots, int n) {
-  if (ngroups <= 0) return 1;
-  int k = slots / ngroups;
-  const int by_len = (n + 4 * kFixKeys - 1) / (4 * kFixKeys);
-  if (k > by_len) k = by_len;
-  return k < 1 ? 1 : (k > kFixMaxParts ? kFixMaxParts : k);
-}
-
-// Exclusive prefix counts of the set bits of the row-mask words w[0, nw):
-// pre[t] = number of queued rows in words < t, pre[nw] = all of them
-// (nw <= kFixMaxTiles).  All 256 threads of the work-group take part: thread
-// tid counts words 4 tid .. 4 tid + 3, a wave scan and the four wave totals
-// (wtot, LDS) give each thread its offset.  Ends with a barrier.
-__device__ __forceinline__ void fix_mask_prefix(const unsigned long long* w, unsigned* pre, unsigned* wtot, int nw) {
-  constexpr int P = kFixMaxTiles / 256;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  unsigned c[P], sum = 0;
-#pragma unroll
-  for (int j = 0; j < P; ++j) {
-    const int t = P * tid + j;
-    c[j] = t < nw ? static_cast<unsigned>(__popcll(w[t])) : 0u;
-    sum += c[j];
+// The exact-row plan (workspace, int32), for BH heads of n rows and `slots`
+// work-group slots per head:
+//   items [BH][slots] int4   {group, first chunk, end chunk, parts of the group}
+//   hdr   [BH] int2          {work items, 1 if the items table is used}
+//   rows  [BH][n]            queued rows of the head in row order
+//   gfirst [BH][n / 32 + 1]  first item of each group, then the item count
+struct FixPlan {
+  int4* items;
+  int2* hdr;
+  int* rows;
+  int* gfirst;
+  int n, slots, gstride;
+  __host__ __device__ FixPlan(int* base, int BH, int n_, int slots_)
+      : n(n_), slots(slots_), gstride((n_ + kFixRows - 1) / kFixRows + 1) {
+    items = reinterpret_cast<int4*>(base);
+    hdr = reinterpret_cast<int2*>(base + static_cast<size_t>(BH) * slots * 4);
+    rows = base + static_cast<size_t>(BH) * slots * 4 + static_cast<size_t>(BH) * 2;
+    gfirst = rows + static_cast<size_t>(BH) * n;
   }
-  unsigned x = sum;  // inclusive scan over the wave
+  __host__ __device__ static size_t bytes(int BH, int n, int slots) {
+    return (static_cast<size_t>(BH) * slots * 4 + static_cast<size_t>(BH) * 2 + static_cast<size_t>(BH) * n +
+            static_cast<size_t>(BH) * ((n + kFixRows - 1) / kFixRows + 1)) * sizeof(int);
+  }
+};
+
+// Block-wide exclusive scan of one value per thread over the 256 threads of
+// the work-group; *total receives the sum.  wtot: 4 words of LDS.  Contains
+// two barriers (every thread must call it).
+__device__ __forceinline__ unsigned block_excl_scan(unsigned v, unsigned* wtot, unsigned* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  unsigned x = v;  // inclusive scan over the wave
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     const unsigned y = __shfl_up(x, off);
@@ -1235,15 +1241,135 @@ __device__ __forceinline__ void fix_mask_prefix(const unsigned long long* w, uns
   }
   if (lane == 63) wtot[wave] = x;
   __syncthreads();
-  unsigned acc = x - sum;
-  for (int v = 0; v < wave; ++v) acc += wtot[v];
+  unsigned base = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (w < wave) base += wtot[w];
+    all += wtot[w];
+  }
+  __syncthreads();  // wtot free again
+  *total = all;
+  return base + x - v;
+}
+
+// Exclusive prefix counts of the set bits of the row-mask words w[0, nw):
+// pre[t] = number of queued rows in words < t, pre[nw] = all of them
+// (nw <= kFixMaxTiles); thread tid counts words 4 tid .. 4 tid + 3.  Every
+// thread of the work-group must call it; ends with a barrier.
+__device__ __forceinline__ void fix_mask_prefix(const unsigned long long* w, unsigned* pre, unsigned* wtot, int nw) {
+  constexpr int P = kFixMaxTiles / 256;
+  const int tid = threadIdx.x;
+  unsigned c[P], sum = 0;
+#pragma unroll
+  for (int j = 0; j < P; ++j) {
+    const int t = P * tid + j;
+    c[j] = t < nw ? static_cast<unsigned>(__popcll(w[t])) : 0u;
+    sum += c[j];
+  }
+  unsigned total;
+  unsigned acc = block_excl_scan(sum, wtot, &total);
 #pragma unroll
   for (int j = 0; j < P; ++j) {
     if (P * tid + j < nw) pre[P * tid + j] = acc;
     acc += c[j];
   }
-  if (tid == 255) pre[nw] = acc;  // the last thread's running count is the total
+  if (tid == 0) pre[nw] = total;
   __syncthreads();
+}
+
+// Row of the queued row of rank `rank` (< pre[nw]) from the masks and their
+// prefix counts in LDS: the last word with pre <= rank holds it.
+__device__ __forceinline__ int fix_row_of_rank(unsigned rank, const unsigned long long* w, const unsigned* pre,
+                                               int nw) {
+  int lo = 0, hi = nw;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (pre[mid] <= rank) lo = mid; else hi = mid;
+  }
+  unsigned long long x = w[lo];
+  for (unsigned c = pre[lo]; c < rank; ++c) x &= x - 1ull;
+  return lo * 64 + __ffsll(static_cast<long long>(x)) - 1;
+}
+
+// The plan of one head per work-group.  Its queued rows are listed in row
+// order.  With G groups of 32 rows and G < slots, each group's span of key
+// chunks (from its first and last row and the finite-b range of the head) is
+// cut into ceil(chunks / P) parts of about equal size, P the smallest part
+// size (at least kFixMinPart) that fits every part of the head into the
+// slots: sum_g ceil(c_g / P) <= U / P + G <= slots for P >= U / (slots - G),
+// U the head's chunks.  A head with G >= slots runs its groups whole.
+__global__ __launch_bounds__(256) void k_fix_plan(const unsigned* __restrict__ fix,
+                                                  const unsigned long long* __restrict__ fixmask,
+                                                  const int2* __restrict__ brange, int* __restrict__ plan, int BH,
+                                                  int H, int n, int slots) {
+  __shared__ unsigned long long smask[kFixMaxTiles];
+  __shared__ unsigned spre[kFixMaxTiles + 1];
+  __shared__ int gch[kFixMaxGroups], gc0[kFixMaxGroups];
+  __shared__ unsigned swtot[4];
+  const FixPlan P(plan, BH, n, slots);
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const unsigned count = fix[bh];
+  const int tiles_n = (n + 63) / 64;
+  for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
+  __syncthreads();
+  fix_mask_prefix(smask, spre, swtot, tiles_n);
+  int* __restrict__ rows = P.rows + static_cast<size_t>(bh) * n;
+  for (int t = tid; t < tiles_n; t += 256) {
+    unsigned long long x = smask[t];
+    unsigned r = spre[t];
+    while (x) {
+      rows[r++] = t * 64 + __ffsll(static_cast<long long>(x)) - 1;
+      x &= x - 1ull;
+    }
+  }
+  const int G = static_cast<int>((count + kFixRows - 1) / kFixRows);
+  const int2 br = brange[bh % H];
+  unsigned u = 0;
+  for (int g = tid; g < G; g += 256) {
+    const int first = fix_row_of_rank(static_cast<unsigned>(kFixRows * g), smask, spre, tiles_n);
+    const int last = fix_row_of_rank(min(static_cast<unsigned>(kFixRows * g + kFixRows - 1), count - 1u), smask,
+                                     spre, tiles_n);
+    const int jlo = max(0, first + br.x - (n - 1)), jhi = min(n - 1, last + br.y - (n - 1));
+    const int c0 = jlo / kFixKeys, nch = jhi >= jlo ? jhi / kFixKeys - c0 + 1 : 0;
+    gch[g] = nch;
+    gc0[g] = c0;
+    u += static_cast<unsigned>(nch);
+  }
+  unsigned U;
+  block_excl_scan(u, swtot, &U);  // (also the barrier after gch, gc0)
+  if (G >= slots || G == 0) {
+    if (tid == 0) P.hdr[bh] = make_int2(G, 0);
+    return;
+  }
+  const int part = max(kFixMinPart, static_cast<int>((U + (slots - G) - 1) / static_cast<unsigned>(slots - G)));
+  constexpr int GPT = kFixMaxGroups / 256;  // consecutive groups per thread
+  int np[GPT];
+  unsigned s = 0;
+#pragma unroll
+  for (int j = 0; j < GPT; ++j) {
+    const int g = GPT * tid + j;
+    np[j] = g < G ? max(1, (gch[g] + part - 1) / part) : 0;
+    s += static_cast<unsigned>(np[j]);
+  }
+  unsigned total;
+  unsigned acc = block_excl_scan(s, swtot, &total);
+  int* __restrict__ gfirst = P.gfirst + static_cast<size_t>(bh) * P.gstride;
+  int4* __restrict__ items = P.items + static_cast<size_t>(bh) * slots;
+#pragma unroll
+  for (int j = 0; j < GPT; ++j) {
+    const int g = GPT * tid + j;
+    if (g < G) {
+      gfirst[g] = static_cast<int>(acc);
+      const int c0 = gc0[g], nch = gch[g];
+      for (int p = 0; p < np[j]; ++p)
+        items[acc + p] = make_int4(g, c0 + nch * p / np[j], c0 + nch * (p + 1) / np[j], np[j]);
+    }
+    acc += static_cast<unsigned>(np[j]);
+  }
+  if (tid == 0) {
+    gfirst[G] = static_cast<int>(total);
+    P.hdr[bh] = make_int2(static_cast<int>(total), 1);
+  }
 }
 
 // Range [lo, hi] of s = t + n - 1 where b_t is finite, per head (lo > hi if
@@ -1278,26 +1404,27 @@ template <typename TV, bool MTAIL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_fixup(
     const float* __restrict__ phiq, const float* __restrict__ phik, const TV* __restrict__ vv,
     const float* __restrict__ cexp, float* __restrict__ z, float* __restrict__ den_out,
-    const unsigned* __restrict__ fix, const unsigned long long* __restrict__ fixmask, double* __restrict__ fixpart,
+    const unsigned* __restrict__ fix, const int* __restrict__ plan, double* __restrict__ fixpart,
     const int2* __restrict__ brange, int BH, int H, int n, int ld, int d, int m, int slots) {
   extern __shared__ __align__(16) float sq[];  // phi(q) of the group's rows, [l][32], l < m rounded up to 64
   __shared__ double red[2][16][64];            // another wave's totals (two column tiles)
   __shared__ double rden[4][kFixRows];
   __shared__ int srows[kFixRows];
-  __shared__ int smin, smax;
-  __shared__ unsigned long long smask[kFixMaxTiles];
-  __shared__ unsigned spre[kFixMaxTiles + 1];
-  __shared__ unsigned swtot[4];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
-  // slot-major order: the first item of every head is dispatched first
-  const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
+  // Grid (head, batch, slot): the first item of every head is dispatched
+  // first.  (No division: the indices, and the buffer descriptors built from
+  // them, stay in SGPRs; a descriptor the compiler cannot keep there costs a
+  // loop around every load.)
+  const int h = blockIdx.x, bh = blockIdx.y * H + h, kslot = blockIdx.z;
+  const FixPlan P(const_cast<int*>(plan), BH, n, slots);
+  const int2 hdr = P.hdr[bh];
+  const int items = hdr.x;
+  const bool split = hdr.y != 0;
+  // no item for this slot (its first one, slots - 1 - kslot, is the smallest)
+  if (slots - 1 - kslot >= items) return;  // uniform per work-group
   const unsigned count = fix[bh];
-  const int ngroups = static_cast<int>((count + kFixRows - 1) / kFixRows);
-  const int kparts = fix_key_parts(ngroups, slots, n);
-  const int items = ngroups * kparts;
-  if (kslot >= items) return;  // uniform per work-group
-  const int h = bh % H;
+  const int2 br = brange[h];
   const float* __restrict__ ch = cexp + static_cast<size_t>(h) * (2 * n - 1);
   const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * ld;
   const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * ld;
@@ -1309,42 +1436,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // register sets); the operands of features m .. mr - 1 are zeros
   const int mr = (m + 2 * kFixL - 1) & ~(2 * kFixL - 1);
   const int tiles = (d + 31) / 32;
+  const int* __restrict__ hrows = P.rows + static_cast<size_t>(bh) * n;
 
-  // Queued rows in row order: group g takes the ranks 32 g .. 32 g + 31 of
-  // the set bits of the head's mask words (prefix counts in spre).
-  const int tiles_n = (n + 63) / 64;
-  for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
-  if (tid == 0) {
-    const int2 br = brange[h];
-    smin = br.x;
-    smax = br.y;
-  }
-  __syncthreads();
-  fix_mask_prefix(smask, spre, swtot, tiles_n);
-  // Items in serpentine order: round i takes kslot in [i slots, (i + 1) slots)
-  // counted up for even i and down for odd i, so under a causal mask (group g
-  // sees about 32 (g + 1) keys) every work-group's total is about the same.
+  // Items in serpentine order: round i takes the items of [i slots, (i + 1) slots)
+  // counted down for even i and up for odd i: the last (under a causal mask
+  // the widest) groups start first, and every work-group's total is about
+  // the same.
+  auto item_at = [&](int round) { return (round & 1) ? round * slots + kslot : (round + 1) * slots - 1 - kslot; };
+  // {group, first chunk, end chunk, parts} (the chunks of a whole group below)
+  auto describe = [&](int item) {
+    return split ? P.items[static_cast<size_t>(bh) * slots + item] : make_int4(item, 0, 0, 1);
+  };
+  auto row_of = [&](int grp) {
+    const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
+    return tid < kFixRows && rank < count ? hrows[rank] : -1;
+  };
+  // the item's descriptor and (lanes < 32) row, loaded during the previous item
+  int4 cur = describe(item_at(0));
+  int crow = row_of(cur.x);
   for (int round = 0; round * slots < items; ++round) {
-    const int item = (round & 1) ? (round + 1) * slots - 1 - kslot : round * slots + kslot;
+    const int item = item_at(round);
     if (item >= items) continue;  // uniform per work-group
-    const int grp = item / kparts, kpart = item % kparts;
+    const int nparts = cur.w;
+    int cb = cur.y, ce = cur.z;
     __syncthreads();  // previous item's srows / sq / red consumed
-    if (tid < kFixRows) {
-      const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
-      int row = -1;
-      if (rank < count) {
-        int lo = 0, hi = tiles_n;  // last word with spre <= rank: it holds the bit
-        while (hi - lo > 1) {
-          const int mid = (lo + hi) >> 1;
-          if (spre[mid] <= rank) lo = mid; else hi = mid;
-        }
-        unsigned long long w = smask[lo];
-        for (unsigned c = spre[lo]; c < rank; ++c) w &= w - 1ull;
-        row = lo * 64 + __ffsll(static_cast<long long>(w)) - 1;
-      }
-      srows[tid] = row;
-    }
+    if (tid < kFixRows) srows[tid] = crow;
     __syncthreads();
+    if (const int next = item_at(round + 1); (round + 1) * slots < items && next < items) {
+      cur = describe(next);
+      crow = row_of(cur.x);
+    }
     int first = n, last = -1;
     for (int r = 0; r < kFixRows; ++r) {
       const int i = srows[r];
@@ -1353,8 +1474,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         last = max(last, i);
       }
     }
-    const int jlo = max(0, first + smin - (n - 1));
-    const int jhi = min(n - 1, last + smax - (n - 1));
+    if (!split) {  // the group's whole span of key chunks
+      const int jlo = max(0, first + br.x - (n - 1)), jhi = min(n - 1, last + br.y - (n - 1));
+      cb = jlo / kFixKeys;
+      ce = jhi >= jlo ? jhi / kFixKeys + 1 : cb;
+    }
     {
       // thread tid stages feature rows tid / 32 + 8 k of row srows[tid % 32];
       // the rows m .. mr - 1 are zero
@@ -1370,10 +1494,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int myrow = srows[lr];  // the query row of this lane in S^T and P
     __syncthreads();              // sq staged
 
-    // this item's share of the group's key chunks (contiguous, chunk-aligned)
-    const int c0 = jlo / kFixKeys, nch = jhi >= jlo ? jhi / kFixKeys - c0 + 1 : 0;
-    const int cb = c0 + static_cast<int>(static_cast<long long>(nch) * kpart / kparts);
-    const int ce = c0 + static_cast<int>(static_cast<long long>(nch) * (kpart + 1) / kparts);
     // column tiles of [v]: two per pass (the S^T products are recomputed for
     // a second pass when d > 64)
     for (int t0 = 0; t0 < tiles; t0 += 2) {
@@ -1517,7 +1637,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       // wave 0 holds the totals: row 8 (e / 4) + 4 lh + e % 4, column (t0 + t) 32 + lr
       if (wave == 0) {
         double* __restrict__ out =
-            kparts == 1 ? nullptr : fixpart + (static_cast<size_t>(bh) * slots + item) * kFixRows * (d + 1);
+            nparts == 1 ? nullptr : fixpart + (static_cast<size_t>(bh) * slots + item) * kFixRows * (d + 1);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = 8 * (e >> 2) + 4 * lh + (e & 3);
@@ -1527,14 +1647,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
           for (int t = 0; t < 2; ++t) {
             const int col = (t0 + t) * 32 + lr;
             if (i < 0 || t0 + t >= tiles || col >= d) continue;
-            if (kparts == 1) {
+            if (nparts == 1) {
               z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[t][e] / den);
             } else {
               out[row * (d + 1) + col] = zt[t][e];
             }
           }
           if (t0 == 0 && lr == 0) {
-            if (kparts == 1) {
+            if (nparts == 1) {
               if (den_out && i >= 0) den_out[static_cast<size_t>(bh) * n + i] = static_cast<float>(den);
             } else {
               out[row * (d + 1) + d] = den;
@@ -1546,52 +1666,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
 }
 
-// Sums the key shares of every group k_fixup split (in share order, so the
-// result is deterministic) and writes the rows.  Work-group (bh, slot) takes
-// groups slot, slot + slots, ...
-__global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restrict__ fix,
-                                                       const unsigned long long* __restrict__ fixmask,
+// Sums the parts of every group k_fixup split (in part order, so the result
+// is deterministic) and writes the rows.  Work-group (bh, slot) takes groups
+// slot, slot + slots, ...
+__global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restrict__ fix, const int* __restrict__ plan,
                                                        const double* __restrict__ fixpart, float* __restrict__ z,
                                                        float* __restrict__ den_out, int BH, int n, int d, int slots) {
-  __shared__ unsigned long long smask[kFixMaxTiles];
-  __shared__ unsigned spre[kFixMaxTiles + 1];
-  __shared__ unsigned swtot[4];
   __shared__ int srows[kFixRows];
   const int bh = blockIdx.x % BH, kslot = blockIdx.x / BH;
+  const FixPlan P(const_cast<int*>(plan), BH, n, slots);
+  const int2 hdr = P.hdr[bh];
   const unsigned count = fix[bh];
   const int ngroups = static_cast<int>((count + kFixRows - 1) / kFixRows);
-  const int kparts = fix_key_parts(ngroups, slots, n);
-  if (kparts == 1 || kslot >= ngroups) return;
+  if (hdr.y == 0 || kslot >= ngroups) return;
   const int tid = threadIdx.x;
-  const int tiles_n = (n + 63) / 64;
-  for (int t = tid; t < tiles_n; t += 256) smask[t] = fixmask[static_cast<size_t>(bh) * tiles_n + t];
-  __syncthreads();
-  fix_mask_prefix(smask, spre, swtot, tiles_n);
+  const int* __restrict__ gfirst = P.gfirst + static_cast<size_t>(bh) * P.gstride;
   for (int grp = kslot; grp < ngroups; grp += slots) {
+    const int first = gfirst[grp], nparts = gfirst[grp + 1] - first;
+    if (nparts == 1) continue;  // written by k_fixup
     __syncthreads();
     if (tid < kFixRows) {
       const unsigned rank = static_cast<unsigned>(grp * kFixRows + tid);
-      int row = -1;
-      if (rank < count) {
-        int lo = 0, hi = tiles_n;
-        while (hi - lo > 1) {
-          const int mid = (lo + hi) >> 1;
-          if (spre[mid] <= rank) lo = mid; else hi = mid;
-        }
-        unsigned long long w = smask[lo];
-        for (unsigned c = spre[lo]; c < rank; ++c) w &= w - 1ull;
-        row = lo * 64 + __ffsll(static_cast<long long>(w)) - 1;
-      }
-      srows[tid] = row;
+      srows[tid] = rank < count ? P.rows[static_cast<size_t>(bh) * n + rank] : -1;
     }
     __syncthreads();
-    const double* __restrict__ base = fixpart + (static_cast<size_t>(bh) * slots + grp * kparts) * kFixRows * (d + 1);
+    const double* __restrict__ base = fixpart + (static_cast<size_t>(bh) * slots + first) * kFixRows * (d + 1);
     for (int e = tid; e < kFixRows * d; e += 256) {
       const int row = e / d, c = e % d;
       const int i = srows[row];
       if (i < 0) continue;
       double num = 0.0, den = 0.0;
-      for (int p = 0; p < kparts; ++p) {
+      for (int p = 0; p < nparts; ++p) {
         const double* part = base + static_cast<size_t>(p) * kFixRows * (d + 1) + row * (d + 1);
         num += part[c];
         den += part[d];
@@ -2107,11 +2212,17 @@ int fix_slots(int BH) {
   return s < 32 ? 32 : (s > 512 ? 512 : s);
 }
 
+size_t fix_plan_bytes(int BH, int n) { return FixPlan::bytes(BH, n, fix_slots(BH)); }
+
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b, float* z,
-                        float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart, int2* brange,
-                        float* cexp, int BH, int H, int n, int ld, int d, int m, hipStream_t st) {
+                        float* den_out, const unsigned* fix, const unsigned long long* fixmask, int* plan,
+                        double* fixpart, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
+                        hipStream_t st) {
   const int slots = fix_slots(BH);
   hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, cexp, n);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_fix_plan, dim3(static_cast<unsigned>(BH)), dim3(256), 0, st, fix, fixmask, brange, plan, BH, H,
+                     n, slots);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   const long long blocks = static_cast<long long>(BH) * slots;
   const size_t lds = static_cast<size_t>((m + 2 * kFixL - 1) & ~(2 * kFixL - 1)) * kFixRows * sizeof(float);
@@ -2131,9 +2242,10 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
     if (once != hipSuccess) return once;
   }
   const bool mtail = m % (2 * kFixL) != 0;
+  const dim3 grid(static_cast<unsigned>(H), static_cast<unsigned>(BH / H), static_cast<unsigned>(slots));
   auto go = [&](auto kernel, const auto* vt) {
-    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, st, phiq, phik, vt, cexp, z,
-                       den_out, fix, fixmask, fixpart, brange, BH, H, n, ld, d, m, slots);
+    hipLaunchKernelGGL(kernel, grid, dim3(256), lds, st, phiq, phik, vt, cexp, z, den_out, fix, plan, fixpart, brange,
+                       BH, H, n, ld, d, m, slots);
   };
   if (bf16) {
     const auto* vt = static_cast<const uint16_t*>(v);
@@ -2143,7 +2255,7 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
     if (mtail) go(k_fixup<float, true>, vt); else go(k_fixup<float, false>, vt);
   }
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, fixmask, fixpart, z,
+  hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, plan, fixpart, z,
                      den_out, BH, n, d, slots);
   return hipGetLastError();
 }

@@ -28,6 +28,7 @@ struct AttnLayout {
   size_t fix;        // uint   [BH + 1]          rows queued per head, then their total
   size_t fixmask;    // uint64 [BH][ceil(n/64)]  queued rows: bit i % 64 of word i / 64
   size_t fixpart;    // double [BH][slots][32][d+1] key-share partial sums of the exact rows
+  size_t fixplan;    // int32: the queued rows and work items of the exact rows (fix_plan_bytes)
   size_t brange;     // int2   [H]               range of finite b per head
   size_t cexp;       // float  [H][2n-1]         c = exp(b) (exact rows)
   size_t total;
@@ -77,6 +78,7 @@ struct LongLayout {
   size_t zb;           // float  [BH][nbk][d]
   size_t maskb, maskf; // uint64 [BH][nbk/64], [BH][ceil(n/64)]
   size_t fixpart;      // double [BH][slots][32][d+1]
+  size_t fixplan;      // int32 (fix_plan_bytes)
   size_t brange;       // int2   [H]
   size_t cexp;         // float  [H][2n-1]       c = exp(b) (exact rows)
   size_t total;
@@ -136,11 +138,13 @@ hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb
                           float* den_out, unsigned* fix, unsigned long long* fixmask, int BH, int H, int n, int l2,
                           int d, int m, int nsplit, hipStream_t st);
 // Work-group slots per head of the exact-row kernels, and their partial sums:
-// fixpart holds BH * fix_slots(BH) * 32 * (d + 1) doubles.
+// fixpart holds BH * fix_slots(BH) * 32 * (d + 1) doubles; plan holds
+// fix_plan_bytes(BH, n) bytes (the queued rows and the work items).
 int fix_slots(int BH);
+size_t fix_plan_bytes(int BH, int n);
 hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, bool bf16, const float* b,
-                        float* z, float* den_out, const unsigned* fix, const unsigned long long* fixmask, double* fixpart,
-                        int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
+                        float* z, float* den_out, const unsigned* fix, const unsigned long long* fixmask, int* plan,
+                        double* fixpart, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
 // Long sequences (long_seq.hip): block copies of phi rows, bias windows of a
