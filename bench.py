@@ -347,8 +347,10 @@ def main() -> int:
                          "the library picks and, where that is the direct one, by the FFT route too)")
     ap.add_argument("--feature-map", choices=["prf", "trf", "elu"], default="prf",
                     help="feature map of Section 2: PRF (Eq. (5)), trigonometric (2m features) or elu + 1 (m = d)")
-    ap.add_argument("--route", choices=["auto", "fft", "direct"], default="auto",
-                    help="forward route: FFT (Sec. 3.2), direct quadratic evaluation, or by length")
+    ap.add_argument("--route", choices=["auto", "fft", "direct"], default="fft",
+                    help="forward route timed: the FFT route of Sec. 3.2 (default: a step then runs the whole "
+                         "path, feature maps, Toeplitz products by FFT and contraction), the direct quadratic "
+                         "evaluation, or the one the library picks by its cost model")
     ap.add_argument("--backward", action="store_true",
                     help="also time krpe_attention_bwd (dq, dk, dv, db) on the same inputs, reported in config")
     ap.add_argument("--nprf", action="store_true",
@@ -494,7 +496,7 @@ def main() -> int:
             dst.copy_(src)
         torch.cuda.synchronize()
         result["config"]["copy_calibration_bytes"] = src.numel() * 4
-    if not args.no_configs and fm == "prf" and not args.nprf and rt == "auto":
+    if not args.no_configs and fm == "prf" and not args.nprf and rt != "direct":
         per = {}
         for wid in range(1, 6):
             res = time_config(wid, max(3, min(args.steps, 10)), max(1, min(args.warmup, 3)), "auto")

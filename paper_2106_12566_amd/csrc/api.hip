@@ -97,7 +97,8 @@ bool direct_is_faster(long long BH, int n, int M, int d, bool causal) {
   const double L = 2.0 * static_cast<double>(1 << l2);
   const double heads = static_cast<double>(BH);
   const double pairs = causal ? 0.5 * static_cast<double>(n) * (n + 1) : static_cast<double>(n) * n;
-  const double direct = 2.45e-14 * heads * pairs * (M + d + 1) + 5.0e-5;
+  // (the exact-row kernel runs the features in steps of 64)
+  const double direct = 1.94e-14 * heads * pairs * (((M + 63) / 64) * 64 + d + 1) + 7.4e-5;
   const double rate = l2 <= 12 ? 1.65e-13 : (l2 == 13 ? 3.8e-13 : 3.0e-13);
   // (a causal mask leaves nb (nb + 1) / 2 of the block pairs live; the others are skipped)
   const double blocks = causal ? 0.5 * nb * (nb + 1) : static_cast<double>(nb) * nb;

@@ -222,7 +222,8 @@ def test_route_query(lib):
     assert route(8, 12, 4096, 64, 128, 8) == 8 and route(8, 12, 128, 64, 64, 16) == 16
     assert route(8, 12, 128, 64, 64, 0) == 8            # short: direct
     assert route(8, 12, 512, 64, 64, 0) == 8
-    assert route(8, 12, 4096, 64, 128, 0) == 16         # the long-n4096 layer: FFT
+    assert route(8, 12, 4096, 64, 128, 0) == 8          # the long-n4096 layer: direct at 96 heads
+    assert route(1, 2, 16384, 64, 128, 0) == 16
     assert route(1, 16, 16384, 64, 256, 0) == 16
     assert route(1, 1, 1000, 64, 64, 0) == 8            # one head: the FFT route's fixed cost dominates
     assert route(1, 1, 40000, 64, 128, 0) == 16 and route(1, 16, 65536, 64, 256, 0) == 16
@@ -233,3 +234,4 @@ def test_route_query(lib):
     # the causal-n65536 one stays on the FFT route; a route bit still wins over the hint
     assert route(1, 16, 16384, 64, 256, 32) == 8 and route(1, 16, 65536, 64, 256, 32) == 16
     assert route(1, 16, 16384, 64, 256, 32 | 16) == 16 and route(8, 12, 4096, 64, 128, 32) == 8
+    assert route(1, 2, 16384, 64, 128, 32) == 8
