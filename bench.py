@@ -107,13 +107,15 @@ def measured_traffic(kernel: str, workload: str):
 
 
 def device_source_hash() -> str:
-    """sha256 of the HIP sources with comments and blank space removed (comment edits keep it)."""
-    import glob
+    """sha256 of the translation unit the convolution and the other forward kernels are compiled
+    from (kernels.hip and the headers it includes), comments and blank space removed (comment
+    edits keep it; host code in the other sources does not change it)."""
     import hashlib
     import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2106_12566_amd", "csrc")
-    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.hpp"))):
+    for name in ("common.hpp", "fft.hpp", "kernels.hip", "launch.hpp"):
+        f = os.path.join(csrc, name)
         text = open(f).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
         text = re.sub(r"//[^\n]*", "", text)
