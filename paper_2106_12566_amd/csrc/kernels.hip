@@ -352,6 +352,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FEATURE_MAJ
   sq += __shfl_xor(sq, 32);  // ||x||^2 of position i0 + c
   const int n_store = FEATURE_MAJOR ? ld : n;
   const int M = trf ? 2 * m : m;
+  // Whole tiles of the PRF map in the feature-major layout: position i0 + c
+  // of this lane; phi = 2^(a s log2(e) + e0) with e0 = -h log2(e) - log2(sqrt(m))
+  // (s, h: the row scale and ||x||^2 / 2 of the epilogue below), stored
+  // through a buffer resource over this (source, batch-head)'s rows: the
+  // lane's offset in a VGPR, the feature's in an SGPR.
+  constexpr float kLog2e = 1.44269504088896341f;
+  const bool nzl = sq > 0.f;
+  const float hs_l = nprf ? (nzl ? 0.5f : 0.f) : 0.5f * sq;
+  const float rs_l = (nprf ? (nzl ? rsqrtf(sq) : 0.f) : 1.f) * kLog2e;
+  const float e0_l = fmaf(-hs_l, kLog2e, __log2f(inv_sqrt_m));
+  const bool pos_ok = i0 + c < n;  // positions n .. ld - 1 are zeros
+  const __amdgpu_buffer_rsrc_t out_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      phi + static_cast<size_t>(bh) * M * ld, 0, FEATURE_MAJOR ? M * ld * 4 : 0, 0x00020000);
+  const uint32_t out_voff = static_cast<uint32_t>(4 * half * ld + i0 + c) * 4u;
   for (int l0 = 0; l0 < m; l0 += 64) {
     if (l0 % 128 == 0) {
       __syncthreads();  // x rows / the previous W features consumed
@@ -372,6 +386,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FEATURE_MAJ
         else
           acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(xr[s2], wr[s2], acc[t], 0, 0, 0);
       }
+    }
+    if (FEATURE_MAJOR && !trf && i0 + 32 <= n_store && l0 + 64 <= m) {  // uniform
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          // feature l0 + 32 t + 8 (v / 4) + 4 (lane / 32) + v % 4 of position i0 + c
+          const float val = pos_ok ? __builtin_amdgcn_exp2f(fmaf(acc[t][v], rs_l, e0_l)) : 0.f;
+          const uint32_t soff = static_cast<uint32_t>((l0 + 32 * t + 8 * (v >> 2) + (v & 3)) * ld) * 4u;
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(val), out_rsrc, out_voff, soff, 0);
+        }
+      continue;
     }
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -581,6 +607,131 @@ __global__ __launch_bounds__(256) void k_vscale(const TV* __restrict__ v, long l
     if (r < np) {
       a = ca < nv ? tile[ca][r] / scale[ca] : (ca < nc ? 1.f : 0.f);
       b2 = cb < nv ? tile[cb][r] / scale[cb] : (cb < nc ? 1.f : 0.f);
+    }
+    if (pos0 + r < N) vsc[(static_cast<size_t>(bh) * pairs + c0 / 2 + pl) * N + pos0 + r] = make_float2(a, b2);
+  }
+}
+
+// The same two passes for rows of v contiguous in the columns (sc == 1) with
+// ncols, the row stride and the base 4-element aligned: every thread reads
+// 4-column quads (16 bytes in fp32, 8 in bf16), quad t % 16 of rows t / 16,
+// + 16, ...; rows past a chunk or past n read a valid row instead (the max
+// is unchanged, the scaled values of positions >= n are written as zeros).
+// Grids (column group, chunk or 64-position tile, batch-head).
+template <typename TV>
+__device__ __forceinline__ float4 load_quad(const TV* __restrict__ p) {
+  if constexpr (sizeof(TV) == 4) {
+    return *reinterpret_cast<const float4*>(p);
+  } else {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xffff0000u));
+  }
+}
+
+template <typename TV>
+__global__ __launch_bounds__(256) void k_vmax_q(const TV* __restrict__ v, int sp, long long bh_stride, int ncols,
+                                                int n, int nchunk, float* __restrict__ pmax) {
+  __shared__ float wm[4][64];
+  const int cg = blockIdx.x, ch = blockIdx.y, bh = blockIdx.z;
+  const int tid = threadIdx.x, q = tid & 15, r0 = tid >> 4, lane = tid & 63, wave = tid >> 6;
+  const int c0 = cg * 64, nq = min(16, (ncols - c0) / 4);
+  const int pos0 = ch * kVmaxChunk, np = min(kVmaxChunk, n - pos0);
+  // the chunk's first row (uniform), then 32-bit offsets; all loads before any use
+  const TV* __restrict__ vb = v + bh * bh_stride + static_cast<long long>(pos0) * sp + c0;
+  const int qo = 4 * min(q, nq - 1);
+  constexpr int J = kVmaxChunk / 16;
+  float4 x[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) x[j] = load_quad(vb + (min(r0 + 16 * j, np - 1) * sp + qo));
+  float m0 = 0.f, m1 = 0.f, m2 = 0.f, m3 = 0.f;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    m0 = fmaxf(m0, fabsf(x[j].x));
+    m1 = fmaxf(m1, fabsf(x[j].y));
+    m2 = fmaxf(m2, fabsf(x[j].z));
+    m3 = fmaxf(m3, fabsf(x[j].w));
+  }
+  // lanes q, q + 16, q + 32, q + 48 of a wave hold the same quad
+#pragma unroll
+  for (int off = 16; off < 64; off <<= 1) {
+    m0 = fmaxf(m0, __shfl_xor(m0, off));
+    m1 = fmaxf(m1, __shfl_xor(m1, off));
+    m2 = fmaxf(m2, __shfl_xor(m2, off));
+    m3 = fmaxf(m3, __shfl_xor(m3, off));
+  }
+  if (lane < 16) {
+    wm[wave][4 * lane] = m0;
+    wm[wave][4 * lane + 1] = m1;
+    wm[wave][4 * lane + 2] = m2;
+    wm[wave][4 * lane + 3] = m3;
+  }
+  __syncthreads();
+  if (tid < 4 * nq)
+    pmax[(static_cast<size_t>(bh) * nchunk + ch) * ncols + c0 + tid] =
+        fmaxf(fmaxf(wm[0][tid], wm[1][tid]), fmaxf(wm[2][tid], wm[3][tid]));
+}
+
+// Group cg holds columns [64 cg, 64 cg + 64) of v' (the ones column too when
+// it falls there); when ncols is a multiple of 64 the ones column's pair
+// (1, 0) is written by the last group.
+template <typename TV>
+__global__ __launch_bounds__(256) void k_vscale_q(const TV* __restrict__ v, int sp, long long bh_stride,
+                                                  int ncols, int with_ones, int n, int N, int nchunk,
+                                                  const float* __restrict__ pmax, float* __restrict__ colmax,
+                                                  float2* __restrict__ vsc) {
+  __shared__ float tile[64][65];  // [column][position]
+  __shared__ float scale[64];
+  const int cg = blockIdx.x, pt = blockIdx.y, bh = blockIdx.z;
+  const int cols = ncols + with_ones, pairs = (cols + 1) / 2;
+  const int tid = threadIdx.x;
+  const int c0 = cg * 64, nv = min(64, ncols - c0), nc = min(64, cols - c0);
+  const bool extra = with_ones && cg == static_cast<int>(gridDim.x) - 1 && ncols - c0 == 64;
+  const int pos0 = pt * 64;
+  const int np = max(0, min(64, n - pos0));
+  // this tile's quads first (their latency overlaps the scale reduction)
+  const int q = tid & 15, r0 = tid >> 4;
+  float4 x[4];
+  const TV* __restrict__ vb = v + bh * bh_stride + c0;
+  const int qo = 4 * min(q, nv / 4 - 1);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) x[j] = load_quad(vb + (min(pos0 + r0 + 16 * j, n - 1) * sp + qo));
+  if (tid < nc) {
+    const int c = c0 + tid;
+    float sv = 1.f;  // the ones column
+    if (c < ncols) {
+      sv = 0.f;
+      const float* __restrict__ pm = pmax + static_cast<size_t>(bh) * nchunk * ncols + c;
+      int ch = 0;
+      for (; ch + 4 <= nchunk; ch += 4)
+        sv = fmaxf(fmaxf(sv, fmaxf(pm[ch * ncols], pm[(ch + 1) * ncols])),
+                   fmaxf(pm[(ch + 2) * ncols], pm[(ch + 3) * ncols]));
+      for (; ch < nchunk; ++ch) sv = fmaxf(sv, pm[ch * ncols]);
+    }
+    if (pt == 0) colmax[static_cast<size_t>(bh) * cols + c] = sv;
+    scale[tid] = sv > 0.f ? sv : 1.f;
+  }
+  if (extra && pt == 0 && tid == 0) colmax[static_cast<size_t>(bh) * cols + ncols] = 1.f;
+  if (q < nv / 4) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + 16 * j;
+      tile[4 * q][r] = x[j].x;
+      tile[4 * q + 1][r] = x[j].y;
+      tile[4 * q + 2][r] = x[j].z;
+      tile[4 * q + 3][r] = x[j].w;
+    }
+  }
+  __syncthreads();
+  const int npairs = (nc + 1) / 2 + (extra ? 1 : 0);
+  const int ones = ncols - c0;  // the ones column, group-relative (may lie past this group)
+  for (int e = tid; e < npairs * 64; e += 256) {
+    const int pl = e >> 6, r = e & 63;
+    const int ca = 2 * pl, cb = 2 * pl + 1;
+    float a = 0.f, b2 = 0.f;
+    if (r < np) {
+      a = ca < nv ? tile[ca][r] / scale[ca] : (with_ones && ca == ones ? 1.f : 0.f);
+      b2 = cb < nv ? tile[cb][r] / scale[cb] : (with_ones && cb == ones ? 1.f : 0.f);
     }
     if (pos0 + r < N) vsc[(static_cast<size_t>(bh) * pairs + c0 / 2 + pl) * N + pos0 + r] = make_float2(a, b2);
   }
@@ -2136,6 +2287,25 @@ hipError_t launch_vprep(bool bf16, const void* v, long long sp, long long sc, lo
   const int nchunk = vmax_chunks(n);
   const int vgroups = (ncols + 63) / 64, sgroups = (cols + 63) / 64;
   const dim3 block(256);
+  const size_t esz = bf16 ? 2 : 4;
+  if (sc == 1 && ncols > 0 && ncols % 4 == 0 && sp % 4 == 0 && bh_stride % 4 == 0 &&
+      reinterpret_cast<uintptr_t>(v) % (4 * esz) == 0 && static_cast<long long>(n) * sp < (1ll << 31)) {
+    const int spi = static_cast<int>(sp);
+    const dim3 gmax(static_cast<unsigned>(vgroups), static_cast<unsigned>(nchunk), static_cast<unsigned>(BH));
+    const dim3 gscale(static_cast<unsigned>(vgroups), static_cast<unsigned>((N + 63) / 64), static_cast<unsigned>(BH));
+    if (bf16) {
+      const uint16_t* vv = static_cast<const uint16_t*>(v);
+      hipLaunchKernelGGL(k_vmax_q<uint16_t>, gmax, block, 0, st, vv, spi, bh_stride, ncols, n, nchunk, pmax);
+      hipLaunchKernelGGL(k_vscale_q<uint16_t>, gscale, block, 0, st, vv, spi, bh_stride, ncols, with_ones ? 1 : 0, n,
+                         N, nchunk, pmax, colmax, vsc);
+    } else {
+      const float* vv = static_cast<const float*>(v);
+      hipLaunchKernelGGL(k_vmax_q<float>, gmax, block, 0, st, vv, spi, bh_stride, ncols, n, nchunk, pmax);
+      hipLaunchKernelGGL(k_vscale_q<float>, gscale, block, 0, st, vv, spi, bh_stride, ncols, with_ones ? 1 : 0, n, N,
+                         nchunk, pmax, colmax, vsc);
+    }
+    return hipGetLastError();
+  }
   const dim3 grid_max(static_cast<unsigned>(static_cast<long long>(BH) * nchunk * vgroups));
   const dim3 grid_scale(static_cast<unsigned>(static_cast<long long>(BH) * ((N + 63) / 64) * sgroups));
   if (bf16) {
