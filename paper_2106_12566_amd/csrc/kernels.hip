@@ -267,16 +267,17 @@ __global__ __launch_bounds__(256) void k_feature_map(const TX* __restrict__ x0, 
 }
 
 // k_feature_map for d = 64 with the operands loaded straight into registers.
-// d = 64.  Work-group: 128 positions of one (source, batch-head) and every
-// feature, four waves of 32 positions each.  The x rows are read once with
+// d = 64.  Work-group: 256 positions of one (source, batch-head) and every
+// feature, eight waves of 32 positions each.  The x rows are read once with
 // coalesced 16-byte loads (consecutive threads, consecutive addresses),
 // staged through LDS (rows padded to 68 floats: the 16-byte reads of 16
 // lanes then fall in distinct banks) and kept in registers; W then streams
-// through the same LDS buffer 128 features at a time (35 KiB of LDS: four
-// work-groups per CU).  The MFMA sums over k in any order both
+// through the same LDS buffer 128 features at a time (70 KiB of LDS: two
+// work-groups, 16 waves per CU).  The MFMA sums over k in any order both
 // operands agree on: half-wave h supplies k = 32 h + s at step s.  Same
 // outputs and epilogue as k_feature_map.
-constexpr int kFm64Pos = 128;
+constexpr int kFm64Pos = 256;
+constexpr int kFmThreads = 2 * kFm64Pos;  // 8 waves of 32 positions
 constexpr int kFm64Stride = 68;
 
 template <typename TX>
@@ -284,13 +285,13 @@ __device__ __forceinline__ void stage_rows64(const TX* __restrict__ src, int row
                                              int nrows) {
   // nrows x 64 values -> dst[row][kFm64Stride], zero past rows_ok
   if constexpr (std::is_same<TX, float>::value) {
-    for (int e = threadIdx.x; e < nrows * 16; e += 256) {
+    for (int e = threadIdx.x; e < nrows * 16; e += kFmThreads) {
       const int row = e >> 4, c4 = e & 15;
       const float4 v = row < rows_ok ? reinterpret_cast<const float4*>(src)[e] : make_float4(0.f, 0.f, 0.f, 0.f);
       *reinterpret_cast<float4*>(dst + row * kFm64Stride + 4 * c4) = v;
     }
   } else {
-    for (int e = threadIdx.x; e < nrows * 8; e += 256) {
+    for (int e = threadIdx.x; e < nrows * 8; e += kFmThreads) {
       const int row = e >> 3, c8 = e & 7;
       const uint4 v = row < rows_ok ? reinterpret_cast<const uint4*>(src)[e] : make_uint4(0u, 0u, 0u, 0u);
       const unsigned w[4] = {v.x, v.y, v.z, v.w};
@@ -318,7 +319,7 @@ __device__ __forceinline__ void lds_half_row64(const float* __restrict__ rows, i
 }
 
 template <typename TX, bool FEATURE_MAJOR>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FEATURE_MAJOR ? 4 : 1))) void k_feature_map64(const TX* __restrict__ x0, const TX* __restrict__ x1,
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(FEATURE_MAJOR ? 4 : 1))) void k_feature_map64(const TX* __restrict__ x0, const TX* __restrict__ x1,
                                                        const float* __restrict__ W, float* __restrict__ phi0,
                                                        float* __restrict__ phi1, int H, int n, int ld, int m,
                                                        float inv_sqrt_m, int tiles_n, int BH,
@@ -2233,10 +2234,11 @@ hipError_t launch_feature_map(bool bf16, const void* x0, const void* x1, const f
   const dim3 grid(static_cast<unsigned>(blocks));
   const int np = nprf ? 1 : 0, trf = kind == kFeatTrf ? 1 : 0;
   if (d == 64) {
-    // 128 positions and every feature per work-group
-    const int tiles128 = (rows + kFm64Pos - 1) / kFm64Pos;
-    const dim3 grid(static_cast<unsigned>(static_cast<long long>(tiles128) * BH * nsrc));
-    const int tiles_n = tiles128;
+    // 256 positions and every feature per work-group
+    const int tiles_fm = (rows + kFm64Pos - 1) / kFm64Pos;
+    const dim3 grid(static_cast<unsigned>(static_cast<long long>(tiles_fm) * BH * nsrc));
+    const int tiles_n = tiles_fm;
+    const dim3 block(kFmThreads);
     if (bf16) {
       const uint16_t* a = static_cast<const uint16_t*>(x0);
       const uint16_t* c = static_cast<const uint16_t*>(x1);
