@@ -1226,6 +1226,7 @@ __global__ __launch_bounds__(256) void k_bound_weights(const float* __restrict__
 // relative bound exceeds kTau is queued for k_fixup.  Block: 64 rows of one
 // (batch, head); dynamic LDS holds the (d + 1) x 64 tile of sums and the
 // m + 1 weights.
+template <int NS>
 __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part, const float* __restrict__ phiq,
                                                  const float2* __restrict__ Wb, const float2* __restrict__ hnorm,
                                                  float* __restrict__ z, float* __restrict__ den_out,
@@ -1243,23 +1244,49 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
   const int h = bh % H;
   const int tid = threadIdx.x, li = tid & 63, qg = tid >> 6;
   const float* __restrict__ p0 = part + static_cast<size_t>(bh) * nsplit * cols * n;
-  for (int e = tid; e < cols * 64; e += 256) {
-    const int c = e >> 6, i = e & 63;
-    const int pos = i0 + i;
-    float t = 1.f;
-    if (pos < n) {
-      // the partials' loads issued together, summed in split order
-      const float* __restrict__ pc = p0 + static_cast<size_t>(c) * n + pos;
-      const size_t step = static_cast<size_t>(cols) * n;
-      t = pc[0];
-      int sp = 1;
-      for (; sp + 3 <= nsplit; sp += 3) {
-        const float a1 = pc[sp * step], a2 = pc[(sp + 1) * step], a3 = pc[(sp + 2) * step];
-        t = ((t + a1) + a2) + a3;
+  if constexpr (NS > 0) {
+    // NS partials per value, four values per thread at a time: 4 NS loads in
+    // flight before any is used, each value summed in split order
+    const size_t step = static_cast<size_t>(cols) * n;
+    for (int e0 = tid; e0 < cols * 64; e0 += 4 * 256) {
+      float a[4][NS];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = e0 + 256 * u, c = min(e >> 6, cols - 1), pos = min(i0 + (e & 63), n - 1);
+        const float* __restrict__ pc = p0 + static_cast<size_t>(c) * n + pos;
+#pragma unroll
+        for (int sp = 0; sp < NS; ++sp) a[u][sp] = pc[sp * step];
       }
-      for (; sp < nsplit; ++sp) t += pc[sp * step];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int e = e0 + 256 * u;
+        if (e < cols * 64) {
+          float t = a[u][0];
+#pragma unroll
+          for (int sp = 1; sp < NS; ++sp) t += a[u][sp];
+          tile[(e >> 6) * 65 + (e & 63)] = i0 + (e & 63) < n ? t : 1.f;
+        }
+      }
     }
-    tile[c * 65 + i] = t;
+  } else {
+    for (int e = tid; e < cols * 64; e += 256) {
+      const int c = e >> 6, i = e & 63;
+      const int pos = i0 + i;
+      float t = 1.f;
+      if (pos < n) {
+        // the partials' loads issued together, summed in split order
+        const float* __restrict__ pc = p0 + static_cast<size_t>(c) * n + pos;
+        const size_t step = static_cast<size_t>(cols) * n;
+        t = pc[0];
+        int sp = 1;
+        for (; sp + 3 <= nsplit; sp += 3) {
+          const float a1 = pc[sp * step], a2 = pc[(sp + 1) * step], a3 = pc[(sp + 2) * step];
+          t = ((t + a1) + a2) + a3;
+        }
+        for (; sp < nsplit; ++sp) t += pc[sp * step];
+      }
+      tile[c * 65 + i] = t;
+    }
   }
   for (int l = tid; l <= m; l += 256) wl[l] = Wb[static_cast<size_t>(bh) * (m + 1) + l];
   __syncthreads();
@@ -1270,6 +1297,7 @@ __global__ __launch_bounds__(256) void k_combine(const float* __restrict__ part,
     float bA = 0.f, bD = 0.f;
     if (pos < n) {
       const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * N + pos;
+#pragma unroll 8
       for (int l = qg; l < m; l += 4) {
         const float f = fabsf(pq[static_cast<size_t>(l) * N]);  // signed features (TRF)
         const float2 w = wl[l];
@@ -2374,8 +2402,17 @@ hipError_t launch_combine(const float* part, const float* phiq, const float2* Wb
   const int tiles_n = (n + 63) / 64;
   const size_t lds = (static_cast<size_t>((d + 1) * 65 + 1) & ~static_cast<size_t>(1)) * sizeof(float) +
                      static_cast<size_t>(m + 1) * sizeof(float2);
-  hipLaunchKernelGGL(k_combine, dim3(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n)), dim3(256), lds, st,
-                     part, phiq, Wb, hnorm, z, den_out, fix, fixmask, BH, H, n, 1 << l2, l2, d, m, nsplit, tiles_n);
+  const dim3 grid(static_cast<unsigned>(static_cast<long long>(BH) * tiles_n));
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, grid, dim3(256), lds, st, part, phiq, Wb, hnorm, z, den_out, fix, fixmask, BH, H, n,
+                       1 << l2, l2, d, m, nsplit, tiles_n);
+  };
+  switch (nsplit) {
+    case 2: go(k_combine<2>); break;
+    case 4: go(k_combine<4>); break;
+    case 8: go(k_combine<8>); break;
+    default: go(k_combine<0>); break;
+  }
   return hipGetLastError();
 }
 
