@@ -1381,7 +1381,7 @@ constexpr int kFixL = 32;  // features staged per step
 constexpr int kFixMaxTiles = (1 << kMaxLongLog2N) / 64;
 constexpr int kFixMaxGroups = (1 << kMaxLongLog2N) / kFixRows;
 // smallest part (chunks) worth a work item of its own
-constexpr int kFixMinPart = 8;
+constexpr int kFixMinPart = 16;
 
 // The exact-row plan (workspace, int32), for BH heads of n rows and `slots`
 // work-group slots per head:
