@@ -1093,23 +1093,25 @@ k_conv_contract(
 // 32 features 32 (w & 1) .. and the 32-pair tiles w >> 1, (w >> 1) + 2.
 constexpr int kMaxPairs = (kMaxD + 2) / 2;
 constexpr int kGramPT = (kMaxPairs + 31) / 32;  // 32-pair tiles
+constexpr int kGramL = 128;                      // features per work-group (eight waves of 32 x 32-pair tiles)
 
-__global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, const float2* __restrict__ vsc,
+__global__ __launch_bounds__(512) void k_gram(const float* __restrict__ phik, const float2* __restrict__ vsc,
                                               float* __restrict__ X2, int m, int N, int pairs, int ltiles,
                                               int ksplit) {
-  __shared__ float4 A4[64][17];           // phi^2, [position][feature quad]
+  __shared__ float4 A4[64][kGramL / 4 + 1];  // phi^2, [position][feature quad]
   __shared__ float Bq[64][kMaxPairs | 1];  // |vsc|^2, [position][pair]
   int bid = blockIdx.x;
   const int ks = bid % ksplit;
   bid /= ksplit;
   const int lt = bid % ltiles, bh = bid / ltiles;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int ft = wave & 1, pt0 = wave >> 1, lr = lane & 31, lk = lane >> 5;
-  const int l0 = lt * 64;
+  const int ft = wave & 3, pt0 = wave >> 2, lr = lane & 31, lk = lane >> 5;
+  const int l0 = lt * kGramL;
   const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * N;
   const float2* __restrict__ vb = vsc + static_cast<size_t>(bh) * pairs * N;
   const int slice = N / ksplit, pos_begin = ks * slice, pos_end = pos_begin + slice;
-  const float* __restrict__ Af = reinterpret_cast<const float*>(&A4[0][0]);  // [position][68]: feature f at f
+  constexpr int AS = 4 * (kGramL / 4 + 1);  // floats per position row of A4
+  const float* __restrict__ Af = reinterpret_cast<const float*>(&A4[0][0]);  // [position][AS]: feature f at f
   floatx16 acc[2];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
@@ -1117,8 +1119,8 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
     for (int e = 0; e < 16; ++e) acc[t][e] = 0.f;
   // The next chunk's values are loaded into registers while the current
   // chunk is multiplied out of LDS (thread tid holds positions tid & 63 of
-  // feature quads tid >> 6 + 4 e and of pairs tid >> 6 + 4 e).
-  constexpr int kGramPB = (kMaxPairs + 3) / 4;
+  // feature quads tid >> 6 + 8 e and of pairs tid >> 6 + 8 e).
+  constexpr int kGramPB = (kMaxPairs + 7) / 8;
   float na[4][4];
   float2 nb[kGramPB];
   const int xl = tid & 63, ql = tid >> 6;
@@ -1127,12 +1129,12 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
     for (int e = 0; e < 4; ++e)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int l = l0 + 4 * (ql + 4 * e) + j;
+        const int l = l0 + 4 * (ql + 8 * e) + j;
         na[e][j] = (l < m && p0 + xl < pos_end) ? pk[static_cast<size_t>(l) * N + p0 + xl] : 0.f;
       }
 #pragma unroll
     for (int e = 0; e < kGramPB; ++e) {
-      const int p = ql + 4 * e;
+      const int p = ql + 8 * e;
       nb[e] = (p < pairs && p0 + xl < pos_end) ? vb[static_cast<size_t>(p) * N + p0 + xl] : make_float2(0.f, 0.f);
     }
   };
@@ -1141,11 +1143,11 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      A4[xl][ql + 4 * e] = make_float4(na[e][0] * na[e][0], na[e][1] * na[e][1], na[e][2] * na[e][2],
+      A4[xl][ql + 8 * e] = make_float4(na[e][0] * na[e][0], na[e][1] * na[e][1], na[e][2] * na[e][2],
                                        na[e][3] * na[e][3]);
 #pragma unroll
     for (int e = 0; e < kGramPB; ++e) {
-      const int p = ql + 4 * e;
+      const int p = ql + 8 * e;
       if (p < pairs) Bq[xl][p] = nb[e].x * nb[e].x + nb[e].y * nb[e].y;
     }
     __syncthreads();
@@ -1158,7 +1160,7 @@ __global__ __launch_bounds__(256) void k_gram(const float* __restrict__ phik, co
 #pragma unroll 8
         for (int s2 = 0; s2 < 32; ++s2) {
           const int x = 2 * s2 + lk;
-          const float a = Af[x * 68 + 32 * ft + lr];
+          const float a = Af[x * AS + 32 * ft + lr];
           const float bq = p < pairs ? Bq[x][p] : 0.f;
           acc[t] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, bq, acc[t], 0, 0, 0);
         }
@@ -2204,7 +2206,7 @@ int conv_splits(int l2) {
 
 int gram_splits(int BH, int m, int N) {
   // enough blocks to fill the GPU, slices of at least 1024 positions
-  const int ltiles = (m + 63) / 64;
+  const int ltiles = (m + kGramL - 1) / kGramL;
   int ks = 1;
   while (ks < 16 && static_cast<long long>(BH) * ltiles * ks < 1024 && N / (2 * ks) >= 1024) ks *= 2;
   return ks;
@@ -2381,9 +2383,9 @@ int conv_units(int l2, int BH, int cols) {
 
 hipError_t launch_gram(const float* phik, const float2* vsc, float* X2, int BH, int m, int N, int pairs,
                        int ksplit, hipStream_t st) {
-  const int ltiles = (m + 63) / 64;
+  const int ltiles = (m + kGramL - 1) / kGramL;
   const long long blocks = static_cast<long long>(BH) * ltiles * ksplit;
-  hipLaunchKernelGGL(k_gram, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, phik, vsc, X2, m, N, pairs,
+  hipLaunchKernelGGL(k_gram, dim3(static_cast<unsigned>(blocks)), dim3(512), 0, st, phik, vsc, X2, m, N, pairs,
                      ltiles, ksplit);
   return hipGetLastError();
 }
