@@ -6,7 +6,9 @@ Sizes whose tails do not fill the kernels' tiles:
 * the feature count is not a multiple of its 64-feature steps, odd included;
 * the sequence is shorter than the 128-key chunks;
 * d is not a multiple of the 32-column tiles;
-* at n = 2000 and 4000 the convolutions load phi a feature ahead.
+* at n = 2000 and 4000 the convolutions load phi a feature ahead;
+* d = 128, 100 and 2: value columns in two groups of 64, a partial last
+  group, and a count the 4-column loads of the value preparation do not take.
 
 Every input sits at the start of an allocation whose remainder is NaN, and
 the workspace and the output are NaN before the call.  Any value read past
@@ -48,6 +50,11 @@ CASES = [
     (1, 2, 97, 32, 1, "f32", "fft", "normal"),
     (2, 2, 2000, 64, 33, "f32", "fft", "causal"),
     (1, 2, 4000, 64, 96, "bf16", "fft", "normal"),
+    # value columns in two groups of 64 (the ones column's pair on its own),
+    # a partial last group, and a column count the quad loads do not take
+    (1, 2, 300, 128, 64, "bf16", "fft", "normal"),
+    (1, 2, 1000, 100, 64, "f32", "fft", "causal"),
+    (1, 2, 513, 2, 8, "f32", "fft", "normal"),
 ]
 
 
