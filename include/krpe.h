@@ -102,12 +102,13 @@ typedef enum {
 #define KRPE_FEAT_TRF 2u
 #define KRPE_FEAT_ELU 4u
 /*
- * Route of the forward pass (at most one; neither: chosen by sequence length
- * from the measured crossover).  KRPE_ROUTE_FFT: the O(n log n) FFT
+ * Route of the forward pass (at most one; neither: chosen by the measured
+ * cost model of krpe_attention_fwd_route, from the sizes and the head
+ * count).  KRPE_ROUTE_FFT: the O(n log n) FFT
  * convolution of Section 3.2 (rows it cannot certify evaluated directly).
  * KRPE_ROUTE_DIRECT: every row evaluated directly from Eq. (10) as
  * (phi(Q) phi(K)^T o C) [v, 1] on fp32 MFMA tiles with fp64 totals, O(n^2);
- * faster than the FFT route for short sequences.  Same results to the
+ * faster than the FFT route for short sequences and many heads.  Same results to the
  * tolerance of the FFT route (the direct route is the more accurate).
  */
 #define KRPE_ROUTE_DIRECT 8u
