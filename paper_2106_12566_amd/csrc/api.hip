@@ -351,10 +351,16 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
         return s;
       vv = vw;
     }
-    if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixplan, fixpart,
-                                                 brange, cexp, BHi, H, n, N, d, M, st),
-                                    "direct launch"))
+    if (M <= kDirMaxM) {
+      if (krpe_status_t s = hip_check(launch_direct_rows(phiq, phik, static_cast<const float*>(vv), b, z, den_out,
+                                                         brange, cexp, BHi, H, n, N, d, M, st),
+                                      "direct launch"))
+        return s;
+    } else if (krpe_status_t s = hip_check(launch_fixup(phiq, phik, vv, false, b, z, den_out, fix, fixmask, fixplan,
+                                                        fixpart, brange, cexp, BHi, H, n, N, d, M, st),
+                                           "direct launch")) {
       return s;
+    }
     return record(events, 4, st);
   }
   if (krpe_status_t s = record(events, 0, st)) return s;

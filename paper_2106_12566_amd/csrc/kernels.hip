@@ -1889,6 +1889,179 @@ __global__ __launch_bounds__(256) void k_fixup_combine(const unsigned* __restric
   }
 }
 
+// Direct route with at most 128 features: every row of every head, one wave
+// per 32 query rows.  A work-group holds 128 consecutive rows of one
+// (batch, head), each wave its own 32 (phi(q) of them staged in LDS), and
+// each wave walks every key block of 32 in its rows' finite-b range with the
+// products of k_fixup:
+//   S^T = phi(k_keys) phi(q_rows)^T, P = S^T * c_{j-i}, Z += P^T [v, ...]
+// (fp32 MFMA; per 32 keys the fp32 sums added into fp64 totals, blocks in
+// key order), then writes its rows.  No wave shares a row, so there is no
+// reduction across waves and no plan.  Work-groups take the row tiles from
+// the last one down: under a causal mask the last rows see the most keys.
+constexpr int kDirRows = 4 * kFixRows;  // rows per work-group
+
+template <bool MTAIL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_direct_rows(
+    const float* __restrict__ phiq, const float* __restrict__ phik, const float* __restrict__ vv,
+    const float* __restrict__ cexp, float* __restrict__ z, float* __restrict__ den_out,
+    const int2* __restrict__ brange, int H, int n, int ld, int d, int m) {
+  extern __shared__ __align__(16) float sqw[];  // [wave][l][32], l < m rounded up to 64
+  __shared__ double wden[4][kFixRows];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 31, lh = lane >> 5;
+  const int ntile = (n + kDirRows - 1) / kDirRows;
+  const int tile = ntile - 1 - static_cast<int>(blockIdx.x);
+  const int h = blockIdx.z, bh = blockIdx.y * H + h;  // grid (row tile, batch, head): no division
+  const int row0 = tile * kDirRows + kFixRows * wave;
+  const int mr = (m + 2 * kFixL - 1) & ~(2 * kFixL - 1);
+  float* __restrict__ sq = sqw + wave * mr * kFixRows;
+  const float* __restrict__ pq = phiq + static_cast<size_t>(bh) * m * ld;
+  const float* __restrict__ pk = phik + static_cast<size_t>(bh) * m * ld;
+  const float* __restrict__ vh = vv + static_cast<size_t>(bh) * n * d;
+  const float* __restrict__ ch = cexp + static_cast<size_t>(h) * (2 * n - 1);
+  const BufRd bk(pk, static_cast<uint32_t>(m) * ld * 4u), bv(vh, static_cast<uint32_t>(n) * d * 4u);
+  const BufRd bc(ch, static_cast<uint32_t>(2 * n - 1) * 4u), bq(pq, static_cast<uint32_t>(m) * ld * 4u);
+  // this wave's rows' phi(q): lane stages feature rows lane / 32 + 2 k of row
+  // row0 + lane % 32 (zero past m and past n)
+  {
+    const int r = lr, i = row0 + r, l1 = lh;
+    const uint32_t voff = static_cast<uint32_t>(l1 * ld + min(i, n - 1)) * 4u;
+#pragma unroll 8
+    for (int l = l1; l < m; l += 2) {
+      const float x = bq.f32(voff, static_cast<uint32_t>((l - l1) * ld) * 4u);
+      sq[l * kFixRows + r] = i < n ? x : 0.f;
+    }
+    for (int l = m + l1; l < mr; l += 2) sq[l * kFixRows + r] = 0.f;
+  }
+  __syncthreads();  // (each wave reads only its own rows; one barrier orders the stores)
+  if (row0 >= n) return;  // uniform per wave; no barrier follows
+  const int myrow = row0 + lr < n ? row0 + lr : -1;
+  const int last = min(row0 + kFixRows, n) - 1;
+  const int2 br = brange[h];
+  const int jlo = max(0, row0 + br.x - (n - 1)), jhi = min(n - 1, last + br.y - (n - 1));
+  const int tiles = (d + 31) / 32;
+  for (int t0 = 0; t0 < tiles; t0 += 2) {
+    double zt[2][16];
+    double dsum = 0.0;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) zt[t][e] = 0.0;
+    // phi(k) operands as in k_fixup: A[key jc + lr][feature l0 + 2 q + lh], two
+    // register sets over 32-feature steps; keys past n read key n - 1 (masked
+    // in P); with MTAIL the feature offset is range-checked (zeros past m)
+    float ka[kFixL / 2], kc[kFixL / 2];
+    auto load_k = [&](float (&dst)[kFixL / 2], int jc, int l0) {
+      uint32_t voff = static_cast<uint32_t>(lh * ld + min(jc + lr, n - 1)) * 4u;
+      if constexpr (MTAIL) {
+        voff += static_cast<uint32_t>(l0 * ld) * 4u;
+        asm volatile("" : "+v"(voff));
+      }
+#pragma unroll
+      for (int q = 0; q < kFixL / 2; ++q) {
+        const uint32_t fo = static_cast<uint32_t>((MTAIL ? 2 * q : l0 + 2 * q) * ld) * 4u;
+        dst[q] = MTAIL ? bk.f32(voff + fo, 0u) : bk.f32(voff, fo);
+      }
+    };
+    auto s_step = [&](const float (&kk)[kFixL / 2], int l0, floatx16& acc) {
+#pragma unroll
+      for (int q = 0; q < kFixL / 2; ++q) {
+        const float qb = sq[(l0 + 2 * q + lh) * kFixRows + lr];
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(kk[q], qb, acc, 0, 0, 0);
+      }
+    };
+    const int jend = jhi >= jlo ? jhi + 1 : 0;
+    int jc = jlo & ~31;
+    if (jc < jend) load_k(ka, jc, 0);
+    for (; jc < jend; jc += 32) {
+      const bool full = jc + 32 <= n;  // uniform
+      float vb[2][16];
+      auto load_v = [&](auto tail) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const int col = (t0 + t) * 32 + lr;
+          const uint32_t voff = static_cast<uint32_t>((jc + 4 * lh) * d + min(col, d - 1)) * 4u;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const uint32_t eoff = static_cast<uint32_t>((8 * (e >> 2) + (e & 3)) * d) * 4u;
+            const float x = decltype(tail)::value ? bv.f32(voff + eoff, 0u) : bv.f32(voff, eoff);
+            vb[t][e] = col < d ? x : 0.f;
+          }
+        }
+      };
+      if (full) {
+        load_v(std::false_type{});
+      } else {
+        load_v(std::true_type{});
+      }
+      floatx16 sacc;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
+      for (int l0 = 0; l0 < mr; l0 += 2 * kFixL) {
+        load_k(kc, jc, l0 + kFixL);
+        s_step(ka, l0, sacc);
+        if (l0 + 2 * kFixL < mr) {
+          load_k(ka, jc, l0 + 2 * kFixL);
+        } else if (jc + 32 < jend) {
+          load_k(ka, jc + 32, 0);  // the next key block's first step
+        }
+        s_step(kc, l0 + kFixL, sacc);
+      }
+      // P = S^T c_{j-i}, lane: keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow
+      float pv[16];
+      float ds = 0.f;
+      const uint32_t coff = static_cast<uint32_t>(jc + 4 * lh - max(myrow, 0) + n - 1) * 4u;
+      float cv[16];
+      if (full) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff, static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff + static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u, 0u);
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = jc + 8 * (e >> 2) + 4 * lh + (e & 3);
+        pv[e] = (myrow >= 0 && key < n) ? sacc[e] * cv[e] : 0.f;
+        ds += pv[e];
+      }
+      dsum += static_cast<double>(ds);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        if (t0 + t < tiles) {
+          floatx16 zc;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) zc[e] = 0.f;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) zc = __builtin_amdgcn_mfma_f32_32x32x2f32(pv[e], vb[t][e], zc, 0, 0, 0);
+#pragma unroll
+          for (int e = 0; e < 16; ++e) zt[t][e] += static_cast<double>(zc[e]);
+        }
+      }
+    }
+    // row lr's denominator: this half-wave's keys plus the other half's
+    dsum += __shfl_xor(dsum, 32);
+    if (lh == 0) wden[wave][lr] = dsum;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    // lane holds rows 8 (e / 4) + 4 lh + e % 4, column (t0 + t) 32 + lr
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int row = 8 * (e >> 2) + 4 * lh + (e & 3), i = row0 + row;
+      const double den = wden[wave][row];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int col = (t0 + t) * 32 + lr;
+        if (i < n && t0 + t < tiles && col < d)
+          z[(static_cast<size_t>(bh) * n + i) * d + col] = static_cast<float>(zt[t][e] / den);
+      }
+      if (t0 == 0 && lr == 0 && den_out && i < n) den_out[static_cast<size_t>(bh) * n + i] = static_cast<float>(den);
+    }
+    __builtin_amdgcn_wave_barrier();  // wden read before the next pass writes it
+  }
+}
+
 // Direct (quadratic) route: every row of every head queued for k_fixup, which
 // then evaluates Eq. (10) as S = phi(Q) phi(K)^T o C and S [v, 1] on MFMA.
 // fixmask[bh][t] holds the bits of the rows < n of tile t; fix[bh] = n,
@@ -2468,6 +2641,24 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
   hipLaunchKernelGGL(k_fixup_combine, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, fix, plan, fixpart, z,
                      den_out, BH, n, d, slots);
+  return hipGetLastError();
+}
+
+hipError_t launch_direct_rows(const float* phiq, const float* phik, const float* v, const float* b, float* z,
+                              float* den_out, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(k_brange, dim3(static_cast<unsigned>(H)), dim3(256), 0, st, b, brange, cexp, n);
+  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  const int mr = (m + 2 * kFixL - 1) & ~(2 * kFixL - 1);
+  const size_t lds = static_cast<size_t>(4) * mr * kFixRows * sizeof(float);
+  const dim3 grid(static_cast<unsigned>((n + kDirRows - 1) / kDirRows), static_cast<unsigned>(BH / H),
+                  static_cast<unsigned>(H));
+  if (m % (2 * kFixL) != 0)
+    hipLaunchKernelGGL(k_direct_rows<true>, grid, dim3(256), lds, st, phiq, phik, v, cexp, z, den_out, brange, H, n, ld,
+                       d, m);
+  else
+    hipLaunchKernelGGL(k_direct_rows<false>, grid, dim3(256), lds, st, phiq, phik, v, cexp, z, den_out, brange, H, n,
+                       ld, d, m);
   return hipGetLastError();
 }
 

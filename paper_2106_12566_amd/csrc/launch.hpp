@@ -146,6 +146,12 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
                         float* z, float* den_out, const unsigned* fix, const unsigned long long* fixmask, int* plan,
                         double* fixpart, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
+// The direct route for m <= kDirMaxM features (fp32 values): one wave per 32
+// query rows, no cross-wave reduction.
+constexpr int kDirMaxM = 128;
+hipError_t launch_direct_rows(const float* phiq, const float* phik, const float* v, const float* b, float* z,
+                              float* den_out, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
+                              hipStream_t st);
 hipError_t launch_ones(float* ones, int n, int N, hipStream_t st);
 // Long sequences (long_seq.hip): block copies of phi rows, bias windows of a
 // block pair, sums over key blocks, certification weights, row masks, rows.
