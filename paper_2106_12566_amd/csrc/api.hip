@@ -98,7 +98,7 @@ bool direct_is_faster(long long BH, int n, int M, int d, bool causal) {
   const double heads = static_cast<double>(BH);
   const double pairs = causal ? 0.5 * static_cast<double>(n) * (n + 1) : static_cast<double>(n) * n;
   // (the exact-row kernel runs the features in steps of 64)
-  const double direct = 1.94e-14 * heads * pairs * (((M + 63) / 64) * 64 + d + 1) + 7.4e-5;
+  const double direct = 1.89e-14 * heads * pairs * (((M + 63) / 64) * 64 + d + 1) + 7.4e-5;
   const double rate = l2 <= 12 ? 1.65e-13 : (l2 == 13 ? 3.8e-13 : 3.0e-13);
   // (a causal mask leaves nb (nb + 1) / 2 of the block pairs live; the others are skipped)
   const double blocks = causal ? 0.5 * nb * (nb + 1) : static_cast<double>(nb) * nb;
@@ -351,7 +351,7 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
         return s;
       vv = vw;
     }
-    if (M <= kDirMaxM) {
+    if (M <= kDirMaxM && static_cast<long long>(BHi) * ((n + 31) / 32) >= kDirMinWaves) {
       if (krpe_status_t s = hip_check(launch_direct_rows(phiq, phik, static_cast<const float*>(vv), b, z, den_out,
                                                          brange, cexp, BHi, H, n, N, d, M, st),
                                       "direct launch"))

@@ -147,8 +147,12 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
                         double* fixpart, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
                         hipStream_t st);
 // The direct route for m <= kDirMaxM features (fp32 values): one wave per 32
-// query rows, no cross-wave reduction.
+// query rows, no cross-wave reduction.  Taken when the rows give at least
+// kDirMinWaves waves (one and a half per SIMD): with fewer, each wave walking
+// all keys of its rows alone is slower than the exact-row kernel, whose
+// work-groups split a group's keys.
 constexpr int kDirMaxM = 128;
+constexpr long long kDirMinWaves = 1536;
 hipError_t launch_direct_rows(const float* phiq, const float* phik, const float* v, const float* b, float* z,
                               float* den_out, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
                               hipStream_t st);
