@@ -331,7 +331,10 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
   const int pairs = (d + 2) / 2;
 
   if (direct) {
-    // phi(q), phi(k), then every row through the exact-row kernel
+    // phi(q), phi(k), then every row evaluated directly: by the row-parallel
+    // kernel, or by the exact-row kernel over a queue of every row.  The queue
+    // is marked on both paths: its count is the number of rows evaluated
+    // exactly that krpe_attention_fwd_stats reports.
     for (int e = 0; e < 2; ++e)
       if (krpe_status_t s = record(events, e, st)) return s;
     if (krpe_status_t s = hip_check(launch_feature_map(bf16, q, k, W, phiq, phik, 2, true, N, BHi, H, n, d, m,
