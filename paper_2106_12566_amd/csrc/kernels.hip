@@ -1594,11 +1594,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   __shared__ int srows[kFixRows];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lr = lane & 31, lh = lane >> 5;
-  // Grid (head, batch, slot): the first item of every head is dispatched
-  // first.  (No division: the indices, and the buffer descriptors built from
-  // them, stay in SGPRs; a descriptor the compiler cannot keep there costs a
-  // loop around every load.)
-  const int h = blockIdx.x, bh = blockIdx.y * H + h, kslot = blockIdx.z;
+  // Grid (head, batch, slot), slots counted down along z: the work-groups
+  // holding a head's first items (the only ones with work when a head has
+  // fewer items than slots) are dispatched before the empty ones, which
+  // return at once.  (No division: the indices, and the buffer descriptors
+  // built from them, stay in SGPRs; a descriptor the compiler cannot keep
+  // there costs a loop around every load.)
+  const int h = blockIdx.x, bh = blockIdx.y * H + h, kslot = slots - 1 - static_cast<int>(blockIdx.z);
   const FixPlan P(const_cast<int*>(plan), BH, n, slots);
   const int2 hdr = P.hdr[bh];
   const int items = hdr.x;
@@ -1995,6 +1997,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       } else {
         load_v(std::true_type{});
       }
+      // the c-table entries of these keys (P below), loaded ahead of the S
+      // product so that their latency passes under it
+      const uint32_t coff = static_cast<uint32_t>(jc + 4 * lh - max(myrow, 0) + n - 1) * 4u;
+      float cv[16];
+      if (full) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff, static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff + static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u, 0u);
+      }
       floatx16 sacc;
 #pragma unroll
       for (int e = 0; e < 16; ++e) sacc[e] = 0.f;
@@ -2011,15 +2024,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       // P = S^T c_{j-i}, lane: keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow
       float pv[16];
       float ds = 0.f;
-      const uint32_t coff = static_cast<uint32_t>(jc + 4 * lh - max(myrow, 0) + n - 1) * 4u;
-      float cv[16];
-      if (full) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff, static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) cv[e] = bc.f32(coff + static_cast<uint32_t>(8 * (e >> 2) + (e & 3)) * 4u, 0u);
-      }
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int key = jc + 8 * (e >> 2) + 4 * lh + (e & 3);

@@ -8,7 +8,9 @@ Sizes whose tails do not fill the kernels' tiles:
 * d is not a multiple of the 32-column tiles;
 * at n = 2000 and 4000 the convolutions load phi a feature ahead;
 * d = 128, 100 and 2: value columns in two groups of 64, a partial last
-  group, and a count the 4-column loads of the value preparation do not take.
+  group, and a count the 4-column loads of the value preparation do not take;
+* the same tails on the direct route's row-parallel kernel (enough heads for
+  it to be taken).
 
 Every input sits at the start of an allocation whose remainder is NaN, and
 the workspace and the output are NaN before the call.  Any value read past
@@ -55,6 +57,14 @@ CASES = [
     (1, 2, 300, 128, 64, "bf16", "fft", "normal"),
     (1, 2, 1000, 100, 64, "f32", "fft", "causal"),
     (1, 2, 513, 2, 8, "f32", "fft", "normal"),
+    # the direct route's row-parallel kernel (m <= 128 and at least 1536 waves
+    # of 32 rows): a feature count that is not a multiple of 64, value columns
+    # in two passes, a last row tile whose last waves start past n, causal
+    # key ranges; a partial last key block with bf16 values and d = 2; a
+    # sequence one past a multiple of 32 with d = 128
+    (4, 16, 900, 100, 33, "f32", "direct", "causal"),
+    (2, 24, 1000, 2, 64, "bf16", "direct", "normal"),
+    (3, 16, 1025, 128, 128, "f32", "direct", "normal"),
 ]
 
 
