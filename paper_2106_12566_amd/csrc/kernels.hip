@@ -2021,14 +2021,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         }
         s_step(kc, l0 + kFixL, sacc);
       }
-      // P = S^T c_{j-i}, lane: keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow
+      // P = S^T c_{j-i}, lane: keys jc + 8 (e / 4) + 4 lh + e % 4 of row myrow.
+      // A lane without a row (past n) has S = 0 (its phi(q) is staged as
+      // zeros) and its P, sums and totals are never stored, so only keys
+      // past n, in the last block, are masked: there v reads zero but the
+      // denominator would take them.
       float pv[16];
       float ds = 0.f;
+      if (full) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = jc + 8 * (e >> 2) + 4 * lh + (e & 3);
-        pv[e] = (myrow >= 0 && key < n) ? sacc[e] * cv[e] : 0.f;
-        ds += pv[e];
+        for (int e = 0; e < 16; ++e) {
+          pv[e] = sacc[e] * cv[e];
+          ds += pv[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = jc + 8 * (e >> 2) + 4 * lh + (e & 3);
+          pv[e] = key < n ? sacc[e] * cv[e] : 0.f;
+          ds += pv[e];
+        }
       }
       dsum += static_cast<double>(ds);
 #pragma unroll
