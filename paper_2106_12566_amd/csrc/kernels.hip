@@ -1987,8 +1987,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const uint32_t eoff = static_cast<uint32_t>((8 * (e >> 2) + (e & 3)) * d) * 4u;
-            const float x = decltype(tail)::value ? bv.f32(voff + eoff, 0u) : bv.f32(voff, eoff);
-            vb[t][e] = col < d ? x : 0.f;
+            // (a column past d reads column d - 1: it feeds only columns of Z
+            // that are not stored)
+            vb[t][e] = decltype(tail)::value ? bv.f32(voff + eoff, 0u) : bv.f32(voff, eoff);
           }
         }
       };
