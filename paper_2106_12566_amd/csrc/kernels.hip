@@ -1910,7 +1910,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     const int2* __restrict__ brange, int H, int n, int ld, int d, int m) {
   extern __shared__ __align__(16) float sqw[];  // [wave][l][32], l < m rounded up to 64
   __shared__ double wden[4][kFixRows];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // (the wave index read from the first lane: the compiler then knows it,
+  // and every row and key bound derived from it, to be wave-uniform, so the
+  // key-block loop runs on scalar registers and branches)
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lr = lane & 31, lh = lane >> 5;
   const int ntile = (n + kDirRows - 1) / kDirRows;
   const int tile = ntile - 1 - static_cast<int>(blockIdx.x);
