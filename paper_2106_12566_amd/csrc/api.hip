@@ -75,19 +75,22 @@ constexpr unsigned kBwdFlags = KRPE_NPRF | KRPE_ROUTE_DIRECT | KRPE_ROUTE_FFT | 
 
 // Whether the direct route is the faster one for BH heads of length n with M
 // features and d value columns.  Cost model fitted to MI355X timings of both
-// routes (B H = 1, 16, 96; d = 64; M = 64, 128; n = 512 .. 16384, not
-// causal): each route's time is its work over all heads at a measured rate
-// plus a fixed cost (the launch chain and its latency-bound small kernels).
-// Direct: 2.45e-14 s per (query, key) pair and unit of M + d + 1, plus
-// 5e-5 s.  FFT: per column pair, feature and point of the length-2N
-// transform times log2(2N), 1.65e-13 s up to N = 4096, 3.8e-13 s at N = 8192
-// and 3.0e-13 s at N = 16384, over the nb^2 block pairs of a blocked
-// sequence, plus 1.5e-4 s.  All n^2 pairs are counted, as the host does not
-// read b, unless the caller states a causal mask (KRPE_HINT_CAUSAL): the
-// exact-row kernel then visits the n (n + 1) / 2 pairs j <= i only (measured
-// at n = 16384, 16 heads, m = 256: 14.8 ms direct, 19.1 ms FFT), and a blocked
-// FFT route runs the nb (nb + 1) / 2 block pairs on or below the diagonal.
-// The route bits force either route.
+// routes at 80 shapes (B H = 1, 16, 96; d = 64; M = 32 .. 128; n = 512 ..
+// 40000, not causal): each route's time is its work over all heads at a
+// measured rate plus a fixed cost (the launch chain and its latency-bound
+// small kernels).  Direct: per (query, key) pair and unit of M rounded up to
+// a multiple of 64, plus d + 1, 1.74e-14 s on the row-parallel kernel and
+// 1.9e-14 s on the exact-row kernel (few heads, or M > 128), plus 7.4e-5 s.
+// FFT: per column pair, feature and point of the length-2N transform times
+// log2(2N), 1.65e-13 s up to N = 4096, 3.8e-13 s at N = 8192 and 3.1e-13 s
+// at N = 16384, over the nb^2 block pairs of a blocked sequence, plus
+// 1.5e-4 s.
+// All n^2 pairs are counted, as the host does not read b, unless the caller
+// states a causal mask (KRPE_HINT_CAUSAL): the direct kernels then visit the
+// n (n + 1) / 2 pairs j <= i only (measured at n = 16384, 16 heads, m = 256:
+// 11.7 ms direct, 17.8 ms FFT), and a blocked FFT route runs the
+// nb (nb + 1) / 2 block pairs on or below the diagonal.  The route bits force
+// either route.
 bool direct_is_faster(long long BH, int n, int M, int d, bool causal) {
   int l2 = 0;
   while ((1 << l2) < n) ++l2;
@@ -97,9 +100,10 @@ bool direct_is_faster(long long BH, int n, int M, int d, bool causal) {
   const double L = 2.0 * static_cast<double>(1 << l2);
   const double heads = static_cast<double>(BH);
   const double pairs = causal ? 0.5 * static_cast<double>(n) * (n + 1) : static_cast<double>(n) * n;
-  // (the exact-row kernel runs the features in steps of 64)
-  const double direct = 1.89e-14 * heads * pairs * (((M + 63) / 64) * 64 + d + 1) + 7.4e-5;
-  const double rate = l2 <= 12 ? 1.65e-13 : (l2 == 13 ? 3.8e-13 : 3.0e-13);
+  // (both direct kernels run the features in steps of 64)
+  const double per_pair = direct_rows_path(BH, n, M) ? 1.74e-14 : 1.9e-14;
+  const double direct = per_pair * heads * pairs * (((M + 63) / 64) * 64 + d + 1) + 7.4e-5;
+  const double rate = l2 <= 12 ? 1.65e-13 : (l2 == 13 ? 3.8e-13 : 3.1e-13);
   // (a causal mask leaves nb (nb + 1) / 2 of the block pairs live; the others are skipped)
   const double blocks = causal ? 0.5 * nb * (nb + 1) : static_cast<double>(nb) * nb;
   const double fft = rate * heads * M * ((d + 2) / 2) * L * (l2 + 1) * blocks + 1.5e-4;
@@ -354,7 +358,7 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
         return s;
       vv = vw;
     }
-    if (M <= kDirMaxM && static_cast<long long>(BHi) * ((n + 31) / 32) >= kDirMinWaves) {
+    if (direct_rows_path(BHi, n, M)) {
       if (krpe_status_t s = hip_check(launch_direct_rows(phiq, phik, static_cast<const float*>(vv), b, z, den_out,
                                                          brange, cexp, BHi, H, n, N, d, M, st),
                                       "direct launch"))

@@ -153,6 +153,11 @@ hipError_t launch_fixup(const float* phiq, const float* phik, const void* v, boo
 // work-groups split a group's keys.
 constexpr int kDirMaxM = 128;
 constexpr long long kDirMinWaves = 1536;
+// Whether the direct route runs the row-parallel kernel (else the exact-row
+// kernel over a queue of every row).
+inline bool direct_rows_path(long long BH, int n, int M) {
+  return M <= kDirMaxM && BH * ((n + 31) / 32) >= kDirMinWaves;
+}
 hipError_t launch_direct_rows(const float* phiq, const float* phik, const float* v, const float* b, float* z,
                               float* den_out, int2* brange, float* cexp, int BH, int H, int n, int ld, int d, int m,
                               hipStream_t st);
