@@ -1113,6 +1113,7 @@ __global__ __launch_bounds__(512) void k_gram(const float* __restrict__ phik, co
   constexpr int AS = 4 * (kGramL / 4 + 1);  // floats per position row of A4
   const float* __restrict__ Af = reinterpret_cast<const float*>(&A4[0][0]);  // [position][AS]: feature f at f
   floatx16 acc[2];
+  float vs[2] = {0.f, 0.f};
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -1155,8 +1156,16 @@ __global__ __launch_bounds__(512) void k_gram(const float* __restrict__ phik, co
     // A[feature][position] = phi^2, B[position][pair] = |vsc|^2, 2 positions per step
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      const int p = 32 * (pt0 + 2 * t) + lr;
-      if (pt0 + 2 * t < kGramPT && 32 * (pt0 + 2 * t) < pairs) {
+      const int p0 = 32 * (pt0 + 2 * t), p = p0 + lr;
+      if (pt0 + 2 * t < kGramPT && p0 + 1 == pairs) {
+        // a tile with one pair (the last, e.g. the ones column's): lane sums
+        // its feature 32 ft + lr over the positions of its half, on the VALU
+#pragma unroll 8
+        for (int s2 = 0; s2 < 32; ++s2) {
+          const int x = 2 * s2 + lk;
+          vs[t] = fmaf(Af[x * AS + 32 * ft + lr], Bq[x][p0], vs[t]);
+        }
+      } else if (pt0 + 2 * t < kGramPT && p0 < pairs) {
 #pragma unroll 8
         for (int s2 = 0; s2 < 32; ++s2) {
           const int x = 2 * s2 + lk;
@@ -1171,8 +1180,12 @@ __global__ __launch_bounds__(512) void k_gram(const float* __restrict__ phik, co
   float* __restrict__ out = X2 + (static_cast<size_t>(bh) * ksplit + ks) * m * pairs;
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    const int p = 32 * (pt0 + 2 * t) + lr;
-    if (pt0 + 2 * t < kGramPT && p < pairs) {
+    const int p0 = 32 * (pt0 + 2 * t), p = p0 + lr;
+    if (pt0 + 2 * t < kGramPT && p0 + 1 == pairs) {
+      const float v = vs[t] + __shfl_xor(vs[t], 32);  // both halves of the positions
+      const int l = l0 + 32 * ft + lr;
+      if (lk == 0 && l < m) out[static_cast<size_t>(l) * pairs + p0] = v;
+    } else if (pt0 + 2 * t < kGramPT && p < pairs) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int l = l0 + 32 * ft + 8 * (e >> 2) + 4 * lk + (e & 3);
