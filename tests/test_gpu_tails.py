@@ -9,6 +9,7 @@ Sizes whose tails do not fill the kernels' tiles:
 * at n = 2000 and 4000 the convolutions load phi a feature ahead;
 * d = 128, 100 and 2: value columns in two groups of 64, a partial last
   group, and a count the 4-column loads of the value preparation do not take;
+* d = 1 and 65: the gram kernel's last pair tile holds a single pair;
 * the same tails on the direct route's row-parallel kernel (enough heads for
   it to be taken).
 
@@ -57,6 +58,10 @@ CASES = [
     (1, 2, 300, 128, 64, "bf16", "fft", "normal"),
     (1, 2, 1000, 100, 64, "f32", "fft", "causal"),
     (1, 2, 513, 2, 8, "f32", "fft", "normal"),
+    # one value pair in the last pair tile of the gram kernel: d = 1 (the
+    # pair [v, 1] alone) and d = 65 (the 33rd pair [v_64, 1])
+    (1, 2, 200, 1, 16, "f32", "fft", "normal"),
+    (1, 2, 700, 65, 40, "bf16", "fft", "causal"),
     # the direct route's row-parallel kernel (m <= 128 and at least 1536 waves
     # of 32 rows): a feature count that is not a multiple of 64, value columns
     # in two passes, a last row tile whose last waves start past n, causal
