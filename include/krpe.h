@@ -37,8 +37,9 @@
  *   undefined on return.
  * - Supported sizes: 1 <= n <= 16384 (any n; the FFT length is 2N with N the
  *   next power of two >= n), except the attention forward pass
- *   (krpe_attention_fwd*, krpe_feature_map*): 1 <= n <= 65536, longer
- *   sequences taking the Toeplitz matrix in blocks of 16384 positions;
+ *   (krpe_attention_fwd*, krpe_feature_map*) and the Toeplitz product
+ *   (krpe_toeplitz_conv*): 1 <= n <= 65536, longer sequences taking the
+ *   Toeplitz matrix in blocks of 16384 positions;
  *   1 <= d <= 128, 1 <= m <= 1024, B, H >= 0, C >= 0.
  *   B*H == 0 (or C == 0) is a valid empty call that enqueues nothing.
  * - Precondition (not checked: it would need to read device memory): every
@@ -163,6 +164,10 @@ size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n);
  * b : [H, 2n-1] fp32     a, y : [B, H, C, n] fp32 (sequence-contiguous channels)
  * Computed as a zero-padded length-2N FFT convolution (split into residue
  * classes of its frequency bins, each a transform of at most 8192 points).
+ * For n > 16384 the matrix is taken in blocks of 16384 positions, y_I =
+ * sum_J C_IJ a_J, each block of C itself Toeplitz (its window of b); blocks
+ * of C that are all zero (b = -inf throughout, e.g. above the diagonal under
+ * a causal mask) cost no transforms.
  */
 krpe_status_t krpe_toeplitz_conv(const float* b, const float* a, float* y,
                                  int B, int H, int C, int n,

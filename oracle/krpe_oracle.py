@@ -19,6 +19,9 @@ float64 (inputs given in fp32 or bf16 are converted exactly):
                            "naive" quadratic route that the FFT replaces
                            (Eqs. (12)-(13)); FFT and direct product agree
                            exactly up to rounding, so this is the reference.
+* ``toeplitz_rows``     -- the same product for selected output positions
+                           only, one row of C at a time, so that sequences
+                           too long for an n x n matrix can be checked.
 * ``attention``         -- Eq. (10): z_i = phi(q_i) sum_j c_{j-i} phi(k_j)^T v_j
                            / phi(q_i) sum_j c_{j-i} phi(k_j)^T, O(n^2), for
                            any of the three feature maps.
@@ -54,7 +57,7 @@ from __future__ import annotations
 import numpy as np
 
 __all__ = ["prf_features", "trf_features", "elu_features", "features", "toeplitz_matrix",
-           "toeplitz_product", "attention", "attention_rows", "attention_grad", "normalize_rows"]
+           "toeplitz_product", "toeplitz_rows", "attention", "attention_rows", "attention_grad", "normalize_rows"]
 
 
 def _f64(x) -> np.ndarray:
@@ -139,6 +142,24 @@ def toeplitz_product(b, a) -> np.ndarray:
     for h in range(b.shape[0]):
         C = toeplitz_matrix(b[h])
         out[:, h] = a[:, h] @ C.T
+    return out
+
+
+def toeplitz_rows(b, a, rows) -> np.ndarray:
+    """y[beta, h, c, r] = sum_j exp(b[h, j - i_r + n - 1]) a[beta, h, c, j] for i_r = rows[r].
+
+    Row i of C of Eqs. (12)-(13) is c_{j-i} = exp(b_{j-i}) over the keys j,
+    i.e. the window b[h, n-1-i : 2n-1-i] (Section 3.2, below Eq. (13)).
+    b : [H, 2n-1];  a : [B, H, C, n];  rows : output positions.  Returns
+    [B, H, C, len(rows)] float64.
+    """
+    b = _f64(b)
+    a = _f64(a)
+    n = a.shape[-1]
+    out = np.empty(a.shape[:-1] + (len(rows),))
+    for r, i in enumerate(rows):
+        c_row = np.exp(b[:, n - 1 - i:2 * n - 1 - i])       # [H, n]: c_{j-i} for j = 0..n-1
+        out[..., r] = np.einsum("bhcj,hj->bhc", a, c_row)
     return out
 
 

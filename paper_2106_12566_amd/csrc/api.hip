@@ -288,8 +288,11 @@ size_t fwd_workspace(int B, int H, int n, int d, int M, bool direct) {
 
 ConvLayout conv_layout(int B, int H, int C, int n) {
   ConvLayout L{};
-  L.l2 = log2_ceil(n);
-  const size_t N = static_cast<size_t>(1) << L.l2;
+  const bool blocked = n > (1 << kMaxLog2N);
+  L.l2 = blocked ? kMaxLog2N : log2_ceil(n);
+  L.nbk = blocked ? 1 << kMaxLog2N : n;
+  L.nb = blocked ? (n + L.nbk - 1) / L.nbk : 1;
+  const size_t N = static_cast<size_t>(1) << L.l2, nb = static_cast<size_t>(L.nb);
   const size_t bh = static_cast<size_t>(B) * H;
   const size_t pairs = (static_cast<size_t>(C) + 1) / 2;
   size_t off = 0;
@@ -299,12 +302,16 @@ ConvLayout conv_layout(int B, int H, int C, int n) {
     return at;
   };
   L.tw = take(static_cast<size_t>(twiddle_slots(L.l2)) * sizeof(float2));
-  L.hs = take(static_cast<size_t>(H) * 2 * N * sizeof(float2));
+  L.hs = take(nb * H * 2 * N * sizeof(float2));
+  L.hnorm = take(blocked ? nb * H * sizeof(float2) : 0);
+  L.bwin = take(blocked ? nb * H * (2 * N - 1) * sizeof(float) : 0);
   L.ones = take(phi_bytes(1, N));
-  L.vsc = take(bh * pairs * N * sizeof(float2));
-  L.colmax = take(bh * C * sizeof(float));
-  L.vmax = take(bh * vmax_chunks(n) * static_cast<size_t>(C) * sizeof(float));
-  L.part = take(conv_splits(L.l2) > 1 ? bh * conv_splits(L.l2) * C * n * sizeof(float) : 0);
+  L.vsc = take(nb * bh * pairs * N * sizeof(float2));
+  L.colmax = take(nb * bh * C * sizeof(float));
+  L.vmax = take(bh * vmax_chunks(L.nbk) * static_cast<size_t>(C) * sizeof(float));
+  // (a blocked product sums nb key blocks x the class splits per row)
+  const size_t nsplit = nb * static_cast<size_t>(conv_splits(L.l2));
+  L.part = take(nsplit > 1 ? bh * nsplit * C * static_cast<size_t>(L.nbk) * sizeof(float) : 0);
   L.total = off;
   return L;
 }
@@ -398,7 +405,7 @@ krpe_status_t run_forward(const AttnLayout& L, char* w, const void* q, const voi
   int nsum = L.fsplit * conv_splits(L.l2);
   if (L.fsplit > 1 && static_cast<long long>(BHi) * ((n + 63) / 64) < 4096) {
     float* psum = reinterpret_cast<float*>(w + L.psum);
-    if (krpe_status_t s = hip_check(launch_sum_splits(part, psum, BHi, d + 1, n, nsum, st), "sum launch"))
+    if (krpe_status_t s = hip_check(launch_sum_splits(part, psum, BHi, d + 1, n, n, nsum, st), "sum launch"))
       return s;
     sums = psum;
     nsum = 1;
@@ -480,7 +487,7 @@ krpe_status_t run_forward_long(const LongLayout& L, char* w, const void* q, cons
                                     "weight launch"))
       return s;
     unsigned long long* maskb = reinterpret_cast<unsigned long long*>(w + L.maskb);
-    if (krpe_status_t s = hip_check(launch_sum_splits(F(L.part), F(L.psum), BHi, cols, lenI, nb * L.fsplit * splits, st),
+    if (krpe_status_t s = hip_check(launch_sum_splits(F(L.part), F(L.psum), BHi, cols, lenI, lenI, nb * L.fsplit * splits, st),
                                     "sum launch"))
       return s;
     if (krpe_status_t s = hip_check(launch_combine(F(L.psum), pqb, F2(L.wbi), F2(L.hunit), F(L.zb), nullptr, fix, maskb,
@@ -553,7 +560,7 @@ krpe_status_t scratch_address(hipStream_t stream, void** out) {
 krpe_status_t toeplitz_conv(const float* b, const float* a, float* y, int B, int H, int C, int n, void* ws,
                             size_t ws_bytes, void* stream) {
   if (C < 0) return fail(KRPE_ERR_SHAPE, "negative size");
-  if (krpe_status_t s = check_dims(B, H, n, 0, 0, false)) return s;
+  if (krpe_status_t s = check_dims(B, H, n, 0, 0, false, kMaxLongLog2N)) return s;
   if (static_cast<long long>(B) * H * C * n >= (1LL << 31))
     return fail(KRPE_ERR_UNSUPPORTED, "B * H * C * n >= 2^31 is not supported");
   const size_t bh = static_cast<size_t>(B) * H;
@@ -584,6 +591,43 @@ krpe_status_t toeplitz_conv(const float* b, const float* a, float* y, int B, int
   const int splits = conv_splits(L.l2);
   // The product runs through the attention's convolution kernel with one
   // feature equal to 1 everywhere: a_c plays the role of the value column c.
+  if (L.nb > 1) {
+    // Blocks of nbk positions (Eqs. (12)-(13) per block of C): y_I =
+    // sum_J C_IJ a_J, block row I as one launch over the nb key blocks J
+    // (blocks of C that are all zero, e.g. above the diagonal under a causal
+    // mask, skip their transforms), its partial sums added into y_I.
+    const int nbk = L.nbk, nb = L.nb;
+    const size_t pairs = (static_cast<size_t>(C) + 1) / 2;
+    auto len_of = [&](int K) { return n - K * nbk < nbk ? n - K * nbk : nbk; };
+    float* bwin = reinterpret_cast<float*>(w + L.bwin);
+    float2* hnorm = reinterpret_cast<float2*>(w + L.hnorm);
+    if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
+    if (krpe_status_t s = hip_check(launch_ones(ones, nbk, nbk, st), "ones launch")) return s;
+    for (int J = 0; J < nb; ++J) {
+      // key block J's channels, zero past its length
+      if (krpe_status_t s = hip_check(launch_vprep(false, a + static_cast<size_t>(J) * nbk, 1, n,
+                                                   static_cast<long long>(C) * n, C, false, BHi, len_of(J), nbk,
+                                                   vmax, colmax + static_cast<size_t>(J) * bh * C,
+                                                   vsc + static_cast<size_t>(J) * bh * pairs * nbk, st),
+                                      "column launch"))
+        return s;
+    }
+    for (int I = 0; I < nb; ++I) {
+      const int lenI = len_of(I);
+      if (krpe_status_t s = hip_check(launch_bias_window(b, bwin, H, n, nbk, nb, I, st), "bias launch")) return s;
+      if (krpe_status_t s = hip_check(launch_spectrum(L.l2, bwin, tw, Hs, hnorm, nb * H, nbk, st), "spectrum launch"))
+        return s;
+      if (krpe_status_t s = hip_check(launch_conv_split(L.l2, ones, ones, 0, vsc, colmax, Hs, hnorm, tw, part, BHi, H,
+                                                        lenI, C, 1, nb, 1, st),
+                                      "conv launch"))
+        return s;
+      if (krpe_status_t s = hip_check(launch_sum_splits(part, y + static_cast<size_t>(I) * nbk, BHi, C, lenI, n,
+                                                        nb * splits, st),
+                                      "sum launch"))
+        return s;
+    }
+    return KRPE_OK;
+  }
   if (krpe_status_t s = hip_check(launch_twiddles(tw, L.l2, st), "twiddle launch")) return s;
   if (krpe_status_t s = hip_check(launch_spectrum(L.l2, b, tw, Hs, nullptr, H, n, st), "spectrum launch")) return s;
   if (krpe_status_t s = hip_check(launch_ones(ones, n, N, st), "ones launch")) return s;
@@ -595,7 +639,7 @@ krpe_status_t toeplitz_conv(const float* b, const float* a, float* y, int B, int
                                               H, n, C, 1, st),
                                   "conv launch"))
     return s;
-  if (splits > 1) return hip_check(launch_sum_splits(part, y, BHi, C, n, splits, st), "sum launch");
+  if (splits > 1) return hip_check(launch_sum_splits(part, y, BHi, C, n, n, splits, st), "sum launch");
   return KRPE_OK;
 }
 
@@ -653,7 +697,7 @@ krpe_status_t krpe_feature_map(const void* x, int x_dtype, const float* W, float
 }
 
 size_t krpe_toeplitz_conv_workspace(int B, int H, int C, int n) {
-  if (B < 0 || H < 0 || C < 0 || n < 1 || n > (1 << kMaxLog2N)) return 0;
+  if (B < 0 || H < 0 || C < 0 || n < 1 || n > (1 << kMaxLongLog2N)) return 0;
   return conv_layout(B, H, C, n).total;
 }
 
@@ -668,7 +712,7 @@ krpe_status_t krpe_toeplitz_conv_noalloc(const float* b, const float* a, float* 
   g_last_error.clear();
   // sizes first (no HIP call for a rejected request), then the workspace
   if (C < 0) return fail(KRPE_ERR_SHAPE, "negative size");
-  if (krpe_status_t s = check_dims(B, H, n, 0, 0, false)) return s;
+  if (krpe_status_t s = check_dims(B, H, n, 0, 0, false, kMaxLongLog2N)) return s;
   if (static_cast<long long>(B) * H * C * n >= (1LL << 31))
     return fail(KRPE_ERR_UNSUPPORTED, "B * H * C * n >= 2^31 is not supported");
   if (static_cast<size_t>(B) * H == 0 || C == 0) return KRPE_OK;

@@ -2128,12 +2128,13 @@ __global__ void k_ones(float* __restrict__ ones, int n, int N) {
 }
 
 // y[bh][c][i] = sum_s part[bh][s][c][i]
-__global__ void k_sum_splits(const float* __restrict__ part, float* __restrict__ y, int C, int n, int nsplit,
-                             long long total) {
+__global__ void k_sum_splits(const float* __restrict__ part, float* __restrict__ y, int C, int n, int ldy,
+                             int nsplit, long long total) {
   const long long e = static_cast<long long>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (e >= total) return;
   const long long per = static_cast<long long>(C) * n;
   const long long bh = e / per, r = e % per;
+  const long long row = bh * C + r / n, i = r % n;  // output row (bh, c) and position
   // independent loads in flight (sums in split order, as a plain loop)
   const float* __restrict__ p = part + bh * nsplit * per + r;
   float s = 0.f;
@@ -2143,7 +2144,7 @@ __global__ void k_sum_splits(const float* __restrict__ part, float* __restrict__
     s = (((s + a0) + a1) + a2) + a3;
   }
   for (; sp < nsplit; ++sp) s += p[sp * per];
-  y[e] = s;
+  y[row * ldy + i] = s;
 }
 
 // ============================================================= backward ==
@@ -2755,10 +2756,11 @@ hipError_t launch_ones(float* ones, int n, int N, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st) {
+hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int ldy, int nsplit,
+                             hipStream_t st) {
   const long long total = static_cast<long long>(BH) * C * n;
   hipLaunchKernelGGL(k_sum_splits, dim3(static_cast<unsigned>((total + 255) / 256)), dim3(256), 0, st, part, y, C,
-                     n, nsplit, total);
+                     n, ldy, nsplit, total);
   return hipGetLastError();
 }
 

@@ -88,9 +88,13 @@ LongLayout long_layout(int B, int H, int n, int d, int M);
 int conv_fsplit(int l2, int BH, int cols, int M, int nkb);
 
 // Workspace of krpe_toeplitz_conv.
+// Workspace of krpe_toeplitz_conv.  For n > 2^kMaxLog2N the Toeplitz matrix is
+// taken in nb x nb blocks of nbk = 2^kMaxLog2N positions (nb = 1 otherwise):
+// hs, hnorm and bwin then hold the spectra, norms and bias windows of one
+// block row, vsc and colmax the channels of every key block.
 struct ConvLayout {
-  int l2;
-  size_t tw, hs, ones, vsc, colmax, vmax, part, total;
+  int l2, nb, nbk;
+  size_t tw, hs, hnorm, bwin, ones, vsc, colmax, vmax, part, total;
 };
 ConvLayout conv_layout(int B, int H, int C, int n);
 
@@ -192,6 +196,7 @@ hipError_t launch_db(int l2, const float* phiq, const float* phik, long long phi
 hipError_t launch_feature_bwd(bool bf16, const void* x, const float* W, const float* phi, const float* part,
                               float* dx, int BH, int H, int n, int N, int d, int m, int nsplit, bool nprf,
                               hipStream_t st);
-hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int nsplit, hipStream_t st);
+// y[bh][c][i] (row stride ldy) = sum over s of part[bh][s][c][i], i < n.
+hipError_t launch_sum_splits(const float* part, float* y, int BH, int C, int n, int ldy, int nsplit, hipStream_t st);
 
 }  // namespace krpe

@@ -81,9 +81,10 @@ def test_workspace_queries(lib):
     assert fft_long >= 2 * 2 * 64 * 49152 * 4 * 2
     assert lib.krpe_attention_fwd_workspace_ex(1, 2, 40000, 64, 64, 8) > 0
     assert lib.krpe_attention_fwd_workspace_ex(1, 1, 65536, 64, 64, 0) > 0
-    # the backward and the plain Toeplitz product stay within one block
+    # the backward stays within one block; the plain Toeplitz product goes to 65536 in blocks
     assert lib.krpe_attention_bwd_workspace(1, 1, 16385, 4, 4, 0) == 0
-    assert lib.krpe_toeplitz_conv_workspace(1, 1, 1, 16385) == 0
+    assert lib.krpe_toeplitz_conv_workspace(1, 1, 1, 16385) > lib.krpe_toeplitz_conv_workspace(1, 1, 1, 16384) > 0
+    assert lib.krpe_toeplitz_conv_workspace(1, 1, 1, 65536) > 0 and lib.krpe_toeplitz_conv_workspace(1, 1, 1, 65537) == 0
     assert lib.krpe_attention_fwd_workspace(1, 1, 8, 129, 4) == 0
     assert lib.krpe_toeplitz_conv_workspace(1, 2, 3, 100) > 0
     assert lib.krpe_toeplitz_conv_workspace(1, 2, 3, 0) == 0
@@ -154,7 +155,8 @@ def test_toeplitz_validation(lib):
     assert call(a=None) == NULL
     assert call(n=0) == SHAPE
     assert call(C=-1) == SHAPE
-    assert call(n=20000) == UNSUP
+    assert call(n=65537) == UNSUP
+    assert call(n=20000) == WS               # a valid length whose workspace is larger
     assert call(wb=8) == WS
     assert call(y=Q) == ALIAS
     assert call(y=Z + 8) == ALIGN
@@ -169,7 +171,7 @@ def test_toeplitz_noalloc_refuses_sizes_beyond_the_scratch(lib):
     assert lib.krpe_toeplitz_conv_noalloc(None, None, None, *big, None) == UNSUP
     assert b"static scratch" in lib.krpe_last_error()
     assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, -1, 10, None) == SHAPE
-    assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, 2, 20000, None) == UNSUP
+    assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, 2, 65537, None) == UNSUP
     assert lib.krpe_toeplitz_conv_noalloc(None, None, None, 1, 1, 0, 10, None) == OK
 
 

@@ -110,3 +110,38 @@ def test_long_sequence_value_shift(gpu_lib):
     err = rownorm_err((z1 - 3.0).cpu().numpy(), z0.cpu().numpy())
     _say(f"long value shift: {err:.3e}")
     assert err <= 2 * TOL["f32"], err
+
+
+# ------------------------------------------- Toeplitz product beyond 16384 --
+@pytest.mark.parametrize("B,H,C,n,bias", [
+    (1, 2, 3, 16385, "normal"),   # one position in the second block
+    (2, 1, 5, 40000, "causal"),   # three blocks, the last partial; zero blocks above the diagonal
+    (1, 2, 2, 65536, "normal"),   # the largest length, four whole blocks
+])
+def test_toeplitz_conv_long(gpu_lib, B, H, C, n, bias):
+    """krpe_toeplitz_conv past one transform block: y_I = sum_J C_IJ a_J over blocks of
+    16384 positions, against the fp64 oracle's rows of C a at sampled positions and on both
+    sides of every block boundary; the no-allocation entry point gives the same bits."""
+    _say(f"toeplitz long B={B} H={H} C={C} n={n} {bias}")
+    rng = np.random.default_rng([17, n, C])
+    b = 0.5 * rng.standard_normal((H, 2 * n - 1))
+    if bias == "causal":
+        b[:, n:] = -np.inf                       # b_t = -inf for t > 0
+    b = b.astype(np.float32)
+    a = rng.standard_normal((B, H, C, n)).astype(np.float32)
+    bg, ag = to_gpu(b), to_gpu(a)
+    y = gpu_lib.toeplitz_conv(bg, ag)
+    rows = set(rng.integers(0, n, 24).tolist()) | {0, 1, n - 1}
+    for edge in range(NBK, n, NBK):
+        rows |= {edge - 1, edge, edge + 1}
+    rows = sorted(i for i in rows if 0 <= i < n)
+    ref = oracle.toeplitz_rows(b, a, rows)
+    got = y.cpu().numpy()[..., rows]
+    assert np.all(np.isfinite(got))
+    err = rownorm_err(got, ref)
+    _say(f"  {len(rows)} rows: err={err:.3e}")
+    assert err <= 2e-4, err
+    if gpu_lib.toeplitz_conv_workspace(B, H, C, n) <= 64 << 20:
+        y0 = gpu_lib.toeplitz_conv_noalloc(bg, ag)
+        torch.cuda.synchronize()
+        assert torch.equal(y0, y)

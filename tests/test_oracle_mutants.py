@@ -26,6 +26,10 @@ MUTANTS = {
     "values_replaced_by_keys": ("num = mt @ v[beta, h]", "num = mt @ k[beta, h]"),
     "toeplitz_transposed": ("out[:, h] = a[:, h] @ C.T", "out[:, h] = a[:, h] @ C"),
     "toeplitz_matrix_sign": ("return np.exp(b_h[j - i + n - 1])", "return np.exp(b_h[i - j + n - 1])"),
+    "toeplitz_rows_window_reversed": ("c_row = np.exp(b[:, n - 1 - i:2 * n - 1 - i])",
+                                      "c_row = np.exp(b[:, i:i + n][:, ::-1])"),
+    "toeplitz_rows_window_off_by_one": ("c_row = np.exp(b[:, n - 1 - i:2 * n - 1 - i])",
+                                        "c_row = np.exp(b[:, n - i:2 * n - i])"),
     "rows_offset_sign": ("c = np.exp(b[h][np.arange(n) - i + n - 1])", "c = np.exp(b[h][i - np.arange(n) + n - 1])"),
     "rows_wrong_head_features": ("cache[(beta, h)] = fmap(k[beta, h], W[h])", "cache[(beta, h)] = fmap(k[beta, h], W[0])"),
     "nprf_keys_not_normalised": ("        q, k = normalize_rows(q), normalize_rows(k)\n    Bn", "        q = normalize_rows(q)\n    Bn"),

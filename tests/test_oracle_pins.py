@@ -292,6 +292,35 @@ def check_toeplitz_special_cases(impl):
     assert np.allclose(y, ref, rtol=1e-13, atol=1e-13)
 
 
+def check_toeplitz_rows(impl):
+    """Selected rows of C a: scalar brute force on random b, and the special cases of the
+    full product (identity, shift, all ones, causal ones) at the rows asked for."""
+    rng = np.random.default_rng(23)
+    n = 13
+    a = rng.standard_normal((2, 2, 3, n))
+    rows = [0, 1, 6, n - 1]
+    b = rng.standard_normal((2, 2 * n - 1))
+    y = impl.toeplitz_rows(b, a, rows)
+    assert y.shape == (2, 2, 3, len(rows))
+    for r, i in enumerate(rows):
+        ref = np.zeros((2, 2, 3))
+        for h in range(2):
+            for j in range(n):
+                ref[:, h] += math.exp(b[h, j - i + n - 1]) * a[:, h, :, j]
+        assert np.allclose(y[..., r], ref, rtol=1e-13, atol=1e-13)
+    t = np.arange(-(n - 1), n)
+    ident = np.where(t == 0, 0.0, -np.inf)[None].repeat(2, 0)
+    assert np.array_equal(impl.toeplitz_rows(ident, a, rows), a[..., rows])
+    shift = np.where(t == -1, 0.0, -np.inf)[None].repeat(2, 0)
+    ys = impl.toeplitz_rows(shift, a, rows)
+    assert np.all(ys[..., 0] == 0) and np.array_equal(ys[..., 1:], a[..., [i - 1 for i in rows[1:]]])
+    ones = np.zeros((2, 2 * n - 1))
+    assert np.allclose(impl.toeplitz_rows(ones, a, rows), a.sum(-1)[..., None].repeat(len(rows), -1), rtol=1e-13)
+    causal = np.where(t <= 0, 0.0, -np.inf)[None].repeat(2, 0)
+    assert np.allclose(impl.toeplitz_rows(causal, a, rows), np.cumsum(a, axis=-1)[..., rows], rtol=1e-12,
+                       atol=1e-14)
+
+
 def _brute_normalize(x_row):
     """x / ||x||_2 with scalar arithmetic (Algorithm 1, first step); zero stays zero."""
     nrm = math.sqrt(sum(t * t for t in x_row))
@@ -526,7 +555,7 @@ def check_grad_invariants(impl):
 ALL_CHECKS = [check_brute_force, check_toeplitz_factorisation, check_single_position,
               check_const_bias_is_linear_attention, check_causal_prefix_sums,
               check_only_diagonal, check_shift_kernel, check_invariants,
-              check_causality, check_prf_variance_lemma, check_toeplitz_special_cases,
+              check_causality, check_prf_variance_lemma, check_toeplitz_special_cases, check_toeplitz_rows,
               check_rows_match_full, check_nprf_brute_force, check_nprf_scale_invariance,
               check_trf_brute_force, check_trf_kernel_identity, check_trf_unbiased,
               check_elu_brute_force, check_feature_maps_linear_route,
