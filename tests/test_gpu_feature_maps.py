@@ -135,3 +135,26 @@ def test_trf_exact_rows_and_option_effect(gpu_lib):
     assert rownorm_err(np.stack([zt[0, 0, i] for _, _, i in rows]), ref) <= TOL["f32"]
     zp = gpu_lib.attention_fwd(q, k, v, b, W, nprf=True).cpu().numpy()
     assert rownorm_err(zt, zp) > 1e-3
+
+
+@pytest.mark.parametrize("features,nprf,bias", [("trf", True, "causal"), ("elu", False, "normal"),
+                                                ("prf", True, "normal")])
+def test_feature_maps_row_parallel_direct_kernel(gpu_lib, features, nprf, bias):
+    """The other feature maps through the direct route's row-parallel kernel (enough heads that
+    the rows give at least 1536 waves, features per position <= 128): signed trigonometric
+    features (M = 2m = 64), elu + 1 (M = d = 64); sampled rows against the oracle."""
+    B, H, n, d, m = 4, 12, 1000, 64, 32
+    assert B * H * ((n + 31) // 32) >= 1536
+    _say(f"row-parallel direct {features} nprf={nprf} {bias}")
+    small_qk = features == "trf" and not nprf
+    dd = synth.custom(B, H, n, d, m, seed=47, bias=bias, qk_scale=0.2 if small_qk else None)
+    W = None if features == "elu" else dd["W"]
+    q, k, v, b = (to_gpu(dd[x]) for x in ("q", "k", "v", "b"))
+    z = gpu_lib.attention_fwd(q, k, v, b, None if W is None else to_gpu(W), nprf=nprf, features=features,
+                              route="direct").cpu().numpy()
+    assert np.all(np.isfinite(z))
+    rows = sample_rows(B, H, n, 64, seed=3, extra=[(0, 0, 0), (0, 0, 1), (B - 1, H - 1, n - 1)])
+    ref, den = oracle.attention_rows(dd["q"], dd["k"], dd["v"], dd["b"], W, rows, nprf=nprf, kind=features)
+    err = rownorm_err(np.stack([z[bb, h, i] for bb, h, i in rows]), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL["f32"], err
