@@ -62,6 +62,7 @@ CASES = [
     (2, 2, 256, 64, 32, "f32", "normal", True),
     (1, 1, 1000, 64, 64, "bf16", "causal", True),
     (1, 1, 1025, 128, 40, "f32", "decay", True),   # d = 128, just past a power of two
+    (4, 12, 1000, 64, 32, "f32", "normal", False),  # forward (z, denominators) by the row-parallel direct kernel
 ]
 
 
