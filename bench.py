@@ -107,14 +107,14 @@ def measured_traffic(kernel: str, workload: str):
 
 
 def device_source_hash() -> str:
-    """sha256 of the translation unit the convolution and the other forward kernels are compiled
-    from (kernels.hip and the headers it includes), comments and blank space removed (comment
-    edits keep it; host code in the other sources does not change it)."""
+    """sha256 of the translation units the convolution and the other forward kernels are compiled
+    from (kernels.hip, conv_top.hip and the headers they include), comments and blank space
+    removed (comment edits keep it; host code in the other sources does not change it)."""
     import hashlib
     import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2106_12566_amd", "csrc")
-    for name in ("common.hpp", "fft.hpp", "kernels.hip", "launch.hpp"):
+    for name in ("common.hpp", "conv.hpp", "conv_top.hip", "fft.hpp", "kernels.hip", "launch.hpp"):
         f = os.path.join(csrc, name)
         text = open(f).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
